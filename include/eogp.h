@@ -1,0 +1,221 @@
+/*
+ * eogp.h -- C ABI of the EOGP hot path (eigenbasis-corrected one-bit gradient
+ * projection) on AMD Instinct MI355X (gfx950).
+ *
+ * The path has two parts. Storing: each example's per-module gradient
+ * G = sum_t ds_t a_t^T is rotated into the K-FAC Kronecker eigenbasis
+ * Q_A (x) Q_S one token at a time, the coordinates with the m largest
+ * corrected eigenvalues are kept and half-whitened (first stage), projected by
+ * the PCA matrix P (second stage) and stored as packed sign bits plus one fp16
+ * scale. Scoring: unquantized query coordinates are scored against the stored
+ * codes and a per-query top-k is kept.
+ *
+ * Conventions for every call:
+ *   - Array arguments are DEVICE pointers owned by the caller unless a comment
+ *     says "host". The library never frees caller memory. Only
+ *     eogp_plan_create allocates (the plan's own memory, released by
+ *     eogp_plan_destroy); scratch for the other calls comes from a caller
+ *     workspace whose size the matching *_workspace_size call returns.
+ *   - Arrays are row-major and contiguous unless a leading dimension ("ld",
+ *     in elements) or a row stride is given.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream). Calls
+ *     only enqueue work on it and return, except eogp_plan_create and the
+ *     one-shot eogp_rotate_retain, which synchronise `stream` once.
+ *   - Argument errors return EOGP_ERR_INVALID before anything is enqueued;
+ *     EOGP_ERR_UNSUPPORTED marks a valid but unimplemented dtype/shape mix;
+ *     EOGP_ERR_DEVICE a HIP launch or runtime error; EOGP_ERR_WORKSPACE a
+ *     workspace smaller than required. eogp_last_error() describes the last
+ *     failure on the calling thread.
+ */
+#ifndef EOGP_H
+#define EOGP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t eogp_status;
+#define EOGP_OK 0
+#define EOGP_ERR_INVALID (-1)
+#define EOGP_ERR_UNSUPPORTED (-2)
+#define EOGP_ERR_DEVICE (-3)
+#define EOGP_ERR_WORKSPACE (-4)
+
+typedef enum { EOGP_F32 = 0, EOGP_BF16 = 1, EOGP_F16 = 2 } eogp_dtype;
+
+/* Arithmetic of the dense contractions. FAST: one MFMA pass on operands
+ * rounded to bf16 (or fp16 where an operand is given in fp16), fp32
+ * accumulation. ACCURATE: every fp32 operand is split into a high and a low
+ * 16-bit part and the cross products are accumulated in fp32 (three MFMA
+ * passes when both operands are fp32, two when one is already 16-bit), which
+ * carries about 16 significant bits into each product. */
+typedef enum { EOGP_PREC_FAST = 0, EOGP_PREC_ACCURATE = 1 } eogp_prec;
+
+/* ------------------------------------------------------------------------
+ * Fitting shared projections: retained-axis selection (Algorithm 1, first
+ * block, "select Q_{u,m}, Lambda_{u,m} using the m_u largest corrected
+ * eigenvalues"; Section 3.2 first stage and eq. sigma_ekfac, which makes the
+ * m largest corrected eigenvalues the top-m PCA axes of Sigma_proxy).
+ *
+ * A plan holds, for one module, the m retained axes in canonical order
+ * (Lambda descending, then flat index j*d_in + k ascending), their
+ * half-whitening weights (Lambda_r + lambda)^-1/2 (eq. first_stage), and the
+ * eigenvector columns of Q_A and Q_S those axes use, gathered so the first
+ * stage runs as dense contractions without forming Q_m (eq.
+ * app_projection_maps, "Kronecker factors and retained-coordinate indices").
+ *
+ *   eigvals  [d_out, d_in] fp32: corrected eigenvalue Lambda[j, k] of the
+ *            axis Q_A[:, k] (x) Q_S[:, j] (eq. ekfac_eigendecompose).
+ *   damping  lambda > 0.
+ *   m        1 <= m <= d_in * d_out.
+ *   Q_A      [d_in, d_in] fp32, column k = k-th eigenvector of A = E[a a^T].
+ *   Q_S      [d_out, d_out] fp32, column j = j-th eigenvector of S.
+ *   out      receives the plan (host handle).
+ * Errors: EOGP_ERR_INVALID for bad sizes, NULL pointers, damping <= 0, a NaN
+ * anywhere in eigvals, or a retained Lambda_r + lambda <= 0. Runs on `stream`
+ * and synchronises it once (it reads back the retained-set sizes).
+ * ------------------------------------------------------------------------ */
+typedef struct eogp_plan eogp_plan;
+
+typedef struct {
+  int64_t d_out, d_in, m;
+  double damping;
+  int64_t n_rows;   /* |J|: distinct Q_S columns used by the retained set   */
+  int64_t n_cols;   /* |K|: distinct Q_A columns used by the retained set   */
+  int64_t n_tiles;  /* 32 x 32 blocks of (row, column) pairs holding retained axes */
+  const int32_t* retained_flat;    /* device [m]: j*d_in + k, canonical order */
+  const float* retained_weight;    /* device [m]: (Lambda_r + lambda)^-1/2     */
+} eogp_plan_info;
+
+eogp_status eogp_plan_create(const float* eigvals, int64_t d_out, int64_t d_in,
+                             double damping, int64_t m, const float* Q_A,
+                             const float* Q_S, void* stream, eogp_plan** out);
+void eogp_plan_destroy(eogp_plan* plan);
+eogp_status eogp_plan_get_info(const eogp_plan* plan, eogp_plan_info* info);
+/* Copy the retained axes (flat index j*d_in + k, int32 [m]) and their
+ * half-whitening weights (fp32 [m]) into caller device buffers; either output
+ * may be NULL. Enqueued on `stream`. */
+eogp_status eogp_plan_copy_retained(const eogp_plan* plan, int32_t* flat_out,
+                                    float* weight_out, void* stream);
+
+/* ------------------------------------------------------------------------
+ * First stage (eq. first_stage; eq. app_projection_maps; Algorithm 1,
+ * storing: x_{i,u} <- T_u(L_u g_{i,u})). For every example i:
+ *   Z[i, r] = (Lambda_r + lambda)^-1/2
+ *             * sum_{t : token_mask[i, t] != 0} (Q_S[:, j_r] . ds[i, t])
+ *                                               (Q_A[:, k_r] . a[i, t])
+ * for the retained axes r = 0..m-1 of the plan, in canonical order. The
+ * gradient is never formed: valid tokens are compacted, rotated onto the
+ * needed eigenvectors with MFMA contractions, and the retained products are
+ * summed per example (the loss is token-summed over valid positions).
+ *
+ *   acts       [N, T, d_in]  in `in_dtype` (EOGP_F32 or EOGP_BF16).
+ *   out_grads  [N, T, d_out] in `in_dtype`.
+ *   token_mask [N, T] uint8, or NULL for all tokens valid. Masked tokens are
+ *              never read and may hold anything, NaN included.
+ *   Z          [N, ldz] fp32, ldz >= m; columns m..ldz-1 are not written.
+ *   prec       EOGP_PREC_ACCURATE keeps about 16 bits per product (use for
+ *              fp32 inputs); EOGP_PREC_FAST rounds operands to bf16.
+ *   ws         workspace of at least eogp_rotate_retain_workspace_size bytes.
+ * ------------------------------------------------------------------------ */
+size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64_t T);
+eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
+                                       const void* out_grads, eogp_dtype in_dtype,
+                                       const uint8_t* token_mask, int64_t N, int64_t T,
+                                       float* Z, int64_t ldz, eogp_prec prec,
+                                       void* ws, size_t ws_bytes, void* stream);
+
+/* One-shot form with the paper's arguments: builds a plan from
+ * (eigvals, damping, m, Q_A, Q_S), runs the first stage, releases the plan.
+ * Synchronises `stream`. Workspace: eogp_rotate_retain_oneshot_workspace_size. */
+size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d_in,
+                                                 int64_t d_out);
+eogp_status eogp_rotate_retain(const void* acts, const void* out_grads,
+                               eogp_dtype in_dtype, const uint8_t* token_mask,
+                               int64_t N, int64_t T, int64_t d_in, int64_t d_out,
+                               const float* Q_A, const float* Q_S, const float* eigvals,
+                               double damping, int64_t m, float* Z, int64_t ldz,
+                               eogp_prec prec, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Second stage (eq. second_stage; appendix "Implementation": one correction
+ * matrix applied to a whole batch of cached first-stage coordinates):
+ *   X[i, c] = sum_r Z[i, r] P[r, c],  i.e. x_i = P^T z_i.
+ *
+ *   Z   [N, ldz] fp32 (first m columns used).
+ *   P   the m x k PCA matrix stored COLUMN-major: direction c occupies
+ *       P + c*ldp .. P + c*ldp + m - 1 (ldp >= m), in `p_dtype` (EOGP_F16 as
+ *       the paper stores it, EOGP_BF16 or EOGP_F32).
+ *   X   [N, ldx] fp32, ldx >= k.
+ *   ws  needed only for p_dtype == EOGP_F32 (the split copy of P):
+ *       eogp_pca_project_workspace_size bytes; otherwise may be NULL.
+ * With p_dtype EOGP_F16 the fp32 Z is converted to fp16 (split into two fp16
+ * parts under EOGP_PREC_ACCURATE); Z must then lie within the fp16 range.
+ * ------------------------------------------------------------------------ */
+size_t eogp_pca_project_workspace_size(int64_t m, int64_t k, eogp_dtype p_dtype,
+                                       eogp_prec prec);
+eogp_status eogp_pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m,
+                             const void* P, eogp_dtype p_dtype, int64_t ldp, int64_t k,
+                             float* X, int64_t ldx, eogp_prec prec, void* ws,
+                             size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * One-bit encoding (eq. onebit; Algorithm 1, "store packed binary signs and
+ * s = FP16(||x||_1 / k)"; payload layout of eq. app_payload):
+ *   bit c of row i = (X[i, c] >= 0)  (so -0.0 -> 1, NaN -> 0), stored in byte
+ *   c >> 3, bit c & 7 of codes + i*code_row_stride (ceil(k/8) bytes written);
+ *   scales[i*scale_stride] = fp16 bits of ||X[i, :k]||_1 / k, summed in fp64 and
+ *   rounded once to nearest even (overflow gives +inf).
+ * Strides let each module's codes and scale land inside a multi-module row.
+ * ------------------------------------------------------------------------ */
+eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k,
+                           uint8_t* codes, int64_t code_row_stride, uint16_t* scales,
+                           int64_t scale_stride, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Scoring (eq. onebit_influence, eq. app_stored_influence; Algorithm 1,
+ * "scoring a query") with a per-query top-k:
+ *   score(q, i) = sum_{u = 0..U-1, ascending} s_{i,u} <y_{q,u}, b_{i,u}>,
+ * b in {-1, +1}. Each query module vector y_{q,u} is taken in fixed point:
+ * f = 14 - e for max_c |y_c| = mu 2^e (mu in [0.5, 1)), y_int = rint(y 2^f)
+ * (nearest even), so <y_int, b> is an exact integer n and each term
+ * s * n * 2^-f is exact in fp64; an all-zero y_{q,u} contributes 0. Terms are
+ * summed in fp64 in module order. Ranking: score descending, then example
+ * index ascending.
+ *
+ *   codes        [N, code_row_stride] bytes; module u occupies bytes
+ *                sum_{v<u} k_v/8 .. + k_u/8 of each row (eogp_sign_pack layout).
+ *   scales       [N, U] fp16 bit patterns.
+ *   k_per_module HOST [U]; each k_u must be a positive multiple of 64.
+ *   Y            [Q, ldy] fp32 query coordinates (modules concatenated),
+ *                ldy >= sum_u k_u.
+ *   out_idx      [Q, topk] int64 example indices; out_score [Q, topk] fp32
+ *                (the fp64 score rounded once). If N < topk the tail holds
+ *                index -1 and score -inf.
+ *   full_scores  [Q, N] fp32, or NULL to skip writing every score.
+ *   topk         1..256.
+ *   ws           eogp_score_topk_workspace_size(N, Q, U, k_per_module, topk) bytes.
+ * Requirements: code_row_stride a multiple of 8 and codes 8-byte aligned;
+ * Y finite. The per-module table is copied to the device from host memory.
+ * ------------------------------------------------------------------------ */
+size_t eogp_score_topk_workspace_size(int64_t N, int64_t Q, int32_t U,
+                                      const int64_t* k_per_module, int32_t topk);
+eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride,
+                            const uint16_t* scales, int64_t N, int32_t U,
+                            const int64_t* k_per_module, const float* Y, int64_t ldy,
+                            int64_t Q, int32_t topk, int64_t* out_idx, float* out_score,
+                            float* full_scores, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+const char* eogp_status_string(eogp_status status);
+const char* eogp_last_error(void);
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t eogp_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* EOGP_H */

@@ -1,0 +1,104 @@
+// Second stage (eq. second_stage) and one-bit encoding (eq. onebit).
+#include <algorithm>
+
+#include "gemm.h"
+
+namespace eogp {
+namespace {
+
+// One wave per row: a ballot of (x >= 0) over 64 consecutive coordinates is
+// exactly 8 bytes of the least-significant-bit-first code; |x| is summed in
+// fp64 (per lane in coordinate order, then a fixed butterfly) and the mean is
+// rounded once to fp16.
+__global__ __launch_bounds__(256) void k_sign_pack(const float* __restrict__ X, int64_t ldx,
+                                                   int64_t N, int64_t k,
+                                                   uint8_t* __restrict__ codes, int64_t cstride,
+                                                   uint16_t* __restrict__ scales,
+                                                   int64_t sstride, int word_store) {
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= N) return;
+  const float* x = X + i * ldx;
+  uint8_t* c = codes + i * cstride;
+  double acc = 0.0;
+  for (int64_t c0 = 0; c0 < k; c0 += 64) {
+    const int64_t cc = c0 + lane;
+    const bool in = cc < k;
+    const float v = in ? x[cc] : 0.f;
+    const uint64_t word = __ballot(in && v >= 0.f);
+    if (in) acc += fabs((double)v);
+    const int64_t nbytes = std::min<int64_t>(8, (k - c0 + 7) >> 3);
+    if (word_store && nbytes == 8) {
+      if (lane == 0) *reinterpret_cast<uint64_t*>(c + (c0 >> 3)) = word;
+    } else if (lane < nbytes) {
+      c[(c0 >> 3) + lane] = (uint8_t)(word >> (8 * lane));
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (lane == 0) scales[i * sstride] = f64_to_f16_rne(acc / (double)k);
+}
+
+// fp32 P (column-major, [k][ldp]) -> bf16 high and low parts [k][ldo].
+__global__ void k_split_p(const float* __restrict__ P, int64_t ldp, int64_t m, int64_t k,
+                          int64_t ldo, uint16_t* __restrict__ hi, uint16_t* __restrict__ lo) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t col = idx / ldo, r = idx % ldo;
+  if (col >= k) return;
+  const float v = r < m ? P[col * ldp + r] : 0.f;
+  const uint16_t h = to_bf16_bits(v);
+  hi[idx] = h;
+  lo[idx] = to_bf16_bits(v - bf16_bits_to_f32(h));
+}
+
+}  // namespace
+
+eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t* codes,
+                      int64_t cstride, uint16_t* scales, int64_t sstride, hipStream_t s) {
+  if (N == 0) return EOGP_OK;
+  const int word_store = ((uintptr_t)codes % 8 == 0) && (cstride % 8 == 0);
+  hipLaunchKernelGGL(k_sign_pack, dim3((unsigned)ceil_div(N, 4)), dim3(256), 0, s, X, ldx, N, k,
+                     codes, cstride, scales, sstride, word_store);
+  EOGP_LAUNCH_CHECK("sign_pack");
+  return EOGP_OK;
+}
+
+size_t pca_ws(int64_t m, int64_t k, eogp_dtype p_dtype) {
+  if (p_dtype != EOGP_F32) return 0;
+  const int64_t ldo = round_up(m, 8);
+  return 2 * align256((size_t)k * ldo * 2);
+}
+
+eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const void* P,
+                        eogp_dtype p_dtype, int64_t ldp, int64_t k, float* X, int64_t ldx,
+                        bool accurate, void* ws, size_t ws_bytes, hipStream_t s) {
+  if (N == 0 || k == 0) return EOGP_OK;
+  GemmArgs g;
+  g.A = Z;
+  g.lda = ldz;
+  g.C = X;
+  g.ldc = ldx;
+  g.M = N;
+  g.N = k;
+  g.K = m;
+  g.n_major = true;
+  if (p_dtype == EOGP_F32) {
+    const int64_t ldo = round_up(m, 8);
+    if (ws_bytes < pca_ws(m, k, p_dtype)) return fail(EOGP_ERR_WORKSPACE, "pca_project: workspace too small");
+    Carve cv(ws, ws_bytes);
+    uint16_t* hi = cv.take<uint16_t>((size_t)k * ldo);
+    uint16_t* lo = cv.take<uint16_t>((size_t)k * ldo);
+    const int64_t total = k * ldo;
+    hipLaunchKernelGGL(k_split_p, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, s,
+                       static_cast<const float*>(P), ldp, m, k, ldo, hi, lo);
+    EOGP_LAUNCH_CHECK("pca split");
+    g.B_hi = hi;
+    g.B_lo = lo;
+    g.ldb = ldo;
+    return gemm_nt(g, AType::F32, accurate ? 2 : 1, accurate ? 2 : 1, false, s);
+  }
+  g.B_hi = static_cast<const uint16_t*>(P);
+  g.ldb = ldp;
+  return gemm_nt(g, AType::F32, accurate ? 2 : 1, 1, p_dtype == EOGP_F16, s);
+}
+
+}  // namespace eogp

@@ -1,0 +1,36 @@
+// MFMA contraction C[M, N] = A[M, K] * B[N, K]^T for gfx950 (both operands
+// K-contiguous, fp32 accumulation). Used by the Kronecker rotations (A =
+// gathered token rows of activations or output-gradients, B = a gathered
+// eigenvector panel) and by the PCA projection (A = first-stage coordinates,
+// B = the PCA directions).
+#pragma once
+#include "common.h"
+
+namespace eogp {
+
+enum class AType : int { F32 = 0, B16 = 1 };   // B16: bf16 or fp16 bit patterns
+
+struct GemmArgs {
+  // A: row r of the product reads row (a_rows ? a_rows[r] : r) of A.
+  const void* A = nullptr;
+  int64_t lda = 0;
+  const int32_t* a_rows = nullptr;
+  // B: [N][ldb] 16-bit; b_lo (optional) is the low part of a split operand.
+  const uint16_t* B_hi = nullptr;
+  const uint16_t* B_lo = nullptr;
+  int64_t ldb = 0;
+  float* C = nullptr;
+  int64_t ldc = 0;
+  int64_t M = 0;                 // rows (upper bound if M_dev is set)
+  const int32_t* M_dev = nullptr;  // device-side row count (<= M), or null
+  int64_t N = 0, K = 0;
+  bool n_major = false;          // tile order: N-tiles outer (PCA: share B across M)
+};
+
+// Launch one contraction. a_type: element type of A; a_parts: 1 = rounded to
+// the MFMA type, 2 = split into high+low parts (fp32 A only); b_parts: 1 or 2
+// (2 needs B_lo); f16: MFMA operands are fp16 (else bf16).
+eogp_status gemm_nt(const GemmArgs& g, AType a_type, int a_parts, int b_parts, bool f16,
+                    hipStream_t s);
+
+}  // namespace eogp

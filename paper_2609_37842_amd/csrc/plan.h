@@ -1,0 +1,38 @@
+// The retained-axis plan of one module (internal layout).
+#pragma once
+#include "common.h"
+
+struct eogp_plan {
+  int64_t d_out = 0, d_in = 0, m = 0;
+  double damping = 0;
+  int64_t n_rows = 0;      // |J|
+  int64_t n_cols = 0;      // |K|
+  int64_t rows_pad = 0;    // |J| rounded up to the GEMM column tile
+  int64_t cols_pad = 0;    // |K| rounded up likewise
+  int64_t ld_out = 0;      // panel row length for Q_S columns (>= d_out, multiple of 8)
+  int64_t ld_in = 0;       // panel row length for Q_A columns (>= d_in, multiple of 8)
+  int64_t n_tiles = 0;     // active 32x32 (row, column) blocks
+  int device = 0;
+
+  // Device arrays, all owned by the plan (one allocation, `mem`).
+  void* mem = nullptr;
+  int32_t* ret_flat = nullptr;   // [m]   j*d_in + k, canonical order
+  float* ret_w = nullptr;        // [m]   (Lambda_r + lambda)^-1/2
+  int32_t* tiles = nullptr;      // [n_tiles][4] = {row block, col block, entry begin, entry end}
+  int32_t* ent_r = nullptr;      // [m]   retained position of each entry, grouped by tile
+  uint16_t* ent_loc = nullptr;   // [m]   (row in block) * 32 + (col in block)
+  uint16_t* qs_hi = nullptr;     // [rows_pad][ld_out] bf16: Q_S[:, J[p]] high part
+  uint16_t* qs_lo = nullptr;     // [rows_pad][ld_out] bf16: low part
+  uint16_t* qa_hi = nullptr;     // [cols_pad][ld_in]  bf16: Q_A[:, K[p]] high part
+  uint16_t* qa_lo = nullptr;     // [cols_pad][ld_in]
+};
+
+namespace eogp {
+constexpr int kPanelTile = 128;   // GEMM column-tile width the panels are padded to
+constexpr int kBlk = 32;          // retained-product block edge
+
+eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double damping,
+                       int64_t m, const float* Q_A, const float* Q_S, hipStream_t s,
+                       eogp_plan** out);
+void free_plan(eogp_plan* p);
+}  // namespace eogp

@@ -1,0 +1,191 @@
+// First stage of EOGP (eq. first_stage, eq. app_projection_maps):
+//   Z[i, r] = w_r * sum_{valid t} (Q_S[:, j_r] . ds[i, t]) (Q_A[:, k_r] . a[i, t])
+//
+// 1. Token compaction: the valid tokens of the batch are listed example by
+//    example (the loss is token-summed over valid positions), so padded and
+//    masked tokens cost nothing and are never read.
+// 2. Two MFMA contractions rotate every valid token onto just the eigenvector
+//    columns the retained axes use: S~ = DS_valid Q_S[:, J], A~ = A_valid Q_A[:, K].
+// 3. Retained products: for every example and every 32 x 32 block of
+//    (row, column) pairs that holds retained axes, the block of sums
+//    sum_t S~[t, j] A~[t, k] over the example's tokens is formed and the
+//    retained entries are scaled by w_r and written to their canonical
+//    positions in Z.
+#include <algorithm>
+
+#include "gemm.h"
+#include "plan.h"
+#include "scan.h"
+
+namespace eogp {
+namespace {
+
+// ---- token compaction ---------------------------------------------------------
+__global__ __launch_bounds__(256) void k_count_valid(const uint8_t* __restrict__ mask, int64_t N,
+                                                     int64_t T, int32_t* __restrict__ cnt) {
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= N) return;
+  int c = 0;
+  for (int64_t t = lane; t < T; t += 64) c += mask ? (mask[i * T + t] != 0) : 1;
+  for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
+  if (lane == 0) cnt[i] = c;
+}
+
+__global__ __launch_bounds__(256) void k_write_tokens(const uint8_t* __restrict__ mask, int64_t N,
+                                                      int64_t T, const int32_t* __restrict__ off,
+                                                      int32_t* __restrict__ tok) {
+  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (i >= N) return;
+  int32_t pos = off[i];
+  for (int64_t t0 = 0; t0 < T; t0 += 64) {
+    const int64_t t = t0 + lane;
+    const bool v = (t < T) && (mask ? (mask[i * T + t] != 0) : true);
+    uint64_t bm;
+    const int pre = wave_prefix_count(v, &bm);
+    if (v) tok[pos + pre] = (int32_t)(i * T + t);
+    pos += __popcll(bm);
+  }
+}
+
+// ---- retained products --------------------------------------------------------
+// One workgroup per (active block, example). Thread (ty, tx) of a 16 x 16 grid
+// owns the 2 x 2 outputs (2ty..2ty+1, 2tx..2tx+1) of the 32 x 32 block.
+// Tokens are staged through LDS 32 at a time and summed in token order.
+__global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, int64_t ldS,
+                                                  const float* __restrict__ At, int64_t ldA,
+                                                  const int32_t* __restrict__ ex_off,
+                                                  const int32_t* __restrict__ tiles,
+                                                  const int32_t* __restrict__ ent_r,
+                                                  const uint16_t* __restrict__ ent_loc,
+                                                  const float* __restrict__ w,
+                                                  float* __restrict__ Z, int64_t ldz,
+                                                  int64_t ex0) {
+  __shared__ __attribute__((aligned(16))) float sS[32][36];
+  __shared__ __attribute__((aligned(16))) float sA[32][36];
+  __shared__ float blk[32][33];
+  const int tile = blockIdx.x;
+  const int64_t i = ex0 + blockIdx.y;
+  const int jt = tiles[4 * tile + 0], kt = tiles[4 * tile + 1];
+  const int e0 = tiles[4 * tile + 2], e1 = tiles[4 * tile + 3];
+  const int64_t t0 = ex_off[i], t1 = ex_off[i + 1];
+  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  const int lr = tid >> 3, lc = (tid & 7) * 4;   // staging: token row, 4 columns
+
+  float c00 = 0.f, c01 = 0.f, c10 = 0.f, c11 = 0.f;
+  for (int64_t tb = t0; tb < t1; tb += 32) {
+    const int64_t t = tb + lr;
+    float4 vs = make_float4(0.f, 0.f, 0.f, 0.f), va = vs;
+    if (t < t1) {
+      vs = *reinterpret_cast<const float4*>(St + t * ldS + (int64_t)jt * 32 + lc);
+      va = *reinterpret_cast<const float4*>(At + t * ldA + (int64_t)kt * 32 + lc);
+    }
+    *reinterpret_cast<float4*>(&sS[lr][lc]) = vs;
+    *reinterpret_cast<float4*>(&sA[lr][lc]) = va;
+    __syncthreads();
+    const int nt = (int)std::min<int64_t>(32, t1 - tb);
+    for (int u = 0; u < nt; ++u) {
+      const float2 s2 = *reinterpret_cast<const float2*>(&sS[u][2 * ty]);
+      const float2 a2 = *reinterpret_cast<const float2*>(&sA[u][2 * tx]);
+      c00 = fmaf(s2.x, a2.x, c00);
+      c01 = fmaf(s2.x, a2.y, c01);
+      c10 = fmaf(s2.y, a2.x, c10);
+      c11 = fmaf(s2.y, a2.y, c11);
+    }
+    __syncthreads();
+  }
+  blk[2 * ty][2 * tx] = c00;
+  blk[2 * ty][2 * tx + 1] = c01;
+  blk[2 * ty + 1][2 * tx] = c10;
+  blk[2 * ty + 1][2 * tx + 1] = c11;
+  __syncthreads();
+  for (int e = e0 + tid; e < e1; e += 256) {
+    const int r = ent_r[e];
+    const int loc = ent_loc[e];
+    Z[i * ldz + r] = w[r] * blk[loc >> 5][loc & 31];
+  }
+}
+
+struct Work {
+  int32_t* cnt;   // [N + 1] per-example valid-token counts, scanned in place
+  int32_t* tok;   // [N*T] global token index of each valid token
+  float* St;      // [N*T][rows_pad]
+  float* At;      // [N*T][cols_pad]
+};
+
+size_t work_bytes(const eogp_plan* p, int64_t N, int64_t T) {
+  size_t b = 0;
+  b += align256((N + 1) * 4);
+  b += align256((size_t)N * T * 4);
+  b += align256((size_t)N * T * p->rows_pad * 4);
+  b += align256((size_t)N * T * p->cols_pad * 4);
+  return b;
+}
+
+}  // namespace
+
+size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T) { return work_bytes(p, N, T); }
+
+eogp_status rotate_retain(const eogp_plan* p, const void* acts, const void* grads, bool bf16_in,
+                          const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
+                          bool accurate, void* ws, size_t ws_bytes, hipStream_t s) {
+  if (ws_bytes < work_bytes(p, N, T)) return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
+  Carve cv(ws, ws_bytes);
+  Work w;
+  w.cnt = cv.take<int32_t>(N + 1);
+  w.tok = cv.take<int32_t>((size_t)N * T);
+  w.St = cv.take<float>((size_t)N * T * p->rows_pad);
+  w.At = cv.take<float>((size_t)N * T * p->cols_pad);
+
+  // 1. compaction
+  const unsigned g4 = (unsigned)ceil_div(N, 4);
+  hipLaunchKernelGGL(k_count_valid, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt);
+  EOGP_HIP(scan_exclusive(w.cnt, N, s));
+  hipLaunchKernelGGL(k_write_tokens, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt, w.tok);
+  EOGP_LAUNCH_CHECK("token compaction");
+
+  // 2. rotations onto the used eigenvectors (rows = valid tokens; count on device)
+  const AType at = bf16_in ? AType::B16 : AType::F32;
+  const int a_parts = (accurate && !bf16_in) ? 2 : 1;
+  const int b_parts = accurate ? 2 : 1;
+  GemmArgs gs;
+  gs.A = grads;
+  gs.lda = p->d_out;
+  gs.a_rows = w.tok;
+  gs.B_hi = p->qs_hi;
+  gs.B_lo = p->qs_lo;
+  gs.ldb = p->ld_out;
+  gs.C = w.St;
+  gs.ldc = p->rows_pad;
+  gs.M = N * T;
+  gs.M_dev = w.cnt + N;
+  gs.N = p->rows_pad;
+  gs.K = p->d_out;
+  eogp_status st = gemm_nt(gs, at, a_parts, b_parts, false, s);
+  if (st != EOGP_OK) return st;
+  GemmArgs ga = gs;
+  ga.A = acts;
+  ga.lda = p->d_in;
+  ga.B_hi = p->qa_hi;
+  ga.B_lo = p->qa_lo;
+  ga.ldb = p->ld_in;
+  ga.C = w.At;
+  ga.ldc = p->cols_pad;
+  ga.N = p->cols_pad;
+  ga.K = p->d_in;
+  st = gemm_nt(ga, at, a_parts, b_parts, false, s);
+  if (st != EOGP_OK) return st;
+
+  // 3. retained products, half-whitened, in canonical order
+  for (int64_t ex0 = 0; p->n_tiles > 0 && ex0 < N; ex0 += 65535) {
+    const int64_t nex = std::min<int64_t>(65535, N - ex0);
+    hipLaunchKernelGGL(k_retained, dim3((unsigned)p->n_tiles, (unsigned)nex), dim3(256), 0, s,
+                       w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, p->ent_r,
+                       p->ent_loc, p->ret_w, Z, ldz, ex0);
+    EOGP_LAUNCH_CHECK("retained products");
+  }
+  return EOGP_OK;
+}
+
+}  // namespace eogp

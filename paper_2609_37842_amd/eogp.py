@@ -1,0 +1,305 @@
+"""Python binding of the EOGP C ABI (include/eogp.h).
+
+Argument marshalling only: every step of the hot path runs in the HIP kernels of
+libeogp.so. torch supplies device memory (tensors) and the current HIP stream.
+The functions carry the same names as the C entry points. If the library is
+missing the import of any entry point raises; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libeogp.so")
+
+F32, BF16, F16 = 0, 1, 2
+PREC_FAST, PREC_ACCURATE = 0, 1
+
+_DTYPE_CODE = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
+
+c_i64 = ctypes.c_int64
+c_i32 = ctypes.c_int32
+c_vp = ctypes.c_void_p
+c_sz = ctypes.c_size_t
+
+
+class EogpError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"eogp status {status}: {msg}")
+        self.status = status
+
+
+class PlanInfo(ctypes.Structure):
+    _fields_ = [("d_out", c_i64), ("d_in", c_i64), ("m", c_i64), ("damping", ctypes.c_double),
+                ("n_rows", c_i64), ("n_cols", c_i64), ("n_tiles", c_i64),
+                ("retained_flat", c_vp), ("retained_weight", c_vp)]
+
+
+_lib = None
+
+EXPORTED = (
+    "eogp_plan_create", "eogp_plan_destroy", "eogp_plan_get_info", "eogp_plan_copy_retained",
+    "eogp_rotate_retain_workspace_size", "eogp_rotate_retain_planned",
+    "eogp_rotate_retain_oneshot_workspace_size", "eogp_rotate_retain",
+    "eogp_pca_project_workspace_size", "eogp_pca_project",
+    "eogp_sign_pack",
+    "eogp_score_topk_workspace_size", "eogp_score_topk",
+    "eogp_status_string", "eogp_last_error", "eogp_version",
+)
+
+
+def load(path: str | None = None):
+    """Load libeogp.so once and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    path = path or LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} not found; build it with "
+                           "`python -m paper_2609_37842_amd.build`")
+    L = ctypes.CDLL(path)
+    sig = {
+        "eogp_plan_create": (c_i32, [c_vp, c_i64, c_i64, ctypes.c_double, c_i64, c_vp, c_vp, c_vp,
+                                     ctypes.POINTER(c_vp)]),
+        "eogp_plan_destroy": (None, [c_vp]),
+        "eogp_plan_get_info": (c_i32, [c_vp, ctypes.POINTER(PlanInfo)]),
+        "eogp_plan_copy_retained": (c_i32, [c_vp, c_vp, c_vp, c_vp]),
+        "eogp_rotate_retain_workspace_size": (c_sz, [c_vp, c_i64, c_i64]),
+        "eogp_rotate_retain_planned": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_i64, c_i64, c_vp,
+                                               c_i64, c_i32, c_vp, c_sz, c_vp]),
+        "eogp_rotate_retain_oneshot_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64]),
+        "eogp_rotate_retain": (c_i32, [c_vp, c_vp, c_i32, c_vp, c_i64, c_i64, c_i64, c_i64, c_vp,
+                                       c_vp, c_vp, ctypes.c_double, c_i64, c_vp, c_i64, c_i32,
+                                       c_vp, c_sz, c_vp]),
+        "eogp_pca_project_workspace_size": (c_sz, [c_i64, c_i64, c_i32, c_i32]),
+        "eogp_pca_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i32, c_i64, c_i64, c_vp,
+                                     c_i64, c_i32, c_vp, c_sz, c_vp]),
+        "eogp_sign_pack": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp]),
+        "eogp_score_topk_workspace_size": (c_sz, [c_i64, c_i64, c_i32, ctypes.POINTER(c_i64),
+                                                  c_i32]),
+        "eogp_score_topk": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64), c_vp,
+                                    c_i64, c_i64, c_i32, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
+        "eogp_status_string": (ctypes.c_char_p, [c_i32]),
+        "eogp_last_error": (ctypes.c_char_p, []),
+        "eogp_version": (c_i32, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        L = load()
+        raise EogpError(status, L.eogp_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _need_cuda(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda):
+            raise ValueError("EOGP arguments must be device tensors")
+
+
+def _workspace(nbytes: int, device, ws=None):
+    if nbytes == 0:
+        return None, 0
+    if ws is not None:
+        if ws.numel() * ws.element_size() < nbytes:
+            raise ValueError(f"workspace needs {nbytes} bytes")
+        return ws, ws.numel() * ws.element_size()
+    return torch.empty(nbytes, dtype=torch.uint8, device=device), nbytes
+
+
+# ---------------------------------------------------------------------------
+# Plans (fitting shared projections)
+# ---------------------------------------------------------------------------
+class eogp_plan:
+    """Retained-axis plan of one module; see eogp_plan_create in eogp.h."""
+
+    def __init__(self, eigvals, damping: float, m: int, Q_A, Q_S, stream=None):
+        L = load()
+        _need_cuda(eigvals, Q_A, Q_S)
+        for t in (eigvals, Q_A, Q_S):
+            if t.dtype != torch.float32 or not t.is_contiguous():
+                raise ValueError("eigvals, Q_A, Q_S must be contiguous float32")
+        d_out, d_in = eigvals.shape
+        if tuple(Q_A.shape) != (d_in, d_in) or tuple(Q_S.shape) != (d_out, d_out):
+            raise ValueError("Q_A must be [d_in, d_in] and Q_S [d_out, d_out]")
+        h = c_vp()
+        _check(L.eogp_plan_create(_ptr(eigvals), d_out, d_in, float(damping), int(m), _ptr(Q_A),
+                                  _ptr(Q_S), _stream(stream), ctypes.byref(h)))
+        self._h = h
+        self.device = eigvals.device
+        info = PlanInfo()
+        _check(L.eogp_plan_get_info(h, ctypes.byref(info)))
+        self.d_out, self.d_in, self.m = int(info.d_out), int(info.d_in), int(info.m)
+        self.damping = float(info.damping)
+        self.n_rows, self.n_cols, self.n_tiles = int(info.n_rows), int(info.n_cols), int(info.n_tiles)
+        self._flat_ptr, self._w_ptr = info.retained_flat, info.retained_weight
+
+    def retained(self):
+        """(flat index int32 [m], weight float32 [m]) copied to new device tensors."""
+        flat = torch.empty(self.m, dtype=torch.int32, device=self.device)
+        w = torch.empty(self.m, dtype=torch.float32, device=self.device)
+        _check(load().eogp_plan_copy_retained(self._h, _ptr(flat), _ptr(w), _stream()))
+        return flat, w
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            load().eogp_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def eogp_plan_create(eigvals, damping, m, Q_A, Q_S, stream=None) -> eogp_plan:
+    return eogp_plan(eigvals, damping, m, Q_A, Q_S, stream)
+
+
+# ---------------------------------------------------------------------------
+# First stage
+# ---------------------------------------------------------------------------
+def _acts_dtype(acts, out_grads):
+    if acts.dtype != out_grads.dtype or acts.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("acts and out_grads must both be float32 or both bfloat16")
+    return _DTYPE_CODE[acts.dtype]
+
+
+def eogp_rotate_retain_workspace_size(plan: eogp_plan, N: int, T: int) -> int:
+    return int(load().eogp_rotate_retain_workspace_size(plan._h, N, T))
+
+
+def eogp_rotate_retain_planned(plan: eogp_plan, acts, out_grads, token_mask=None, Z=None,
+                               prec=PREC_ACCURATE, ws=None, stream=None):
+    """Z [N, m] (float32) of the batch; see eogp_rotate_retain_planned in eogp.h."""
+    L = load()
+    _need_cuda(acts, out_grads, token_mask, Z)
+    N, T, d_in = acts.shape
+    if tuple(out_grads.shape) != (N, T, plan.d_out) or d_in != plan.d_in:
+        raise ValueError("acts [N,T,d_in] / out_grads [N,T,d_out] do not match the plan")
+    if not (acts.is_contiguous() and out_grads.is_contiguous()):
+        raise ValueError("acts and out_grads must be contiguous")
+    if token_mask is not None and (token_mask.dtype != torch.uint8 or tuple(token_mask.shape) != (N, T)
+                                   or not token_mask.is_contiguous()):
+        raise ValueError("token_mask must be contiguous uint8 [N, T]")
+    if Z is None:
+        Z = torch.empty((N, plan.m), dtype=torch.float32, device=acts.device)
+    if Z.dtype != torch.float32 or Z.dim() != 2 or Z.stride(1) != 1 or Z.shape[0] != N:
+        raise ValueError("Z must be float32 [N, >= m] with unit column stride")
+    need = eogp_rotate_retain_workspace_size(plan, N, T)
+    ws, wsb = _workspace(need, acts.device, ws)
+    _check(L.eogp_rotate_retain_planned(plan._h, _ptr(acts), _ptr(out_grads),
+                                        _acts_dtype(acts, out_grads), _ptr(token_mask), N, T,
+                                        _ptr(Z), Z.stride(0), prec, _ptr(ws), wsb, _stream(stream)))
+    return Z
+
+
+def eogp_rotate_retain(acts, out_grads, token_mask, Q_A, Q_S, eigvals, damping, m, Z=None,
+                       prec=PREC_ACCURATE, ws=None, stream=None):
+    """One-shot first stage with the paper's arguments (builds and frees a plan)."""
+    L = load()
+    _need_cuda(acts, out_grads, token_mask, Q_A, Q_S, eigvals, Z)
+    N, T, d_in = acts.shape
+    d_out = out_grads.shape[2]
+    if Z is None:
+        Z = torch.empty((N, m), dtype=torch.float32, device=acts.device)
+    need = int(L.eogp_rotate_retain_oneshot_workspace_size(N, T, d_in, d_out))
+    ws, wsb = _workspace(need, acts.device, ws)
+    _check(L.eogp_rotate_retain(_ptr(acts), _ptr(out_grads), _acts_dtype(acts, out_grads),
+                                _ptr(token_mask), N, T, d_in, d_out, _ptr(Q_A), _ptr(Q_S),
+                                _ptr(eigvals), float(damping), int(m), _ptr(Z), Z.stride(0), prec,
+                                _ptr(ws), wsb, _stream(stream)))
+    return Z
+
+
+# ---------------------------------------------------------------------------
+# Second stage, encoding, scoring
+# ---------------------------------------------------------------------------
+def eogp_pca_project(Z, Pt, X=None, prec=PREC_FAST, ws=None, stream=None):
+    """X [N, k] = Z [N, m] @ P, with P given as Pt [k, m] (each direction
+    contiguous, i.e. P column-major) in float16, bfloat16 or float32."""
+    L = load()
+    _need_cuda(Z, Pt, X)
+    N, m = Z.shape
+    k, m2 = Pt.shape
+    if m2 != m or Pt.stride(1) != 1 or Z.stride(1) != 1:
+        raise ValueError("Pt must be [k, m] with unit column stride; Z [N, m]")
+    if Z.dtype != torch.float32:
+        raise ValueError("Z must be float32")
+    if X is None:
+        X = torch.empty((N, k), dtype=torch.float32, device=Z.device)
+    pd = _DTYPE_CODE[Pt.dtype]
+    need = int(L.eogp_pca_project_workspace_size(m, k, pd, prec))
+    ws, wsb = _workspace(need, Z.device, ws)
+    _check(L.eogp_pca_project(_ptr(Z), Z.stride(0), N, m, _ptr(Pt), pd, Pt.stride(0), k, _ptr(X),
+                              X.stride(0), prec, _ptr(ws), wsb, _stream(stream)))
+    return X
+
+
+def eogp_sign_pack(X, codes=None, scales=None, stream=None):
+    """Packed sign bits [N, ceil(k/8)] (uint8) and fp16 scales [N] (uint16 bits)."""
+    L = load()
+    _need_cuda(X, codes, scales)
+    N, k = X.shape
+    if codes is None:
+        codes = torch.empty((N, (k + 7) // 8), dtype=torch.uint8, device=X.device)
+    if scales is None:
+        scales = torch.empty((N, 1), dtype=torch.int16, device=X.device)
+    sstride = scales.stride(0) if scales.dim() == 2 else 1
+    _check(L.eogp_sign_pack(_ptr(X), X.stride(0), N, k, _ptr(codes), codes.stride(0),
+                            _ptr(scales), sstride, _stream(stream)))
+    return codes, scales
+
+
+def eogp_score_topk_workspace_size(N, Q, k_per_module, topk) -> int:
+    ks = (c_i64 * len(k_per_module))(*[int(k) for k in k_per_module])
+    return int(load().eogp_score_topk_workspace_size(N, Q, len(k_per_module), ks, topk))
+
+
+def eogp_score_topk(codes, scales, k_per_module, Y, topk, full_scores=False, out_idx=None,
+                    out_score=None, ws=None, stream=None):
+    """Per-query top-k (index int64 [Q, topk], score float32 [Q, topk]) and
+    optionally every score (float32 [Q, N])."""
+    L = load()
+    _need_cuda(codes, scales, Y)
+    N = codes.shape[0]
+    Q = Y.shape[0]
+    U = len(k_per_module)
+    ks = (c_i64 * U)(*[int(k) for k in k_per_module])
+    if scales.dtype not in (torch.int16, torch.float16) or scales.numel() != N * U:
+        raise ValueError("scales must be fp16 bits [N, U]")
+    if out_idx is None:
+        out_idx = torch.empty((Q, topk), dtype=torch.int64, device=Y.device)
+    if out_score is None:
+        out_score = torch.empty((Q, topk), dtype=torch.float32, device=Y.device)
+    full = torch.empty((Q, N), dtype=torch.float32, device=Y.device) if full_scores else None
+    need = int(L.eogp_score_topk_workspace_size(N, Q, U, ks, topk))
+    ws, wsb = _workspace(need, Y.device, ws)
+    _check(L.eogp_score_topk(_ptr(codes), codes.stride(0), _ptr(scales), N, U, ks, _ptr(Y),
+                             Y.stride(0), Q, topk, _ptr(out_idx), _ptr(out_score), _ptr(full),
+                             _ptr(ws), wsb, _stream(stream)))
+    return out_idx, out_score, full
+
+
+def eogp_version() -> int:
+    return int(load().eogp_version())

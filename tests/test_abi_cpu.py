@@ -1,0 +1,90 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every entry point the header declares, and rejects bad arguments before
+launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_37842_amd import eogp as E
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    hdr = open(os.path.join(ROOT, "include", "eogp.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    return sorted(set(re.findall(r"\b(eogp_[a-z_]+)\s*\(", hdr)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = E.load()
+    names = header_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(E.EXPORTED)
+
+
+def test_status_strings_and_version():
+    L = E.load()
+    assert L.eogp_status_string(0) == b"ok"
+    assert L.eogp_status_string(-1) == b"invalid argument"
+    assert L.eogp_status_string(-4) == b"workspace too small"
+    assert E.eogp_version() >= 100
+
+
+def test_plan_argument_validation_without_device():
+    L = E.load()
+    h = ctypes.c_void_p()
+    fake = ctypes.c_void_p(0x1000)
+    # NULL eigvals
+    assert L.eogp_plan_create(None, 4, 4, 0.1, 3, fake, fake, None, ctypes.byref(h)) == -1
+    assert b"NULL" in L.eogp_last_error()
+    # m out of range, damping <= 0, bad sizes
+    assert L.eogp_plan_create(fake, 4, 4, 0.1, 17, fake, fake, None, ctypes.byref(h)) == -1
+    assert L.eogp_plan_create(fake, 4, 4, 0.1, 0, fake, fake, None, ctypes.byref(h)) == -1
+    assert L.eogp_plan_create(fake, 4, 4, 0.0, 3, fake, fake, None, ctypes.byref(h)) == -1
+    assert L.eogp_plan_create(fake, 4, 4, float("nan"), 3, fake, fake, None, ctypes.byref(h)) == -1
+    assert L.eogp_plan_create(fake, 0, 4, 0.1, 3, fake, fake, None, ctypes.byref(h)) == -1
+    assert L.eogp_plan_create(fake, 1 << 16, 1 << 16, 0.1, 3, fake, fake, None, ctypes.byref(h)) == -1
+
+
+def test_encode_and_score_argument_validation_without_device():
+    L = E.load()
+    fake = ctypes.c_void_p(0x1000)
+    # sign_pack: k < 1, ldx < k, stride too small
+    assert L.eogp_sign_pack(fake, 8, 2, 0, fake, 1, fake, 1, None) == -1
+    assert L.eogp_sign_pack(fake, 8, 2, 16, fake, 2, fake, 1, None) == -1
+    assert L.eogp_sign_pack(fake, 16, 2, 16, fake, 1, fake, 1, None) == -1
+    # pca: k > m, ld too small
+    assert L.eogp_pca_project(fake, 8, 2, 8, fake, 2, 8, 9, fake, 9, 0, None, 0, None) == -1
+    assert L.eogp_pca_project(fake, 4, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -1
+    # score: k_u not a multiple of 64, topk out of range, misaligned stride
+    ks = (ctypes.c_int64 * 2)(64, 100)
+    assert L.eogp_score_topk(fake, 32, fake, 4, 2, ks, fake, 164, 1, 3, fake, fake, None,
+                             fake, 1 << 20, None) == -1
+    ks = (ctypes.c_int64 * 1)(64)
+    assert L.eogp_score_topk(fake, 8, fake, 4, 1, ks, fake, 64, 1, 0, fake, fake, None,
+                             fake, 1 << 20, None) == -1
+    assert L.eogp_score_topk(fake, 8, fake, 4, 1, ks, fake, 64, 1, 257, fake, fake, None,
+                             fake, 1 << 20, None) == -1
+    assert L.eogp_score_topk(fake, 12, fake, 4, 1, ks, fake, 64, 1, 5, fake, fake, None,
+                             fake, 1 << 20, None) == -1
+    # workspace too small
+    assert L.eogp_score_topk(fake, 8, fake, 4, 1, ks, fake, 64, 1, 5, fake, fake, None,
+                             fake, 16, None) == -4
+
+
+def test_workspace_size_queries_are_consistent():
+    ks = [128, 256]
+    small = E.eogp_score_topk_workspace_size(100, 3, ks, 10)
+    big = E.eogp_score_topk_workspace_size(100000, 40, ks, 10)
+    assert 0 < small < big
+    L = E.load()
+    a = L.eogp_rotate_retain_oneshot_workspace_size(4, 16, 64, 64)
+    b = L.eogp_rotate_retain_oneshot_workspace_size(8, 16, 64, 64)
+    assert 0 < a < b
+    assert L.eogp_pca_project_workspace_size(512, 128, 2, 0) == 0      # fp16 P: none
+    assert L.eogp_pca_project_workspace_size(512, 128, 0, 1) > 0       # fp32 P: split copy

@@ -1,0 +1,397 @@
+"""GPU parity: every C-ABI entry point against the fp64 oracle on the same
+seeded inputs.
+
+Bars (stated per test): bit-exact for integer/byte/index work (selection,
+codes from given coordinates, scores and top-k from given codes); relative
+error per example-module row, ||gpu - oracle|| / ||oracle||, at most 1e-3 for
+fp32 inputs in accurate mode and 2e-2 for bf16 inputs; sign bits of the full
+pipeline identical except where |x| < 1e-3 * rms(x) of the oracle row.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2609_37842_amd import eogp as E
+from paper_2609_37842_amd import synth as S
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need an MI355X"
+    E.load()
+    yield
+
+
+def d(x, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(x)).to(DEV)
+    return t if dtype is None else t.to(dtype)
+
+
+def rel_rows(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    num = np.linalg.norm(a - b, axis=-1)
+    den = np.linalg.norm(b, axis=-1)
+    return num / np.maximum(den, 1e-300)
+
+
+def random_problem(seed, N, T, d_in, d_out, m, lens_lo=None, nan_masked=True):
+    g = np.random.default_rng(seed)
+    a = (g.standard_normal((N, T, d_in)) * np.sqrt(g.lognormal(0, 1, d_in))).astype(np.float32)
+    ds = (0.01 * g.standard_normal((N, T, d_out))).astype(np.float32)
+    lo = T if lens_lo is None else lens_lo
+    lens = g.integers(lo, T + 1, size=N)
+    mask = S.prefix_mask(lens, T)
+    QA = S.haar_orthogonal(g, d_in).astype(np.float32)
+    QS = S.haar_orthogonal(g, d_out).astype(np.float32)
+    lam = (g.lognormal(0, 1, d_out)[:, None] * g.lognormal(0, 1, d_in)[None, :]
+           * np.exp(0.25 * g.standard_normal((d_out, d_in))) * 1e-3).astype(np.float32)
+    if nan_masked:
+        a = S.fill_masked(a, mask)
+        ds = S.fill_masked(ds, mask)
+    return a, ds, mask, QA, QS, lam
+
+
+def oracle_Z(a, ds, mask, QA, QS, lam, damping, m):
+    ret = O.select_retained(lam, damping, m)
+    return O.first_stage_batch(a, ds, mask, QA, QS, ret), ret
+
+
+# ---------------------------------------------------------------------------
+# One-bit encoding
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("k", [64, 128, 100, 8192, 13])
+def test_sign_pack_bit_exact(k):
+    say(f"[sign_pack] k={k}")
+    g = np.random.default_rng(k)
+    X = g.standard_normal((37, k)).astype(np.float32)
+    X[0, :5] = [0.0, -0.0, 1e-30, -1e-30, 0.0]
+    X[1, :] = 0.0
+    codes, scales = E.eogp_sign_pack(d(X))
+    torch.cuda.synchronize()
+    oc, os_ = O.encode(X)
+    assert np.array_equal(codes.cpu().numpy(), oc)
+    assert np.array_equal(scales.cpu().numpy().view(np.uint16)[:, 0], os_)
+
+
+def test_sign_pack_into_multi_module_rows():
+    say("[sign_pack] strided rows")
+    g = np.random.default_rng(5)
+    ks = [128, 64, 256]
+    N = 19
+    row = sum(k // 8 for k in ks)
+    codes = torch.zeros((N, row + 8), dtype=torch.uint8, device=DEV)
+    scales = torch.zeros((N, len(ks)), dtype=torch.int16, device=DEV)
+    Xs = [g.standard_normal((N, k)).astype(np.float32) * (u + 1) for u, k in enumerate(ks)]
+    off = 0
+    for u, (k, X) in enumerate(zip(ks, Xs)):
+        E.eogp_sign_pack(d(X), codes[:, off:off + k // 8], scales[:, u:u + 1])
+        off += k // 8
+    torch.cuda.synchronize()
+    c = codes.cpu().numpy()
+    s = scales.cpu().numpy().view(np.uint16)
+    off = 0
+    for u, (k, X) in enumerate(zip(ks, Xs)):
+        oc, os_ = O.encode(X)
+        assert np.array_equal(c[:, off:off + k // 8], oc)
+        assert np.array_equal(s[:, u], os_)
+        off += k // 8
+    assert np.all(c[:, row:] == 0)
+
+
+# ---------------------------------------------------------------------------
+# Second stage
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("p_dtype,prec,tol", [
+    (torch.float32, E.PREC_ACCURATE, 1e-5),
+    (torch.float16, E.PREC_ACCURATE, 1e-5),
+    (torch.float16, E.PREC_FAST, 1e-3),
+    (torch.bfloat16, E.PREC_ACCURATE, 1e-5),
+    (torch.bfloat16, E.PREC_FAST, 2e-2),
+    (torch.float32, E.PREC_FAST, 2e-2),
+])
+def test_pca_project(p_dtype, prec, tol):
+    say(f"[pca] {p_dtype} prec={prec}")
+    g = np.random.default_rng(7)
+    N, m, k = 300, 1000, 200          # several tiles plus ragged tails in every dim
+    Z = g.standard_normal((N, m)).astype(np.float32)
+    P = S.haar_orthogonal(g, m)[:, :k]
+    Pt = torch.from_numpy(np.ascontiguousarray(P.T).astype(np.float32)).to(DEV).to(p_dtype)
+    X = E.eogp_pca_project(d(Z), Pt, prec=prec)
+    torch.cuda.synchronize()
+    P_used = Pt.float().cpu().numpy().astype(np.float64).T      # P exactly as stored
+    ref = O.pca_project(Z, P_used)
+    err = rel_rows(X.cpu().numpy(), ref)
+    say(f"   max rel {err.max():.2e}")
+    assert err.max() <= tol
+
+
+def test_pca_project_leading_dims_and_empty():
+    g = np.random.default_rng(8)
+    Zbig = torch.from_numpy(g.standard_normal((40, 300)).astype(np.float32)).to(DEV)
+    Z = Zbig[:, :256]                                   # ldz = 300
+    P = S.haar_orthogonal(g, 256)[:, :64]
+    Pt = torch.from_numpy(np.ascontiguousarray(P.T).astype(np.float32)).to(DEV).half()
+    Xbig = torch.full((40, 70), 7.0, device=DEV)
+    E.eogp_pca_project(Z, Pt, X=Xbig[:, :64], prec=E.PREC_ACCURATE)
+    torch.cuda.synchronize()
+    ref = O.pca_project(Z.cpu().numpy(), Pt.float().cpu().numpy().T)
+    assert rel_rows(Xbig[:, :64].cpu().numpy(), ref).max() < 1e-5
+    assert torch.all(Xbig[:, 64:] == 7.0)
+    empty = E.eogp_pca_project(torch.empty((0, 256), device=DEV), Pt)
+    assert empty.shape == (0, 64)
+
+
+# ---------------------------------------------------------------------------
+# Selection (plan)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("d_out,d_in,m", [(64, 64, 512), (130, 97, 1000), (3, 5, 15), (300, 200, 1)])
+def test_plan_selection_bit_exact(d_out, d_in, m):
+    say(f"[plan] {d_out}x{d_in} m={m}")
+    g = np.random.default_rng(d_out * 1000 + d_in)
+    lam = g.lognormal(0, 1, (d_out, d_in)).astype(np.float32)
+    QA = S.haar_orthogonal(g, d_in).astype(np.float32)
+    QS = S.haar_orthogonal(g, d_out).astype(np.float32)
+    damping = 0.05
+    plan = E.eogp_plan_create(d(lam), damping, m, d(QA), d(QS))
+    flat, w = plan.retained()
+    torch.cuda.synchronize()
+    ret = O.select_retained(lam, damping, m)
+    assert np.array_equal(flat.cpu().numpy().astype(np.int64), ret.flat)
+    assert np.array_equal(w.cpu().numpy(), ret.w.astype(np.float32))
+    assert plan.n_rows == np.unique(ret.j).size
+    assert plan.n_cols == np.unique(ret.k).size
+    plan.close()
+
+
+def test_plan_ties_and_negative_values():
+    say("[plan] ties")
+    lam = np.array([[1.0, 3.0, 3.0, -1.0], [3.0, 2.0, 3.0, 3.0], [0.5, 3.0, -0.0, 0.0]],
+                   dtype=np.float32)
+    QA = np.eye(4, dtype=np.float32)
+    QS = np.eye(3, dtype=np.float32)
+    for m in range(1, 11):
+        plan = E.eogp_plan_create(d(lam), 2.0, m, d(QA), d(QS))
+        flat, _ = plan.retained()
+        torch.cuda.synchronize()
+        assert flat.cpu().numpy().tolist() == O.select_retained(lam, 2.0, m).flat.tolist()
+        plan.close()
+
+
+def test_plan_rejects_nan_and_nonpositive_weights():
+    lam = np.ones((8, 8), dtype=np.float32)
+    I8 = d(np.eye(8, dtype=np.float32))
+    lam_nan = lam.copy()
+    lam_nan[3, 3] = np.nan
+    with pytest.raises(E.EogpError):
+        E.eogp_plan_create(d(lam_nan), 0.1, 4, I8, I8)
+    with pytest.raises(E.EogpError):
+        E.eogp_plan_create(d(-2.0 * lam), 0.5, 4, I8, I8)   # Lambda + lambda <= 0
+
+
+# ---------------------------------------------------------------------------
+# First stage
+# ---------------------------------------------------------------------------
+def test_rotate_retain_tiny_workload(tiny_fit):
+    say("[first stage] tiny workload")
+    raw, art = tiny_fit["raw"], tiny_fit["art"]
+    w = S.TINY
+    Z = E.eogp_rotate_retain(d(raw["a"]), d(raw["ds"]), d(raw["mask"]), d(art["Q_A"]),
+                             d(art["Q_S"]), d(art["eigvals"]), art["damping"], w.m,
+                             prec=E.PREC_ACCURATE)
+    torch.cuda.synchronize()
+    ref, _ = oracle_Z(raw["a"], raw["ds"], raw["mask"], art["Q_A"], art["Q_S"], art["eigvals"],
+                      art["damping"], w.m)
+    err = rel_rows(Z.cpu().numpy(), ref)
+    say(f"   max rel {err.max():.2e} median {np.median(err):.2e}")
+    assert err.max() <= 1e-3
+
+
+@pytest.mark.parametrize("shape", [
+    # N, T, d_in, d_out, m, lens_lo
+    (5, 37, 97, 130, 1000, 0),       # ragged masks incl. empty examples, odd widths
+    (3, 200, 769, 64, 700, 64),      # GPT-2-like input width (bias column)
+    (2, 16, 5, 3, 15, 16),           # full basis retained
+    (4, 70, 64, 257, 333, 1),
+])
+def test_rotate_retain_planned_fp32(shape):
+    N, T, d_in, d_out, m, lo = shape
+    say(f"[first stage] fp32 planned {shape}")
+    a, ds, mask, QA, QS, lam = random_problem(sum(shape), N, T, d_in, d_out, m, lens_lo=lo)
+    if lo == 0:
+        mask[0, :] = 0                # an example with no valid token
+    damping = 1e-4
+    plan = E.eogp_plan_create(d(lam), damping, m, d(QA), d(QS))
+    Z = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask), prec=E.PREC_ACCURATE)
+    torch.cuda.synchronize()
+    ref, _ = oracle_Z(a, ds, mask, QA, QS, lam, damping, m)
+    Zg = Z.cpu().numpy()
+    assert np.all(np.isfinite(Zg))
+    nz = np.linalg.norm(ref, axis=1) > 0
+    err = rel_rows(Zg[nz], ref[nz])
+    say(f"   max rel {err.max():.2e}")
+    assert err.max() <= 1e-3
+    assert np.all(Zg[~nz] == 0)
+    plan.close()
+
+
+def test_rotate_retain_bf16_inputs_fast_and_accurate():
+    say("[first stage] bf16")
+    N, T, d_in, d_out, m = 6, 96, 256, 384, 2048
+    a, ds, mask, QA, QS, lam = random_problem(11, N, T, d_in, d_out, m, lens_lo=8)
+    at = d(a, torch.bfloat16)
+    dt = d(ds, torch.bfloat16)
+    a_used = at.float().cpu().numpy()
+    d_used = dt.float().cpu().numpy()
+    plan = E.eogp_plan_create(d(lam), 1e-4, m, d(QA), d(QS))
+    ref, _ = oracle_Z(a_used, d_used, mask, QA, QS, lam, 1e-4, m)
+    for prec, tol in ((E.PREC_FAST, 2e-2), (E.PREC_ACCURATE, 1e-3)):
+        Z = E.eogp_rotate_retain_planned(plan, at, dt, d(mask), prec=prec)
+        torch.cuda.synchronize()
+        err = rel_rows(Z.cpu().numpy(), ref)
+        say(f"   prec={prec} max rel {err.max():.2e}")
+        assert err.max() <= tol
+    plan.close()
+
+
+def test_rotate_retain_no_mask_and_ldz():
+    N, T, d_in, d_out, m = 3, 20, 40, 50, 100
+    a, ds, mask, QA, QS, lam = random_problem(12, N, T, d_in, d_out, m, nan_masked=False)
+    plan = E.eogp_plan_create(d(lam), 1e-3, m, d(QA), d(QS))
+    Zbig = torch.full((N, m + 9), -5.0, device=DEV)
+    E.eogp_rotate_retain_planned(plan, d(a), d(ds), None, Z=Zbig[:, :m], prec=E.PREC_ACCURATE)
+    torch.cuda.synchronize()
+    ref, _ = oracle_Z(a, ds, np.ones((N, T), np.uint8), QA, QS, lam, 1e-3, m)
+    assert rel_rows(Zbig[:, :m].cpu().numpy(), ref).max() <= 1e-3
+    assert torch.all(Zbig[:, m:] == -5.0)
+    plan.close()
+
+
+def test_rotate_retain_deterministic():
+    N, T, d_in, d_out, m = 4, 64, 128, 96, 500
+    a, ds, mask, QA, QS, lam = random_problem(13, N, T, d_in, d_out, m, lens_lo=10)
+    plan = E.eogp_plan_create(d(lam), 1e-3, m, d(QA), d(QS))
+    Z1 = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask))
+    Z2 = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask))
+    torch.cuda.synchronize()
+    assert torch.equal(Z1, Z2)
+    plan.close()
+
+
+# ---------------------------------------------------------------------------
+# Scoring
+# ---------------------------------------------------------------------------
+def random_store(seed, N, ks, Q):
+    g = np.random.default_rng(seed)
+    nbytes = sum(k // 8 for k in ks)
+    codes = g.integers(0, 256, size=(N, nbytes), dtype=np.uint8)
+    scales = np.exp(g.standard_normal((N, len(ks)))).astype(np.float16).view(np.uint16)
+    Y = g.standard_normal((Q, sum(ks))).astype(np.float32)
+    return codes, scales, Y
+
+
+@pytest.mark.parametrize("N,ks,Q,topk", [
+    (300, [128], 8, 10),
+    (1000, [64, 512, 192], 20, 37),
+    (5, [256], 3, 10),               # fewer examples than topk
+    (4097, [1024], 17, 100),
+    (256, [64] * 5, 16, 256),
+])
+def test_score_topk_bit_exact(N, ks, Q, topk):
+    say(f"[score] N={N} ks={ks} Q={Q} topk={topk}")
+    codes, scales, Y = random_store(N + Q, N, ks, Q)
+    Y[0, :] = 0.0                      # an all-zero query
+    idx, sc, full = E.eogp_score_topk(d(codes), d(scales.view(np.int16)), ks, d(Y), topk,
+                                      full_scores=True)
+    torch.cuda.synchronize()
+    ref = O.score(codes, scales, ks, Y)
+    assert np.array_equal(full.cpu().numpy(), ref.astype(np.float32))
+    oi, ov = O.topk(ref, topk)
+    assert np.array_equal(idx.cpu().numpy(), oi)
+    assert np.array_equal(sc.cpu().numpy(), ov)
+
+
+def test_score_integral_queries_give_exact_real_scores():
+    g = np.random.default_rng(21)
+    ks = [256, 128]
+    codes, scales, _ = random_store(22, 200, ks, 5)
+    Y = g.integers(-3000, 3000, size=(5, 384)).astype(np.float32)
+    idx, sc, full = E.eogp_score_topk(d(codes), d(scales.view(np.int16)), ks, d(Y), 10,
+                                      full_scores=True)
+    torch.cuda.synchronize()
+    real = O.score_real(codes, scales, ks, Y)
+    assert np.array_equal(full.cpu().numpy(), real.astype(np.float32))
+
+
+def test_score_ties_resolved_by_index():
+    # identical codes and scales: every score ties; ranking must be by index
+    N, ks = 600, [128]
+    codes = np.tile(np.random.default_rng(3).integers(0, 256, (1, 16), dtype=np.uint8), (N, 1))
+    scales = np.full((N, 1), np.float16(1.5)).view(np.uint16)
+    Y = np.random.default_rng(4).standard_normal((3, 128)).astype(np.float32)
+    idx, sc, _ = E.eogp_score_topk(d(codes), d(scales.view(np.int16)), ks, d(Y), 50)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), np.tile(np.arange(50), (3, 1)))
+
+
+# ---------------------------------------------------------------------------
+# Whole path on the tiny workload
+# ---------------------------------------------------------------------------
+def test_end_to_end_tiny(tiny_fit):
+    say("[end to end] tiny")
+    raw, art = tiny_fit["raw"], tiny_fit["art"]
+    w = S.TINY
+    plan = E.eogp_plan_create(d(art["eigvals"]), art["damping"], w.m, d(art["Q_A"]), d(art["Q_S"]))
+    Pt = d(np.ascontiguousarray(art["P"].T))
+    Z = E.eogp_rotate_retain_planned(plan, d(raw["a"]), d(raw["ds"]), d(raw["mask"]),
+                                     prec=E.PREC_ACCURATE)
+    X = E.eogp_pca_project(Z, Pt, prec=E.PREC_ACCURATE)
+    codes, scales = E.eogp_sign_pack(X)
+    Zq = E.eogp_rotate_retain_planned(plan, d(raw["qa"]), d(raw["qds"]), d(raw["qmask"]),
+                                      prec=E.PREC_ACCURATE)
+    Y = E.eogp_pca_project(Zq, Pt, prec=E.PREC_ACCURATE)
+    idx, sc, full = E.eogp_score_topk(codes, scales, [w.k], Y, w.topk, full_scores=True)
+    torch.cuda.synchronize()
+
+    Zo, Xo, co, so = O.store(raw["a"], raw["ds"], raw["mask"], art["Q_A"], art["Q_S"],
+                             art["eigvals"], art["damping"], w.m, art["P"])
+    Yo = O.query(raw["qa"], raw["qds"], raw["qmask"], art["Q_A"], art["Q_S"], art["eigvals"],
+                 art["damping"], w.m, art["P"])
+    ex = rel_rows(X.cpu().numpy(), Xo)
+    ey = rel_rows(Y.cpu().numpy(), Yo)
+    say(f"   x max rel {ex.max():.2e}, y max rel {ey.max():.2e}")
+    assert ex.max() <= 1e-3 and ey.max() <= 1e-3
+    # sign bits: identical except where |x| < 1e-3 rms(x)
+    bits_g = O.unpack_bits(codes.cpu().numpy(), w.k)
+    bits_o = O.unpack_bits(co, w.k)
+    rms = np.sqrt(np.mean(Xo ** 2, axis=1, keepdims=True))
+    diff = bits_g != bits_o
+    assert not np.any(diff & (np.abs(Xo) >= 1e-3 * rms))
+    say(f"   sign mismatch fraction {diff.mean():.2e}")
+    # scales: within one fp16 ulp of the oracle
+    sg = scales.cpu().numpy().view(np.float16)[:, 0].astype(np.float64)
+    so16 = so.view(np.float16).astype(np.float64)
+    assert np.all(np.abs(sg - so16) <= np.spacing(so.view(np.float16)).astype(np.float64))
+    # scores and top-k: bit-exact for the codes, scales and queries the GPU produced
+    cg = codes.cpu().numpy()
+    sgb = scales.cpu().numpy().view(np.uint16)
+    Yg = Y.cpu().numpy()
+    ref = O.score(cg, sgb, [w.k], Yg)
+    assert np.array_equal(full.cpu().numpy(), ref.astype(np.float32))
+    oi, ov = O.topk(ref, w.topk)
+    assert np.array_equal(idx.cpu().numpy(), oi)
+    assert np.array_equal(sc.cpu().numpy(), ov)
+    plan.close()
