@@ -1,0 +1,395 @@
+#!/usr/bin/env python3
+"""EOGP hot-path benchmark on one MI355X.
+
+Workload (GPT-2-small shaped, fp32 activations and output-gradients): 12 blocks
+x 4 attributed linears (c_attn 769->2304, attn.c_proj 769->768, c_fc 769->3072,
+mlp.c_proj 3073->768; the +1 input column is the attributed bias), T = 512 with
+lengths ~ U{64..512}, m = 16384 retained coordinates and k = 8192 code bits per
+module, a store of 20,000 examples and 256 queries.
+
+One step is one pass of the whole hot path over one batch:
+  * store B = 625 training examples: for every module, first stage (valid-token
+    compaction, MFMA rotations, retained products, half-whitening), PCA
+    projection with the module's fp16 P, sign packing into the store;
+  * project 8 queries through every module (unquantized);
+  * score those 8 queries against all 20,000 stored codes with top-100.
+32 steps are the whole job (20,000 examples, 256 queries). Inputs, shared
+artifacts and the store are resident in device memory before timing starts.
+
+Printed: one JSON line with the metric, the roofline of the dominant kernel
+(the first-stage rotation contraction, timed live with HIP events on its
+stream), the oracle CPU baseline, and the scoring-at-scale measurement
+(8,388,608 codes x 16,384 bits, 512 queries, top-100).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2516.6    # dense MFMA bf16/fp16, 256 CU x 2.4 GHz x 4096 flop/clk
+
+
+def parse(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--batch", type=int, default=625)
+    ap.add_argument("--queries-per-step", type=int, default=8)
+    ap.add_argument("--blocks", type=int, default=12)
+    ap.add_argument("--prec", choices=["accurate", "fast"], default="accurate",
+                    help="first-stage contractions (fp32 inputs need accurate for 1e-3)")
+    ap.add_argument("--pca-prec", choices=["accurate", "fast"], default="fast",
+                    help="PCA projection with fp16 P (fast = fp16 coordinates, as the paper caches them)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-scoring", action="store_true", help="skip the scoring-at-scale pass")
+    ap.add_argument("--scoring-queries", type=int, default=512)
+    ap.add_argument("--scoring-codes", type=int, default=8 * 1024 * 1024)
+    ap.add_argument("--only-scoring", action="store_true")
+    return ap.parse_args(argv)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------------------
+# GPT-2-small-shaped store-and-query step
+# ---------------------------------------------------------------------------
+class Gpt2Step:
+    def __init__(self, args, dev):
+        import torch
+        from paper_2609_37842_amd import eogp as E
+        from paper_2609_37842_amd import synth as S
+        self.E, self.S, self.torch = E, S, torch
+        w = S.GPT2_SMALL
+        self.w = w
+        self.dev = dev
+        self.B = args.batch
+        self.Qb = args.queries_per_step
+        self.T = w.T
+        self.m, self.k = w.m, w.k
+        self.prec = E.PREC_ACCURATE if args.prec == "accurate" else E.PREC_FAST
+        self.pca_prec = E.PREC_ACCURATE if args.pca_prec == "accurate" else E.PREC_FAST
+        self.modules = [(n, di, do) for b in range(args.blocks) for (n, di, do) in w.block]
+        self.shapes = list(w.block)
+        U = len(self.modules)
+        self.U = U
+        self.kb = self.k // 8
+        self.N_store = w.N
+        t0 = time.time()
+        # per-shape inputs (the same bytes serve that linear in every block)
+        self.A, self.D, self.QA, self.QD = {}, {}, {}, {}
+        mask = None
+        for si, (name, di, do) in enumerate(self.shapes):
+            a, ds, mk = S.torch_inputs(w, si, self.B, self.T, di, do, dev, torch.float32)
+            qa, qds, qmk = S.torch_inputs(w, si, self.Qb, self.T, di, do, dev, torch.float32,
+                                          stream_base=32)
+            self.A[name], self.D[name], self.QA[name], self.QD[name] = a, ds, qa, qds
+            if mask is None:
+                mask, qmask = mk, qmk
+        self.mask, self.qmask = mask, qmask
+        self.valid_tokens = int(mask.sum().item())
+        self.valid_q_tokens = int(qmask.sum().item())
+        log(f"inputs ready ({time.time() - t0:.1f}s), valid tokens {self.valid_tokens}")
+        # shared artifacts and plans (fitting phase: not part of a step)
+        cache = {}
+        self.plans, self.Pt = [], []
+        t_plan = 0.0
+        for u, (name, di, do) in enumerate(self.modules):
+            art = S.torch_module_artifacts(w, u, di, do, dev, torch.float16, cache)
+            torch.cuda.synchronize()
+            t1 = time.time()
+            plan = E.eogp_plan_create(art["eigvals"], art["damping"], self.m, art["Q_A"], art["Q_S"])
+            torch.cuda.synchronize()
+            t_plan += time.time() - t1
+            self.plans.append(plan)
+            self.Pt.append(art["Pt"])
+            del art
+        self.plan_ms = 1000.0 * t_plan
+        log(f"plans ready ({time.time() - t0:.1f}s), plan build {self.plan_ms:.1f} ms total")
+        # buffers
+        f32 = torch.float32
+        self.Z = torch.empty((self.B, self.m), dtype=f32, device=dev)
+        self.X = torch.empty((self.B, self.k), dtype=f32, device=dev)
+        self.Zq = torch.empty((self.Qb, self.m), dtype=f32, device=dev)
+        self.Y = torch.empty((self.Qb, U * self.k), dtype=f32, device=dev)
+        g = S.torch_generator(w.config_id, 900001, dev)
+        self.codes = torch.randint(0, 256, (self.N_store, U * self.kb), dtype=torch.uint8,
+                                   device=dev, generator=g)
+        self.scales = torch.exp(torch.randn((self.N_store, U), device=dev, generator=g)).half()
+        self.scales = self.scales.view(torch.int16)
+        ws = 0
+        for p in self.plans:
+            ws = max(ws, E.eogp_rotate_retain_workspace_size(p, self.B, self.T),
+                     E.eogp_rotate_retain_workspace_size(p, self.Qb, self.T))
+        self.ws = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.topk = w.topk
+        self.score_ws = torch.empty(
+            E.eogp_score_topk_workspace_size(self.N_store, self.Qb, [self.k] * U, self.topk),
+            dtype=torch.uint8, device=dev)
+        self.out_idx = torch.empty((self.Qb, self.topk), dtype=torch.int64, device=dev)
+        self.out_score = torch.empty((self.Qb, self.topk), dtype=f32, device=dev)
+        self.n_slots = max(1, self.N_store // self.B)
+        self.shape_of = {n: n for (n, _, _) in self.shapes}
+        torch.cuda.synchronize()
+        log(f"setup done ({time.time() - t0:.1f}s)")
+
+    def step(self, s):
+        E = self.E
+        slot = s % self.n_slots
+        codes = self.codes[slot * self.B:(slot + 1) * self.B]
+        scales = self.scales[slot * self.B:(slot + 1) * self.B]
+        for u, (name, di, do) in enumerate(self.modules):
+            E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
+                                         Z=self.Z, prec=self.prec, ws=self.ws)
+            E.eogp_pca_project(self.Z, self.Pt[u], X=self.X, prec=self.pca_prec)
+            E.eogp_sign_pack(self.X, codes[:, u * self.kb:(u + 1) * self.kb],
+                             scales[:, u:u + 1])
+        for u, (name, di, do) in enumerate(self.modules):
+            E.eogp_rotate_retain_planned(self.plans[u], self.QA[name], self.QD[name], self.qmask,
+                                         Z=self.Zq, prec=self.prec, ws=self.ws)
+            E.eogp_pca_project(self.Zq, self.Pt[u], X=self.Y[:, u * self.k:(u + 1) * self.k],
+                               prec=self.pca_prec)
+        E.eogp_score_topk(self.codes, self.scales, [self.k] * self.U, self.Y, self.topk,
+                          out_idx=self.out_idx, out_score=self.out_score, ws=self.score_ws)
+
+    def rotation_flops_per_step(self):
+        """Algorithmic flops of the rotation contractions in one step:
+        2 * valid tokens * (d_out |J| + d_in |K|) per module, batch and queries."""
+        tot = 0
+        for u, (name, di, do) in enumerate(self.modules):
+            p = self.plans[u]
+            per_tok = 2 * (do * p.n_rows + di * p.n_cols)
+            tot += per_tok * (self.valid_tokens + self.valid_q_tokens)
+        return tot
+
+    def rotation_bytes_per_step(self):
+        """Algorithmic HBM bytes of the rotation contractions: each valid token
+        row read once (fp32), the rotated rows written once (fp32)."""
+        tot = 0
+        for u, (name, di, do) in enumerate(self.modules):
+            p = self.plans[u]
+            tot += 4 * (di + do + p.n_rows + p.n_cols) * (self.valid_tokens + self.valid_q_tokens)
+        return tot
+
+
+# ---------------------------------------------------------------------------
+# Oracle CPU baseline on a bounded sample of the same workload
+# ---------------------------------------------------------------------------
+def cpu_baseline(st: Gpt2Step, budget_s=25.0):
+    import numpy as np
+    import torch
+
+    import oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    n_ex = 2
+    per_shape = {}
+    for si, (name, di, do) in enumerate(st.shapes):
+        u = si                                     # block 0 module of this shape
+        S_ = st.S
+        art = S_.torch_module_artifacts(st.w, u, di, do, st.dev, torch.float16, {})
+        QA = art["Q_A"].double().cpu().numpy()
+        QS = art["Q_S"].double().cpu().numpy()
+        lam = art["eigvals"].cpu().numpy()
+        P = art["Pt"].double().cpu().numpy().T
+        a = st.A[name][:n_ex].double().cpu().numpy()
+        ds = st.D[name][:n_ex].double().cpu().numpy()
+        mk = st.mask[:n_ex].cpu().numpy()
+        ret = O.select_retained(lam, art["damping"], st.m)      # fitting phase, not timed
+        t0 = time.perf_counter()
+        Z = np.stack([O.first_stage_tokens(a[i], ds[i], mk[i], QA, QS, ret) for i in range(n_ex)])
+        X = O.pca_project(Z, P)
+        O.encode(X)
+        per_shape[name] = (time.perf_counter() - t0) / n_ex
+        del P
+    per_example = len(st.modules) // len(st.shapes) * sum(per_shape.values())
+    # queries of one step: same first stage + PCA, plus scoring against the store
+    n_codes = 1000
+    codes = st.codes[:n_codes].cpu().numpy()
+    scales = st.scales[:n_codes].cpu().numpy().view(np.uint16)
+    Y = st.Y.cpu().numpy()
+    t0 = time.perf_counter()
+    sc = O.score(codes, scales, [st.k] * st.U, Y)
+    O.topk(sc, st.topk)
+    t_score = (time.perf_counter() - t0) * (st.N_store / n_codes)
+    step_s = (st.B + st.Qb) * per_example + t_score
+    return {
+        "value": st.B / step_s,
+        "unit": "train examples/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"first stage + PCA + encode of {n_ex} examples for one module of each of the "
+                   f"4 GPT-2 linear shapes (x{len(st.modules) // len(st.shapes)} blocks), and "
+                   f"scoring {st.Qb} queries against {n_codes} stored codes over {st.U} modules "
+                   f"(x{st.N_store // n_codes}); extrapolated to one step of {st.B} examples and "
+                   f"{st.Qb} queries"),
+        "seconds_per_step": step_s,
+    }
+
+
+# ---------------------------------------------------------------------------
+# Scoring at scale: 8M codes x 16384 bits, 512 queries, top-100
+# ---------------------------------------------------------------------------
+def scoring_at_scale(args, dev):
+    import torch
+    from paper_2609_37842_amd import eogp as E
+    from paper_2609_37842_amd import synth as S
+    w = S.SCORING
+    N, k, Q, topk = args.scoring_codes, w.k, args.scoring_queries, w.topk
+    g = S.torch_generator(w.config_id, 1, dev)
+    codes = torch.empty((N, k // 8), dtype=torch.uint8, device=dev)
+    chunk = 1 << 20
+    for i0 in range(0, N, chunk):
+        i1 = min(N, i0 + chunk)
+        codes[i0:i1] = torch.randint(0, 256, (i1 - i0, k // 8), dtype=torch.uint8, device=dev,
+                                     generator=g)
+    scales = torch.exp(torch.randn((N, 1), device=dev, generator=g)).half().view(torch.int16)
+    Y = torch.randn((Q, k), device=dev, generator=g)
+    ws = torch.empty(E.eogp_score_topk_workspace_size(N, Q, [k], topk), dtype=torch.uint8,
+                     device=dev)
+    idx = torch.empty((Q, topk), dtype=torch.int64, device=dev)
+    val = torch.empty((Q, topk), dtype=torch.float32, device=dev)
+    E.eogp_score_topk(codes, scales, [k], Y[:16], topk, out_idx=idx[:16], out_score=val[:16],
+                      ws=ws)                                   # warm-up
+    torch.cuda.synchronize()
+    for c in range(8):
+        E.eogp_timing_read(c)
+    E.eogp_timing_enable(True)
+    t0 = time.perf_counter()
+    E.eogp_score_topk(codes, scales, [k], Y, topk, out_idx=idx, out_score=val, ws=ws)
+    torch.cuda.synchronize()
+    total_s = time.perf_counter() - t0
+    pass_ms, passes = E.eogp_timing_read(E.KT_SCORE_PASS)
+    merge_ms, _ = E.eogp_timing_read(E.KT_SCORE_MERGE)
+    prep_ms, _ = E.eogp_timing_read(E.KT_SCORE_PREP)
+    E.eogp_timing_enable(False)
+    bytes_per_pass = N * (k // 8 + 2)
+    avg = pass_ms / max(1, passes)
+    gbs = bytes_per_pass / (avg * 1e-3) / 1e9
+    return {
+        "workload": w.name,
+        "codes": N, "bits": k, "queries": Q, "topk": topk,
+        "queries_per_pass": 16, "passes": passes,
+        "bytes_per_pass": bytes_per_pass,
+        "ms_per_pass": avg,
+        "hbm_GBps": gbs,
+        "peak_GBps": HBM_PEAK_GBS,
+        "frac": gbs / HBM_PEAK_GBS,
+        "merge_ms_total": merge_ms, "prep_ms": prep_ms,
+        "job_ms": 1000.0 * total_s,
+    }
+
+
+def main(argv=None):
+    args = parse(argv)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
+              "(the hot path runs on a single MI355X; see DESIGN.md for how it would shard)",
+              file=sys.stderr)
+        return 2
+    import torch
+    from paper_2609_37842_amd import eogp as E
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    E.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    out = {}
+    if not args.only_scoring:
+        st = Gpt2Step(args, dev)
+        for s in range(args.warmup):
+            st.step(s)
+        torch.cuda.synchronize()
+        for c in range(8):
+            E.eogp_timing_read(c)
+        E.eogp_timing_enable(True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s in range(args.steps):
+            st.step(args.warmup + s)
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        kt = {name: E.eogp_timing_read(c) for name, c in E.KERNEL_CLASSES.items()}
+        E.eogp_timing_enable(False)
+        ms_per_step = 1000.0 * elapsed / args.steps
+        value = st.B * args.steps / elapsed
+        rot_ms, rot_n = kt["rotation_gemm"]
+        flops_launch = st.rotation_flops_per_step() * args.steps / max(1, rot_n)
+        bytes_launch = st.rotation_bytes_per_step() * args.steps / max(1, rot_n)
+        avg_ms = rot_ms / max(1, rot_n)
+        achieved = flops_launch / (avg_ms * 1e-3) / 1e12
+        passes = 3 if st.prec == E.PREC_ACCURATE else 1
+        out.update({
+            "metric": "train examples/s compressed to 1-bit codes",
+            "value": value,
+            "unit": "train examples/s",
+            "n_gpus": 1,
+            "steps": args.steps,
+            "warmup": args.warmup,
+            "ms_per_step": ms_per_step,
+            "higher_is_better": True,
+            "scaling": "weak",
+            "vs_baseline": None,
+            "dtype": "bf16x3 (fp32 inputs, split into bf16 pairs, fp32 accumulation)"
+                     if st.prec == E.PREC_ACCURATE else "bf16",
+            "data": "synthetic",
+            "config": {"workload": st.w.name, "modules": st.U, "batch_per_step": st.B,
+                       "queries_per_step": st.Qb, "store": st.N_store, "T": st.T,
+                       "valid_tokens_per_batch": st.valid_tokens, "m": st.m, "k": st.k,
+                       "topk": st.topk, "pca": f"fp16 P, {args.pca_prec}",
+                       "first_stage": args.prec},
+            "roofline": {
+                "kernel": "first-stage rotation contraction (k_gemm)",
+                "bound": "mfma",
+                "achieved": achieved,
+                "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s",
+                "frac": achieved / BF16_PEAK_TFLOPS,
+                "traffic": None,
+                "mfma_passes_per_flop": passes,
+                "executed_frac": passes * achieved / BF16_PEAK_TFLOPS,
+                "alg_flops_per_launch": flops_launch,
+                "alg_bytes_per_launch": bytes_launch,
+                "avg_launch_ms": avg_ms,
+                "launches": rot_n,
+            },
+            "kernel_ms_per_step": {name: ms / args.steps for name, (ms, n) in kt.items()},
+            "plan_ms_total": st.plan_ms,
+        })
+        log(f"step {ms_per_step:.2f} ms, {value:.1f} ex/s, rotation {achieved:.1f} TFLOP/s alg")
+        if not args.no_cpu_baseline:
+            t0 = time.time()
+            out["cpu_baseline"] = cpu_baseline(st)
+            log(f"cpu baseline done ({time.time() - t0:.1f}s)")
+        del st
+        torch.cuda.empty_cache()
+    if not args.no_scoring:
+        sc = scoring_at_scale(args, dev)
+        log(f"scoring: {sc['ms_per_pass']:.3f} ms/pass, {sc['hbm_GBps']:.0f} GB/s")
+        if args.only_scoring:
+            out.update({"metric": "code-scoring HBM GB/s", "value": sc["hbm_GBps"],
+                        "unit": "GB/s", "n_gpus": 1, "higher_is_better": True,
+                        "data": "synthetic", "config": {"workload": sc["workload"]}})
+        out["scoring"] = sc
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

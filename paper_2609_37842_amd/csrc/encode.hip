@@ -2,6 +2,7 @@
 #include <algorithm>
 
 #include "gemm.h"
+#include "timing.h"
 
 namespace eogp {
 namespace {
@@ -56,6 +57,7 @@ eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t
                       int64_t cstride, uint16_t* scales, int64_t sstride, hipStream_t s) {
   if (N == 0) return EOGP_OK;
   const int word_store = ((uintptr_t)codes % 8 == 0) && (cstride % 8 == 0);
+  timing::Scope ts(EOGP_KT_SIGN_PACK, s);
   hipLaunchKernelGGL(k_sign_pack, dim3((unsigned)ceil_div(N, 4)), dim3(256), 0, s, X, ldx, N, k,
                      codes, cstride, scales, sstride, word_store);
   EOGP_LAUNCH_CHECK("sign_pack");
@@ -81,6 +83,7 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
   g.N = k;
   g.K = m;
   g.n_major = true;
+  g.timing_class = EOGP_KT_PCA_GEMM;
   if (p_dtype == EOGP_F32) {
     const int64_t ldo = round_up(m, 8);
     if (ws_bytes < pca_ws(m, k, p_dtype)) return fail(EOGP_ERR_WORKSPACE, "pca_project: workspace too small");

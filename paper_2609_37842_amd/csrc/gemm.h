@@ -25,6 +25,7 @@ struct GemmArgs {
   const int32_t* M_dev = nullptr;  // device-side row count (<= M), or null
   int64_t N = 0, K = 0;
   bool n_major = false;          // tile order: N-tiles outer (PCA: share B across M)
+  int timing_class = EOGP_KT_ROTATION_GEMM;
 };
 
 // Launch one contraction. a_type: element type of A; a_parts: 1 = rounded to

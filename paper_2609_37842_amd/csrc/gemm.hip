@@ -16,6 +16,7 @@
 #include <algorithm>
 
 #include "gemm.h"
+#include "timing.h"
 
 namespace eogp {
 namespace {
@@ -241,6 +242,7 @@ eogp_status launch(const KParams& kp, hipStream_t s) {
   if (tiles == 0) return EOGP_OK;
   int64_t grid = std::min<int64_t>(tiles, 2 * kCus);
   if (grid >= kXcds) grid = grid / kXcds * kXcds;
+  timing::Scope ts(g.timing_class, s);
   hipLaunchKernelGGL((k_gemm<AT, AP, BP, F16>), dim3((unsigned)grid), dim3(256), 0, s, kp);
   EOGP_LAUNCH_CHECK("gemm launch");
   return EOGP_OK;

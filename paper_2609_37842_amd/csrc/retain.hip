@@ -16,6 +16,7 @@
 #include "gemm.h"
 #include "plan.h"
 #include "scan.h"
+#include "timing.h"
 
 namespace eogp {
 namespace {
@@ -140,9 +141,12 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, const void* grad
 
   // 1. compaction
   const unsigned g4 = (unsigned)ceil_div(N, 4);
-  hipLaunchKernelGGL(k_count_valid, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt);
-  EOGP_HIP(scan_exclusive(w.cnt, N, s));
-  hipLaunchKernelGGL(k_write_tokens, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt, w.tok);
+  {
+    timing::Scope ts(EOGP_KT_COMPACTION, s);
+    hipLaunchKernelGGL(k_count_valid, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt);
+    EOGP_HIP(scan_exclusive(w.cnt, N, s));
+    hipLaunchKernelGGL(k_write_tokens, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt, w.tok);
+  }
   EOGP_LAUNCH_CHECK("token compaction");
 
   // 2. rotations onto the used eigenvectors (rows = valid tokens; count on device)
@@ -180,6 +184,7 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, const void* grad
   // 3. retained products, half-whitened, in canonical order
   for (int64_t ex0 = 0; p->n_tiles > 0 && ex0 < N; ex0 += 65535) {
     const int64_t nex = std::min<int64_t>(65535, N - ex0);
+    timing::Scope ts(EOGP_KT_RETAINED, s);
     hipLaunchKernelGGL(k_retained, dim3((unsigned)p->n_tiles, (unsigned)nex), dim3(256), 0, s,
                        w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, p->ent_r,
                        p->ent_loc, p->ret_w, Z, ldz, ex0);

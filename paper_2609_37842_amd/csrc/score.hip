@@ -25,6 +25,7 @@
 #include <vector>
 
 #include "common.h"
+#include "timing.h"
 
 namespace eogp {
 namespace {
@@ -415,12 +416,15 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     ks += KSTEP * ((kmod[u] + 511) / 512);
   }
   EOGP_HIP(hipMemcpyAsync(mods, hm.data(), sizeof(ModInfo) * U, hipMemcpyHostToDevice, s));
+  timing::Scope tprep(EOGP_KT_SCORE_PREP, s);
   hipLaunchKernelGGL(k_query_stats, dim3((unsigned)Q, (unsigned)U), dim3(256), 0, s, Y, ldy, U,
                      mods, fq, ys);
   const int64_t pbytes = L.n_groups * L.KS * 1024;
   hipLaunchKernelGGL(k_query_planes, dim3((unsigned)ceil_div(pbytes, 256)), dim3(256), 0, s, Y,
                      ldy, Q, U, mods, fq, L.KS, L.n_groups, ph, pl);
   EOGP_LAUNCH_CHECK("query preparation");
+  timing::end(tprep.slot, s);
+  tprep.slot = -1;
   for (int64_t grp = 0; grp < L.n_groups; ++grp) {
     ScoreArgs a;
     a.codes = codes;
@@ -440,7 +444,11 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     a.full = full;
     a.ckey = ck;
     a.cidx = ci;
-    hipLaunchKernelGGL(k_score, dim3((unsigned)L.grid), dim3(256), 0, s, a);
+    {
+      timing::Scope tp(EOGP_KT_SCORE_PASS, s);
+      hipLaunchKernelGGL(k_score, dim3((unsigned)L.grid), dim3(256), 0, s, a);
+    }
+    timing::Scope tm(EOGP_KT_SCORE_MERGE, s);
     hipLaunchKernelGGL(k_merge, dim3(QB), dim3(256), 0, s, ck, ci, (int)L.grid, grp, Q, topk,
                        out_idx, out_score);
     EOGP_LAUNCH_CHECK("score pass");

@@ -47,6 +47,7 @@ EXPORTED = (
     "eogp_pca_project_workspace_size", "eogp_pca_project",
     "eogp_sign_pack",
     "eogp_score_topk_workspace_size", "eogp_score_topk",
+    "eogp_timing_enable", "eogp_timing_read",
     "eogp_status_string", "eogp_last_error", "eogp_version",
 )
 
@@ -82,6 +83,8 @@ def load(path: str | None = None):
                                                   c_i32]),
         "eogp_score_topk": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64), c_vp,
                                     c_i64, c_i64, c_i32, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
+        "eogp_timing_enable": (c_i32, [c_i32]),
+        "eogp_timing_read": (c_i32, [c_i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_i64)]),
         "eogp_status_string": (ctypes.c_char_p, [c_i32]),
         "eogp_last_error": (ctypes.c_char_p, []),
         "eogp_version": (c_i32, []),
@@ -303,3 +306,24 @@ def eogp_score_topk(codes, scales, k_per_module, Y, topk, full_scores=False, out
 
 def eogp_version() -> int:
     return int(load().eogp_version())
+
+
+# ---------------------------------------------------------------------------
+# Kernel timing (measurement harnesses)
+# ---------------------------------------------------------------------------
+KT_ROTATION_GEMM, KT_RETAINED, KT_PCA_GEMM, KT_SIGN_PACK = 0, 1, 2, 3
+KT_SCORE_PASS, KT_SCORE_MERGE, KT_SCORE_PREP, KT_COMPACTION = 4, 5, 6, 7
+KERNEL_CLASSES = {"rotation_gemm": 0, "retained": 1, "pca_gemm": 2, "sign_pack": 3,
+                  "score_pass": 4, "score_merge": 5, "score_prep": 6, "compaction": 7}
+
+
+def eogp_timing_enable(on: bool = True):
+    _check(load().eogp_timing_enable(1 if on else 0))
+
+
+def eogp_timing_read(kernel_class: int):
+    """(total milliseconds, launches) of one kernel class since the last read."""
+    ms = ctypes.c_double()
+    n = c_i64()
+    _check(load().eogp_timing_read(int(kernel_class), ctypes.byref(ms), ctypes.byref(n)))
+    return float(ms.value), int(n.value)
