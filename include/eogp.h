@@ -112,8 +112,12 @@ eogp_status eogp_plan_copy_retained(const eogp_plan* plan, int32_t* flat_out,
  * needed eigenvectors with MFMA contractions, and the retained products are
  * summed per example (the loss is token-summed over valid positions).
  *
- *   acts       [N, T, d_in]  in `in_dtype` (EOGP_F32 or EOGP_BF16).
- *   out_grads  [N, T, d_out] in `in_dtype`.
+ *   acts       [N, T, d_in]  in `in_dtype` (EOGP_F32 or EOGP_BF16); token
+ *              (i, t) starts at element (i*T + t) * ld_acts (ld_acts >= d_in,
+ *              or 0 for d_in). Rows whose byte offset is a multiple of 16 take
+ *              the fast load path (fp32: ld_acts % 4 == 0; bf16: % 8 == 0);
+ *              16-bit rows must satisfy it.
+ *   out_grads  [N, T, d_out] in `in_dtype`, token stride ld_grads likewise.
  *   token_mask [N, T] uint8, or NULL for all tokens valid. Masked tokens are
  *              never read and may hold anything, NaN included.
  *   Z          [N, ldz] fp32, ldz >= m; columns m..ldz-1 are not written.
@@ -123,7 +127,8 @@ eogp_status eogp_plan_copy_retained(const eogp_plan* plan, int32_t* flat_out,
  * ------------------------------------------------------------------------ */
 size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64_t T);
 eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
-                                       const void* out_grads, eogp_dtype in_dtype,
+                                       int64_t ld_acts, const void* out_grads,
+                                       int64_t ld_grads, eogp_dtype in_dtype,
                                        const uint8_t* token_mask, int64_t N, int64_t T,
                                        float* Z, int64_t ldz, eogp_prec prec,
                                        void* ws, size_t ws_bytes, void* stream);
@@ -133,8 +138,9 @@ eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
  * Synchronises `stream`. Workspace: eogp_rotate_retain_oneshot_workspace_size. */
 size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d_in,
                                                  int64_t d_out);
-eogp_status eogp_rotate_retain(const void* acts, const void* out_grads,
-                               eogp_dtype in_dtype, const uint8_t* token_mask,
+eogp_status eogp_rotate_retain(const void* acts, int64_t ld_acts, const void* out_grads,
+                               int64_t ld_grads, eogp_dtype in_dtype,
+                               const uint8_t* token_mask,
                                int64_t N, int64_t T, int64_t d_in, int64_t d_out,
                                const float* Q_A, const float* Q_S, const float* eigvals,
                                double damping, int64_t m, float* Z, int64_t ldz,
@@ -150,12 +156,15 @@ eogp_status eogp_rotate_retain(const void* acts, const void* out_grads,
  *       P + c*ldp .. P + c*ldp + m - 1 (ldp >= m), in `p_dtype` (EOGP_F16 as
  *       the paper stores it, EOGP_BF16 or EOGP_F32).
  *   X   [N, ldx] fp32, ldx >= k.
- *   ws  needed only for p_dtype == EOGP_F32 (the split copy of P):
- *       eogp_pca_project_workspace_size bytes; otherwise may be NULL.
+ *   ws  eogp_pca_project_workspace_size(N, ...) bytes: the split copy of an
+ *       fp32 P, then scratch that lets small batches split the m-long sums
+ *       across workgroups (partial sums are added in a fixed order, so the
+ *       result does not depend on the split). For EOGP_F16 / EOGP_BF16 P the
+ *       workspace may be NULL (no split; slower for small N).
  * With p_dtype EOGP_F16 the fp32 Z is converted to fp16 (split into two fp16
  * parts under EOGP_PREC_ACCURATE); Z must then lie within the fp16 range.
  * ------------------------------------------------------------------------ */
-size_t eogp_pca_project_workspace_size(int64_t m, int64_t k, eogp_dtype p_dtype,
+size_t eogp_pca_project_workspace_size(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype,
                                        eogp_prec prec);
 eogp_status eogp_pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m,
                              const void* P, eogp_dtype p_dtype, int64_t ldp, int64_t k,
@@ -208,6 +217,27 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride,
                             const int64_t* k_per_module, const float* Y, int64_t ldy,
                             int64_t Q, int32_t topk, int64_t* out_idx, float* out_score,
                             float* full_scores, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Kernel timing, for measurement harnesses. While enabled, each launch of a
+ * kernel class below is bracketed by two HIP events recorded on the stream it
+ * is launched on. eogp_timing_read waits for the recorded events of one class,
+ * returns the summed elapsed time and the number of launches, and forgets
+ * them. Disabled by default; costs nothing when disabled.
+ * ------------------------------------------------------------------------ */
+typedef enum {
+  EOGP_KT_ROTATION_GEMM = 0,  /* first-stage rotations (two per first-stage call) */
+  EOGP_KT_RETAINED = 1,       /* retained products + half-whitening              */
+  EOGP_KT_PCA_GEMM = 2,       /* second-stage projection                         */
+  EOGP_KT_SIGN_PACK = 3,      /* one-bit encoding                                */
+  EOGP_KT_SCORE_PASS = 4,     /* one streaming pass over the codes               */
+  EOGP_KT_SCORE_MERGE = 5,    /* top-k merge after a pass                        */
+  EOGP_KT_SCORE_PREP = 6,     /* fixed-point query preparation                   */
+  EOGP_KT_COMPACTION = 7,     /* valid-token compaction                          */
+  EOGP_KT_COUNT = 8
+} eogp_kernel_class;
+eogp_status eogp_timing_enable(int32_t enable);
+eogp_status eogp_timing_read(int32_t kernel_class, double* total_ms, int64_t* launches);
 
 /* ------------------------------------------------------------------------ */
 const char* eogp_status_string(eogp_status status);

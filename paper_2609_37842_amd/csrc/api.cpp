@@ -1,6 +1,7 @@
 // C ABI entry points: argument validation, then enqueue on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <string>
 
@@ -10,12 +11,14 @@
 namespace eogp {
 // implemented in the kernel sources
 size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T);
-eogp_status rotate_retain(const eogp_plan* p, const void* acts, const void* grads, bool bf16_in,
+eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
+                          int64_t ld_grads, bool bf16_in,
                           const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
                           bool accurate, void* ws, size_t ws_bytes, hipStream_t s);
 eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t* codes,
                       int64_t cstride, uint16_t* scales, int64_t sstride, hipStream_t s);
-size_t pca_ws(int64_t m, int64_t k, eogp_dtype p_dtype);
+size_t pca_ws(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype);
+size_t pca_split_copy_bytes(int64_t m, int64_t k, eogp_dtype p_dtype);
 eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const void* P,
                         eogp_dtype p_dtype, int64_t ldp, int64_t k, float* X, int64_t ldx,
                         bool accurate, void* ws, size_t ws_bytes, hipStream_t s);
@@ -137,20 +140,31 @@ size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64
 }
 
 eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
-                                       const void* out_grads, eogp_dtype in_dtype,
-                                       const uint8_t* token_mask, int64_t N, int64_t T, float* Z,
-                                       int64_t ldz, eogp_prec prec, void* ws, size_t ws_bytes,
-                                       void* stream) {
+                                       int64_t ld_acts, const void* out_grads, int64_t ld_grads,
+                                       eogp_dtype in_dtype, const uint8_t* token_mask, int64_t N,
+                                       int64_t T, float* Z, int64_t ldz, eogp_prec prec, void* ws,
+                                       size_t ws_bytes, void* stream) {
   eogp_status st = check_first_stage(plan, acts, out_grads, in_dtype, N, T, Z, ldz);
   if (st != EOGP_OK) return st;
+  if (ld_acts == 0) ld_acts = plan->d_in;
+  if (ld_grads == 0) ld_grads = plan->d_out;
+  if (ld_acts < plan->d_in || ld_grads < plan->d_out)
+    return fail(EOGP_ERR_INVALID, "rotate_retain: token stride smaller than the width");
+  if (in_dtype == EOGP_BF16 &&
+      (ld_acts % 8 || ld_grads % 8 || (uintptr_t)acts % 16 || (uintptr_t)out_grads % 16))
+    return fail(EOGP_ERR_UNSUPPORTED,
+                "rotate_retain: bf16 token rows must start on 16-byte boundaries");
+  if (N * T * std::max(ld_acts, ld_grads) >= ((int64_t)1 << 62))
+    return fail(EOGP_ERR_INVALID, "rotate_retain: inputs too large");
   if (N == 0) return EOGP_OK;
   if (ws_bytes < rotate_retain_ws(plan, N, T) || !ws)
     return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
   int dev = -1;
   if (hipGetDevice(&dev) == hipSuccess && dev != plan->device)
     return fail(EOGP_ERR_INVALID, "rotate_retain: plan belongs to another device");
-  return rotate_retain(plan, acts, out_grads, in_dtype == EOGP_BF16, token_mask, N, T, Z, ldz,
-                       prec == EOGP_PREC_ACCURATE, ws, ws_bytes, S(stream));
+  return rotate_retain(plan, acts, ld_acts, out_grads, ld_grads, in_dtype == EOGP_BF16,
+                       token_mask, N, T, Z, ldz, prec == EOGP_PREC_ACCURATE, ws, ws_bytes,
+                       S(stream));
 }
 
 size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d_in,
@@ -162,7 +176,8 @@ size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d
   return rotate_retain_ws(&probe, N, T);
 }
 
-eogp_status eogp_rotate_retain(const void* acts, const void* out_grads, eogp_dtype in_dtype,
+eogp_status eogp_rotate_retain(const void* acts, int64_t ld_acts, const void* out_grads,
+                               int64_t ld_grads, eogp_dtype in_dtype,
                                const uint8_t* token_mask, int64_t N, int64_t T, int64_t d_in,
                                int64_t d_out, const float* Q_A, const float* Q_S,
                                const float* eigvals, double damping, int64_t m, float* Z,
@@ -176,18 +191,19 @@ eogp_status eogp_rotate_retain(const void* acts, const void* out_grads, eogp_dty
   eogp_plan* plan = nullptr;
   st = build_plan(eigvals, d_out, d_in, damping, m, Q_A, Q_S, S(stream), &plan);
   if (st != EOGP_OK) return st;
-  st = eogp_rotate_retain_planned(plan, acts, out_grads, in_dtype, token_mask, N, T, Z, ldz, prec,
-                                  ws, ws_bytes, stream);
+  st = eogp_rotate_retain_planned(plan, acts, ld_acts, out_grads, ld_grads, in_dtype, token_mask,
+                                  N, T, Z, ldz, prec, ws, ws_bytes, stream);
   hipError_t e = hipStreamSynchronize(S(stream));
   free_plan(plan);
   if (st == EOGP_OK && e != hipSuccess) return check_hip(e, "rotate_retain");
   return st;
 }
 
-size_t eogp_pca_project_workspace_size(int64_t m, int64_t k, eogp_dtype p_dtype, eogp_prec prec) {
+size_t eogp_pca_project_workspace_size(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype,
+                                       eogp_prec prec) {
   (void)prec;
-  if (m < 1 || k < 1) return 0;
-  return pca_ws(m, k, p_dtype);
+  if (N < 0 || m < 1 || k < 1) return 0;
+  return pca_ws(N, m, k, p_dtype);
 }
 
 eogp_status eogp_pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const void* P,
@@ -199,7 +215,7 @@ eogp_status eogp_pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, 
   if (ldz < m || ldp < m || ldx < k) return fail(EOGP_ERR_INVALID, "pca_project: leading dimension too small");
   if (p_dtype != EOGP_F32 && p_dtype != EOGP_BF16 && p_dtype != EOGP_F16)
     return fail(EOGP_ERR_INVALID, "pca_project: bad P dtype");
-  if (p_dtype == EOGP_F32 && ws_bytes < pca_ws(m, k, p_dtype))
+  if (ws_bytes < pca_split_copy_bytes(m, k, p_dtype) || (p_dtype == EOGP_F32 && !ws))
     return fail(EOGP_ERR_WORKSPACE, "pca_project: workspace too small for fp32 P");
   return pca_project(Z, ldz, N, m, P, p_dtype, ldp, k, X, ldx, prec == EOGP_PREC_ACCURATE, ws,
                      ws_bytes, S(stream));

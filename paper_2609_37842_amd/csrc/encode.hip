@@ -44,8 +44,7 @@ __global__ void k_split_p(const float* __restrict__ P, int64_t ldp, int64_t m, i
                           int64_t ldo, uint16_t* __restrict__ hi, uint16_t* __restrict__ lo) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t col = idx / ldo, r = idx % ldo;
-  if (col >= k) return;
-  const float v = r < m ? P[col * ldp + r] : 0.f;
+  const float v = (r < m && col < k) ? P[col * ldp + r] : 0.f;   // zero padding
   const uint16_t h = to_bf16_bits(v);
   hi[idx] = h;
   lo[idx] = to_bf16_bits(v - bf16_bits_to_f32(h));
@@ -64,10 +63,18 @@ eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t
   return EOGP_OK;
 }
 
-size_t pca_ws(int64_t m, int64_t k, eogp_dtype p_dtype) {
+constexpr int kPcaMaxSplits = 8;
+
+// Workspace: the split copy of an fp32 P (padded panel), then split-K partials.
+size_t pca_split_copy_bytes(int64_t m, int64_t k, eogp_dtype p_dtype) {
   if (p_dtype != EOGP_F32) return 0;
-  const int64_t ldo = round_up(m, 8);
-  return 2 * align256((size_t)k * ldo * 2);
+  const int64_t ldo = round_up(m, 32), rows = round_up(k, 256);
+  return 2 * align256((size_t)rows * ldo * 2);
+}
+
+size_t pca_ws(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype) {
+  return pca_split_copy_bytes(m, k, p_dtype) +
+         align256(gemm_partial_bytes(N, k, kPcaMaxSplits));
 }
 
 eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const void* P,
@@ -84,23 +91,33 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
   g.K = m;
   g.n_major = true;
   g.timing_class = EOGP_KT_PCA_GEMM;
+  const size_t copy = pca_split_copy_bytes(m, k, p_dtype);
+  if (ws_bytes < copy) return fail(EOGP_ERR_WORKSPACE, "pca_project: workspace too small");
+  // Split-K scratch is optional: without it the projection runs unsplit.
+  if (ws && ws_bytes >= copy + gemm_partial_bytes(N, k, 2)) {
+    g.partial = reinterpret_cast<float*>(static_cast<char*>(ws) + copy);
+    g.max_splits = (int)std::min<int64_t>(
+        kPcaMaxSplits, (int64_t)((ws_bytes - copy) / gemm_partial_bytes(N, k, 1)));
+  }
   if (p_dtype == EOGP_F32) {
-    const int64_t ldo = round_up(m, 8);
-    if (ws_bytes < pca_ws(m, k, p_dtype)) return fail(EOGP_ERR_WORKSPACE, "pca_project: workspace too small");
+    const int64_t ldo = round_up(m, 32), rows = round_up(k, 256);
     Carve cv(ws, ws_bytes);
-    uint16_t* hi = cv.take<uint16_t>((size_t)k * ldo);
-    uint16_t* lo = cv.take<uint16_t>((size_t)k * ldo);
-    const int64_t total = k * ldo;
+    uint16_t* hi = cv.take<uint16_t>((size_t)rows * ldo);
+    uint16_t* lo = cv.take<uint16_t>((size_t)rows * ldo);
+    const int64_t total = rows * ldo;
     hipLaunchKernelGGL(k_split_p, dim3((unsigned)ceil_div(total, 256)), dim3(256), 0, s,
                        static_cast<const float*>(P), ldp, m, k, ldo, hi, lo);
     EOGP_LAUNCH_CHECK("pca split");
     g.B_hi = hi;
     g.B_lo = lo;
     g.ldb = ldo;
+    g.b_padded = true;
     return gemm_nt(g, AType::F32, accurate ? 2 : 1, accurate ? 2 : 1, false, s);
   }
   g.B_hi = static_cast<const uint16_t*>(P);
   g.ldb = ldp;
+  // A caller's P needs no bounds checks when its shape already matches the tiles.
+  g.b_padded = (m % 32 == 0) && (k % 256 == 0);
   return gemm_nt(g, AType::F32, accurate ? 2 : 1, 1, p_dtype == EOGP_F16, s);
 }
 

@@ -15,16 +15,22 @@ struct GemmArgs {
   const void* A = nullptr;
   int64_t lda = 0;
   const int32_t* a_rows = nullptr;
-  // B: [N][ldb] 16-bit; b_lo (optional) is the low part of a split operand.
+  // B: [N][ldb] 16-bit; B_lo (optional) is the low part of a split operand.
   const uint16_t* B_hi = nullptr;
   const uint16_t* B_lo = nullptr;
   int64_t ldb = 0;
+  // B is a padded panel: at least round_up(N, 256) rows and round_up(K, 32)
+  // columns per row are readable, zero beyond N and K.
+  bool b_padded = false;
   float* C = nullptr;
   int64_t ldc = 0;
-  int64_t M = 0;                 // rows (upper bound if M_dev is set)
+  int64_t M = 0;                   // rows (upper bound if M_dev is set)
   const int32_t* M_dev = nullptr;  // device-side row count (<= M), or null
   int64_t N = 0, K = 0;
-  bool n_major = false;          // tile order: N-tiles outer (PCA: share B across M)
+  bool n_major = false;            // unit order: N-tiles outer (PCA: share B across M)
+  // Split-K scratch (host-known M only): max_splits partial [M][N] fp32 tiles.
+  float* partial = nullptr;
+  int max_splits = 1;
   int timing_class = EOGP_KT_ROTATION_GEMM;
 };
 
@@ -33,5 +39,8 @@ struct GemmArgs {
 // (2 needs B_lo); f16: MFMA operands are fp16 (else bf16).
 eogp_status gemm_nt(const GemmArgs& g, AType a_type, int a_parts, int b_parts, bool f16,
                     hipStream_t s);
+
+// Bytes of split-K scratch for an M x N product with up to max_splits splits.
+size_t gemm_partial_bytes(int64_t M, int64_t N, int max_splits);
 
 }  // namespace eogp

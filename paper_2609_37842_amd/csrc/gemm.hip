@@ -1,18 +1,33 @@
 // MFMA contraction core for gfx950: C = A * B^T, K-contiguous operands.
 //
-// Tiling: a 256-thread workgroup (4 wave64s in a 2 x 2 grid) owns a 128 x 128
-// output tile; each wave computes 64 x 64 with 2 x 2 v_mfma_f32_32x32x16
-// blocks. K advances 32 at a time through LDS (rows padded to 40 halves so
-// the 16-byte fragment reads of 16 consecutive rows hit distinct banks); the
-// next K-slice is fetched into registers while the current one is multiplied.
-// fp32 A is converted while it is staged: rounded to the MFMA type, or split
-// into high and low parts for the accurate mode, whose cross terms
-// (A_lo*B_hi, A_hi*B_lo, A_hi*B_hi) accumulate in the same fp32 registers.
+// Tiling. A 256-thread workgroup (4 wave64s, one per SIMD) owns a 256 x BN
+// output tile (BN = 256 or 128, whichever pads N less); the waves form a 2 x 2
+// grid and each computes 128 x BN/2 with v_mfma_f32_32x32x16 blocks whose
+// accumulators live in the accumulation registers, so every fragment read
+// from LDS feeds BN/64 (A) or 4 (B) MFMAs. K advances 32 at a time through two
+// LDS stages. LDS rows are 64 bytes (32 halves) without padding; the four
+// 16-byte chunks of a row are XOR-swizzled by (row / 4) so that 16 lanes
+// reading one chunk of 16 consecutive rows touch distinct banks.
 //
-// The grid is persistent. Tiles are dealt out in contiguous ranges per XCD
-// (workgroup b runs on XCD b % 8), so the workgroups that share an A row-block
-// (rotations) or a B column-block (PCA, n_major) run together on one XCD and
-// hit the same L2.
+// Pipeline. Slice k+1 sits in registers while slice k is multiplied from LDS;
+// right after the multiplies it is converted and written to the other stage
+// and slice k+2 is requested, then one barrier. The steady-state loop has no
+// branches: rows beyond M read a copy of a valid row (their products land in
+// output rows that are never stored), and a
+// ragged last K-slice is processed first, in the prologue, by the only
+// bounds-checked load. B operands are padded panels (rows to 256, K to a
+// multiple of 32, zero-filled) or, for general caller layouts, checked loads.
+//
+// Precision. fp32 A is converted while it is staged: rounded to the MFMA type,
+// or split into high and low parts (accurate mode), whose cross terms
+// (A_lo*B_hi, A_hi*B_lo, A_hi*B_hi) accumulate into the same fp32 registers.
+//
+// Schedule. The grid is persistent, one workgroup per CU. Work units
+// (tile, K-split) are dealt out in contiguous ranges per XCD (workgroup b runs
+// on XCD b % 8), so workgroups sharing an A row-block (rotations) or a B
+// column-block (PCA, n_major) run together on one XCD and hit the same L2.
+// Small-M problems split K; each split writes its own fp32 partial tile and a
+// second kernel adds the partials in split order (deterministic).
 #include <algorithm>
 
 #include "gemm.h"
@@ -21,13 +36,25 @@
 namespace eogp {
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 32, LDK = BK + 8;
+constexpr int BM = 256, BK = 32, NTHR = 256;
 
 struct KParams {
   GemmArgs g;
-  int a_vec;  // A rows allow 16-byte loads
-  int b_vec;  // B rows allow 16-byte loads
+  int64_t kc;       // K per split (multiple of BK)
+  int splits;
 };
+
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4u mk4(uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+  v4u r;
+  r.x = a; r.y = b; r.z = c; r.w = d;
+  return r;
+}
+__device__ __forceinline__ uint32_t pack2(uint32_t lo, uint32_t hi) {
+  return (lo & 0xFFFFu) | (hi << 16);
+}
 
 template <bool F16>
 __device__ __forceinline__ uint16_t cvt16(float v) {
@@ -35,13 +62,13 @@ __device__ __forceinline__ uint16_t cvt16(float v) {
   else return to_bf16_bits(v);
 }
 template <bool F16>
-__device__ __forceinline__ float back16(uint16_t b) {
-  if constexpr (F16) return f16_bits_to_f32(b);
-  else return bf16_bits_to_f32(b);
+__device__ __forceinline__ float back16(uint32_t b) {
+  if constexpr (F16) return f16_bits_to_f32((uint16_t)b);
+  else return bf16_bits_to_f32((uint16_t)b);
 }
 
 template <bool F16>
-__device__ __forceinline__ f32x16 mfma32(const uint4& a, const uint4& b, f32x16 c) {
+__device__ __forceinline__ f32x16 mfma32(const v4u& a, const v4u& b, f32x16 c) {
   if constexpr (F16) {
     return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
                                                   __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
@@ -51,225 +78,429 @@ __device__ __forceinline__ f32x16 mfma32(const uint4& a, const uint4& b, f32x16 
   }
 }
 
-__device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) {
-  return (uint32_t)lo | ((uint32_t)hi << 16);
+// Offset (in halves) of 16-byte chunk `c` (0..3) of LDS row `r`. The XOR key
+// ((r >> 1) ^ (r >> 3)) & 3 spreads 8 (or 16) consecutive rows read at one
+// chunk over distinct 16-byte bank groups of a 128-byte (or 256-byte) bank
+// window, so 16-byte fragment reads and staging writes are conflict-free.
+__device__ __forceinline__ int swz(int r, int c) {
+  return r * BK + ((c ^ (((r >> 1) ^ (r >> 3)) & 3)) << 3);
 }
 
-template <int AT, int AP, int BP, bool F16>
-__global__ __launch_bounds__(256, 2) void k_gemm(KParams kp) {
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2v __attribute__((ext_vector_type(2)));
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+
+// Two fp32 values -> one packed pair of the MFMA type (round to nearest even).
+template <bool F16>
+__device__ __forceinline__ uint32_t cvt_pair(float a, float b) {
+  f32x2v v;
+  v.x = a;
+  v.y = b;
+  if constexpr (F16) return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2v));
+  else return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
+}
+// The two fp32 values a packed pair represents.
+template <bool F16>
+__device__ __forceinline__ f32x2v uncvt_pair(uint32_t p) {
+  if constexpr (F16) {
+    return __builtin_convertvector(__builtin_bit_cast(f16x2v, p), f32x2v);
+  } else {
+    f32x2v r;
+    r.x = __uint_as_float(p << 16);
+    r.y = __uint_as_float(p & 0xFFFF0000u);
+    return r;
+  }
+}
+
+// AT: 0 = fp32 A, 1 = 16-bit A. AV: A rows allow 16-byte loads (else fp32 A is
+// loaded one element per lane, 32 lanes per row). BC: B is bounds-checked.
+template <int AT, int AP, int BP, bool F16, int BN, bool AV, bool BC>
+__global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
+  constexpr int WI = 4;                  // 32-high row blocks per wave (128 rows)
+  constexpr int WJ = BN / 64;            // 32-wide column blocks per wave (BN/2 columns)
   const GemmArgs& g = kp.g;
-  __shared__ __attribute__((aligned(16))) uint16_t sA[AP][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[BP][BN * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][AP][BM * BK];
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BP][BN * BK];
+  __shared__ int64_t sOff[BM];           // element offset of each A row (clamped to a valid row)
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int64_t M = g.M_dev ? (int64_t)(*g.M_dev) : g.M;
   const int64_t N = g.N, K = g.K;
   const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  const int64_t n_tiles = tiles_m * tiles_n;
-  const int64_t nk = (K + BK - 1) / BK;
+  const int64_t n_units = tiles_m * tiles_n * kp.splits;
 
   const int G = gridDim.x, b = blockIdx.x;
   int64_t t_begin, t_end, t_step;
   if (G >= kXcds && G % kXcds == 0) {
     const int xcd = b % kXcds;
-    const int64_t per = G / kXcds, chunk = (n_tiles + kXcds - 1) / kXcds;
+    const int64_t per = G / kXcds, chunk = (n_units + kXcds - 1) / kXcds;
     t_begin = xcd * chunk + b / kXcds;
-    t_end = std::min<int64_t>((int64_t)(xcd + 1) * chunk, n_tiles);
+    t_end = std::min<int64_t>((int64_t)(xcd + 1) * chunk, n_units);
     t_step = per;
   } else {
     t_begin = b;
-    t_end = n_tiles;
+    t_end = n_units;
     t_step = G;
   }
 
-  const int ar = tid >> 1, ak = (tid & 1) * 16;   // A staging: row, first k
-  const int br = tid >> 1, bk = (tid & 1) * 16;   // B staging
-  const int wm = (wid >> 1) * 64, wn = (wid & 1) * 64;
+  const int wm = (wid >> 1) * 128, wn = (wid & 1) * (BN / 2);
+  // Staging maps consecutive lanes to consecutive 16-byte pieces of one row, so
+  // a wave-wide 16-byte load covers whole cache lines:
+  //   fp32 A:   8 lanes per row (128 bytes), rows (tid >> 3) + 32 q, q = 0..7;
+  //   16-bit A: 4 lanes per row (64 bytes),  rows (tid >> 2) + 64 q, q = 0..3;
+  //   B:        4 lanes per row per part,    rows (tid >> 2) + 64 q, q < BN/64.
+  constexpr int AQ = AT == 0 ? 8 : 4;     // A pieces per thread per slice
+  constexpr int BQ = BN / 64;             // B pieces per thread per slice and part
+  const int a_r0 = AT == 0 ? (tid >> 3) : (tid >> 2);
+  const int a_rs = AT == 0 ? 32 : 64;
+  const int a_pc = AT == 0 ? (tid & 7) : (tid & 3);   // piece index within the row
+  const int b_r0 = tid >> 2, b_pc = tid & 3;
+  const int sc = tid & 31, sr = tid >> 5;   // element A path: column, first row (rows sr + 8e)
 
-  for (int64_t t = t_begin; t < t_end; t += t_step) {
+  for (int64_t u = t_begin; u < t_end; u += t_step) {
+    const int64_t t = u / kp.splits;
+    const int split = (int)(u % kp.splits);
     int64_t tm, tn;
     if (g.n_major) { tn = t / tiles_m; tm = t % tiles_m; }
     else { tm = t / tiles_n; tn = t % tiles_n; }
     const int64_t m0 = tm * BM, n0 = tn * BN;
+    const int64_t kbeg = split * kp.kc;
+    const int64_t kend = std::min<int64_t>(K, kbeg + kp.kc);
+    const int64_t nk = (kend - kbeg + BK - 1) / BK;
+    const bool ragged = ((kend - kbeg) % BK) != 0;
 
-    const int64_t arow = m0 + ar;
-    const bool a_ok = arow < M;
-    int64_t asrc = 0;
-    if (a_ok) asrc = g.a_rows ? (int64_t)g.a_rows[arow] : arow;
-    const int64_t brow = n0 + br;
-    const bool b_ok = brow < N;
-
-    // staging registers
-    float ra[AT == 0 ? 16 : 1];
-    uint4 ra16[2];
-    uint4 rb[BP][2];
-
-    auto load = [&](int64_t kt) {
-      const int64_t ka = kt * BK + ak;
-      if constexpr (AT == 0) {
-        const float* p = static_cast<const float*>(g.A) + asrc * g.lda + ka;
-        if (a_ok && kp.a_vec && ka + 16 <= K) {
+    __syncthreads();                     // previous unit's readers of sOff / stages are done
+    {
+      const int64_t r = m0 + tid;
+      const bool ok = r < M;
+      const int64_t src = g.a_rows ? (int64_t)g.a_rows[ok ? r : m0] : (ok ? r : m0);
+      sOff[tid] = src * g.lda;
+    }
+    __syncthreads();
+    constexpr bool A16B = (AT == 1) || AV;      // 16-byte A path
+    int64_t a_off[A16B ? AQ : 1];
+    if constexpr (A16B) {
 #pragma unroll
-          for (int v = 0; v < 4; ++v) {
-            float4 x = reinterpret_cast<const float4*>(p)[v];
-            ra[4 * v + 0] = x.x; ra[4 * v + 1] = x.y; ra[4 * v + 2] = x.z; ra[4 * v + 3] = x.w;
+      for (int q = 0; q < AQ; ++q) a_off[q] = sOff[a_r0 + a_rs * q];
+    }
+    // B rows n0 + b_r0 + 64 q; rows beyond N (which feed unstored columns)
+    // read row 0 instead.
+    int64_t b_off[BQ];
+#pragma unroll
+    for (int q = 0; q < BQ; ++q) {
+      const int64_t brow = n0 + b_r0 + 64 * q;
+      b_off[q] = (brow < N ? brow : 0) * g.ldb + 8 * b_pc;
+    }
+
+    // Slice order: a ragged last slice first, then the full slices in order.
+    auto slice_k0 = [&](int64_t i) -> int64_t {
+      const int64_t s = ragged ? (i == 0 ? nk - 1 : i - 1) : i;
+      return kbeg + s * BK;
+    };
+
+    v4f ra[AT == 0 && AV ? AQ : 1];       // fp32 A staging (16-byte path)
+    float re[AT == 0 && !AV ? 32 : 1];    // fp32 A staging (element path)
+    v4u ra16[AT == 0 ? 1 : AQ];           // 16-bit A staging
+    v4u rb[BP][BQ];
+
+    // Full slice, unconditional 16-byte loads.
+    auto load_full = [&](int64_t k0) {
+      if constexpr (AT == 0) {
+        const float* A = static_cast<const float*>(g.A);
+        if constexpr (AV) {
+#pragma unroll
+          for (int q = 0; q < AQ; ++q) ra[q] = *reinterpret_cast<const v4f*>(A + a_off[q] + k0 + 4 * a_pc);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 32; ++e) re[e] = A[sOff[sr + 8 * e] + k0 + sc];
+        }
+      } else {
+        const uint16_t* A = static_cast<const uint16_t*>(g.A);
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) ra16[q] = *reinterpret_cast<const v4u*>(A + a_off[q] + k0 + 8 * a_pc);
+      }
+#pragma unroll
+      for (int part = 0; part < BP; ++part)
+#pragma unroll
+        for (int q = 0; q < BQ; ++q) {
+          const uint16_t* p = (part == 0 ? g.B_hi : g.B_lo) + b_off[q] + k0;
+          if constexpr (!BC) {
+            rb[part][q] = *reinterpret_cast<const v4u*>(p);
+          } else {
+            const int64_t brow = n0 + b_r0 + 64 * q;
+            uint32_t h[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int64_t kk = k0 + 8 * b_pc + e;
+              h[e] = (brow < N && kk < kend) ? (uint32_t)p[e] : 0u;
+            }
+            rb[part][q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
+          }
+        }
+    };
+    // The ragged slice: element-wise, bounds-checked.
+    auto load_tail = [&](int64_t k0) {
+      if constexpr (AT == 0) {
+        const float* A = static_cast<const float*>(g.A);
+        if constexpr (AV) {
+#pragma unroll
+          for (int q = 0; q < AQ; ++q) {
+            const int64_t kk = k0 + 4 * a_pc;
+            v4f x;
+            x.x = (kk + 0 < kend) ? A[a_off[q] + kk + 0] : 0.f;
+            x.y = (kk + 1 < kend) ? A[a_off[q] + kk + 1] : 0.f;
+            x.z = (kk + 2 < kend) ? A[a_off[q] + kk + 2] : 0.f;
+            x.w = (kk + 3 < kend) ? A[a_off[q] + kk + 3] : 0.f;
+            ra[q] = x;
           }
         } else {
 #pragma unroll
-          for (int e = 0; e < 16; ++e) ra[e] = (a_ok && ka + e < K) ? p[e] : 0.f;
+          for (int e = 0; e < 32; ++e) re[e] = (k0 + sc < kend) ? A[sOff[sr + 8 * e] + k0 + sc] : 0.f;
         }
       } else {
-        const uint16_t* p = static_cast<const uint16_t*>(g.A) + asrc * g.lda + ka;
-        if (a_ok && kp.a_vec && ka + 16 <= K) {
-          ra16[0] = reinterpret_cast<const uint4*>(p)[0];
-          ra16[1] = reinterpret_cast<const uint4*>(p)[1];
-        } else {
-          uint16_t h[16];
+        const uint16_t* A = static_cast<const uint16_t*>(g.A);
 #pragma unroll
-          for (int e = 0; e < 16; ++e) h[e] = (a_ok && ka + e < K) ? p[e] : (uint16_t)0;
-          ra16[0] = make_uint4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
-          ra16[1] = make_uint4(pack2(h[8], h[9]), pack2(h[10], h[11]), pack2(h[12], h[13]), pack2(h[14], h[15]));
+        for (int q = 0; q < AQ; ++q) {
+          uint32_t h[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int64_t kk = k0 + 8 * a_pc + e;
+            h[e] = kk < kend ? (uint32_t)A[a_off[q] + kk] : 0u;
+          }
+          ra16[q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
         }
       }
-      const int64_t kb = kt * BK + bk;
 #pragma unroll
-      for (int part = 0; part < BP; ++part) {
-        const uint16_t* base = part == 0 ? g.B_hi : g.B_lo;
-        const uint16_t* p = base + brow * g.ldb + kb;
-        if (b_ok && kp.b_vec && kb + 16 <= K) {
-          rb[part][0] = reinterpret_cast<const uint4*>(p)[0];
-          rb[part][1] = reinterpret_cast<const uint4*>(p)[1];
-        } else {
-          uint16_t h[16];
+      for (int part = 0; part < BP; ++part)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) h[e] = (b_ok && kb + e < K) ? p[e] : (uint16_t)0;
-          rb[part][0] = make_uint4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
-          rb[part][1] = make_uint4(pack2(h[8], h[9]), pack2(h[10], h[11]), pack2(h[12], h[13]), pack2(h[14], h[15]));
+        for (int q = 0; q < BQ; ++q) {
+          const int64_t brow = n0 + b_r0 + 64 * q;
+          const uint16_t* p = (part == 0 ? g.B_hi : g.B_lo) + b_off[q] + k0;
+          uint32_t h[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int64_t kk = k0 + 8 * b_pc + e;
+            h[e] = (brow < N && kk < kend) ? (uint32_t)p[e] : 0u;
+          }
+          rb[part][q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
         }
-      }
     };
 
-    auto stage = [&]() {
-      uint4* dA0 = reinterpret_cast<uint4*>(&sA[0][ar * LDK + ak]);
+    // Registers -> LDS stage `st`. Rows beyond M hold a copy of a valid row:
+    // they only feed output rows that are never stored, so they are staged as
+    // they are.
+    auto stage = [&](int st) {
       if constexpr (AT == 0) {
-        uint16_t hi[16], lo[16];
+        if constexpr (AV) {
+          // 4 floats = half of a 16-byte chunk of 8 halves
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          hi[e] = cvt16<F16>(ra[e]);
-          if constexpr (AP == 2) lo[e] = cvt16<F16>(ra[e] - back16<F16>(hi[e]));
-        }
-        dA0[0] = make_uint4(pack2(hi[0], hi[1]), pack2(hi[2], hi[3]), pack2(hi[4], hi[5]), pack2(hi[6], hi[7]));
-        dA0[1] = make_uint4(pack2(hi[8], hi[9]), pack2(hi[10], hi[11]), pack2(hi[12], hi[13]), pack2(hi[14], hi[15]));
-        if constexpr (AP == 2) {
-          uint4* dA1 = reinterpret_cast<uint4*>(&sA[AP - 1][ar * LDK + ak]);
-          dA1[0] = make_uint4(pack2(lo[0], lo[1]), pack2(lo[2], lo[3]), pack2(lo[4], lo[5]), pack2(lo[6], lo[7]));
-          dA1[1] = make_uint4(pack2(lo[8], lo[9]), pack2(lo[10], lo[11]), pack2(lo[12], lo[13]), pack2(lo[14], lo[15]));
+          for (int q = 0; q < AQ; ++q) {
+            const int r = a_r0 + a_rs * q;
+            const int o = swz(r, a_pc >> 1) + 4 * (a_pc & 1);
+            const v4f x = ra[q];
+            const uint32_t h0 = cvt_pair<F16>(x.x, x.y), h1 = cvt_pair<F16>(x.z, x.w);
+            typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+            v2u hv;
+            hv.x = h0;
+            hv.y = h1;
+            *reinterpret_cast<v2u*>(&sA[st][0][o]) = hv;
+            if constexpr (AP == 2) {
+              const f32x2v b0 = uncvt_pair<F16>(h0), b1 = uncvt_pair<F16>(h1);
+              v2u lv;
+              lv.x = cvt_pair<F16>(x.x - b0.x, x.y - b0.y);
+              lv.y = cvt_pair<F16>(x.z - b1.x, x.w - b1.y);
+              *reinterpret_cast<v2u*>(&sA[st][AP - 1][o]) = lv;
+            }
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 32; ++e) {
+            const int r = sr + 8 * e;
+            const int o = swz(r, sc >> 3) + (sc & 7);
+            const float x = re[e];
+            const uint16_t h = cvt16<F16>(x);
+            sA[st][0][o] = h;
+            if constexpr (AP == 2) sA[st][AP - 1][o] = cvt16<F16>(x - back16<F16>(h));
+          }
         }
       } else {
-        dA0[0] = ra16[0];
-        dA0[1] = ra16[1];
+#pragma unroll
+        for (int q = 0; q < AQ; ++q)
+          *reinterpret_cast<v4u*>(&sA[st][0][swz(a_r0 + a_rs * q, a_pc)]) = ra16[q];
       }
 #pragma unroll
-      for (int part = 0; part < BP; ++part) {
-        uint4* dB = reinterpret_cast<uint4*>(&sB[part][br * LDK + bk]);
-        dB[0] = rb[part][0];
-        dB[1] = rb[part][1];
-      }
+      for (int part = 0; part < BP; ++part)
+#pragma unroll
+        for (int q = 0; q < BQ; ++q)
+          *reinterpret_cast<v4u*>(&sB[st][part][swz(b_r0 + 64 * q, b_pc)]) = rb[part][q];
     };
 
-    f32x16 acc[2][2];
+    f32x16 acc[WI][WJ];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WI; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < WJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    load(0);
-    stage();
-    __syncthreads();
-    for (int64_t kt = 0; kt < nk; ++kt) {
-      if (kt + 1 < nk) load(kt + 1);
+    // Each pass sweeps all WI x WJ accumulators, so consecutive MFMAs never
+    // depend on each other's result.
+    auto compute = [&](int st) {
 #pragma unroll
       for (int ks = 0; ks < BK / 16; ++ks) {
-        const int ko = ks * 16 + 8 * (lane >> 5);
-        uint4 fa[AP][2], fb[BP][2];
+        const int ch = 2 * ks + (lane >> 5);
+        v4u fa[AP][WI], fb[BP][WJ];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < WI; ++i)
 #pragma unroll
           for (int part = 0; part < AP; ++part)
-            fa[part][i] = *reinterpret_cast<const uint4*>(&sA[part][(wm + 32 * i + (lane & 31)) * LDK + ko]);
+            fa[part][i] = *reinterpret_cast<const v4u*>(&sA[st][part][swz(wm + 32 * i + (lane & 31), ch)]);
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < WJ; ++j)
 #pragma unroll
           for (int part = 0; part < BP; ++part)
-            fb[part][j] = *reinterpret_cast<const uint4*>(&sB[part][(wn + 32 * j + (lane & 31)) * LDK + ko]);
+            fb[part][j] = *reinterpret_cast<const v4u*>(&sB[st][part][swz(wn + 32 * j + (lane & 31), ch)]);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int j = 0; j < WJ; ++j)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            if constexpr (AP == 2) acc[i][j] = mfma32<F16>(fa[AP - 1][i], fb[0][j], acc[i][j]);
-            if constexpr (BP == 2) acc[i][j] = mfma32<F16>(fa[0][i], fb[BP - 1][j], acc[i][j]);
-            acc[i][j] = mfma32<F16>(fa[0][i], fb[0][j], acc[i][j]);
-          }
+          for (int i = 0; i < WI; ++i) acc[i][j] = mfma32<F16>(fa[0][i], fb[0][j], acc[i][j]);
+        if constexpr (BP == 2) {
+#pragma unroll
+          for (int j = 0; j < WJ; ++j)
+#pragma unroll
+            for (int i = 0; i < WI; ++i) acc[i][j] = mfma32<F16>(fa[0][i], fb[BP - 1][j], acc[i][j]);
+        }
+        if constexpr (AP == 2) {
+#pragma unroll
+          for (int j = 0; j < WJ; ++j)
+#pragma unroll
+            for (int i = 0; i < WI; ++i) acc[i][j] = mfma32<F16>(fa[AP - 1][i], fb[0][j], acc[i][j]);
+        }
       }
+    };
+
+    // prologue: slice 0 (possibly the ragged one) staged, slice 1 in registers
+    if (ragged) load_tail(slice_k0(0));
+    else load_full(slice_k0(0));
+    stage(0);
+    if (nk > 1) load_full(slice_k0(1));
+    __syncthreads();
+    // steady state: branch-free body
+    for (int64_t kt = 0; kt + 1 < nk; ++kt) {
+      const int st = (int)(kt & 1);
+      compute(st);
+      stage(st ^ 1);                                     // slice kt+1
+      load_full(slice_k0(std::min<int64_t>(kt + 2, nk - 1)));
       __syncthreads();
-      if (kt + 1 < nk) {
-        stage();
-        __syncthreads();
-      }
     }
+    compute((int)((nk - 1) & 1));
 
     // epilogue: lane holds column (lane & 31), rows 8*(r/4) + 4*(lane/32) + r%4
+    float* C = g.C;
+    int64_t ldc = g.ldc;
+    if (kp.splits > 1) {
+      C = g.partial + (int64_t)split * M * N;
+      ldc = N;
+    }
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < WI; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
+      for (int j = 0; j < WJ; ++j) {
         const int64_t col = n0 + wn + 32 * j + (lane & 31);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t row = m0 + wm + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (row < M && col < N) g.C[row * g.ldc + col] = acc[i][j][r];
+          if (row < M && col < N) C[row * ldc + col] = acc[i][j][r];
         }
       }
   }
 }
 
+// C[row, col] = sum over splits, in split order, of the partial tiles.
+__global__ void k_split_sum(const float* __restrict__ part, int splits, int64_t M, int64_t N,
+                            float* __restrict__ C, int64_t ldc) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= M * N) return;
+  const int64_t row = idx / N, col = idx % N;
+  float s = 0.f;
+  for (int p = 0; p < splits; ++p) s += part[(int64_t)p * M * N + idx];
+  C[row * ldc + col] = s;
+}
+
+template <int AT, int AP, int BP, bool F16, int BN>
+void pick(const KParams& kp, bool av, bool bc, unsigned grid, hipStream_t s) {
+  if constexpr (AT == 0) {
+    if (av && !bc) hipLaunchKernelGGL((k_gemm<AT, AP, BP, F16, BN, true, false>), dim3(grid), dim3(NTHR), 0, s, kp);
+    else if (av && bc) hipLaunchKernelGGL((k_gemm<AT, AP, BP, F16, BN, true, true>), dim3(grid), dim3(NTHR), 0, s, kp);
+    else if (!bc) hipLaunchKernelGGL((k_gemm<AT, AP, BP, F16, BN, false, false>), dim3(grid), dim3(NTHR), 0, s, kp);
+    else hipLaunchKernelGGL((k_gemm<AT, AP, BP, F16, BN, false, true>), dim3(grid), dim3(NTHR), 0, s, kp);
+  } else {
+    if (!bc) hipLaunchKernelGGL((k_gemm<AT, AP, BP, F16, BN, true, false>), dim3(grid), dim3(NTHR), 0, s, kp);
+    else hipLaunchKernelGGL((k_gemm<AT, AP, BP, F16, BN, true, true>), dim3(grid), dim3(NTHR), 0, s, kp);
+  }
+}
+
 template <int AT, int AP, int BP, bool F16>
-eogp_status launch(const KParams& kp, hipStream_t s) {
-  const GemmArgs& g = kp.g;
-  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
-  if (tiles == 0) return EOGP_OK;
-  int64_t grid = std::min<int64_t>(tiles, 2 * kCus);
+eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
+  if (g.M == 0 || g.N == 0) return EOGP_OK;
+  const int64_t pad256 = ((g.N + 255) / 256) * 256, pad128 = ((g.N + 127) / 128) * 128;
+  const bool wide = pad256 * 10 <= pad128 * 11;      // at most 10% more padding
+  const int bn = wide ? 256 : 128;
+  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + bn - 1) / bn);
+  KParams kp;
+  kp.g = g;
+  kp.splits = 1;
+  kp.kc = ((g.K + BK - 1) / BK) * BK;
+  const int64_t nk_all = (g.K + BK - 1) / BK;
+  if (!g.M_dev && g.partial && tiles < kCus) {
+    // split K so that there are about two work units per CU, >= 16 slices each
+    int sp = (int)std::min<int64_t>((2 * kCus + tiles - 1) / tiles, nk_all / 16);
+    sp = std::min(sp, g.max_splits);
+    if (sp > 1) {
+      kp.kc = ((nk_all + sp - 1) / sp) * BK;
+      kp.splits = (int)((nk_all * BK + kp.kc - 1) / kp.kc);
+    }
+  }
+  int64_t grid = std::min<int64_t>(tiles * kp.splits, kCus);
   if (grid >= kXcds) grid = grid / kXcds * kXcds;
   timing::Scope ts(g.timing_class, s);
-  hipLaunchKernelGGL((k_gemm<AT, AP, BP, F16>), dim3((unsigned)grid), dim3(256), 0, s, kp);
+  if (wide) pick<AT, AP, BP, F16, 256>(kp, av, bc, (unsigned)grid, s);
+  else pick<AT, AP, BP, F16, 128>(kp, av, bc, (unsigned)grid, s);
   EOGP_LAUNCH_CHECK("gemm launch");
+  if (kp.splits > 1) {
+    const int64_t total = g.M * g.N;
+    hipLaunchKernelGGL(k_split_sum, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                       g.partial, kp.splits, g.M, g.N, g.C, g.ldc);
+    EOGP_LAUNCH_CHECK("gemm split sum");
+  }
   return EOGP_OK;
 }
 
 }  // namespace
 
+size_t gemm_partial_bytes(int64_t M, int64_t N, int max_splits) {
+  return (size_t)M * N * 4 * (size_t)std::max(1, max_splits);
+}
+
 eogp_status gemm_nt(const GemmArgs& g, AType a_type, int a_parts, int b_parts, bool f16,
                     hipStream_t s) {
-  KParams kp;
-  kp.g = g;
-  const size_t a_elem = a_type == AType::F32 ? 4 : 2;
-  const int a_align = a_type == AType::F32 ? 4 : 8;
-  kp.a_vec = (g.lda % a_align == 0) && ((uintptr_t)g.A % 16 == 0);
-  kp.b_vec = (g.ldb % 8 == 0) && ((uintptr_t)g.B_hi % 16 == 0) &&
-             (g.B_lo == nullptr || (uintptr_t)g.B_lo % 16 == 0);
-  (void)a_elem;
   const bool A32 = a_type == AType::F32;
+  const int a_align = A32 ? 4 : 8;
+  const bool av = (g.lda % a_align == 0) && ((uintptr_t)g.A % 16 == 0);
+  if (!A32 && !av) return fail(EOGP_ERR_UNSUPPORTED, "gemm: 16-bit A rows must be 16-byte aligned");
+  // B needs no checks when rows are padded to the tile and K to the slice.
+  const bool bc = !(g.b_padded && (g.ldb % 8 == 0) && ((uintptr_t)g.B_hi % 16 == 0) &&
+                    (g.B_lo == nullptr || (uintptr_t)g.B_lo % 16 == 0));
   if (b_parts == 2 && g.B_lo == nullptr) return fail(EOGP_ERR_INVALID, "gemm: missing B low part");
   if (!A32 && a_parts != 1) return fail(EOGP_ERR_INVALID, "gemm: 16-bit A cannot be split");
-  if (A32 && a_parts == 1 && b_parts == 1 && !f16) return launch<0, 1, 1, false>(kp, s);
-  if (A32 && a_parts == 2 && b_parts == 2 && !f16) return launch<0, 2, 2, false>(kp, s);
-  if (A32 && a_parts == 2 && b_parts == 1 && !f16) return launch<0, 2, 1, false>(kp, s);
-  if (A32 && a_parts == 1 && b_parts == 1 && f16) return launch<0, 1, 1, true>(kp, s);
-  if (A32 && a_parts == 2 && b_parts == 1 && f16) return launch<0, 2, 1, true>(kp, s);
-  if (!A32 && b_parts == 1 && !f16) return launch<1, 1, 1, false>(kp, s);
-  if (!A32 && b_parts == 2 && !f16) return launch<1, 1, 2, false>(kp, s);
+  if (A32 && a_parts == 1 && b_parts == 1 && !f16) return launch<0, 1, 1, false>(g, av, bc, s);
+  if (A32 && a_parts == 2 && b_parts == 2 && !f16) return launch<0, 2, 2, false>(g, av, bc, s);
+  if (A32 && a_parts == 2 && b_parts == 1 && !f16) return launch<0, 2, 1, false>(g, av, bc, s);
+  if (A32 && a_parts == 1 && b_parts == 1 && f16) return launch<0, 1, 1, true>(g, av, bc, s);
+  if (A32 && a_parts == 2 && b_parts == 1 && f16) return launch<0, 2, 1, true>(g, av, bc, s);
+  if (!A32 && b_parts == 1 && !f16) return launch<1, 1, 1, false>(g, av, bc, s);
+  if (!A32 && b_parts == 2 && !f16) return launch<1, 1, 2, false>(g, av, bc, s);
+  if (!A32 && b_parts == 1 && f16) return launch<1, 1, 1, true>(g, av, bc, s);
   return fail(EOGP_ERR_UNSUPPORTED, "gemm: unsupported operand combination");
 }
 

@@ -9,8 +9,8 @@ struct eogp_plan {
   int64_t n_cols = 0;      // |K|
   int64_t rows_pad = 0;    // |J| rounded up to the GEMM column tile
   int64_t cols_pad = 0;    // |K| rounded up likewise
-  int64_t ld_out = 0;      // panel row length for Q_S columns (>= d_out, multiple of 8)
-  int64_t ld_in = 0;       // panel row length for Q_A columns (>= d_in, multiple of 8)
+  int64_t ld_out = 0;      // panel row length for Q_S columns (>= d_out, multiple of 32)
+  int64_t ld_in = 0;       // panel row length for Q_A columns (>= d_in, multiple of 32)
   int64_t n_tiles = 0;     // active 32x32 (row, column) blocks
   int device = 0;
 
@@ -28,7 +28,7 @@ struct eogp_plan {
 };
 
 namespace eogp {
-constexpr int kPanelTile = 128;   // GEMM column-tile width the panels are padded to
+constexpr int kPanelTile = 256;   // widest GEMM column tile; panels are padded to it
 constexpr int kBlk = 32;          // retained-product block edge
 
 eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double damping,

@@ -128,7 +128,8 @@ size_t work_bytes(const eogp_plan* p, int64_t N, int64_t T) {
 
 size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T) { return work_bytes(p, N, T); }
 
-eogp_status rotate_retain(const eogp_plan* p, const void* acts, const void* grads, bool bf16_in,
+eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
+                          int64_t ld_grads, bool bf16_in,
                           const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
                           bool accurate, void* ws, size_t ws_bytes, hipStream_t s) {
   if (ws_bytes < work_bytes(p, N, T)) return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
@@ -155,28 +156,31 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, const void* grad
   const int b_parts = accurate ? 2 : 1;
   GemmArgs gs;
   gs.A = grads;
-  gs.lda = p->d_out;
+  gs.lda = ld_grads;
   gs.a_rows = w.tok;
   gs.B_hi = p->qs_hi;
   gs.B_lo = p->qs_lo;
   gs.ldb = p->ld_out;
+  gs.b_padded = true;
   gs.C = w.St;
   gs.ldc = p->rows_pad;
   gs.M = N * T;
   gs.M_dev = w.cnt + N;
-  gs.N = p->rows_pad;
+  // Columns n_rows..rows_pad-1 of S~ are left unwritten: they only feed
+  // block outputs that no retained axis reads.
+  gs.N = p->n_rows;
   gs.K = p->d_out;
   eogp_status st = gemm_nt(gs, at, a_parts, b_parts, false, s);
   if (st != EOGP_OK) return st;
   GemmArgs ga = gs;
   ga.A = acts;
-  ga.lda = p->d_in;
+  ga.lda = ld_acts;
   ga.B_hi = p->qa_hi;
   ga.B_lo = p->qa_lo;
   ga.ldb = p->ld_in;
   ga.C = w.At;
   ga.ldc = p->cols_pad;
-  ga.N = p->cols_pad;
+  ga.N = p->n_cols;
   ga.K = p->d_in;
   st = gemm_nt(ga, at, a_parts, b_parts, false, s);
   if (st != EOGP_OK) return st;

@@ -410,8 +410,8 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   p->n_cols = hst.n_cols;
   p->rows_pad = round_up(std::max<int64_t>(p->n_rows, 1), kPanelTile);
   p->cols_pad = round_up(std::max<int64_t>(p->n_cols, 1), kPanelTile);
-  p->ld_out = round_up(d_out, 8);
-  p->ld_in = round_up(d_in, 8);
+  p->ld_out = round_up(d_out, 32);
+  p->ld_in = round_up(d_in, 32);
   p->n_tiles = n_active;
   (void)hipGetDevice(&p->device);
   size_t pb = 0;

@@ -69,13 +69,13 @@ def load(path: str | None = None):
         "eogp_plan_get_info": (c_i32, [c_vp, ctypes.POINTER(PlanInfo)]),
         "eogp_plan_copy_retained": (c_i32, [c_vp, c_vp, c_vp, c_vp]),
         "eogp_rotate_retain_workspace_size": (c_sz, [c_vp, c_i64, c_i64]),
-        "eogp_rotate_retain_planned": (c_i32, [c_vp, c_vp, c_vp, c_i32, c_vp, c_i64, c_i64, c_vp,
-                                               c_i64, c_i32, c_vp, c_sz, c_vp]),
+        "eogp_rotate_retain_planned": (c_i32, [c_vp, c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64,
+                                               c_i64, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
         "eogp_rotate_retain_oneshot_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64]),
-        "eogp_rotate_retain": (c_i32, [c_vp, c_vp, c_i32, c_vp, c_i64, c_i64, c_i64, c_i64, c_vp,
-                                       c_vp, c_vp, ctypes.c_double, c_i64, c_vp, c_i64, c_i32,
-                                       c_vp, c_sz, c_vp]),
-        "eogp_pca_project_workspace_size": (c_sz, [c_i64, c_i64, c_i32, c_i32]),
+        "eogp_rotate_retain": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64, c_i64,
+                                       c_i64, c_vp, c_vp, c_vp, ctypes.c_double, c_i64, c_vp, c_i64,
+                                       c_i32, c_vp, c_sz, c_vp]),
+        "eogp_pca_project_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i32, c_i32]),
         "eogp_pca_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i32, c_i64, c_i64, c_vp,
                                      c_i64, c_i32, c_vp, c_sz, c_vp]),
         "eogp_sign_pack": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp]),
@@ -182,6 +182,15 @@ def eogp_plan_create(eigvals, damping, m, Q_A, Q_S, stream=None) -> eogp_plan:
 # ---------------------------------------------------------------------------
 # First stage
 # ---------------------------------------------------------------------------
+def _token_stride(x, name):
+    """Row stride (elements) of a [N, T, d] token tensor whose tokens are laid
+    out at a constant stride, e.g. a column slice of a wider padded buffer."""
+    if x.dim() != 3 or x.stride(2) != 1 or x.stride(0) != x.shape[1] * x.stride(1):
+        raise ValueError(f"{name} must be [N, T, d] with unit column stride and tokens at a "
+                         "constant row stride")
+    return x.stride(1)
+
+
 def _acts_dtype(acts, out_grads):
     if acts.dtype != out_grads.dtype or acts.dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("acts and out_grads must both be float32 or both bfloat16")
@@ -200,8 +209,7 @@ def eogp_rotate_retain_planned(plan: eogp_plan, acts, out_grads, token_mask=None
     N, T, d_in = acts.shape
     if tuple(out_grads.shape) != (N, T, plan.d_out) or d_in != plan.d_in:
         raise ValueError("acts [N,T,d_in] / out_grads [N,T,d_out] do not match the plan")
-    if not (acts.is_contiguous() and out_grads.is_contiguous()):
-        raise ValueError("acts and out_grads must be contiguous")
+    ld_a, ld_g = _token_stride(acts, "acts"), _token_stride(out_grads, "out_grads")
     if token_mask is not None and (token_mask.dtype != torch.uint8 or tuple(token_mask.shape) != (N, T)
                                    or not token_mask.is_contiguous()):
         raise ValueError("token_mask must be contiguous uint8 [N, T]")
@@ -211,7 +219,7 @@ def eogp_rotate_retain_planned(plan: eogp_plan, acts, out_grads, token_mask=None
         raise ValueError("Z must be float32 [N, >= m] with unit column stride")
     need = eogp_rotate_retain_workspace_size(plan, N, T)
     ws, wsb = _workspace(need, acts.device, ws)
-    _check(L.eogp_rotate_retain_planned(plan._h, _ptr(acts), _ptr(out_grads),
+    _check(L.eogp_rotate_retain_planned(plan._h, _ptr(acts), ld_a, _ptr(out_grads), ld_g,
                                         _acts_dtype(acts, out_grads), _ptr(token_mask), N, T,
                                         _ptr(Z), Z.stride(0), prec, _ptr(ws), wsb, _stream(stream)))
     return Z
@@ -224,11 +232,12 @@ def eogp_rotate_retain(acts, out_grads, token_mask, Q_A, Q_S, eigvals, damping, 
     _need_cuda(acts, out_grads, token_mask, Q_A, Q_S, eigvals, Z)
     N, T, d_in = acts.shape
     d_out = out_grads.shape[2]
+    ld_a, ld_g = _token_stride(acts, "acts"), _token_stride(out_grads, "out_grads")
     if Z is None:
         Z = torch.empty((N, m), dtype=torch.float32, device=acts.device)
     need = int(L.eogp_rotate_retain_oneshot_workspace_size(N, T, d_in, d_out))
     ws, wsb = _workspace(need, acts.device, ws)
-    _check(L.eogp_rotate_retain(_ptr(acts), _ptr(out_grads), _acts_dtype(acts, out_grads),
+    _check(L.eogp_rotate_retain(_ptr(acts), ld_a, _ptr(out_grads), ld_g, _acts_dtype(acts, out_grads),
                                 _ptr(token_mask), N, T, d_in, d_out, _ptr(Q_A), _ptr(Q_S),
                                 _ptr(eigvals), float(damping), int(m), _ptr(Z), Z.stride(0), prec,
                                 _ptr(ws), wsb, _stream(stream)))
@@ -252,7 +261,7 @@ def eogp_pca_project(Z, Pt, X=None, prec=PREC_FAST, ws=None, stream=None):
     if X is None:
         X = torch.empty((N, k), dtype=torch.float32, device=Z.device)
     pd = _DTYPE_CODE[Pt.dtype]
-    need = int(L.eogp_pca_project_workspace_size(m, k, pd, prec))
+    need = int(L.eogp_pca_project_workspace_size(N, m, k, pd, prec))
     ws, wsb = _workspace(need, Z.device, ws)
     _check(L.eogp_pca_project(_ptr(Z), Z.stride(0), N, m, _ptr(Pt), pd, Pt.stride(0), k, _ptr(X),
                               X.stride(0), prec, _ptr(ws), wsb, _stream(stream)))

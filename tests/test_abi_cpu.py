@@ -86,5 +86,7 @@ def test_workspace_size_queries_are_consistent():
     a = L.eogp_rotate_retain_oneshot_workspace_size(4, 16, 64, 64)
     b = L.eogp_rotate_retain_oneshot_workspace_size(8, 16, 64, 64)
     assert 0 < a < b
-    assert L.eogp_pca_project_workspace_size(512, 128, 2, 0) == 0      # fp16 P: none
-    assert L.eogp_pca_project_workspace_size(512, 128, 0, 1) > 0       # fp32 P: split copy
+    f16 = L.eogp_pca_project_workspace_size(100, 512, 128, 2, 0)     # fp16 P: split-K scratch
+    f32 = L.eogp_pca_project_workspace_size(100, 512, 128, 0, 1)     # fp32 P: + split copy
+    assert 0 < f16 < f32
+    assert L.eogp_pca_project_workspace_size(1000, 512, 128, 2, 0) > f16

@@ -280,6 +280,35 @@ def test_rotate_retain_no_mask_and_ldz():
     plan.close()
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_rotate_retain_strided_token_rows(dtype):
+    """Tokens passed as column slices of wider, 16-byte aligned buffers
+    (769 -> 776 and 65 -> 72 columns), the way a caller hands over GPT-2's
+    bias-augmented activations."""
+    N, T, d_in, d_out, m = 3, 50, 769, 65, 900
+    say(f"[first stage] strided rows {dtype}")
+    a, ds, mask, QA, QS, lam = random_problem(14, N, T, d_in, d_out, m, lens_lo=5)
+    abuf = torch.full((N, T, 776), float("nan"), device=DEV, dtype=dtype)
+    gbuf = torch.full((N, T, 72), float("nan"), device=DEV, dtype=dtype)
+    abuf[:, :, :d_in] = d(a, dtype)
+    gbuf[:, :, :d_out] = d(ds, dtype)
+    a_used = abuf[:, :, :d_in].float().cpu().numpy()
+    d_used = gbuf[:, :, :d_out].float().cpu().numpy()
+    plan = E.eogp_plan_create(d(lam), 1e-4, m, d(QA), d(QS))
+    Z = E.eogp_rotate_retain_planned(plan, abuf[:, :, :d_in], gbuf[:, :, :d_out], d(mask),
+                                     prec=E.PREC_ACCURATE)
+    Z1 = E.eogp_rotate_retain(abuf[:, :, :d_in], gbuf[:, :, :d_out], d(mask), d(QA), d(QS),
+                              d(lam), 1e-4, m, prec=E.PREC_ACCURATE)
+    torch.cuda.synchronize()
+    ref, _ = oracle_Z(S.fill_masked(a_used, mask), S.fill_masked(d_used, mask), mask, QA, QS,
+                      lam, 1e-4, m)
+    for got in (Z, Z1):
+        err = rel_rows(got.cpu().numpy(), ref)
+        say(f"   max rel {err.max():.2e}")
+        assert err.max() <= 1e-3
+    plan.close()
+
+
 def test_rotate_retain_deterministic():
     N, T, d_in, d_out, m = 4, 64, 128, 96, 500
     a, ds, mask, QA, QS, lam = random_problem(13, N, T, d_in, d_out, m, lens_lo=10)
