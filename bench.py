@@ -55,6 +55,9 @@ def parse(argv=None):
     ap.add_argument("--scoring-queries", type=int, default=512)
     ap.add_argument("--scoring-codes", type=int, default=8 * 1024 * 1024)
     ap.add_argument("--only-scoring", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run a plain device copy of this many MiB 4 times (calibrates "
+                         "the FETCH_SIZE / WRITE_SIZE counters against known traffic)")
     return ap.parse_args(argv)
 
 
@@ -87,19 +90,35 @@ class Gpt2Step:
         self.kb = self.k // 8
         self.N_store = w.N
         t0 = time.time()
-        # per-shape inputs (the same bytes serve that linear in every block)
-        self.A, self.D, self.QA, self.QD = {}, {}, {}, {}
-        mask = None
+        # Per-shape inputs (the same bytes serve that linear in every block).
+        # Training examples and the step's queries share one buffer, so one
+        # first-stage and one PCA launch per module cover both; token rows are
+        # padded to a multiple of 32 elements (128 bytes), as a caller that
+        # appends the bias column would lay them out.
+        self.A, self.D = {}, {}
+        Nt = self.B + self.Qb
+        mask = torch.empty((Nt, self.T), dtype=torch.uint8, device=dev)
         for si, (name, di, do) in enumerate(self.shapes):
+            bufs = []
+            for width in (di, do):
+                ld = -(-width // 32) * 32
+                bufs.append(torch.zeros((Nt, self.T, ld), dtype=torch.float32, device=dev))
             a, ds, mk = S.torch_inputs(w, si, self.B, self.T, di, do, dev, torch.float32)
+            bufs[0][:self.B, :, :di] = a
+            bufs[1][:self.B, :, :do] = ds
+            mask[:self.B] = mk
+            del a, ds
             qa, qds, qmk = S.torch_inputs(w, si, self.Qb, self.T, di, do, dev, torch.float32,
                                           stream_base=32)
-            self.A[name], self.D[name], self.QA[name], self.QD[name] = a, ds, qa, qds
-            if mask is None:
-                mask, qmask = mk, qmk
-        self.mask, self.qmask = mask, qmask
-        self.valid_tokens = int(mask.sum().item())
-        self.valid_q_tokens = int(qmask.sum().item())
+            bufs[0][self.B:, :, :di] = qa
+            bufs[1][self.B:, :, :do] = qds
+            mask[self.B:] = qmk
+            del qa, qds
+            self.A[name] = bufs[0][:, :, :di]
+            self.D[name] = bufs[1][:, :, :do]
+        self.mask = mask
+        self.valid_tokens = int(mask[:self.B].sum().item())
+        self.valid_q_tokens = int(mask[self.B:].sum().item())
         log(f"inputs ready ({time.time() - t0:.1f}s), valid tokens {self.valid_tokens}")
         # shared artifacts and plans (fitting phase: not part of a step)
         cache = {}
@@ -117,22 +136,23 @@ class Gpt2Step:
             del art
         self.plan_ms = 1000.0 * t_plan
         log(f"plans ready ({time.time() - t0:.1f}s), plan build {self.plan_ms:.1f} ms total")
-        # buffers
+        # buffers: Z of the batch (training rows then queries), the PCA
+        # coordinates of every module side by side; the query rows of Xall are
+        # the unquantized query coordinates Y [Qb, U*k] that scoring reads
         f32 = torch.float32
-        self.Z = torch.empty((self.B, self.m), dtype=f32, device=dev)
-        self.X = torch.empty((self.B, self.k), dtype=f32, device=dev)
-        self.Zq = torch.empty((self.Qb, self.m), dtype=f32, device=dev)
-        self.Y = torch.empty((self.Qb, U * self.k), dtype=f32, device=dev)
+        self.Z = torch.empty((Nt, self.m), dtype=f32, device=dev)
+        self.Xall = torch.empty((Nt, U * self.k), dtype=f32, device=dev)
+        self.Y = self.Xall[self.B:]
         g = S.torch_generator(w.config_id, 900001, dev)
         self.codes = torch.randint(0, 256, (self.N_store, U * self.kb), dtype=torch.uint8,
                                    device=dev, generator=g)
         self.scales = torch.exp(torch.randn((self.N_store, U), device=dev, generator=g)).half()
         self.scales = self.scales.view(torch.int16)
-        ws = 0
-        for p in self.plans:
-            ws = max(ws, E.eogp_rotate_retain_workspace_size(p, self.B, self.T),
-                     E.eogp_rotate_retain_workspace_size(p, self.Qb, self.T))
+        ws = max(E.eogp_rotate_retain_workspace_size(p, Nt, self.T) for p in self.plans)
         self.ws = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.pca_ws = torch.empty(E.eogp_pca_project_workspace_size(Nt, self.m, self.k, E.F16,
+                                                                    self.pca_prec),
+                                  dtype=torch.uint8, device=dev)
         self.topk = w.topk
         self.score_ws = torch.empty(
             E.eogp_score_topk_workspace_size(self.N_store, self.Qb, [self.k] * U, self.topk),
@@ -149,18 +169,15 @@ class Gpt2Step:
         slot = s % self.n_slots
         codes = self.codes[slot * self.B:(slot + 1) * self.B]
         scales = self.scales[slot * self.B:(slot + 1) * self.B]
+        k = self.k
         for u, (name, di, do) in enumerate(self.modules):
             E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
                                          Z=self.Z, prec=self.prec, ws=self.ws)
-            E.eogp_pca_project(self.Z, self.Pt[u], X=self.X, prec=self.pca_prec)
-            E.eogp_sign_pack(self.X, codes[:, u * self.kb:(u + 1) * self.kb],
+            X = self.Xall[:, u * k:(u + 1) * k]
+            E.eogp_pca_project(self.Z, self.Pt[u], X=X, prec=self.pca_prec, ws=self.pca_ws)
+            E.eogp_sign_pack(X[:self.B], codes[:, u * self.kb:(u + 1) * self.kb],
                              scales[:, u:u + 1])
-        for u, (name, di, do) in enumerate(self.modules):
-            E.eogp_rotate_retain_planned(self.plans[u], self.QA[name], self.QD[name], self.qmask,
-                                         Z=self.Zq, prec=self.prec, ws=self.ws)
-            E.eogp_pca_project(self.Zq, self.Pt[u], X=self.Y[:, u * self.k:(u + 1) * self.k],
-                               prec=self.pca_prec)
-        E.eogp_score_topk(self.codes, self.scales, [self.k] * self.U, self.Y, self.topk,
+        E.eogp_score_topk(self.codes, self.scales, [k] * self.U, self.Y, self.topk,
                           out_idx=self.out_idx, out_score=self.out_score, ws=self.score_ws)
 
     def rotation_flops_per_step(self):
@@ -309,6 +326,16 @@ def main(argv=None):
     E.load()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib << 20
+        src = torch.ones(n // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(4):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n,
+                          "launches": 4}))
+        return 0
 
     out = {}
     if not args.only_scoring:

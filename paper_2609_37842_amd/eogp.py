@@ -247,6 +247,11 @@ def eogp_rotate_retain(acts, out_grads, token_mask, Q_A, Q_S, eigvals, damping, 
 # ---------------------------------------------------------------------------
 # Second stage, encoding, scoring
 # ---------------------------------------------------------------------------
+def eogp_pca_project_workspace_size(N: int, m: int, k: int, p_dtype: int, prec: int) -> int:
+    """Bytes of workspace eogp_pca_project needs for these sizes."""
+    return int(load().eogp_pca_project_workspace_size(N, m, k, p_dtype, prec))
+
+
 def eogp_pca_project(Z, Pt, X=None, prec=PREC_FAST, ws=None, stream=None):
     """X [N, k] = Z [N, m] @ P, with P given as Pt [k, m] (each direction
     contiguous, i.e. P column-major) in float16, bfloat16 or float32."""

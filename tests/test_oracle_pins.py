@@ -310,7 +310,7 @@ def test_payload_and_storage_figures_reproduce_paper_numbers():
     models = {"olmo2-1b": olmo(2048, 8192, 16), "olmo2-7b": olmo(4096, 11008, 32),
               "olmo2-13b": olmo(5120, 13824, 40), "olmo2-32b": olmo(5120, 27648, 64, kv=1024)}
     for name, mods in models.items():
-        row = gold["table3"][name]
+        row = gold["payload_table"][name]
         kb = O.payload_bytes([2048] * len(mods)) / 1000.0
         gb = 2 * sum(di * do for di, do in mods) / 1e9
         assert round(kb, 3) == row["onebit_KB"]
