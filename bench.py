@@ -46,8 +46,9 @@ def parse(argv=None):
     ap.add_argument("--batch", type=int, default=625)
     ap.add_argument("--queries-per-step", type=int, default=8)
     ap.add_argument("--blocks", type=int, default=12)
-    ap.add_argument("--prec", choices=["accurate", "fast"], default="accurate",
-                    help="first-stage contractions (fp32 inputs need accurate for 1e-3)")
+    ap.add_argument("--prec", choices=["f16", "accurate", "fast"], default="f16",
+                    help="first-stage contractions: f16 = fp32 inputs rounded once to fp16 "
+                         "(meets 1e-3), accurate = bf16x3, fast = bf16 (does not meet 1e-3)")
     ap.add_argument("--pca-prec", choices=["accurate", "fast"], default="fast",
                     help="PCA projection with fp16 P (fast = fp16 coordinates, as the paper caches them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -81,7 +82,7 @@ class Gpt2Step:
         self.Qb = args.queries_per_step
         self.T = w.T
         self.m, self.k = w.m, w.k
-        self.prec = E.PREC_ACCURATE if args.prec == "accurate" else E.PREC_FAST
+        self.prec = {"f16": E.PREC_F16, "accurate": E.PREC_ACCURATE, "fast": E.PREC_FAST}[args.prec]
         self.pca_prec = E.PREC_ACCURATE if args.pca_prec == "accurate" else E.PREC_FAST
         self.modules = [(n, di, do) for b in range(args.blocks) for (n, di, do) in w.block]
         self.shapes = list(w.block)
@@ -362,6 +363,9 @@ def main(argv=None):
         avg_ms = rot_ms / max(1, rot_n)
         achieved = flops_launch / (avg_ms * 1e-3) / 1e12
         passes = 3 if st.prec == E.PREC_ACCURATE else 1
+        dtype = {E.PREC_F16: "fp16 (fp32 inputs rounded once to fp16, fp32 accumulation)",
+                 E.PREC_ACCURATE: "bf16x3 (fp32 inputs split into bf16 pairs, fp32 accumulation)",
+                 E.PREC_FAST: "bf16"}[st.prec]
         out.update({
             "metric": "train examples/s compressed to 1-bit codes",
             "value": value,
@@ -373,8 +377,7 @@ def main(argv=None):
             "higher_is_better": True,
             "scaling": "weak",
             "vs_baseline": None,
-            "dtype": "bf16x3 (fp32 inputs, split into bf16 pairs, fp32 accumulation)"
-                     if st.prec == E.PREC_ACCURATE else "bf16",
+            "dtype": dtype,
             "data": "synthetic",
             "config": {"workload": st.w.name, "modules": st.U, "batch_per_step": st.B,
                        "queries_per_step": st.Qb, "store": st.N_store, "T": st.T,
@@ -398,6 +401,9 @@ def main(argv=None):
             },
             "kernel_ms_per_step": {name: ms / args.steps for name, (ms, n) in kt.items()},
             "plan_ms_total": st.plan_ms,
+            "retained_axes_block0": {name: {"J": st.plans[u].n_rows, "K": st.plans[u].n_cols,
+                                            "tiles": st.plans[u].n_tiles}
+                                     for u, (name, _, _) in enumerate(st.shapes)},
         })
         log(f"step {ms_per_step:.2f} ms, {value:.1f} ex/s, rotation {achieved:.1f} TFLOP/s alg")
         if not args.no_cpu_baseline:

@@ -51,8 +51,13 @@ typedef enum { EOGP_F32 = 0, EOGP_BF16 = 1, EOGP_F16 = 2 } eogp_dtype;
  * accumulation. ACCURATE: every fp32 operand is split into a high and a low
  * 16-bit part and the cross products are accumulated in fp32 (three MFMA
  * passes when both operands are fp32, two when one is already 16-bit), which
- * carries about 16 significant bits into each product. */
-typedef enum { EOGP_PREC_FAST = 0, EOGP_PREC_ACCURATE = 1 } eogp_prec;
+ * carries about 16 significant bits into each product. F16 (first stage
+ * with fp32 inputs only): one MFMA pass on operands rounded once to fp16
+ * (11 significant bits, 8 times finer than bf16), fp32 accumulation; inputs
+ * are first multiplied by the plan's power-of-two exponents (see
+ * eogp_plan_set_input_exponents) so they sit inside fp16's normal range
+ * (2^-14 <= |x| < 65504). */
+typedef enum { EOGP_PREC_FAST = 0, EOGP_PREC_ACCURATE = 1, EOGP_PREC_F16 = 2 } eogp_prec;
 
 /* ------------------------------------------------------------------------
  * Fitting shared projections: retained-axis selection (Algorithm 1, first
@@ -100,6 +105,15 @@ eogp_status eogp_plan_get_info(const eogp_plan* plan, eogp_plan_info* info);
  * may be NULL. Enqueued on `stream`. */
 eogp_status eogp_plan_copy_retained(const eogp_plan* plan, int32_t* flat_out,
                                     float* weight_out, void* stream);
+/* Power-of-two input scaling of the plan's EOGP_PREC_F16 first stage:
+ * activations are multiplied by 2^e_acts and output-gradients by 2^e_grads
+ * before they are rounded to fp16, and every coordinate by
+ * 2^-(e_acts + e_grads) afterwards. The first stage is bilinear in (a, ds),
+ * so the result is unchanged up to fp16 rounding; the exponents only move
+ * the inputs into fp16's range (e.g. e_grads = 10 for gradients of order
+ * 1e-5). Both default to 0. Errors: EOGP_ERR_INVALID for a NULL plan or an
+ * exponent outside [-60, 60]. Host-only; affects later calls. */
+eogp_status eogp_plan_set_input_exponents(eogp_plan* plan, int32_t e_acts, int32_t e_grads);
 
 /* ------------------------------------------------------------------------
  * First stage (eq. first_stage; eq. app_projection_maps; Algorithm 1,
@@ -121,8 +135,12 @@ eogp_status eogp_plan_copy_retained(const eogp_plan* plan, int32_t* flat_out,
  *   token_mask [N, T] uint8, or NULL for all tokens valid. Masked tokens are
  *              never read and may hold anything, NaN included.
  *   Z          [N, ldz] fp32, ldz >= m; columns m..ldz-1 are not written.
- *   prec       EOGP_PREC_ACCURATE keeps about 16 bits per product (use for
- *              fp32 inputs); EOGP_PREC_FAST rounds operands to bf16.
+ *   prec       EOGP_PREC_ACCURATE keeps about 16 bits per product;
+ *              EOGP_PREC_F16 (fp32 inputs only) rounds inputs and bases once to
+ *              fp16 (relative error of a row of Z about 4e-4 for inputs inside
+ *              fp16's normal range); EOGP_PREC_FAST rounds operands to bf16
+ *              (about 3e-3 for fp32 inputs; the natural mode for bf16 inputs).
+ *              EOGP_ERR_UNSUPPORTED for EOGP_PREC_F16 with bf16 inputs.
  *   ws         workspace of at least eogp_rotate_retain_workspace_size bytes.
  * ------------------------------------------------------------------------ */
 size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64_t T);

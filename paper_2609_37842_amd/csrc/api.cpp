@@ -14,7 +14,7 @@ size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T);
 eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
                           int64_t ld_grads, bool bf16_in,
                           const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
-                          bool accurate, void* ws, size_t ws_bytes, hipStream_t s);
+                          int prec, void* ws, size_t ws_bytes, hipStream_t s);
 eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t* codes,
                       int64_t cstride, uint16_t* scales, int64_t sstride, hipStream_t s);
 size_t pca_ws(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype);
@@ -68,7 +68,8 @@ eogp_status check_plan_args(const float* eigvals, int64_t d_out, int64_t d_in, d
 }
 
 eogp_status check_first_stage(const eogp_plan* p, const void* acts, const void* grads,
-                              eogp_dtype dt, int64_t N, int64_t T, const float* Z, int64_t ldz) {
+                              eogp_dtype dt, int64_t N, int64_t T, const float* Z, int64_t ldz,
+                              eogp_prec prec) {
   if (!p) return fail(EOGP_ERR_INVALID, "rotate_retain: NULL plan");
   if (N < 0 || T < 0) return fail(EOGP_ERR_INVALID, "rotate_retain: negative size");
   if (N > 0 && T > 0 && (!acts || !grads || !Z)) return fail(EOGP_ERR_INVALID, "rotate_retain: NULL pointer");
@@ -76,6 +77,10 @@ eogp_status check_first_stage(const eogp_plan* p, const void* acts, const void* 
   if (dt != EOGP_F32 && dt != EOGP_BF16)
     return fail(EOGP_ERR_UNSUPPORTED, "rotate_retain: inputs must be fp32 or bf16");
   if (ldz < p->m) return fail(EOGP_ERR_INVALID, "rotate_retain: ldz < m");
+  if (prec != EOGP_PREC_FAST && prec != EOGP_PREC_ACCURATE && prec != EOGP_PREC_F16)
+    return fail(EOGP_ERR_INVALID, "rotate_retain: unknown precision mode");
+  if (prec == EOGP_PREC_F16 && dt != EOGP_F32)
+    return fail(EOGP_ERR_UNSUPPORTED, "rotate_retain: the fp16 mode takes fp32 inputs");
   if (N * T >= kMaxFlat) return fail(EOGP_ERR_INVALID, "rotate_retain: N*T must be < 2^31");
   return EOGP_OK;
 }
@@ -134,6 +139,15 @@ eogp_status eogp_plan_copy_retained(const eogp_plan* p, int32_t* flat_out, float
   return EOGP_OK;
 }
 
+eogp_status eogp_plan_set_input_exponents(eogp_plan* p, int32_t e_acts, int32_t e_grads) {
+  if (!p) return fail(EOGP_ERR_INVALID, "plan_set_input_exponents: NULL plan");
+  if (e_acts < -60 || e_acts > 60 || e_grads < -60 || e_grads > 60)
+    return fail(EOGP_ERR_INVALID, "plan_set_input_exponents: exponents must lie in [-60, 60]");
+  p->e_acts = e_acts;
+  p->e_grads = e_grads;
+  return EOGP_OK;
+}
+
 size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64_t T) {
   if (!plan || N < 0 || T < 0) return 0;
   return rotate_retain_ws(plan, N, T);
@@ -144,7 +158,7 @@ eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
                                        eogp_dtype in_dtype, const uint8_t* token_mask, int64_t N,
                                        int64_t T, float* Z, int64_t ldz, eogp_prec prec, void* ws,
                                        size_t ws_bytes, void* stream) {
-  eogp_status st = check_first_stage(plan, acts, out_grads, in_dtype, N, T, Z, ldz);
+  eogp_status st = check_first_stage(plan, acts, out_grads, in_dtype, N, T, Z, ldz, prec);
   if (st != EOGP_OK) return st;
   if (ld_acts == 0) ld_acts = plan->d_in;
   if (ld_grads == 0) ld_grads = plan->d_out;
@@ -163,8 +177,7 @@ eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
   if (hipGetDevice(&dev) == hipSuccess && dev != plan->device)
     return fail(EOGP_ERR_INVALID, "rotate_retain: plan belongs to another device");
   return rotate_retain(plan, acts, ld_acts, out_grads, ld_grads, in_dtype == EOGP_BF16,
-                       token_mask, N, T, Z, ldz, prec == EOGP_PREC_ACCURATE, ws, ws_bytes,
-                       S(stream));
+                       token_mask, N, T, Z, ldz, (int)prec, ws, ws_bytes, S(stream));
 }
 
 size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d_in,
@@ -211,6 +224,8 @@ eogp_status eogp_pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, 
                              eogp_prec prec, void* ws, size_t ws_bytes, void* stream) {
   if (N < 0 || m < 1 || k < 1) return fail(EOGP_ERR_INVALID, "pca_project: bad sizes");
   if (k > m) return fail(EOGP_ERR_INVALID, "pca_project: need k <= m");
+  if (prec != EOGP_PREC_FAST && prec != EOGP_PREC_ACCURATE)
+    return fail(EOGP_ERR_INVALID, "pca_project: precision must be FAST or ACCURATE");
   if (N > 0 && (!Z || !P || !X)) return fail(EOGP_ERR_INVALID, "pca_project: NULL pointer");
   if (ldz < m || ldp < m || ldx < k) return fail(EOGP_ERR_INVALID, "pca_project: leading dimension too small");
   if (p_dtype != EOGP_F32 && p_dtype != EOGP_BF16 && p_dtype != EOGP_F16)

@@ -15,6 +15,8 @@ struct GemmArgs {
   const void* A = nullptr;
   int64_t lda = 0;
   const int32_t* a_rows = nullptr;
+  // fp16 operands only: fp32 A is multiplied by a_scale before rounding.
+  float a_scale = 1.f;
   // B: [N][ldb] 16-bit; B_lo (optional) is the low part of a split operand.
   const uint16_t* B_hi = nullptr;
   const uint16_t* B_lo = nullptr;

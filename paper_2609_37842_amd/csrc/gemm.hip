@@ -144,6 +144,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
   }
 
   const int wm = (wid >> 1) * 128, wn = (wid & 1) * (BN / 2);
+  const float a_scale = g.a_scale;
   // Staging maps consecutive lanes to consecutive 16-byte pieces of one row, so
   // a wave-wide 16-byte load covers whole cache lines:
   //   fp32 A:   8 lanes per row (128 bytes), rows (tid >> 3) + 32 q, q = 0..7;
@@ -297,7 +298,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
           for (int q = 0; q < AQ; ++q) {
             const int r = a_r0 + a_rs * q;
             const int o = swz(r, a_pc >> 1) + 4 * (a_pc & 1);
-            const v4f x = ra[q];
+            v4f x = ra[q];
+            if constexpr (F16) x *= a_scale;
             const uint32_t h0 = cvt_pair<F16>(x.x, x.y), h1 = cvt_pair<F16>(x.z, x.w);
             typedef unsigned int v2u __attribute__((ext_vector_type(2)));
             v2u hv;
@@ -317,7 +319,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
           for (int e = 0; e < 32; ++e) {
             const int r = sr + 8 * e;
             const int o = swz(r, sc >> 3) + (sc & 7);
-            const float x = re[e];
+            const float x = F16 ? re[e] * a_scale : re[e];
             const uint16_t h = cvt16<F16>(x);
             sA[st][0][o] = h;
             if constexpr (AP == 2) sA[st][AP - 1][o] = cvt16<F16>(x - back16<F16>(h));

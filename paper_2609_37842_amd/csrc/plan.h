@@ -25,6 +25,12 @@ struct eogp_plan {
   uint16_t* qs_lo = nullptr;     // [rows_pad][ld_out] bf16: low part
   uint16_t* qa_hi = nullptr;     // [cols_pad][ld_in]  bf16: Q_A[:, K[p]] high part
   uint16_t* qa_lo = nullptr;     // [cols_pad][ld_in]
+  uint16_t* qs_f16 = nullptr;    // [rows_pad][ld_out] fp16: Q_S[:, J[p]] rounded once
+  uint16_t* qa_f16 = nullptr;    // [cols_pad][ld_in]  fp16: Q_A[:, K[p]] rounded once
+
+  // fp16 mode: inputs are multiplied by 2^e before rounding to fp16, and the
+  // coordinates by 2^-(e_acts + e_grads) (exact while nothing overflows).
+  int32_t e_acts = 0, e_grads = 0;
 };
 
 namespace eogp {

@@ -12,6 +12,7 @@
 //    retained entries are scaled by w_r and written to their canonical
 //    positions in Z.
 #include <algorithm>
+#include <cmath>
 
 #include "gemm.h"
 #include "plan.h"
@@ -61,6 +62,7 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
                                                   const int32_t* __restrict__ ent_r,
                                                   const uint16_t* __restrict__ ent_loc,
                                                   const float* __restrict__ w,
+                                                  float out_scale,
                                                   float* __restrict__ Z, int64_t ldz,
                                                   int64_t ex0) {
   __shared__ __attribute__((aligned(16))) float sS[32][36];
@@ -104,7 +106,7 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
   for (int e = e0 + tid; e < e1; e += 256) {
     const int r = ent_r[e];
     const int loc = ent_loc[e];
-    Z[i * ldz + r] = w[r] * blk[loc >> 5][loc & 31];
+    Z[i * ldz + r] = w[r] * (out_scale * blk[loc >> 5][loc & 31]);
   }
 }
 
@@ -131,7 +133,7 @@ size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T) { return work_
 eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
                           int64_t ld_grads, bool bf16_in,
                           const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
-                          bool accurate, void* ws, size_t ws_bytes, hipStream_t s) {
+                          int prec, void* ws, size_t ws_bytes, hipStream_t s) {
   if (ws_bytes < work_bytes(p, N, T)) return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
   Carve cv(ws, ws_bytes);
   Work w;
@@ -151,6 +153,10 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   EOGP_LAUNCH_CHECK("token compaction");
 
   // 2. rotations onto the used eigenvectors (rows = valid tokens; count on device)
+  // FAST: bf16 operands; ACCURATE: bf16 high+low splits (three products);
+  // F16: fp32 inputs scaled by 2^e and rounded once to fp16, fp16 bases.
+  const bool accurate = prec == EOGP_PREC_ACCURATE;
+  const bool f16 = prec == EOGP_PREC_F16;
   const AType at = bf16_in ? AType::B16 : AType::F32;
   const int a_parts = (accurate && !bf16_in) ? 2 : 1;
   const int b_parts = accurate ? 2 : 1;
@@ -158,7 +164,8 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   gs.A = grads;
   gs.lda = ld_grads;
   gs.a_rows = w.tok;
-  gs.B_hi = p->qs_hi;
+  gs.a_scale = f16 ? std::ldexp(1.f, p->e_grads) : 1.f;
+  gs.B_hi = f16 ? p->qs_f16 : p->qs_hi;
   gs.B_lo = p->qs_lo;
   gs.ldb = p->ld_out;
   gs.b_padded = true;
@@ -170,28 +177,30 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   // block outputs that no retained axis reads.
   gs.N = p->n_rows;
   gs.K = p->d_out;
-  eogp_status st = gemm_nt(gs, at, a_parts, b_parts, false, s);
+  eogp_status st = gemm_nt(gs, at, a_parts, b_parts, f16, s);
   if (st != EOGP_OK) return st;
   GemmArgs ga = gs;
   ga.A = acts;
   ga.lda = ld_acts;
-  ga.B_hi = p->qa_hi;
+  ga.a_scale = f16 ? std::ldexp(1.f, p->e_acts) : 1.f;
+  ga.B_hi = f16 ? p->qa_f16 : p->qa_hi;
   ga.B_lo = p->qa_lo;
   ga.ldb = p->ld_in;
   ga.C = w.At;
   ga.ldc = p->cols_pad;
   ga.N = p->n_cols;
   ga.K = p->d_in;
-  st = gemm_nt(ga, at, a_parts, b_parts, false, s);
+  st = gemm_nt(ga, at, a_parts, b_parts, f16, s);
   if (st != EOGP_OK) return st;
 
   // 3. retained products, half-whitened, in canonical order
+  const float out_scale = f16 ? std::ldexp(1.f, -(p->e_acts + p->e_grads)) : 1.f;
   for (int64_t ex0 = 0; p->n_tiles > 0 && ex0 < N; ex0 += 65535) {
     const int64_t nex = std::min<int64_t>(65535, N - ex0);
     timing::Scope ts(EOGP_KT_RETAINED, s);
     hipLaunchKernelGGL(k_retained, dim3((unsigned)p->n_tiles, (unsigned)nex), dim3(256), 0, s,
                        w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, p->ent_r,
-                       p->ent_loc, p->ret_w, Z, ldz, ex0);
+                       p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
     EOGP_LAUNCH_CHECK("retained products");
   }
   return EOGP_OK;

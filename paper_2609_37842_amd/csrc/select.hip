@@ -286,12 +286,14 @@ __global__ void k_tile_desc(const int* tcount, int64_t nt, int n_kt, const long 
 }
 
 // panel[p][c] = Q[c][list[p]] (eigenvector list[p] stored contiguously),
-// split into bf16 high and low parts; rows >= n_used and columns >= d are 0.
+// split into bf16 high and low parts, and rounded once to fp16; rows >= n_used
+// and columns >= d are 0.
 __global__ __launch_bounds__(256) void k_gather_panel(const float* __restrict__ Q, int64_t d,
                                                       const int* __restrict__ list, int n_used,
                                                       int64_t rows_pad, int64_t ld,
                                                       uint16_t* __restrict__ hi,
-                                                      uint16_t* __restrict__ lo) {
+                                                      uint16_t* __restrict__ lo,
+                                                      uint16_t* __restrict__ h16) {
   __shared__ float t[32][33];
   const int64_t p0 = (int64_t)blockIdx.x * 32, c0 = (int64_t)blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
@@ -309,6 +311,7 @@ __global__ __launch_bounds__(256) void k_gather_panel(const float* __restrict__ 
       uint16_t h = to_bf16_bits(v);
       hi[p * ld + c] = h;
       lo[p * ld + c] = to_bf16_bits(v - bf16_bits_to_f32(h));
+      h16[p * ld + c] = to_f16_bits(v);
     }
   }
 }
@@ -420,6 +423,7 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   size_t q_er = padd(m * 4), q_el = padd(m * 2);
   size_t q_sh = padd(p->rows_pad * p->ld_out * 2), q_sl = padd(p->rows_pad * p->ld_out * 2);
   size_t q_ah = padd(p->cols_pad * p->ld_in * 2), q_al = padd(p->cols_pad * p->ld_in * 2);
+  size_t q_s16 = padd(p->rows_pad * p->ld_out * 2), q_a16 = padd(p->cols_pad * p->ld_in * 2);
   hipError_t e = hipMalloc(&p->mem, pb);
   if (e != hipSuccess) {
     delete p;
@@ -435,6 +439,8 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   p->qs_lo = (uint16_t*)(base + q_sl);
   p->qa_hi = (uint16_t*)(base + q_ah);
   p->qa_lo = (uint16_t*)(base + q_al);
+  p->qs_f16 = (uint16_t*)(base + q_s16);
+  p->qa_f16 = (uint16_t*)(base + q_a16);
 
   if (hipMemcpyAsync(p->ret_flat, ret, m * 4, hipMemcpyDeviceToDevice, s) != hipSuccess ||
       hipMemcpyAsync(p->ret_w, w, m * 4, hipMemcpyDeviceToDevice, s) != hipSuccess) {
@@ -447,10 +453,10 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
                      flag, p->tiles);
   hipLaunchKernelGGL(k_gather_panel, dim3((unsigned)(p->rows_pad / 32), grid_for(p->ld_out, 32)),
                      dim3(256), 0, s, Q_S, d_out, jl, (int)p->n_rows, p->rows_pad, p->ld_out,
-                     p->qs_hi, p->qs_lo);
+                     p->qs_hi, p->qs_lo, p->qs_f16);
   hipLaunchKernelGGL(k_gather_panel, dim3((unsigned)(p->cols_pad / 32), grid_for(p->ld_in, 32)),
                      dim3(256), 0, s, Q_A, d_in, kl, (int)p->n_cols, p->cols_pad, p->ld_in,
-                     p->qa_hi, p->qa_lo);
+                     p->qa_hi, p->qa_lo, p->qa_f16);
   e = hipGetLastError();
   if (e == hipSuccess) e = hipStreamSynchronize(s);
   if (e != hipSuccess) {

@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libeogp.so")
 
 F32, BF16, F16 = 0, 1, 2
-PREC_FAST, PREC_ACCURATE = 0, 1
+PREC_FAST, PREC_ACCURATE, PREC_F16 = 0, 1, 2
 
 _DTYPE_CODE = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
 
@@ -42,6 +42,7 @@ _lib = None
 
 EXPORTED = (
     "eogp_plan_create", "eogp_plan_destroy", "eogp_plan_get_info", "eogp_plan_copy_retained",
+    "eogp_plan_set_input_exponents",
     "eogp_rotate_retain_workspace_size", "eogp_rotate_retain_planned",
     "eogp_rotate_retain_oneshot_workspace_size", "eogp_rotate_retain",
     "eogp_pca_project_workspace_size", "eogp_pca_project",
@@ -68,6 +69,7 @@ def load(path: str | None = None):
         "eogp_plan_destroy": (None, [c_vp]),
         "eogp_plan_get_info": (c_i32, [c_vp, ctypes.POINTER(PlanInfo)]),
         "eogp_plan_copy_retained": (c_i32, [c_vp, c_vp, c_vp, c_vp]),
+        "eogp_plan_set_input_exponents": (c_i32, [c_vp, c_i32, c_i32]),
         "eogp_rotate_retain_workspace_size": (c_sz, [c_vp, c_i64, c_i64]),
         "eogp_rotate_retain_planned": (c_i32, [c_vp, c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64,
                                                c_i64, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
@@ -177,6 +179,11 @@ class eogp_plan:
 
 def eogp_plan_create(eigvals, damping, m, Q_A, Q_S, stream=None) -> eogp_plan:
     return eogp_plan(eigvals, damping, m, Q_A, Q_S, stream)
+
+
+def eogp_plan_set_input_exponents(plan: eogp_plan, e_acts: int, e_grads: int) -> None:
+    """Power-of-two input scaling of the plan's fp16 first stage (see eogp.h)."""
+    _check(load().eogp_plan_set_input_exponents(plan._h, int(e_acts), int(e_grads)))
 
 
 # ---------------------------------------------------------------------------

@@ -49,6 +49,7 @@ def test_plan_argument_validation_without_device():
     assert L.eogp_plan_create(fake, 4, 4, float("nan"), 3, fake, fake, None, ctypes.byref(h)) == -1
     assert L.eogp_plan_create(fake, 0, 4, 0.1, 3, fake, fake, None, ctypes.byref(h)) == -1
     assert L.eogp_plan_create(fake, 1 << 16, 1 << 16, 0.1, 3, fake, fake, None, ctypes.byref(h)) == -1
+    assert L.eogp_plan_set_input_exponents(None, 0, 0) == -1
 
 
 def test_encode_and_score_argument_validation_without_device():

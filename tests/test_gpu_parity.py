@@ -309,6 +309,60 @@ def test_rotate_retain_strided_token_rows(dtype):
     plan.close()
 
 
+@pytest.mark.parametrize("shape", [
+    # N, T, d_in, d_out, m, lens_lo
+    (4, 288, 769, 768, 16384, 64),     # GPT-2 attn.c_proj-like widths and m
+    (3, 100, 97, 130, 1000, 0),        # ragged, odd widths, an empty example
+])
+def test_rotate_retain_fp16_mode(shape):
+    """fp32 inputs and bases rounded once to fp16, one MFMA pass: rows of Z
+    within 1e-3 relative of the fp64 oracle."""
+    N, T, d_in, d_out, m, lo = shape
+    say(f"[first stage] fp16 mode {shape}")
+    a, ds, mask, QA, QS, lam = random_problem(sum(shape) + 1, N, T, d_in, d_out, m, lens_lo=lo)
+    if lo == 0:
+        mask[0, :] = 0
+    plan = E.eogp_plan_create(d(lam), 1e-4, m, d(QA), d(QS))
+    Z = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask), prec=E.PREC_F16)
+    torch.cuda.synchronize()
+    ref, _ = oracle_Z(a, ds, mask, QA, QS, lam, 1e-4, m)
+    Zg = Z.cpu().numpy()
+    nz = np.linalg.norm(ref, axis=1) > 0
+    err = rel_rows(Zg[nz], ref[nz])
+    say(f"   max rel {err.max():.2e}")
+    assert err.max() <= 1e-3
+    assert np.all(Zg[~nz] == 0)
+    plan.close()
+
+
+def test_rotate_retain_fp16_mode_input_exponents():
+    """Gradients of order 1e-7 (below fp16's normal range) are brought into
+    range by the plan's exponent; the result is then as accurate as for
+    ordinary magnitudes, and scaled back exactly."""
+    N, T, d_in, d_out, m = 3, 64, 128, 96, 2000
+    say("[first stage] fp16 mode exponents")
+    a, ds, mask, QA, QS, lam = random_problem(21, N, T, d_in, d_out, m, lens_lo=16)
+    ds = (ds * 1e-5).astype(np.float32)
+    lam = (lam * 1e-10).astype(np.float32)
+    ref, _ = oracle_Z(a, ds, mask, QA, QS, lam, 1e-14, m)
+    plan = E.eogp_plan_create(d(lam), 1e-14, m, d(QA), d(QS))
+    Z0 = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask), prec=E.PREC_F16)
+    E.eogp_plan_set_input_exponents(plan, -2, 20)
+    Z1 = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask), prec=E.PREC_F16)
+    torch.cuda.synchronize()
+    e0 = rel_rows(Z0.cpu().numpy(), ref).max()
+    e1 = rel_rows(Z1.cpu().numpy(), ref).max()
+    say(f"   without exponents {e0:.2e}, with {e1:.2e}")
+    assert e1 <= 1e-3
+    assert e0 > 3 * e1
+    with pytest.raises(E.EogpError):
+        E.eogp_plan_set_input_exponents(plan, 61, 0)
+    with pytest.raises(E.EogpError):
+        E.eogp_rotate_retain_planned(plan, d(a, torch.bfloat16), d(ds, torch.bfloat16), d(mask),
+                                     prec=E.PREC_F16)
+    plan.close()
+
+
 def test_rotate_retain_deterministic():
     N, T, d_in, d_out, m = 4, 64, 128, 96, 500
     a, ds, mask, QA, QS, lam = random_problem(13, N, T, d_in, d_out, m, lens_lo=10)
