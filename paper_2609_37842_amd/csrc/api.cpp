@@ -240,6 +240,7 @@ eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, ui
                            int64_t code_row_stride, uint16_t* scales, int64_t scale_stride,
                            void* stream) {
   if (N < 0 || k < 1) return fail(EOGP_ERR_INVALID, "sign_pack: bad sizes");
+  if (N >= kMaxFlat) return fail(EOGP_ERR_INVALID, "sign_pack: N must be < 2^31");
   if (N > 0 && (!X || !codes || !scales)) return fail(EOGP_ERR_INVALID, "sign_pack: NULL pointer");
   if (ldx < k) return fail(EOGP_ERR_INVALID, "sign_pack: ldx < k");
   if (code_row_stride < (k + 7) / 8) return fail(EOGP_ERR_INVALID, "sign_pack: code row stride too small");

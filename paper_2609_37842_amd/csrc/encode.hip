@@ -7,36 +7,54 @@
 namespace eogp {
 namespace {
 
-// One wave per row: a ballot of (x >= 0) over 64 consecutive coordinates is
-// exactly 8 bytes of the least-significant-bit-first code; |x| is summed in
-// fp64 (per lane in coordinate order, then a fixed butterfly) and the mean is
+// One workgroup (4 waves) per row. A ballot of (x >= 0) over 64 consecutive
+// coordinates is exactly 8 bytes of the least-significant-bit-first code;
+// wave w takes the 64-coordinate chunks w, w + 4, ..., eight at a time so
+// that eight loads are in flight per lane. |x| is summed in fp64 (per lane,
+// then a fixed butterfly, then the four waves in order) and the mean is
 // rounded once to fp16.
+constexpr int kPackUnroll = 8;
+
 __global__ __launch_bounds__(256) void k_sign_pack(const float* __restrict__ X, int64_t ldx,
                                                    int64_t N, int64_t k,
                                                    uint8_t* __restrict__ codes, int64_t cstride,
                                                    uint16_t* __restrict__ scales,
                                                    int64_t sstride, int word_store) {
-  const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (i >= N) return;
+  __shared__ double part[4];
+  const int64_t i = blockIdx.x;
+  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const float* x = X + i * ldx;
   uint8_t* c = codes + i * cstride;
+  const int64_t nchunk = (k + 63) >> 6;
   double acc = 0.0;
-  for (int64_t c0 = 0; c0 < k; c0 += 64) {
-    const int64_t cc = c0 + lane;
-    const bool in = cc < k;
-    const float v = in ? x[cc] : 0.f;
-    const uint64_t word = __ballot(in && v >= 0.f);
-    if (in) acc += fabs((double)v);
-    const int64_t nbytes = std::min<int64_t>(8, (k - c0 + 7) >> 3);
-    if (word_store && nbytes == 8) {
-      if (lane == 0) *reinterpret_cast<uint64_t*>(c + (c0 >> 3)) = word;
-    } else if (lane < nbytes) {
-      c[(c0 >> 3) + lane] = (uint8_t)(word >> (8 * lane));
+  for (int64_t ch0 = wid; ch0 < nchunk; ch0 += 4 * kPackUnroll) {
+    float v[kPackUnroll];
+#pragma unroll
+    for (int u = 0; u < kPackUnroll; ++u) {
+      const int64_t cc = (ch0 + 4 * u) * 64 + lane;
+      v[u] = cc < k ? x[cc] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < kPackUnroll; ++u) {
+      const int64_t ch = ch0 + 4 * u;
+      if (ch >= nchunk) break;                     // uniform across the wave
+      const int64_t c0 = ch * 64;
+      const bool in = c0 + lane < k;
+      const uint64_t word = __ballot(in && v[u] >= 0.f);
+      acc += fabs((double)v[u]);                   // 0 beyond k
+      const int64_t nbytes = std::min<int64_t>(8, (k - c0 + 7) >> 3);
+      if (word_store && nbytes == 8) {
+        if (lane == 0) *reinterpret_cast<uint64_t*>(c + (c0 >> 3)) = word;
+      } else if (lane < nbytes) {
+        c[(c0 >> 3) + lane] = (uint8_t)(word >> (8 * lane));
+      }
     }
   }
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (lane == 0) scales[i * sstride] = f64_to_f16_rne(acc / (double)k);
+  if (lane == 0) part[wid] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    scales[i * sstride] = f64_to_f16_rne(((part[0] + part[1]) + (part[2] + part[3])) / (double)k);
 }
 
 // fp32 P (column-major, [k][ldp]) -> bf16 high and low parts [k][ldo].
@@ -57,7 +75,7 @@ eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t
   if (N == 0) return EOGP_OK;
   const int word_store = ((uintptr_t)codes % 8 == 0) && (cstride % 8 == 0);
   timing::Scope ts(EOGP_KT_SIGN_PACK, s);
-  hipLaunchKernelGGL(k_sign_pack, dim3((unsigned)ceil_div(N, 4)), dim3(256), 0, s, X, ldx, N, k,
+  hipLaunchKernelGGL(k_sign_pack, dim3((unsigned)N), dim3(256), 0, s, X, ldx, N, k,
                      codes, cstride, scales, sstride, word_store);
   EOGP_LAUNCH_CHECK("sign_pack");
   return EOGP_OK;

@@ -8,9 +8,9 @@
 //    columns the retained axes use: S~ = DS_valid Q_S[:, J], A~ = A_valid Q_A[:, K].
 // 3. Retained products: for every example and every 32 x 32 block of
 //    (row, column) pairs that holds retained axes, the block of sums
-//    sum_t S~[t, j] A~[t, k] over the example's tokens is formed and the
-//    retained entries are scaled by w_r and written to their canonical
-//    positions in Z.
+//    sum_t S~[t, j] A~[t, k] over the example's tokens is formed (fp32 MFMA)
+//    and the retained entries are scaled by w_r and written to their
+//    canonical positions in Z.
 #include <algorithm>
 #include <cmath>
 
@@ -52,61 +52,64 @@ __global__ __launch_bounds__(256) void k_write_tokens(const uint8_t* __restrict_
 }
 
 // ---- retained products --------------------------------------------------------
-// One workgroup per (active block, example). Thread (ty, tx) of a 16 x 16 grid
-// owns the 2 x 2 outputs (2ty..2ty+1, 2tx..2tx+1) of the 32 x 32 block.
-// Tokens are staged through LDS 32 at a time and summed in token order.
+// One wave per (active block, example); the four waves of a workgroup take
+// four consecutive blocks of one example (blocks are listed row block first,
+// so they mostly share the S~ columns they read). The block of sums
+//   C[jj][kk] = sum_t S~[t, 32 jb + jj] * A~[t, 32 kb + kk]
+// is one 32 x 32 fp32 MFMA accumulation over the example's tokens, two tokens
+// per v_mfma_f32_32x32x2_f32 (lane l feeds row l % 32 of token l / 32 of each
+// operand straight from memory). Products are exact fp32 products, so the
+// result matches an fp32 dot product up to the order of the additions.
+constexpr int kRetWaves = 4;
+constexpr int kRetUnroll = 8;      // MFMAs (token pairs) per loaded group
+
 __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, int64_t ldS,
                                                   const float* __restrict__ At, int64_t ldA,
                                                   const int32_t* __restrict__ ex_off,
-                                                  const int32_t* __restrict__ tiles,
+                                                  const int32_t* __restrict__ tiles, int n_tiles,
                                                   const int32_t* __restrict__ ent_r,
                                                   const uint16_t* __restrict__ ent_loc,
                                                   const float* __restrict__ w,
                                                   float out_scale,
                                                   float* __restrict__ Z, int64_t ldz,
                                                   int64_t ex0) {
-  __shared__ __attribute__((aligned(16))) float sS[32][36];
-  __shared__ __attribute__((aligned(16))) float sA[32][36];
-  __shared__ float blk[32][33];
-  const int tile = blockIdx.x;
+  __shared__ float blk[kRetWaves][32][33];
+  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tile = blockIdx.x * kRetWaves + wid;
+  if (tile >= n_tiles) return;                 // whole wave leaves; no block barrier below
   const int64_t i = ex0 + blockIdx.y;
-  const int jt = tiles[4 * tile + 0], kt = tiles[4 * tile + 1];
+  const int jb = tiles[4 * tile + 0], kb = tiles[4 * tile + 1];
   const int e0 = tiles[4 * tile + 2], e1 = tiles[4 * tile + 3];
   const int64_t t0 = ex_off[i], t1 = ex_off[i + 1];
-  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
-  const int lr = tid >> 3, lc = (tid & 7) * 4;   // staging: token row, 4 columns
+  const int half = lane >> 5, col = lane & 31;
+  const float* sp = St + (int64_t)jb * 32 + col;
+  const float* ap = At + (int64_t)kb * 32 + col;
 
-  float c00 = 0.f, c01 = 0.f, c10 = 0.f, c11 = 0.f;
-  for (int64_t tb = t0; tb < t1; tb += 32) {
-    const int64_t t = tb + lr;
-    float4 vs = make_float4(0.f, 0.f, 0.f, 0.f), va = vs;
-    if (t < t1) {
-      vs = *reinterpret_cast<const float4*>(St + t * ldS + (int64_t)jt * 32 + lc);
-      va = *reinterpret_cast<const float4*>(At + t * ldA + (int64_t)kt * 32 + lc);
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  for (int64_t tb = t0; tb < t1; tb += 2 * kRetUnroll) {
+    float sv[kRetUnroll], av[kRetUnroll];
+#pragma unroll
+    for (int u = 0; u < kRetUnroll; ++u) {
+      const int64_t t = tb + 2 * u + half;
+      const bool ok = t < t1;
+      sv[u] = ok ? sp[t * ldS] : 0.f;
+      av[u] = ok ? ap[t * ldA] : 0.f;
     }
-    *reinterpret_cast<float4*>(&sS[lr][lc]) = vs;
-    *reinterpret_cast<float4*>(&sA[lr][lc]) = va;
-    __syncthreads();
-    const int nt = (int)std::min<int64_t>(32, t1 - tb);
-    for (int u = 0; u < nt; ++u) {
-      const float2 s2 = *reinterpret_cast<const float2*>(&sS[u][2 * ty]);
-      const float2 a2 = *reinterpret_cast<const float2*>(&sA[u][2 * tx]);
-      c00 = fmaf(s2.x, a2.x, c00);
-      c01 = fmaf(s2.x, a2.y, c01);
-      c10 = fmaf(s2.y, a2.x, c10);
-      c11 = fmaf(s2.y, a2.y, c11);
-    }
-    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kRetUnroll; ++u)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(sv[u], av[u], acc, 0, 0, 0);
   }
-  blk[2 * ty][2 * tx] = c00;
-  blk[2 * ty][2 * tx + 1] = c01;
-  blk[2 * ty + 1][2 * tx] = c10;
-  blk[2 * ty + 1][2 * tx + 1] = c11;
-  __syncthreads();
-  for (int e = e0 + tid; e < e1; e += 256) {
+  // acc[r] holds C[8 (r / 4) + 4 half + r % 4][col]
+#pragma unroll
+  for (int r = 0; r < 16; ++r) blk[wid][8 * (r >> 2) + 4 * half + (r & 3)][col] = acc[r];
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  for (int e = e0 + lane; e < e1; e += 64) {
     const int r = ent_r[e];
     const int loc = ent_loc[e];
-    Z[i * ldz + r] = w[r] * (out_scale * blk[loc >> 5][loc & 31]);
+    Z[i * ldz + r] = w[r] * (out_scale * blk[wid][loc >> 5][loc & 31]);
   }
 }
 
@@ -198,9 +201,10 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   for (int64_t ex0 = 0; p->n_tiles > 0 && ex0 < N; ex0 += 65535) {
     const int64_t nex = std::min<int64_t>(65535, N - ex0);
     timing::Scope ts(EOGP_KT_RETAINED, s);
-    hipLaunchKernelGGL(k_retained, dim3((unsigned)p->n_tiles, (unsigned)nex), dim3(256), 0, s,
-                       w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, p->ent_r,
-                       p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
+    const unsigned gx = (unsigned)ceil_div(p->n_tiles, (int64_t)kRetWaves);
+    hipLaunchKernelGGL(k_retained, dim3(gx, (unsigned)nex), dim3(256), 0, s,
+                       w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,
+                       p->ent_r, p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
     EOGP_LAUNCH_CHECK("retained products");
   }
   return EOGP_OK;
