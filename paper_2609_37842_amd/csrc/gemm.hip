@@ -199,34 +199,45 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
       return kbeg + s * BK;
     };
 
-    v4f ra[AT == 0 && AV ? AQ : 1];       // fp32 A staging (16-byte path)
-    float re[AT == 0 && !AV ? 32 : 1];    // fp32 A staging (element path)
-    v4u ra16[AT == 0 ? 1 : AQ];           // 16-bit A staging
-    v4u rb[BP][BQ];
+    // Register staging of one slice: A rows (from HBM) and B panel rows (small,
+    // L2-resident). On the 16-byte paths A is kept in two buffers, so each A
+    // slice is requested two slices before it is staged; B one slice before.
+    struct ARegs {
+      v4f ra[AT == 0 && AV ? AQ : 1];       // fp32 A (16-byte path)
+      float re[AT == 0 && !AV ? 32 : 1];    // fp32 A (element path)
+      v4u ra16[AT == 0 ? 1 : AQ];           // 16-bit A
+    };
+    struct BRegs {
+      v4u rb[BP][BQ];
+    };
+    ARegs A0, A1;
+    BRegs RB;
 
     // Full slice, unconditional 16-byte loads.
-    auto load_full = [&](int64_t k0) {
+    auto load_a = [&](int64_t k0, ARegs& R) {
       if constexpr (AT == 0) {
         const float* A = static_cast<const float*>(g.A);
         if constexpr (AV) {
 #pragma unroll
-          for (int q = 0; q < AQ; ++q) ra[q] = *reinterpret_cast<const v4f*>(A + a_off[q] + k0 + 4 * a_pc);
+          for (int q = 0; q < AQ; ++q) R.ra[q] = *reinterpret_cast<const v4f*>(A + a_off[q] + k0 + 4 * a_pc);
         } else {
 #pragma unroll
-          for (int e = 0; e < 32; ++e) re[e] = A[sOff[sr + 8 * e] + k0 + sc];
+          for (int e = 0; e < 32; ++e) R.re[e] = A[sOff[sr + 8 * e] + k0 + sc];
         }
       } else {
         const uint16_t* A = static_cast<const uint16_t*>(g.A);
 #pragma unroll
-        for (int q = 0; q < AQ; ++q) ra16[q] = *reinterpret_cast<const v4u*>(A + a_off[q] + k0 + 8 * a_pc);
+        for (int q = 0; q < AQ; ++q) R.ra16[q] = *reinterpret_cast<const v4u*>(A + a_off[q] + k0 + 8 * a_pc);
       }
+    };
+    auto load_b = [&](int64_t k0, BRegs& R) {
 #pragma unroll
       for (int part = 0; part < BP; ++part)
 #pragma unroll
         for (int q = 0; q < BQ; ++q) {
           const uint16_t* p = (part == 0 ? g.B_hi : g.B_lo) + b_off[q] + k0;
           if constexpr (!BC) {
-            rb[part][q] = *reinterpret_cast<const v4u*>(p);
+            R.rb[part][q] = *(const __attribute__((address_space(1))) v4u*)(p);
           } else {
             const int64_t brow = n0 + b_r0 + 64 * q;
             uint32_t h[8];
@@ -235,12 +246,12 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
               const int64_t kk = k0 + 8 * b_pc + e;
               h[e] = (brow < N && kk < kend) ? (uint32_t)p[e] : 0u;
             }
-            rb[part][q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
+            R.rb[part][q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
           }
         }
     };
     // The ragged slice: element-wise, bounds-checked.
-    auto load_tail = [&](int64_t k0) {
+    auto load_tail = [&](int64_t k0, ARegs& RA, BRegs& R) {
       if constexpr (AT == 0) {
         const float* A = static_cast<const float*>(g.A);
         if constexpr (AV) {
@@ -252,11 +263,11 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
             x.y = (kk + 1 < kend) ? A[a_off[q] + kk + 1] : 0.f;
             x.z = (kk + 2 < kend) ? A[a_off[q] + kk + 2] : 0.f;
             x.w = (kk + 3 < kend) ? A[a_off[q] + kk + 3] : 0.f;
-            ra[q] = x;
+            RA.ra[q] = x;
           }
         } else {
 #pragma unroll
-          for (int e = 0; e < 32; ++e) re[e] = (k0 + sc < kend) ? A[sOff[sr + 8 * e] + k0 + sc] : 0.f;
+          for (int e = 0; e < 32; ++e) RA.re[e] = (k0 + sc < kend) ? A[sOff[sr + 8 * e] + k0 + sc] : 0.f;
         }
       } else {
         const uint16_t* A = static_cast<const uint16_t*>(g.A);
@@ -268,7 +279,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
             const int64_t kk = k0 + 8 * a_pc + e;
             h[e] = kk < kend ? (uint32_t)A[a_off[q] + kk] : 0u;
           }
-          ra16[q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
+          RA.ra16[q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
         }
       }
 #pragma unroll
@@ -283,14 +294,18 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
             const int64_t kk = k0 + 8 * b_pc + e;
             h[e] = (brow < N && kk < kend) ? (uint32_t)p[e] : 0u;
           }
-          rb[part][q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
+          R.rb[part][q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
         }
     };
 
     // Registers -> LDS stage `st`. Rows beyond M hold a copy of a valid row:
     // they only feed output rows that are never stored, so they are staged as
     // they are.
-    auto stage = [&](int st) {
+    auto stage = [&](int st, const ARegs& RA, const BRegs& R) {
+      const v4f* ra = RA.ra;
+      const float* re = RA.re;
+      const v4u* ra16 = RA.ra16;
+      const auto& rb = R.rb;
       if constexpr (AT == 0) {
         if constexpr (AV) {
           // 4 floats = half of a 16-byte chunk of 8 halves
@@ -381,21 +396,56 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
       }
     };
 
-    // prologue: slice 0 (possibly the ragged one) staged, slice 1 in registers
-    if (ragged) load_tail(slice_k0(0));
-    else load_full(slice_k0(0));
-    stage(0);
-    if (nk > 1) load_full(slice_k0(1));
-    __syncthreads();
-    // steady state: branch-free body
-    for (int64_t kt = 0; kt + 1 < nk; ++kt) {
-      const int st = (int)(kt & 1);
-      compute(st);
-      stage(st ^ 1);                                     // slice kt+1
-      load_full(slice_k0(std::min<int64_t>(kt + 2, nk - 1)));
-      __syncthreads();
+    auto clamp = [&](int64_t i) { return slice_k0(std::min<int64_t>(i, nk - 1)); };
+    // prologue: slice 0 (possibly the ragged one) staged
+    if (ragged) load_tail(slice_k0(0), A0, RB);
+    else {
+      load_a(slice_k0(0), A0);
+      load_b(slice_k0(0), RB);
     }
-    compute((int)((nk - 1) & 1));
+    stage(0, A0, RB);
+    if constexpr (AV || AT == 1) {
+      // slice 1 into A1 and RB, slice 2 requested into A0
+      load_a(clamp(1), A1);
+      load_b(clamp(1), RB);
+      load_a(clamp(2), A0);
+      __syncthreads();
+      // Steady state, two slices per trip, branch-free: on entry slice p is in
+      // LDS stage 0, slice p+1 in A1 and RB, slice p+2 in flight into A0.
+      int64_t p = 0;
+      for (; p + 2 < nk; p += 2) {
+        compute(0);
+        stage(1, A1, RB);                               // slice p+1
+        load_a(clamp(p + 3), A1);
+        load_b(clamp(p + 2), RB);
+        __syncthreads();
+        compute(1);
+        stage(0, A0, RB);                               // slice p+2
+        load_a(clamp(p + 4), A0);
+        load_b(clamp(p + 3), RB);
+        __syncthreads();
+      }
+      compute(0);
+      if (p + 1 < nk) {
+        stage(1, A1, RB);
+        __syncthreads();
+        compute(1);
+      }
+    } else {
+      // element path: one register slice, requested one slice ahead
+      load_a(clamp(1), A0);
+      load_b(clamp(1), RB);
+      __syncthreads();
+      for (int64_t kt = 0; kt + 1 < nk; ++kt) {
+        const int st = (int)(kt & 1);
+        compute(st);
+        stage(st ^ 1, A0, RB);                          // slice kt+1
+        load_a(clamp(kt + 2), A0);
+        load_b(clamp(kt + 2), RB);
+        __syncthreads();
+      }
+      compute((int)((nk - 1) & 1));
+    }
 
     // epilogue: lane holds column (lane & 31), rows 8*(r/4) + 4*(lane/32) + r%4
     float* C = g.C;
