@@ -10,17 +10,22 @@
 // order, so the score is reproducible bit for bit.
 //
 // Data flow. A pass streams every stored code once for a group of 16 queries
-// (the 16 columns of v_mfma_i32_16x16x64_i8). A 256-thread workgroup owns 256
-// consecutive examples at a time (each wave 4 tiles of 16 rows). Per 512-bit
-// step of a module, the workgroup stages the query planes (16 KB) in LDS once
-// and every wave multiplies its 64 rows against them. Bits are expanded without
-// reordering the stored layout: the 32-bit code word w yields the int8 operand
-// dwords (w >> d) & 0x01010101 (bits d, d+8, d+16, d+24), and the query planes
-// are laid out in that same permuted order when they are prepared.
-// After the last module the workgroup's scores are filtered against a per-query
-// threshold into an LDS candidate list (score desc, index asc), which is pruned
-// to the top-k whenever it could overflow; finally each workgroup writes its
-// top-k per query and a merge kernel reduces them.
+// (the 16 columns of v_mfma_i32_16x16x64_i8). A 512-thread workgroup (8
+// waves) owns 1024 consecutive examples at a time, each wave 8 tiles of 16
+// rows. The pass walks the modules in 512-bit steps; per step the workgroup
+// stages the query planes (16 KB) in LDS once for its 1024 rows,
+// double-buffered, and each wave multiplies its 128 rows against them (each
+// plane fragment read from LDS feeds 8 MFMAs) with its code words for that
+// step, which it requested one step earlier (16-byte loads). Bits are
+// expanded without reordering the stored layout: the 32-bit code word w
+// yields the int8 operand dwords (w >> d) & 0x01010101 (bits d, d+8, d+16,
+// d+24), and the query planes are laid out in that same permuted order when
+// they are prepared.
+// After the last module the workgroup's scores are filtered against a
+// per-query threshold into an LDS candidate list (score desc, index asc). A
+// list that fills up is pruned to the top-k (bitonic sort) and the entries
+// that did not fit are inserted again, so no qualifying row is lost. Finally
+// each workgroup writes its top-k per query and a merge kernel reduces them.
 #include <algorithm>
 #include <vector>
 
@@ -31,12 +36,11 @@ namespace eogp {
 namespace {
 
 constexpr int QB = 16;          // queries per pass
-constexpr int RT = 4;           // 16-row tiles per wave
-constexpr int NW = 4;           // waves per workgroup
-constexpr int ROWS = NW * RT * 16;
+constexpr int NW = 8;           // waves per workgroup
+constexpr int NTHR = NW * 64;
 constexpr int KSTEP = 8;        // MFMA k-steps (64 bits each) per 512-bit step
-constexpr int CAP = 512;        // candidate slots per query (power of two)
-constexpr int MAX_TOPK = CAP - ROWS;
+constexpr int MCAP = 512;       // candidate slots per query in the merge
+constexpr int MAX_TOPK = 256;
 
 struct ModInfo {
   int32_t k;       // bits of the module
@@ -125,25 +129,30 @@ __global__ void k_query_planes(const float* __restrict__ Y, int64_t ldy, int64_t
 }
 
 // ---- candidate lists in LDS ---------------------------------------------------
+template <int CAP>
 struct Cand {
   uint64_t key[QB][CAP];
   uint32_t idx[QB][CAP];
   int cnt[QB];
   uint64_t thr[QB];
+  int overflow;
 };
 
-// Sort list n (all 256 threads), keep its first `topk`, update the threshold.
-__device__ void prune(Cand& cd, int n, int topk) {
+// Sort list n (all NTH threads), keep its first `topk`, update the threshold.
+// Entries past CAP (counted but not stored) are dropped here; their owners
+// insert them again.
+template <int CAP, int NTH>
+__device__ void prune(Cand<CAP>& cd, int n, int topk) {
   const int tid = threadIdx.x;
-  const int c = cd.cnt[n];
-  for (int i = c + tid; i < CAP; i += 256) {
+  const int c = min(cd.cnt[n], CAP);
+  for (int i = c + tid; i < CAP; i += NTH) {
     cd.key[n][i] = 0ull;
     cd.idx[n][i] = 0xFFFFFFFFu;
   }
   __syncthreads();
   for (int k = 2; k <= CAP; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < CAP; i += 256) {
+      for (int i = tid; i < CAP; i += NTH) {
         const int p = i ^ j;
         if (p > i) {
           const uint64_t ka = cd.key[n][i], kb = cd.key[n][p];
@@ -166,6 +175,14 @@ __device__ void prune(Cand& cd, int n, int topk) {
   __syncthreads();
 }
 
+// One step of the pass (one or two 512-bit halves of one module): module,
+// first code byte of the step within a row, first k-step of its query
+// planes, valid code bytes, whether it is the module's last step, and its
+// number of halves.
+struct Step {
+  int32_t u, boff, kbase, bytes, last, halves, pad0, pad1;
+};
+
 struct ScoreArgs {
   const uint8_t* codes;
   int64_t cstride;
@@ -175,6 +192,8 @@ struct ScoreArgs {
   const ModInfo* mods;
   const int8_t* ph;
   const int8_t* pl;
+  const Step* steps;
+  int n_steps;
   int64_t KS;
   int64_t grp;
   const int32_t* fq;
@@ -186,9 +205,18 @@ struct ScoreArgs {
   uint32_t* cidx;
 };
 
-__global__ __launch_bounds__(256, 1) void k_score(ScoreArgs a) {
-  __shared__ __attribute__((aligned(16))) uint4 sB[2][2][KSTEP][64];
-  __shared__ Cand cd;
+// RT: 16-row tiles per wave (rows per block: NW * RT * 16). MULTI: several
+// modules, whose fp64 terms are summed in module order as each ends; else
+// one module, whose term is formed after its last step. HS: 512-bit halves per
+// step; with HS = 2 a lane reads both 64-byte halves of each 128-byte line of
+// its rows in the same step.
+template <int CAP, int RT, bool MULTI, int HS>
+__global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
+  constexpr int ROWS = NW * RT * 16;
+  constexpr int PU = 2 * HS * KSTEP * 64;            // plane uint4 per step
+  constexpr int PV = PU / NTHR;                      // staged per thread
+  __shared__ __attribute__((aligned(16))) uint4 sP[2][2][HS * KSTEP][64];
+  __shared__ Cand<CAP> cd;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int n = lane & 15;           // query column of this lane
   const int g = lane >> 4;           // k-group of this lane
@@ -198,92 +226,143 @@ __global__ __launch_bounds__(256, 1) void k_score(ScoreArgs a) {
     cd.cnt[tid] = 0;
     cd.thr[tid] = 0ull;
   }
+  if (tid == 0) cd.overflow = 0;
   __syncthreads();
   const int64_t n_blocks = (a.N + ROWS - 1) / ROWS;
   const uint4* phv = reinterpret_cast<const uint4*>(a.ph);
   const uint4* plv = reinterpret_cast<const uint4*>(a.pl);
   const uint32_t M1 = 0x01010101u;
+  // plane staging: uint4 number f = PV tid + v of the step is (plane, k-step,
+  // lane) = (f / (HS KSTEP 64), (f / 64) % (HS KSTEP), f % 64); k-steps past
+  // the step's valid halves are staged as zero
+  auto plane_src = [&](const Step& st, int f) -> uint4 {
+    const int plane = f / (HS * KSTEP * 64), ks = (f >> 6) % (HS * KSTEP), ln = f & 63;
+    if (ks >= st.halves * KSTEP) return make_uint4(0u, 0u, 0u, 0u);
+    const int64_t o = (a.grp * a.KS + st.kbase + ks) * 64 + ln;
+    return (plane ? plv : phv)[o];
+  };
+  auto plane_dst = [&](int buf, int f, const uint4& v) {
+    sP[buf][f / (HS * KSTEP * 64)][(f >> 6) % (HS * KSTEP)][f & 63] = v;
+  };
 
   for (int64_t blk = blockIdx.x; blk < n_blocks; blk += gridDim.x) {
     const int64_t row0 = blk * ROWS + (int64_t)wid * (RT * 16);
+    // this lane's code row of tile rt is row0 + 16 rt + n; rows past N read
+    // row N - 1 and are never reported
+    auto load_codes = [&](const Step& st, uint4 (*cw)[HS]) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const int64_t row = std::min<int64_t>(row0 + rt * 16 + n, a.N - 1);
+        const uint8_t* src = a.codes + row * a.cstride + st.boff + 16 * g;
+#pragma unroll
+        for (int h = 0; h < HS; ++h) {
+          const int have = st.bytes - 64 * h - 16 * g;   // valid bytes of this lane's 16
+          uint4 v = make_uint4(0u, 0u, 0u, 0u);
+          if (have >= 16) {
+            v = *reinterpret_cast<const uint4*>(src + 64 * h);
+          } else if (have >= 8) {
+            const uint2 hv = *reinterpret_cast<const uint2*>(src + 64 * h);
+            v.x = hv.x;
+            v.y = hv.y;
+          }
+          cw[rt][h] = v;
+        }
+      }
+    };
+
     double sc[RT][4];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) sc[rt][r] = 0.0;
+    i32x4 acc_h[RT], acc_l[RT];
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      acc_h[rt] = i32x4{0, 0, 0, 0};
+      acc_l[rt] = i32x4{0, 0, 0, 0};
+    }
 
-    for (int u = 0; u < a.U; ++u) {
-      const ModInfo md = a.mods[u];
-      const int nms = (md.k + 511) / 512;
-      const int mbytes = md.k >> 3;
-      i32x4 acc_h[RT], acc_l[RT];
-#pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        acc_h[rt] = i32x4{0, 0, 0, 0};
-        acc_l[rt] = i32x4{0, 0, 0, 0};
-      }
-      for (int ms = 0; ms < nms; ++ms) {
-        const int buf = ms & 1;
-        // stage this step's query planes: 2 planes x 8 k-steps x 64 lanes x 16 B
-        const int64_t kbase = (a.grp * a.KS + md.ksbase + (int64_t)ms * KSTEP) * 64;
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int f = tid * 4 + v;               // 0..1023
-          const int plane = f >> 9, ks = (f >> 6) & 7, ln = f & 63;
-          sB[buf][plane][ks][ln] = (plane ? plv : phv)[kbase + ks * 64 + ln];
-        }
-        // this lane's code words for each row tile (two 8-byte halves)
-        uint32_t wds[RT][4];
-        const int boff = 64 * ms + 16 * g;
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) {
-          const int64_t row = row0 + rt * 16 + n;
-          const uint8_t* src = a.codes + row * a.cstride + md.boff + boff;
-#pragma unroll
-          for (int hf = 0; hf < 2; ++hf) {
-            uint2 v2 = make_uint2(0u, 0u);
-            if (row < a.N && boff + 8 * hf + 8 <= mbytes)
-              v2 = *reinterpret_cast<const uint2*>(src + 8 * hf);
-            wds[rt][2 * hf] = v2.x;
-            wds[rt][2 * hf + 1] = v2.y;
-          }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int s = 0; s < KSTEP; ++s) {
-          const i32x4 bh = __builtin_bit_cast(i32x4, sB[buf][0][s][lane]);
-          const i32x4 bl = __builtin_bit_cast(i32x4, sB[buf][1][s][lane]);
-          const int d0 = 4 * (s & 1);
-#pragma unroll
-          for (int rt = 0; rt < RT; ++rt) {
-            const uint32_t w = wds[rt][s >> 1];
-            i32x4 av;
-            av[0] = (int)((w >> (d0 + 0)) & M1);
-            av[1] = (int)((w >> (d0 + 1)) & M1);
-            av[2] = (int)((w >> (d0 + 2)) & M1);
-            av[3] = (int)((w >> (d0 + 3)) & M1);
-            acc_h[rt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bh, acc_h[rt], 0, 0, 0);
-            acc_l[rt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bl, acc_l[rt], 0, 0, 0);
-          }
-        }
-      }
-      // module term: s * (2 n1 - sum y_int) * 2^-f, added in module order
+    // module term: s * (2 n1 - sum y_int) * 2^-f, added in module order
+    auto fold = [&](int u) {
       const int f = q_ok ? a.fq[q * a.U + u] : 0;
       const int ys = q_ok ? a.ysum[q * a.U + u] : 0;
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt)
+      for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int64_t row = row0 + rt * 16 + 4 * g + r;
           const uint16_t s16 = row < a.N ? a.scales[row * a.U + u] : (uint16_t)0;
           const int n1 = 256 * acc_h[rt][r] + acc_l[rt][r];
           const int nn = 2 * n1 - ys;
-          const double t = ldexp((double)f16_bits_to_f32(s16) * (double)nn, -f);
-          sc[rt][r] += t;
+          sc[rt][r] += ldexp((double)f16_bits_to_f32(s16) * (double)nn, -f);
         }
-    }
+        acc_h[rt] = i32x4{0, 0, 0, 0};
+        acc_l[rt] = i32x4{0, 0, 0, 0};
+      }
+    };
 
-    // candidates of this block
+    // prologue: step 0 staged, its code words in registers
+    uint4 cw[RT][HS], cwn[RT][HS];
+    {
+      const Step st = a.steps[0];
+#pragma unroll
+      for (int v = 0; v < PV; ++v) plane_dst(0, PV * tid + v, plane_src(st, PV * tid + v));
+      load_codes(st, cw);
+    }
+    __syncthreads();
+    for (int sidx = 0; sidx < a.n_steps; ++sidx) {
+      const int buf = sidx & 1;
+      const Step st = a.steps[sidx];
+      const bool more = sidx + 1 < a.n_steps;
+      uint4 pv[PV];
+      if (more) {
+        const Step nx = a.steps[sidx + 1];
+#pragma unroll
+        for (int v = 0; v < PV; ++v) pv[v] = plane_src(nx, PV * tid + v);
+        load_codes(nx, cwn);
+      }
+#pragma unroll
+      for (int h = 0; h < HS; ++h) {
+        if (h < st.halves) {                          // uniform
+#pragma unroll
+          for (int s = 0; s < KSTEP; ++s) {
+            const i32x4 bh = __builtin_bit_cast(i32x4, sP[buf][0][h * KSTEP + s][lane]);
+            const i32x4 bl = __builtin_bit_cast(i32x4, sP[buf][1][h * KSTEP + s][lane]);
+            const int d0 = 4 * (s & 1);
+#pragma unroll
+            for (int rt = 0; rt < RT; ++rt) {
+              const uint4& c = cw[rt][h];
+              const uint32_t w = (s >> 1) == 0 ? c.x : (s >> 1) == 1 ? c.y : (s >> 1) == 2 ? c.z : c.w;
+              i32x4 av;
+              av[0] = (int)((w >> (d0 + 0)) & M1);
+              av[1] = (int)((w >> (d0 + 1)) & M1);
+              av[2] = (int)((w >> (d0 + 2)) & M1);
+              av[3] = (int)((w >> (d0 + 3)) & M1);
+              acc_h[rt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bh, acc_h[rt], 0, 0, 0);
+              acc_l[rt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bl, acc_l[rt], 0, 0, 0);
+              // expand the next operand while these two multiply
+              __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);   // VALU
+              __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
+            }
+          }
+        }
+      }
+      if (MULTI && st.last) fold(st.u);
+      if (more) {
+#pragma unroll
+        for (int v = 0; v < PV; ++v) plane_dst(buf ^ 1, PV * tid + v, pv[v]);
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int h = 0; h < HS; ++h) cw[rt][h] = cwn[rt][h];
+      }
+      __syncthreads();
+    }
+    if (!MULTI) fold(0);
+
+    // candidates of this block; a full list is pruned and the entries that
+    // did not fit are offered again (the loop condition is uniform)
+    uint32_t pend = 0;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -291,20 +370,43 @@ __global__ __launch_bounds__(256, 1) void k_score(ScoreArgs a) {
         const int64_t row = row0 + rt * 16 + 4 * g + r;
         if (row < a.N && q_ok) {
           if (a.full) a.full[q * a.N + row] = (float)sc[rt][r];
-          const uint64_t key = order_key(sc[rt][r]);
-          if (key >= cd.thr[n]) {
-            const int pos = atomicAdd(&cd.cnt[n], 1);
-            cd.key[n][pos] = key;
-            cd.idx[n][pos] = (uint32_t)row;
-          }
+          pend |= 1u << (4 * rt + r);
         }
       }
-    __syncthreads();
-    for (int qq = 0; qq < QB; ++qq)
-      if (cd.cnt[qq] > CAP - ROWS) prune(cd, qq, a.topk);
+    for (;;) {
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const uint32_t bit = 1u << (4 * rt + r);
+          if (pend & bit) {
+            const uint64_t key = order_key(sc[rt][r]);
+            if (key < cd.thr[n]) {
+              pend &= ~bit;
+            } else {
+              const int pos = atomicAdd(&cd.cnt[n], 1);
+              if (pos < CAP) {
+                cd.key[n][pos] = key;
+                cd.idx[n][pos] = (uint32_t)(row0 + rt * 16 + 4 * g + r);
+                pend &= ~bit;
+              } else {
+                cd.overflow = 1;
+              }
+            }
+          }
+        }
+      __syncthreads();
+      const int ov = cd.overflow;
+      __syncthreads();
+      if (!ov) break;
+      for (int qq = 0; qq < QB; ++qq)
+        if (cd.cnt[qq] >= CAP) prune<CAP, NTHR>(cd, qq, a.topk);
+      if (tid == 0) cd.overflow = 0;
+      __syncthreads();
+    }
   }
-  for (int qq = 0; qq < QB; ++qq) prune(cd, qq, a.topk);
-  for (int i = tid; i < QB * a.topk; i += 256) {
+  for (int qq = 0; qq < QB; ++qq) prune<CAP, NTHR>(cd, qq, a.topk);
+  for (int i = tid; i < QB * a.topk; i += NTHR) {
     const int qq = i / a.topk, e = i % a.topk;
     const int64_t o = ((int64_t)blockIdx.x * QB + qq) * a.topk + e;
     const bool have = e < cd.cnt[qq];
@@ -319,7 +421,7 @@ __global__ __launch_bounds__(256, 1) void k_merge(const uint64_t* __restrict__ c
                                                   int64_t grp, int64_t Q, int topk,
                                                   int64_t* __restrict__ out_idx,
                                                   float* __restrict__ out_score) {
-  __shared__ Cand cd;   // only list 0 is used
+  __shared__ Cand<MCAP> cd;   // only list 0 is used
   const int n = blockIdx.x;
   const int64_t q = grp * QB + n;
   if (q >= Q) return;
@@ -344,9 +446,9 @@ __global__ __launch_bounds__(256, 1) void k_merge(const uint64_t* __restrict__ c
       }
     }
     __syncthreads();
-    if (cd.cnt[0] > CAP - 256) prune(cd, 0, topk);
+    if (cd.cnt[0] > MCAP - 256) prune<MCAP, 256>(cd, 0, topk);
   }
-  prune(cd, 0, topk);
+  prune<MCAP, 256>(cd, 0, topk);
   for (int e = tid; e < topk; e += 256) {
     const bool have = e < cd.cnt[0];
     out_idx[q * topk + e] = have ? (int64_t)cd.idx[0][e] : -1;
@@ -354,22 +456,48 @@ __global__ __launch_bounds__(256, 1) void k_merge(const uint64_t* __restrict__ c
   }
 }
 
+// Pass configuration: candidate slots per query (256 when that leaves room
+// for at least 128 new entries after a prune, else 512), 512-bit halves per
+// step (two when the LDS holds both), 16-row tiles per wave and whether
+// several modules are summed. One workgroup per CU either way (LDS).
+struct PassCfg {
+  int cap, hs, rt;
+  bool multi;
+};
+inline PassCfg pass_cfg(int32_t U, int32_t topk) {
+  PassCfg c;
+  c.cap = topk <= 128 ? 256 : 512;
+  c.hs = c.cap == 256 ? 2 : 1;
+  c.rt = (c.hs == 1 && U == 1) ? 8 : 4;
+  c.multi = U > 1;
+  return c;
+}
+
 struct Layout {
   int64_t KS = 0;        // k-steps per query group over all modules
+  int64_t n_steps = 0;   // 512-bit steps over all modules
   int64_t n_groups = 0;
   int64_t grid = 0;      // workgroups of the scoring pass
-  size_t o_mods = 0, o_fq = 0, o_ys = 0, o_ph = 0, o_pl = 0, o_ck = 0, o_ci = 0, total = 0;
+  size_t o_mods = 0, o_steps = 0, o_fq = 0, o_ys = 0, o_ph = 0, o_pl = 0, o_ck = 0, o_ci = 0,
+         total = 0;
 };
 
 Layout layout(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t topk) {
   Layout L;
-  for (int u = 0; u < U; ++u) L.KS += KSTEP * ((kmod[u] + 511) / 512);
+  const PassCfg c = pass_cfg(U, topk);
+  for (int u = 0; u < U; ++u) {
+    const int64_t nms = (kmod[u] + 511) / 512;
+    L.KS += KSTEP * nms;
+    L.n_steps += (nms + c.hs - 1) / c.hs;
+  }
   L.n_groups = (Q + QB - 1) / QB;
-  const int64_t n_blocks = (N + ROWS - 1) / ROWS;
+  const int64_t rows = (int64_t)NW * c.rt * 16;
+  const int64_t n_blocks = (N + rows - 1) / rows;
   L.grid = std::max<int64_t>(1, std::min<int64_t>(n_blocks, kCus));
   size_t b = 0;
   auto add = [&](size_t x) { size_t o = b; b = align256(b + x); return o; };
   L.o_mods = add(sizeof(ModInfo) * U);
+  L.o_steps = add(sizeof(Step) * L.n_steps);
   L.o_fq = add(4 * Q * U);
   L.o_ys = add(4 * Q * U);
   L.o_ph = add((size_t)L.n_groups * L.KS * 1024);
@@ -404,18 +532,36 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
   uint64_t* ck = reinterpret_cast<uint64_t*>(base + L.o_ck);
   uint32_t* ci = reinterpret_cast<uint32_t*>(base + L.o_ci);
 
+  Step* steps = reinterpret_cast<Step*>(base + L.o_steps);
+  const PassCfg cfg = pass_cfg(U, topk);
   std::vector<ModInfo> hm(U);
+  std::vector<Step> hs;
+  hs.reserve(L.n_steps);
   int64_t coff = 0, boff = 0, ks = 0;
   for (int u = 0; u < U; ++u) {
     hm[u].k = (int32_t)kmod[u];
     hm[u].coff = (int32_t)coff;
     hm[u].boff = (int32_t)boff;
     hm[u].ksbase = (int32_t)ks;
+    const int64_t nms = (kmod[u] + 511) / 512, mbytes = kmod[u] / 8;
+    for (int64_t ms = 0; ms < nms; ms += cfg.hs) {
+      Step st{};
+      st.u = u;
+      st.boff = (int32_t)(boff + 64 * ms);
+      st.kbase = (int32_t)(ks + KSTEP * ms);
+      st.bytes = (int32_t)std::min<int64_t>(64 * cfg.hs, mbytes - 64 * ms);
+      st.halves = (int32_t)std::min<int64_t>(cfg.hs, nms - ms);
+      st.last = ms + cfg.hs >= nms;
+      hs.push_back(st);
+    }
     coff += kmod[u];
     boff += kmod[u] / 8;
-    ks += KSTEP * ((kmod[u] + 511) / 512);
+    ks += KSTEP * nms;
   }
+  // the tables are small; copy them synchronously so the host vectors may go
   EOGP_HIP(hipMemcpyAsync(mods, hm.data(), sizeof(ModInfo) * U, hipMemcpyHostToDevice, s));
+  EOGP_HIP(hipMemcpyAsync(steps, hs.data(), sizeof(Step) * hs.size(), hipMemcpyHostToDevice, s));
+  EOGP_HIP(hipStreamSynchronize(s));
   timing::Scope tprep(EOGP_KT_SCORE_PREP, s);
   hipLaunchKernelGGL(k_query_stats, dim3((unsigned)Q, (unsigned)U), dim3(256), 0, s, Y, ldy, U,
                      mods, fq, ys);
@@ -435,6 +581,8 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     a.mods = mods;
     a.ph = ph;
     a.pl = pl;
+    a.steps = steps;
+    a.n_steps = (int)L.n_steps;
     a.KS = L.KS;
     a.grp = grp;
     a.fq = fq;
@@ -446,7 +594,14 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     a.cidx = ci;
     {
       timing::Scope tp(EOGP_KT_SCORE_PASS, s);
-      hipLaunchKernelGGL(k_score, dim3((unsigned)L.grid), dim3(256), 0, s, a);
+      const dim3 gd((unsigned)L.grid), bd(NTHR);
+      if (cfg.cap == 256) {
+        if (cfg.multi) hipLaunchKernelGGL((k_score<256, 4, true, 2>), gd, bd, 0, s, a);
+        else hipLaunchKernelGGL((k_score<256, 4, false, 2>), gd, bd, 0, s, a);
+      } else {
+        if (cfg.multi) hipLaunchKernelGGL((k_score<512, 4, true, 1>), gd, bd, 0, s, a);
+        else hipLaunchKernelGGL((k_score<512, 8, false, 1>), gd, bd, 0, s, a);
+      }
     }
     timing::Scope tm(EOGP_KT_SCORE_MERGE, s);
     hipLaunchKernelGGL(k_merge, dim3(QB), dim3(256), 0, s, ck, ci, (int)L.grid, grp, Q, topk,

@@ -407,6 +407,24 @@ def test_score_topk_bit_exact(N, ks, Q, topk):
     assert np.array_equal(sc.cpu().numpy(), ov)
 
 
+@pytest.mark.parametrize("N,ks,Q,topk", [
+    (600_000, [64], 16, 100),        # one module: several 1024-row blocks per workgroup
+    (300_000, [64, 64], 9, 128),     # two modules: several 512-row blocks per workgroup
+    (70_000, [128], 5, 200),         # the 512-slot candidate lists
+])
+def test_score_topk_bit_exact_large_stores(N, ks, Q, topk):
+    """More rows than one pass of workgroups covers, so every workgroup keeps
+    its candidate lists over several blocks (pruning and re-offering)."""
+    say(f"[score] large N={N} ks={ks} Q={Q} topk={topk}")
+    codes, scales, Y = random_store(N + 7, N, ks, Q)
+    idx, sc, _ = E.eogp_score_topk(d(codes), d(scales.view(np.int16)), ks, d(Y), topk)
+    torch.cuda.synchronize()
+    ref = O.score(codes, scales, ks, Y)
+    oi, ov = O.topk(ref, topk)
+    assert np.array_equal(idx.cpu().numpy(), oi)
+    assert np.array_equal(sc.cpu().numpy(), ov)
+
+
 def test_score_integral_queries_give_exact_real_scores():
     g = np.random.default_rng(21)
     ks = [256, 128]
