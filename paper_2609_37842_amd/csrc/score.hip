@@ -232,9 +232,10 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
   const uint4* phv = reinterpret_cast<const uint4*>(a.ph);
   const uint4* plv = reinterpret_cast<const uint4*>(a.pl);
   const uint32_t M1 = 0x01010101u;
-  // plane staging: uint4 number f = PV tid + v of the step is (plane, k-step,
-  // lane) = (f / (HS KSTEP 64), (f / 64) % (HS KSTEP), f % 64); k-steps past
-  // the step's valid halves are staged as zero
+  // plane staging: uint4 number f = tid + NTHR v of the step is (plane,
+  // k-step, lane) = (f / (HS KSTEP 64), (f / 64) % (HS KSTEP), f % 64), so
+  // consecutive lanes move consecutive 16 bytes; k-steps past the step's
+  // valid halves are staged as zero
   auto plane_src = [&](const Step& st, int f) -> uint4 {
     const int plane = f / (HS * KSTEP * 64), ks = (f >> 6) % (HS * KSTEP), ln = f & 63;
     if (ks >= st.halves * KSTEP) return make_uint4(0u, 0u, 0u, 0u);
@@ -306,7 +307,7 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
     {
       const Step st = a.steps[0];
 #pragma unroll
-      for (int v = 0; v < PV; ++v) plane_dst(0, PV * tid + v, plane_src(st, PV * tid + v));
+      for (int v = 0; v < PV; ++v) plane_dst(0, tid + NTHR * v, plane_src(st, tid + NTHR * v));
       load_codes(st, cw);
     }
     __syncthreads();
@@ -318,16 +319,22 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
       if (more) {
         const Step nx = a.steps[sidx + 1];
 #pragma unroll
-        for (int v = 0; v < PV; ++v) pv[v] = plane_src(nx, PV * tid + v);
+        for (int v = 0; v < PV; ++v) pv[v] = plane_src(nx, tid + NTHR * v);
         load_codes(nx, cwn);
       }
 #pragma unroll
       for (int h = 0; h < HS; ++h) {
         if (h < st.halves) {                          // uniform
+          // plane fragments of k-step s + 1 are read while k-step s multiplies
+          i32x4 fbh = __builtin_bit_cast(i32x4, sP[buf][0][h * KSTEP][lane]);
+          i32x4 fbl = __builtin_bit_cast(i32x4, sP[buf][1][h * KSTEP][lane]);
 #pragma unroll
           for (int s = 0; s < KSTEP; ++s) {
-            const i32x4 bh = __builtin_bit_cast(i32x4, sP[buf][0][h * KSTEP + s][lane]);
-            const i32x4 bl = __builtin_bit_cast(i32x4, sP[buf][1][h * KSTEP + s][lane]);
+            const i32x4 bh = fbh, bl = fbl;
+            if (s + 1 < KSTEP) {
+              fbh = __builtin_bit_cast(i32x4, sP[buf][0][h * KSTEP + s + 1][lane]);
+              fbl = __builtin_bit_cast(i32x4, sP[buf][1][h * KSTEP + s + 1][lane]);
+            }
             const int d0 = 4 * (s & 1);
 #pragma unroll
             for (int rt = 0; rt < RT; ++rt) {
@@ -350,7 +357,7 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
       if (MULTI && st.last) fold(st.u);
       if (more) {
 #pragma unroll
-        for (int v = 0; v < PV; ++v) plane_dst(buf ^ 1, PV * tid + v, pv[v]);
+        for (int v = 0; v < PV; ++v) plane_dst(buf ^ 1, tid + NTHR * v, pv[v]);
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
