@@ -1,10 +1,11 @@
 // MFMA contraction core for gfx950: C = A * B^T, K-contiguous operands.
 //
-// Tiling. A 256-thread workgroup (4 wave64s, one per SIMD) owns a 256 x BN
-// output tile (BN = 256 or 128, whichever pads N less); the waves form a 2 x 2
-// grid and each computes 128 x BN/2 with v_mfma_f32_32x32x16 blocks whose
+// Tiling. A 512-thread workgroup (8 wave64s, two per SIMD, so one wave's LDS
+// waits and barrier are covered by the other's MFMAs) owns a 256 x BN output
+// tile (BN = 256 or 128, whichever pads N less); the waves form a 2 x 4 grid
+// and each computes 128 x BN/4 with v_mfma_f32_32x32x16 blocks whose
 // accumulators live in the accumulation registers, so every fragment read
-// from LDS feeds BN/64 (A) or 4 (B) MFMAs. K advances 32 at a time through two
+// from LDS feeds BN/128 (A) or 4 (B) MFMAs. K advances 32 at a time through two
 // LDS stages. LDS rows are 64 bytes (32 halves) without padding; the four
 // 16-byte chunks of a row are XOR-swizzled by (row / 4) so that 16 lanes
 // reading one chunk of 16 consecutive rows touch distinct banks.
@@ -36,7 +37,7 @@
 namespace eogp {
 namespace {
 
-constexpr int BM = 256, BK = 32, NTHR = 256;
+constexpr int BM = 256, BK = 32, NTHR = 512;
 
 struct KParams {
   GemmArgs g;
@@ -117,7 +118,7 @@ __device__ __forceinline__ f32x2v uncvt_pair(uint32_t p) {
 template <int AT, int AP, int BP, bool F16, int BN, bool AV, bool BC>
 __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
   constexpr int WI = 4;                  // 32-high row blocks per wave (128 rows)
-  constexpr int WJ = BN / 64;            // 32-wide column blocks per wave (BN/2 columns)
+  constexpr int WJ = BN / 128;           // 32-wide column blocks per wave (BN/4 columns)
   const GemmArgs& g = kp.g;
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][AP][BM * BK];
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][BP][BN * BK];
@@ -143,20 +144,21 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
     t_step = G;
   }
 
-  const int wm = (wid >> 1) * 128, wn = (wid & 1) * (BN / 2);
+  const int wm = (wid >> 2) * 128, wn = (wid & 3) * (BN / 4);
   const float a_scale = g.a_scale;
   // Staging maps consecutive lanes to consecutive 16-byte pieces of one row, so
   // a wave-wide 16-byte load covers whole cache lines:
   //   fp32 A:   8 lanes per row (128 bytes), rows (tid >> 3) + 32 q, q = 0..7;
   //   16-bit A: 4 lanes per row (64 bytes),  rows (tid >> 2) + 64 q, q = 0..3;
   //   B:        4 lanes per row per part,    rows (tid >> 2) + 64 q, q < BN/64.
-  constexpr int AQ = AT == 0 ? 8 : 4;     // A pieces per thread per slice
-  constexpr int BQ = BN / 64;             // B pieces per thread per slice and part
+  constexpr int AQ = AT == 0 ? 4 : 2;     // A pieces per thread per slice
+  constexpr int BQ = BN / 128;            // B pieces per thread per slice and part
+  constexpr int NE = BM / (NTHR / 32);    // element A path: rows per thread
   const int a_r0 = AT == 0 ? (tid >> 3) : (tid >> 2);
-  const int a_rs = AT == 0 ? 32 : 64;
+  const int a_rs = AT == 0 ? NTHR / 8 : NTHR / 4;
   const int a_pc = AT == 0 ? (tid & 7) : (tid & 3);   // piece index within the row
   const int b_r0 = tid >> 2, b_pc = tid & 3;
-  const int sc = tid & 31, sr = tid >> 5;   // element A path: column, first row (rows sr + 8e)
+  const int sc = tid & 31, sr = tid >> 5;   // element A path: column, first row (rows sr + 16e)
 
   for (int64_t u = t_begin; u < t_end; u += t_step) {
     const int64_t t = u / kp.splits;
@@ -171,7 +173,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
     const bool ragged = ((kend - kbeg) % BK) != 0;
 
     __syncthreads();                     // previous unit's readers of sOff / stages are done
-    {
+    if (tid < BM) {
       const int64_t r = m0 + tid;
       const bool ok = r < M;
       const int64_t src = g.a_rows ? (int64_t)g.a_rows[ok ? r : m0] : (ok ? r : m0);
@@ -189,7 +191,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
     int64_t b_off[BQ];
 #pragma unroll
     for (int q = 0; q < BQ; ++q) {
-      const int64_t brow = n0 + b_r0 + 64 * q;
+      const int64_t brow = n0 + b_r0 + (NTHR / 4) * q;
       b_off[q] = (brow < N ? brow : 0) * g.ldb + 8 * b_pc;
     }
 
@@ -204,7 +206,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
     // slice is requested two slices before it is staged; B one slice before.
     struct ARegs {
       v4f ra[AT == 0 && AV ? AQ : 1];       // fp32 A (16-byte path)
-      float re[AT == 0 && !AV ? 32 : 1];    // fp32 A (element path)
+      float re[AT == 0 && !AV ? NE : 1];    // fp32 A (element path)
       v4u ra16[AT == 0 ? 1 : AQ];           // 16-bit A
     };
     struct BRegs {
@@ -222,7 +224,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
           for (int q = 0; q < AQ; ++q) R.ra[q] = *reinterpret_cast<const v4f*>(A + a_off[q] + k0 + 4 * a_pc);
         } else {
 #pragma unroll
-          for (int e = 0; e < 32; ++e) R.re[e] = A[sOff[sr + 8 * e] + k0 + sc];
+          for (int e = 0; e < NE; ++e) R.re[e] = A[sOff[sr + (NTHR / 32) * e] + k0 + sc];
         }
       } else {
         const uint16_t* A = static_cast<const uint16_t*>(g.A);
@@ -239,7 +241,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
           if constexpr (!BC) {
             R.rb[part][q] = *(const __attribute__((address_space(1))) v4u*)(p);
           } else {
-            const int64_t brow = n0 + b_r0 + 64 * q;
+            const int64_t brow = n0 + b_r0 + (NTHR / 4) * q;
             uint32_t h[8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -267,7 +269,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
           }
         } else {
 #pragma unroll
-          for (int e = 0; e < 32; ++e) RA.re[e] = (k0 + sc < kend) ? A[sOff[sr + 8 * e] + k0 + sc] : 0.f;
+          for (int e = 0; e < NE; ++e)
+            RA.re[e] = (k0 + sc < kend) ? A[sOff[sr + (NTHR / 32) * e] + k0 + sc] : 0.f;
         }
       } else {
         const uint16_t* A = static_cast<const uint16_t*>(g.A);
@@ -286,7 +289,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
       for (int part = 0; part < BP; ++part)
 #pragma unroll
         for (int q = 0; q < BQ; ++q) {
-          const int64_t brow = n0 + b_r0 + 64 * q;
+          const int64_t brow = n0 + b_r0 + (NTHR / 4) * q;
           const uint16_t* p = (part == 0 ? g.B_hi : g.B_lo) + b_off[q] + k0;
           uint32_t h[8];
 #pragma unroll
@@ -331,8 +334,8 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
           }
         } else {
 #pragma unroll
-          for (int e = 0; e < 32; ++e) {
-            const int r = sr + 8 * e;
+          for (int e = 0; e < NE; ++e) {
+            const int r = sr + (NTHR / 32) * e;
             const int o = swz(r, sc >> 3) + (sc & 7);
             const float x = F16 ? re[e] * a_scale : re[e];
             const uint16_t h = cvt16<F16>(x);
@@ -349,7 +352,7 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
       for (int part = 0; part < BP; ++part)
 #pragma unroll
         for (int q = 0; q < BQ; ++q)
-          *reinterpret_cast<v4u*>(&sB[st][part][swz(b_r0 + 64 * q, b_pc)]) = rb[part][q];
+          *reinterpret_cast<v4u*>(&sB[st][part][swz(b_r0 + (NTHR / 4) * q, b_pc)]) = rb[part][q];
     };
 
     f32x16 acc[WI][WJ];
