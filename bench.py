@@ -66,6 +66,21 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def profiled_traffic():
+    """Calibrated HBM traffic per rotation launch from the committed rocprofv3
+    counter summary, or None when the contraction source has changed since."""
+    import hashlib
+    import re
+    try:
+        md = open(os.path.join(ROOT, "profiles", "rotation_gemm_traffic.md")).read()
+        rec = json.loads(re.search(r"```json\s*(\{.*?\})\s*```", md, re.S).group(1))
+        src = os.path.join(ROOT, "paper_2609_37842_amd", "csrc", "gemm.hip")
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except (OSError, AttributeError, ValueError):
+        return None
+    return rec if rec.get("gemm_hip_sha256") == sha else None
+
+
 # ---------------------------------------------------------------------------
 # GPT-2-small-shaped store-and-query step
 # ---------------------------------------------------------------------------
@@ -214,7 +229,7 @@ def cpu_baseline(st: Gpt2Step, budget_s=25.0):
         threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    n_ex = 2
+    n_ex = 24
     per_shape = {}
     for si, (name, di, do) in enumerate(st.shapes):
         u = si                                     # block 0 module of this shape
@@ -363,6 +378,8 @@ def main(argv=None):
         avg_ms = rot_ms / max(1, rot_n)
         achieved = flops_launch / (avg_ms * 1e-3) / 1e12
         passes = 3 if st.prec == E.PREC_ACCURATE else 1
+        trec = profiled_traffic() if st.prec == E.PREC_F16 else None
+        traffic = trec["traffic_bytes_per_launch"] if trec else None
         dtype = {E.PREC_F16: "fp16 (fp32 inputs rounded once to fp16, fp32 accumulation)",
                  E.PREC_ACCURATE: "bf16x3 (fp32 inputs split into bf16 pairs, fp32 accumulation)",
                  E.PREC_FAST: "bf16"}[st.prec]
@@ -391,11 +408,14 @@ def main(argv=None):
                 "peak": BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s",
                 "frac": achieved / BF16_PEAK_TFLOPS,
-                "traffic": None,
+                "traffic": traffic,
                 "mfma_passes_per_flop": passes,
                 "executed_frac": passes * achieved / BF16_PEAK_TFLOPS,
                 "alg_flops_per_launch": flops_launch,
                 "alg_bytes_per_launch": bytes_launch,
+                "traffic_source": ("profiles/rotation_gemm_traffic.md (FETCH_SIZE x "
+                                   f"{trec['fetch_scale']} + WRITE_SIZE x {trec['write_scale']}, "
+                                   "calibrated on a plain 1 GiB copy)") if trec else None,
                 "avg_launch_ms": avg_ms,
                 "launches": rot_n,
             },
