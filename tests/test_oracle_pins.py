@@ -445,3 +445,19 @@ def test_tiny_store_and_query_roundtrip(tiny_fit):
     rho = [np.corrcoef(sc[q], full[q])[0, 1] for q in range(w.Q)]
     assert min(rho) > 0.6
     assert abs(np.median(rho) - math.sqrt(2 / math.pi)) < 0.08
+
+
+def test_partition_selection_helper_matches_full_sort():
+    """The tests' O(n) selection for very large Lambda agrees with the
+    oracle's full sort, ties included."""
+    from select_helpers import restrict, select_large
+    g = np.random.default_rng(31)
+    lam = np.round(g.lognormal(0, 1, (97, 53)), 1)        # many exact ties
+    for m in (1, 100, 2000, 97 * 53):
+        a = O.select_retained(lam, 0.01, m)
+        b = select_large(lam, 0.01, m)
+        assert np.array_equal(a.flat, b.flat)
+        assert np.allclose(a.w, b.w, rtol=0, atol=0)
+    sub, J, K = restrict(a, np.arange(0, 97 * 53, 7))
+    assert np.array_equal(J[sub.j], a.j[::7]) and np.array_equal(K[sub.k], a.k[::7])
+
