@@ -26,6 +26,10 @@ Readings of points the paper leaves open (each is also listed in the design doc):
     (least significant bit first); codes of several modules are concatenated,
     and scales are stored apart from the bits, one fp16 per (example, module);
   * scale: fp16 of ||x||_1 / k, rounded once, to nearest even;
+  * random second stage (EOGP-R): the Walsh-Hadamard matrix is in Sylvester
+    (natural) order, entry (r, i) = (-1)^popcount(r & i); the random signs
+    and the k kept rows are inputs (drawn by the caller), and coordinate c of
+    the output is transform row rows[c];
   * scoring: the query coordinates are kept to 15 significant bits by a
     per-(query, module) power of two (fixed point), so <y, b> is an exact
     integer; module terms are summed in float64 in ascending module order;
@@ -187,6 +191,46 @@ def first_stage_batch(a, ds, mask, Q_A, Q_S, ret: Retained) -> np.ndarray:
 def pca_project(Z: np.ndarray, P: np.ndarray) -> np.ndarray:
     """Rows of X are P^T z_i for the rows z_i of Z. P is [m, k]."""
     return np.asarray(Z, np.float64) @ np.asarray(P, np.float64)
+
+
+# ---------------------------------------------------------------------------
+# Random second stage, EOGP-R (Appendix B.2, eq. app_srht_definition)
+# ---------------------------------------------------------------------------
+def srht_width(m: int) -> int:
+    """p = 2^ceil(log2 m), the zero-padded width of the transform."""
+    return 1 << max(0, int(m - 1).bit_length())
+
+
+def walsh_hadamard(x: np.ndarray) -> np.ndarray:
+    """Unnormalised Walsh-Hadamard transform in Sylvester (natural) order
+    along the last axis: y[r] = sum_i (-1)^popcount(r & i) x[i], computed by
+    the butterfly recursion H_2n = [[H_n, H_n], [H_n, -H_n]]."""
+    y = np.array(x, dtype=np.float64, copy=True)
+    p = y.shape[-1]
+    h = 1
+    while h < p:
+        v = y.reshape(y.shape[:-1] + (p // (2 * h), 2, h))
+        a = v[..., 0, :].copy()
+        b = v[..., 1, :].copy()
+        v[..., 0, :] = a + b
+        v[..., 1, :] = a - b
+        h *= 2
+    return y
+
+
+def srht_project(Z: np.ndarray, signs: np.ndarray, rows: np.ndarray) -> np.ndarray:
+    """x = sqrt(p/k) R H_p D J z for each row z of Z [N, m]: J zero-pads to
+    p, D multiplies by the random signs [m] (+1 / -1), H_p is the orthonormal
+    Walsh-Hadamard matrix (the unnormalised one over sqrt(p)), and R keeps
+    the rows `rows` [k] in that order; so x = (H (D J z))[rows] / sqrt(k)."""
+    Z = np.asarray(Z, np.float64)
+    N, m = Z.shape
+    p = srht_width(m)
+    k = len(rows)
+    zp = np.zeros((N, p))
+    zp[:, :m] = Z * np.where(np.asarray(signs) < 0, -1.0, 1.0)[None, :]
+    y = walsh_hadamard(zp) / np.sqrt(p)
+    return np.sqrt(p / k) * y[:, np.asarray(rows, np.int64)]
 
 
 # ---------------------------------------------------------------------------

@@ -461,3 +461,71 @@ def test_partition_selection_helper_matches_full_sort():
     sub, J, K = restrict(a, np.arange(0, 97 * 53, 7))
     assert np.array_equal(J[sub.j], a.j[::7]) and np.array_equal(K[sub.k], a.k[::7])
 
+
+# ---------------------------------------------------------------------------
+# SRHT second stage (Appendix B.2)
+# ---------------------------------------------------------------------------
+def test_walsh_hadamard_matches_sylvester_matrix():
+    import scipy.linalg
+    g = np.random.default_rng(41)
+    for p in (1, 2, 8, 64, 1024):
+        x = g.standard_normal((3, p))
+        H = scipy.linalg.hadamard(p).astype(np.float64)
+        assert np.allclose(O.walsh_hadamard(x), x @ H.T, rtol=0, atol=1e-10)
+
+
+def test_srht_width_and_padding():
+    assert [O.srht_width(m) for m in (1, 2, 3, 512, 513, 16384, 32767)] == \
+        [1, 2, 4, 512, 1024, 16384, 32768]
+    # padding: the transform of a width-m vector equals that of its zero-padded copy
+    g = np.random.default_rng(42)
+    z = g.standard_normal((2, 300))
+    signs = g.choice([-1, 1], 300)
+    rows = g.choice(512, 40, replace=False)
+    zp = np.concatenate([z, np.zeros((2, 212))], axis=1)
+    sp = np.concatenate([signs, np.ones(212, int)])
+    assert np.allclose(O.srht_project(z, signs, rows), O.srht_project(zp, sp, rows), atol=1e-12)
+
+
+def test_srht_full_rows_is_orthonormal():
+    """With all p rows kept the map is sqrt(p/p) H D J: orthonormal, so the
+    norm and inner products of the (padded) inputs are preserved."""
+    g = np.random.default_rng(43)
+    m = 200
+    z = g.standard_normal((4, m))
+    signs = g.choice([-1, 1], m)
+    p = O.srht_width(m)
+    x = O.srht_project(z, signs, np.arange(p))
+    assert np.allclose(x @ x.T, z @ z.T, rtol=0, atol=1e-9)
+
+
+def test_srht_explicit_matrix_small_case():
+    """Against the printed definition with explicit matrices: R (k x p row
+    selector), H_p / sqrt(p), D = diag(signs), J (p x m zero padding)."""
+    import scipy.linalg
+    g = np.random.default_rng(44)
+    m, k = 13, 5
+    p = 16
+    z = g.standard_normal((3, m))
+    signs = g.choice([-1, 1], m)
+    rows = g.choice(p, k, replace=False)
+    R = np.eye(p)[rows]
+    H = scipy.linalg.hadamard(p) / np.sqrt(p)
+    D = np.diag(np.concatenate([signs, np.ones(p - m)]))
+    J = np.eye(p)[:, :m]
+    S_ = np.sqrt(p / k) * R @ H @ D @ J
+    assert np.allclose(O.srht_project(z, signs, rows), z @ S_.T, rtol=0, atol=1e-12)
+
+
+def test_srht_preserves_squared_norm_in_expectation():
+    """E over row subsets of ||S z||^2 = ||z||^2 (each row of H D J z has
+    mean square ||z||^2 / p); averaged over many draws."""
+    g = np.random.default_rng(45)
+    m, k = 100, 16
+    z = g.standard_normal((1, m))
+    signs = g.choice([-1, 1], m)
+    p = O.srht_width(m)
+    tot = np.mean([np.sum(O.srht_project(z, signs, g.choice(p, k, replace=False)) ** 2)
+                   for _ in range(4000)])
+    assert abs(tot / np.sum(z ** 2) - 1.0) < 0.03
+
