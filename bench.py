@@ -196,6 +196,33 @@ class Gpt2Step:
         E.eogp_score_topk(self.codes, self.scales, [k] * self.U, self.Y, self.topk,
                           out_idx=self.out_idx, out_score=self.out_score, ws=self.score_ws)
 
+    def prepare_srht(self):
+        """Random draws of each module's SRHT (EOGP-R), resident on the device."""
+        torch, S = self.torch, self.S
+        p = 1 << (self.m - 1).bit_length()
+        self.srht = []
+        for u in range(self.U):
+            signs, rows = S.srht_draws(self.w.config_id, u, self.m, p, self.k)
+            self.srht.append((torch.from_numpy(signs).to(self.dev),
+                              torch.from_numpy(rows).to(self.dev)))
+
+    def step_r(self, s):
+        """One step of the EOGP-R variant: the SRHT replaces the PCA projection."""
+        E = self.E
+        slot = s % self.n_slots
+        codes = self.codes[slot * self.B:(slot + 1) * self.B]
+        scales = self.scales[slot * self.B:(slot + 1) * self.B]
+        k = self.k
+        for u, (name, di, do) in enumerate(self.modules):
+            E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
+                                         Z=self.Z, prec=self.prec, ws=self.ws)
+            X = self.Xall[:, u * k:(u + 1) * k]
+            E.eogp_srht_project(self.Z, self.srht[u][0], self.srht[u][1], X=X)
+            E.eogp_sign_pack(X[:self.B], codes[:, u * self.kb:(u + 1) * self.kb],
+                             scales[:, u:u + 1])
+        E.eogp_score_topk(self.codes, self.scales, [k] * self.U, self.Y, self.topk,
+                          out_idx=self.out_idx, out_score=self.out_score, ws=self.score_ws)
+
     def rotation_flops_per_step(self):
         """Algorithmic flops of the rotation contractions in one step:
         2 * valid tokens * (d_out |J| + d_in |K|) per module, batch and queries."""
@@ -426,6 +453,35 @@ def main(argv=None):
                                      for u, (name, _, _) in enumerate(st.shapes)},
         })
         log(f"step {ms_per_step:.2f} ms, {value:.1f} ex/s, rotation {achieved:.1f} TFLOP/s alg")
+        # EOGP-R: the same step with the SRHT second stage (Appendix B.2)
+        st.prepare_srht()
+        nr = max(1, args.steps // 4)
+        st.step_r(0)
+        torch.cuda.synchronize()
+        for c in range(E.KT_SRHT + 1):
+            E.eogp_timing_read(c)
+        E.eogp_timing_enable(True)
+        t0 = time.perf_counter()
+        for s_ in range(nr):
+            st.step_r(s_)
+        torch.cuda.synchronize()
+        el_r = time.perf_counter() - t0
+        srht_ms, srht_n = E.eogp_timing_read(E.KT_SRHT)
+        E.eogp_timing_enable(False)
+        rows_launch = st.B + st.Qb
+        srht_bytes = rows_launch * 4 * (st.m + st.k)          # read z rows, write x rows
+        srht_avg = srht_ms / max(1, srht_n)
+        srht_gbs = srht_bytes / (srht_avg * 1e-3) / 1e9
+        out["eogp_r"] = {
+            "metric": "train examples/s compressed to 1-bit codes, SRHT second stage",
+            "value": st.B * nr / el_r, "unit": "train examples/s", "steps": nr,
+            "ms_per_step": 1000.0 * el_r / nr,
+            "srht_ms_per_step": srht_ms / nr,
+            "srht_roofline": {"bound": "hbm", "achieved": srht_gbs, "peak": HBM_PEAK_GBS,
+                              "unit": "GB/s", "frac": srht_gbs / HBM_PEAK_GBS,
+                              "alg_bytes_per_launch": srht_bytes, "avg_launch_ms": srht_avg},
+        }
+        log(f"eogp-r: {1000.0 * el_r / nr:.2f} ms/step, srht {srht_gbs:.0f} GB/s")
         if not args.no_cpu_baseline:
             t0 = time.time()
             out["cpu_baseline"] = cpu_baseline(st)

@@ -237,6 +237,30 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride,
                             float* full_scores, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * Random second stage, EOGP-R (Appendix B.2, eq. app_srht_definition): the
+ * subsampled randomized Hadamard transform x = sqrt(p/k) R H_p D J z in place
+ * of the PCA projection, for every row z of Z:
+ *   J zero-pads the m coordinates to p = 2^ceil(log2 m), D multiplies them by
+ *   the random signs, H_p is the orthonormal Walsh-Hadamard matrix in
+ *   Sylvester order (entry (r, i) = (-1)^popcount(r & i) / sqrt(p)), and R
+ *   keeps rows `rows[0..k)` in that order.
+ * The random draws are the caller's (the same realised transform serves the
+ * store and the queries).
+ *
+ *   Z      [N, ldz] fp32, ldz >= m.
+ *   signs  [m] int8: negative = -1, otherwise +1.
+ *   rows   [k] int32 in [0, p); a row outside gives NaN in that output
+ *          column; repeated rows repeat the coordinate.
+ *   X      [N, ldx] fp32, ldx >= k; columns k..ldx-1 are not written.
+ * Errors: EOGP_ERR_INVALID for bad sizes or NULL pointers, k > p, or
+ * ldz < m / ldx < k; EOGP_ERR_UNSUPPORTED for p > 32768 (m > 32768).
+ * Enqueued on `stream`; needs no workspace.
+ * ------------------------------------------------------------------------ */
+eogp_status eogp_srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m,
+                              const int8_t* signs, const int32_t* rows, int64_t k, float* X,
+                              int64_t ldx, void* stream);
+
+/* ------------------------------------------------------------------------
  * Kernel timing, for measurement harnesses. While enabled, each launch of a
  * kernel class below is bracketed by two HIP events recorded on the stream it
  * is launched on. eogp_timing_read waits for the recorded events of one class,
@@ -252,7 +276,8 @@ typedef enum {
   EOGP_KT_SCORE_MERGE = 5,    /* top-k merge after a pass                        */
   EOGP_KT_SCORE_PREP = 6,     /* fixed-point query preparation                   */
   EOGP_KT_COMPACTION = 7,     /* valid-token compaction                          */
-  EOGP_KT_COUNT = 8
+  EOGP_KT_SRHT = 8,           /* random second stage (EOGP-R)                    */
+  EOGP_KT_COUNT = 9
 } eogp_kernel_class;
 eogp_status eogp_timing_enable(int32_t enable);
 eogp_status eogp_timing_read(int32_t kernel_class, double* total_ms, int64_t* launches);

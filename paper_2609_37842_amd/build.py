@@ -18,7 +18,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libeogp.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["api.cpp", "timing.cpp", "select.hip", "gemm.hip", "retain.hip", "encode.hip", "score.hip"]
+SOURCES = ["api.cpp", "timing.cpp", "select.hip", "gemm.hip", "retain.hip", "encode.hip", "score.hip", "srht.hip"]
 ARCH = "gfx950"
 
 

@@ -23,6 +23,9 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
                         eogp_dtype p_dtype, int64_t ldp, int64_t k, float* X, int64_t ldx,
                         bool accurate, void* ws, size_t ws_bytes, hipStream_t s);
 int32_t score_max_topk();
+int srht_max_log();
+eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const int8_t* signs,
+                         const int32_t* rows, int64_t k, float* X, int64_t ldx, hipStream_t s);
 const char* last_error_cstr();
 size_t score_ws(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t topk);
 eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* scales, int64_t N,
@@ -246,6 +249,21 @@ eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, ui
   if (code_row_stride < (k + 7) / 8) return fail(EOGP_ERR_INVALID, "sign_pack: code row stride too small");
   if (scale_stride < 1) return fail(EOGP_ERR_INVALID, "sign_pack: scale stride must be >= 1");
   return sign_pack(X, ldx, N, k, codes, code_row_stride, scales, scale_stride, S(stream));
+}
+
+eogp_status eogp_srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m,
+                              const int8_t* signs, const int32_t* rows, int64_t k, float* X,
+                              int64_t ldx, void* stream) {
+  if (N < 0 || m < 1 || k < 1) return fail(EOGP_ERR_INVALID, "srht_project: bad sizes");
+  if (N >= kMaxFlat) return fail(EOGP_ERR_INVALID, "srht_project: N must be < 2^31");
+  if (m > ((int64_t)1 << srht_max_log()))
+    return fail(EOGP_ERR_UNSUPPORTED, "srht_project: m > 32768 is not supported");
+  int64_t p = 1;
+  while (p < m) p <<= 1;
+  if (k > p) return fail(EOGP_ERR_INVALID, "srht_project: need k <= p = 2^ceil(log2 m)");
+  if (ldz < m || ldx < k) return fail(EOGP_ERR_INVALID, "srht_project: leading dimension too small");
+  if (N > 0 && (!Z || !signs || !rows || !X)) return fail(EOGP_ERR_INVALID, "srht_project: NULL pointer");
+  return srht_project(Z, ldz, N, m, signs, rows, k, X, ldx, S(stream));
 }
 
 size_t eogp_score_topk_workspace_size(int64_t N, int64_t Q, int32_t U, const int64_t* k_per_module,

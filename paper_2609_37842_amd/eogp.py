@@ -46,7 +46,7 @@ EXPORTED = (
     "eogp_rotate_retain_workspace_size", "eogp_rotate_retain_planned",
     "eogp_rotate_retain_oneshot_workspace_size", "eogp_rotate_retain",
     "eogp_pca_project_workspace_size", "eogp_pca_project",
-    "eogp_sign_pack",
+    "eogp_sign_pack", "eogp_srht_project",
     "eogp_score_topk_workspace_size", "eogp_score_topk",
     "eogp_timing_enable", "eogp_timing_read",
     "eogp_status_string", "eogp_last_error", "eogp_version",
@@ -81,6 +81,8 @@ def load(path: str | None = None):
         "eogp_pca_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i32, c_i64, c_i64, c_vp,
                                      c_i64, c_i32, c_vp, c_sz, c_vp]),
         "eogp_sign_pack": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp]),
+        "eogp_srht_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_vp, c_i64, c_vp, c_i64,
+                                      c_vp]),
         "eogp_score_topk_workspace_size": (c_sz, [c_i64, c_i64, c_i32, ctypes.POINTER(c_i64),
                                                   c_i32]),
         "eogp_score_topk": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64), c_vp,
@@ -280,6 +282,26 @@ def eogp_pca_project(Z, Pt, X=None, prec=PREC_FAST, ws=None, stream=None):
     return X
 
 
+def eogp_srht_project(Z, signs, rows, X=None, stream=None):
+    """X [N, k] = the SRHT of each row of Z [N, m] (float32) with random signs
+    [m] (int8) and kept rows [k] (int32); see eogp_srht_project in eogp.h."""
+    L = load()
+    _need_cuda(Z, signs, rows, X)
+    N, m = Z.shape
+    k = rows.shape[0]
+    if Z.dtype != torch.float32 or (Z.numel() > 0 and Z.stride(1) != 1):
+        raise ValueError("Z must be float32 [N, m] with unit column stride")
+    if signs.dtype != torch.int8 or signs.shape[0] != m or not signs.is_contiguous():
+        raise ValueError("signs must be contiguous int8 [m]")
+    if rows.dtype != torch.int32 or not rows.is_contiguous():
+        raise ValueError("rows must be contiguous int32 [k]")
+    if X is None:
+        X = torch.empty((N, k), dtype=torch.float32, device=Z.device)
+    _check(L.eogp_srht_project(_ptr(Z), max(Z.stride(0), m), N, m, _ptr(signs), _ptr(rows), k,
+                               _ptr(X), max(X.stride(0), k), _stream(stream)))
+    return X
+
+
 def eogp_sign_pack(X, codes=None, scales=None, stream=None):
     """Packed sign bits [N, ceil(k/8)] (uint8) and fp16 scales [N] (uint16 bits)."""
     L = load()
@@ -334,8 +356,10 @@ def eogp_version() -> int:
 # ---------------------------------------------------------------------------
 KT_ROTATION_GEMM, KT_RETAINED, KT_PCA_GEMM, KT_SIGN_PACK = 0, 1, 2, 3
 KT_SCORE_PASS, KT_SCORE_MERGE, KT_SCORE_PREP, KT_COMPACTION = 4, 5, 6, 7
+KT_SRHT = 8
 KERNEL_CLASSES = {"rotation_gemm": 0, "retained": 1, "pca_gemm": 2, "sign_pack": 3,
-                  "score_pass": 4, "score_merge": 5, "score_prep": 6, "compaction": 7}
+                  "score_pass": 4, "score_merge": 5, "score_prep": 6, "compaction": 7,
+                  "srht": 8}
 
 
 def eogp_timing_enable(on: bool = True):

@@ -245,6 +245,16 @@ def query_projections(g: np.random.Generator, Q: int, width: int) -> np.ndarray:
     return g.standard_normal((Q, width)).astype(np.float32)
 
 
+def srht_draws(config_id: int, stream: int, m: int, p: int, k: int):
+    """The random draws of one module's SRHT (the same realised transform for
+    the store and the queries): signs [m] (int8, +1 / -1) and k distinct rows
+    of the width-p transform (int32), uniformly without replacement."""
+    g = rng(config_id, 700000 + stream)
+    signs = np.where(g.random(m) < 0.5, -1, 1).astype(np.int8)
+    rows = g.choice(p, size=k, replace=False).astype(np.int32)
+    return signs, rows
+
+
 # ---------------------------------------------------------------------------
 # Tiny workload (numpy): raw per-token inputs for stored examples and queries.
 # ---------------------------------------------------------------------------

@@ -62,6 +62,10 @@ def test_encode_and_score_argument_validation_without_device():
     # pca: k > m, ld too small
     assert L.eogp_pca_project(fake, 8, 2, 8, fake, 2, 8, 9, fake, 9, 0, None, 0, None) == -1
     assert L.eogp_pca_project(fake, 4, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -1
+    # srht: k > p, m too large, ld too small
+    assert L.eogp_srht_project(fake, 100, 2, 100, fake, fake, 129, fake, 129, None) == -1
+    assert L.eogp_srht_project(fake, 40000, 2, 40000, fake, fake, 8, fake, 8, None) == -2
+    assert L.eogp_srht_project(fake, 50, 2, 100, fake, fake, 8, fake, 8, None) == -1
     # score: k_u not a multiple of 64, topk out of range, misaligned stride
     ks = (ctypes.c_int64 * 2)(64, 100)
     assert L.eogp_score_topk(fake, 32, fake, 4, 2, ks, fake, 164, 1, 3, fake, fake, None,

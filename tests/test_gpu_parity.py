@@ -375,6 +375,47 @@ def test_rotate_retain_deterministic():
 
 
 # ---------------------------------------------------------------------------
+# Random second stage (EOGP-R)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("N,m,k", [
+    (5, 1, 1), (7, 3, 4), (9, 512, 128), (4, 700, 300), (3, 16384, 8192), (2, 32768, 16384),
+    (0, 64, 8),
+])
+def test_srht_project(N, m, k):
+    """Against the fp64 oracle; fp32 butterflies keep about 1e-6 relative."""
+    say(f"[srht] N={N} m={m} k={k}")
+    p = O.srht_width(m)
+    signs, rows = S.srht_draws(9, m + k, m, p, k)
+    Z = np.random.default_rng(m).standard_normal((N, m)).astype(np.float32)
+    X = E.eogp_srht_project(d(Z), d(signs), d(rows))
+    torch.cuda.synchronize()
+    if N == 0:
+        assert X.shape == (0, k)
+        return
+    ref = O.srht_project(Z, signs, rows)
+    err = rel_rows(X.cpu().numpy(), ref)
+    say(f"   max rel {err.max():.2e}")
+    assert err.max() <= 1e-5
+
+
+def test_srht_project_strides_and_bad_rows():
+    m, k = 1000, 64
+    p = O.srht_width(m)
+    signs, rows = S.srht_draws(9, 1, m, p, k)
+    rows[5] = p                                  # outside the transform
+    Z = np.random.default_rng(2).standard_normal((3, m + 24)).astype(np.float32)
+    Xb = torch.full((3, k + 7), 7.0, device=DEV)
+    E.eogp_srht_project(d(Z)[:, :m], d(signs), d(rows), X=Xb[:, :k])
+    torch.cuda.synchronize()
+    Xg = Xb.cpu().numpy()
+    assert np.all(np.isnan(Xg[:, 5]))
+    good = np.r_[0:5, 6:k]
+    ref = O.srht_project(Z[:, :m], signs, np.where(rows < p, rows, 0))
+    assert rel_rows(Xg[:, good], ref[:, good]).max() <= 1e-5
+    assert np.all(Xg[:, k:] == 7.0)
+
+
+# ---------------------------------------------------------------------------
 # Scoring
 # ---------------------------------------------------------------------------
 def random_store(seed, N, ks, Q):
