@@ -482,6 +482,37 @@ def main(argv=None):
                               "alg_bytes_per_launch": srht_bytes, "avg_launch_ms": srht_avg},
         }
         log(f"eogp-r: {1000.0 * el_r / nr:.2f} ms/step, srht {srht_gbs:.0f} GB/s")
+        # EK-FAC corrected eigenvalues (the fitting pass before selection): one
+        # batch of the step's examples through each GPT-2 module shape
+        cache, ek_ms, ek_flops = {}, 0.0, 0.0
+        tok = st.valid_tokens + st.valid_q_tokens
+        sq = {}
+        for si, (name, di, do) in enumerate(st.shapes):
+            art = st.S.torch_module_artifacts(st.w, si, di, do, dev, torch.float16, cache)
+            ws_e = torch.empty(E.eogp_ekfac_workspace_size(st.B + st.Qb, st.T, di, do),
+                               dtype=torch.uint8, device=dev)
+            sq[name] = E.eogp_ekfac_eigenvalues(st.A[name], st.D[name], st.mask, art["Q_A"],
+                                                art["Q_S"], prec=st.prec, ws=ws_e)
+            torch.cuda.synchronize()
+            E.eogp_timing_enable(True)
+            t0 = time.perf_counter()
+            E.eogp_ekfac_eigenvalues(st.A[name], st.D[name], st.mask, art["Q_A"], art["Q_S"],
+                                     sq_sum=sq[name], accumulate=True, prec=st.prec, ws=ws_e)
+            torch.cuda.synchronize()
+            ek_ms += 1000.0 * (time.perf_counter() - t0) * (len(st.modules) // len(st.shapes))
+            E.eogp_timing_enable(False)
+            ek_flops += 2.0 * tok * (do * do + di * di + do * di) * (len(st.modules) // len(st.shapes))
+            del art, ws_e
+        sq_ms, _ = E.eogp_timing_read(E.KT_EKFAC)
+        out["ekfac"] = {
+            "metric": "examples/s through the EK-FAC corrected-eigenvalue pass (all 48 modules)",
+            "value": (st.B + st.Qb) / (ek_ms * 1e-3), "unit": "examples/s",
+            "ms_per_batch_all_modules": ek_ms, "batch": st.B + st.Qb,
+            "alg_tflops": ek_flops / (ek_ms * 1e-3) / 1e12,
+            "squares_kernel_ms_4_shapes": sq_ms,
+        }
+        log(f"ekfac: {ek_ms:.1f} ms per batch over all modules")
+        del sq
         if not args.no_cpu_baseline:
             t0 = time.time()
             out["cpu_baseline"] = cpu_baseline(st)

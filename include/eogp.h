@@ -237,6 +237,31 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride,
                             float* full_scores, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * EK-FAC corrected eigenvalues, the fitting pass that precedes selection
+ * (Section 2.2, eq. ekfac_eigendecompose: Lambda[j, k] is the mean over
+ * examples of the squared coordinate (Q_S^T G_i Q_A)[j, k] of each
+ * sequence-level gradient G_i = sum_{valid t} ds_t a_t^T; Appendix C.2).
+ * For the batch given, sq_sum[j, k] receives (accumulate = 0) or is
+ * incremented by (accumulate != 0) the sum over its N examples of that
+ * square; after all batches the caller divides by the total number of
+ * examples. Inputs, strides, mask, dtypes and precision modes are those of
+ * eogp_rotate_retain (the fp16 mode takes no input exponents here).
+ *
+ *   Q_A, Q_S  [d_in, d_in] and [d_out, d_out] fp32 K-FAC eigenbases.
+ *   sq_sum    [d_out, d_in] fp32, row-major (the layout of eigvals).
+ *   ws        at least eogp_ekfac_workspace_size bytes.
+ * Errors as for eogp_rotate_retain. The sum over examples is formed in a
+ * fixed order, so repeated calls give identical results.
+ * ------------------------------------------------------------------------ */
+size_t eogp_ekfac_workspace_size(int64_t N, int64_t T, int64_t d_in, int64_t d_out);
+eogp_status eogp_ekfac_eigenvalues(const void* acts, int64_t ld_acts, const void* out_grads,
+                                   int64_t ld_grads, eogp_dtype in_dtype,
+                                   const uint8_t* token_mask, int64_t N, int64_t T,
+                                   int64_t d_in, int64_t d_out, const float* Q_A,
+                                   const float* Q_S, eogp_prec prec, float* sq_sum,
+                                   int32_t accumulate, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
  * Random second stage, EOGP-R (Appendix B.2, eq. app_srht_definition): the
  * subsampled randomized Hadamard transform x = sqrt(p/k) R H_p D J z in place
  * of the PCA projection, for every row z of Z:
@@ -277,7 +302,8 @@ typedef enum {
   EOGP_KT_SCORE_PREP = 6,     /* fixed-point query preparation                   */
   EOGP_KT_COMPACTION = 7,     /* valid-token compaction                          */
   EOGP_KT_SRHT = 8,           /* random second stage (EOGP-R)                    */
-  EOGP_KT_COUNT = 9
+  EOGP_KT_EKFAC = 9,          /* EK-FAC squared rotated gradients                */
+  EOGP_KT_COUNT = 10
 } eogp_kernel_class;
 eogp_status eogp_timing_enable(int32_t enable);
 eogp_status eogp_timing_read(int32_t kernel_class, double* total_ms, int64_t* launches);

@@ -24,6 +24,11 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
                         bool accurate, void* ws, size_t ws_bytes, hipStream_t s);
 int32_t score_max_topk();
 int srht_max_log();
+size_t ekfac_ws(int64_t N, int64_t T, int64_t d_in, int64_t d_out);
+eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int64_t ld_grads,
+                       bool bf16_in, const uint8_t* mask, int64_t N, int64_t T, int64_t d_in,
+                       int64_t d_out, const float* Q_A, const float* Q_S, int prec, float* sq,
+                       int accumulate, void* ws, size_t ws_bytes, hipStream_t s);
 eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const int8_t* signs,
                          const int32_t* rows, int64_t k, float* X, int64_t ldx, hipStream_t s);
 const char* last_error_cstr();
@@ -249,6 +254,41 @@ eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, ui
   if (code_row_stride < (k + 7) / 8) return fail(EOGP_ERR_INVALID, "sign_pack: code row stride too small");
   if (scale_stride < 1) return fail(EOGP_ERR_INVALID, "sign_pack: scale stride must be >= 1");
   return sign_pack(X, ldx, N, k, codes, code_row_stride, scales, scale_stride, S(stream));
+}
+
+size_t eogp_ekfac_workspace_size(int64_t N, int64_t T, int64_t d_in, int64_t d_out) {
+  if (N < 0 || T < 0 || d_in < 1 || d_out < 1) return 0;
+  return ekfac_ws(N, T, d_in, d_out);
+}
+
+eogp_status eogp_ekfac_eigenvalues(const void* acts, int64_t ld_acts, const void* out_grads,
+                                   int64_t ld_grads, eogp_dtype in_dtype,
+                                   const uint8_t* token_mask, int64_t N, int64_t T,
+                                   int64_t d_in, int64_t d_out, const float* Q_A,
+                                   const float* Q_S, eogp_prec prec, float* sq_sum,
+                                   int32_t accumulate, void* ws, size_t ws_bytes, void* stream) {
+  if (N < 0 || T < 0 || d_in < 1 || d_out < 1) return fail(EOGP_ERR_INVALID, "ekfac: bad sizes");
+  if (d_out * d_in >= kMaxFlat) return fail(EOGP_ERR_INVALID, "ekfac: d_in*d_out must be < 2^31");
+  if (N * T >= kMaxFlat) return fail(EOGP_ERR_INVALID, "ekfac: N*T must be < 2^31");
+  if (!Q_A || !Q_S || !sq_sum) return fail(EOGP_ERR_INVALID, "ekfac: NULL pointer");
+  if (N > 0 && T > 0 && (!acts || !out_grads)) return fail(EOGP_ERR_INVALID, "ekfac: NULL pointer");
+  if (in_dtype != EOGP_F32 && in_dtype != EOGP_BF16)
+    return fail(EOGP_ERR_UNSUPPORTED, "ekfac: inputs must be fp32 or bf16");
+  if (prec != EOGP_PREC_FAST && prec != EOGP_PREC_ACCURATE && prec != EOGP_PREC_F16)
+    return fail(EOGP_ERR_INVALID, "ekfac: unknown precision mode");
+  if (prec == EOGP_PREC_F16 && in_dtype != EOGP_F32)
+    return fail(EOGP_ERR_UNSUPPORTED, "ekfac: the fp16 mode takes fp32 inputs");
+  if (ld_acts == 0) ld_acts = d_in;
+  if (ld_grads == 0) ld_grads = d_out;
+  if (ld_acts < d_in || ld_grads < d_out)
+    return fail(EOGP_ERR_INVALID, "ekfac: token stride smaller than the width");
+  if (in_dtype == EOGP_BF16 &&
+      (ld_acts % 8 || ld_grads % 8 || (uintptr_t)acts % 16 || (uintptr_t)out_grads % 16))
+    return fail(EOGP_ERR_UNSUPPORTED, "ekfac: bf16 token rows must start on 16-byte boundaries");
+  if (ws_bytes < ekfac_ws(N, T, d_in, d_out) || !ws)
+    return fail(EOGP_ERR_WORKSPACE, "ekfac: workspace too small");
+  return ekfac_pass(acts, ld_acts, out_grads, ld_grads, in_dtype == EOGP_BF16, token_mask, N, T,
+                    d_in, d_out, Q_A, Q_S, (int)prec, sq_sum, accumulate, ws, ws_bytes, S(stream));
 }
 
 eogp_status eogp_srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m,

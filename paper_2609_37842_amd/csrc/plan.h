@@ -41,4 +41,9 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
                        int64_t m, const float* Q_A, const float* Q_S, hipStream_t s,
                        eogp_plan** out);
 void free_plan(eogp_plan* p);
+// Panels of a whole eigenbasis (every column, in order): the rows_pad x ld
+// bf16 high/low and fp16 images of Q^T, zero beyond d. `list` is d ints of
+// scratch.
+void basis_panels(const float* Q, int64_t d, int64_t rows_pad, int64_t ld, int* list,
+                  uint16_t* hi, uint16_t* lo, uint16_t* h16, hipStream_t s);
 }  // namespace eogp

@@ -133,18 +133,13 @@ size_t work_bytes(const eogp_plan* p, int64_t N, int64_t T) {
 
 size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T) { return work_bytes(p, N, T); }
 
-eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
-                          int64_t ld_grads, bool bf16_in,
-                          const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
-                          int prec, void* ws, size_t ws_bytes, hipStream_t s) {
-  if (ws_bytes < work_bytes(p, N, T)) return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
-  Carve cv(ws, ws_bytes);
-  Work w;
-  w.cnt = cv.take<int32_t>(N + 1);
-  w.tok = cv.take<int32_t>((size_t)N * T);
-  w.St = cv.take<float>((size_t)N * T * p->rows_pad);
-  w.At = cv.take<float>((size_t)N * T * p->cols_pad);
+namespace {
 
+// Steps 1 and 2: compaction of the valid tokens and the two rotations onto
+// the plan's eigenvector panels; fills w (carved from ws).
+eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
+                          const void* grads, int64_t ld_grads, bool bf16_in, const uint8_t* mask,
+                          int64_t N, int64_t T, int prec, Work& w, hipStream_t s) {
   // 1. compaction
   const unsigned g4 = (unsigned)ceil_div(N, 4);
   {
@@ -177,7 +172,7 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   gs.M = N * T;
   gs.M_dev = w.cnt + N;
   // Columns n_rows..rows_pad-1 of S~ are left unwritten: they only feed
-  // block outputs that no retained axis reads.
+  // block outputs that are never read.
   gs.N = p->n_rows;
   gs.K = p->d_out;
   eogp_status st = gemm_nt(gs, at, a_parts, b_parts, f16, s);
@@ -193,8 +188,30 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   ga.ldc = p->cols_pad;
   ga.N = p->n_cols;
   ga.K = p->d_in;
-  st = gemm_nt(ga, at, a_parts, b_parts, f16, s);
+  return gemm_nt(ga, at, a_parts, b_parts, f16, s);
+}
+
+Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
+  Work w;
+  w.cnt = cv.take<int32_t>(N + 1);
+  w.tok = cv.take<int32_t>((size_t)N * T);
+  w.St = cv.take<float>((size_t)N * T * p->rows_pad);
+  w.At = cv.take<float>((size_t)N * T * p->cols_pad);
+  return w;
+}
+
+}  // namespace
+
+eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
+                          int64_t ld_grads, bool bf16_in,
+                          const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
+                          int prec, void* ws, size_t ws_bytes, hipStream_t s) {
+  if (ws_bytes < work_bytes(p, N, T)) return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
+  Carve cv(ws, ws_bytes);
+  Work w = carve_work(p, N, T, cv);
+  eogp_status st = rotate_tokens(p, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, w, s);
   if (st != EOGP_OK) return st;
+  const bool f16 = prec == EOGP_PREC_F16;
 
   // 3. retained products, half-whitened, in canonical order
   const float out_scale = f16 ? std::ldexp(1.f, -(p->e_acts + p->e_grads)) : 1.f;
@@ -207,6 +224,118 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
                        p->ent_r, p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
     EOGP_LAUNCH_CHECK("retained products");
   }
+  return EOGP_OK;
+}
+
+// ---- EK-FAC corrected eigenvalues ---------------------------------------------
+// Lambda[j, k] = mean over examples of (Q_S^T G_i Q_A)[j, k]^2 (Section 2.2,
+// eq. ekfac_eigendecompose; corrected eigenvalues over examples from
+// sequence-level gradients, Appendix C.2). After the rotations onto every
+// eigenvector, one wave per 32 x 32 block (j, k) walks the examples in order:
+// the block of sums C = sum_t S~[t, j] A~[t, k] over the example's valid
+// tokens is formed with fp32 MFMA and C * C is added to the block's running
+// sum of squares in registers, so the result does not depend on scheduling.
+namespace {
+
+__global__ __launch_bounds__(256) void k_ekfac_sq(const float* __restrict__ St, int64_t ldS,
+                                                  const float* __restrict__ At, int64_t ldA,
+                                                  const int32_t* __restrict__ ex_off, int64_t N,
+                                                  int nbk, int d_out, int d_in,
+                                                  float* __restrict__ sq, int accumulate) {
+  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int jb = blockIdx.y;
+  const int kb = blockIdx.x * 4 + wid;
+  if (kb >= nbk) return;
+  const int half = lane >> 5, col = lane & 31;
+  const float* sp = St + (int64_t)jb * 32 + col;
+  const float* ap = At + (int64_t)kb * 32 + col;
+  f32x16 acc2;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc2[r] = 0.f;
+  for (int64_t i = 0; i < N; ++i) {
+    const int64_t t0 = ex_off[i], t1 = ex_off[i + 1];
+    f32x16 c;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) c[r] = 0.f;
+    for (int64_t tb = t0; tb < t1; tb += 16) {
+      float sv[8], av[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t t = tb + 2 * u + half;
+        const bool ok = t < t1;
+        sv[u] = ok ? sp[t * ldS] : 0.f;
+        av[u] = ok ? ap[t * ldA] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) c = __builtin_amdgcn_mfma_f32_32x32x2f32(sv[u], av[u], c, 0, 0, 0);
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc2[r] = fmaf(c[r], c[r], acc2[r]);
+  }
+  // acc2[r] holds block entry (8 (r / 4) + 4 half + r % 4, col)
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int j = jb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+    const int k = kb * 32 + col;
+    if (j < d_out && k < d_in) {
+      float* o = sq + (int64_t)j * d_in + k;
+      *o = accumulate ? *o + acc2[r] : acc2[r];
+    }
+  }
+}
+
+eogp_plan basis_plan(int64_t d_in, int64_t d_out) {
+  eogp_plan q;
+  q.d_out = d_out;
+  q.d_in = d_in;
+  q.n_rows = d_out;
+  q.n_cols = d_in;
+  q.rows_pad = round_up(d_out, kPanelTile);
+  q.cols_pad = round_up(d_in, kPanelTile);
+  q.ld_out = round_up(d_out, 32);
+  q.ld_in = round_up(d_in, 32);
+  return q;
+}
+
+size_t panel_bytes(const eogp_plan& q) {
+  return 3 * align256((size_t)q.rows_pad * q.ld_out * 2) + 3 * align256((size_t)q.cols_pad * q.ld_in * 2) +
+         align256((size_t)std::max(q.d_in, q.d_out) * 4);
+}
+
+}  // namespace
+
+size_t ekfac_ws(int64_t N, int64_t T, int64_t d_in, int64_t d_out) {
+  const eogp_plan q = basis_plan(d_in, d_out);
+  return work_bytes(&q, N, T) + panel_bytes(q);
+}
+
+eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int64_t ld_grads,
+                       bool bf16_in, const uint8_t* mask, int64_t N, int64_t T, int64_t d_in,
+                       int64_t d_out, const float* Q_A, const float* Q_S, int prec, float* sq,
+                       int accumulate, void* ws, size_t ws_bytes, hipStream_t s) {
+  eogp_plan q = basis_plan(d_in, d_out);
+  if (ws_bytes < work_bytes(&q, N, T) + panel_bytes(q))
+    return fail(EOGP_ERR_WORKSPACE, "ekfac: workspace too small");
+  Carve cv(ws, ws_bytes);
+  Work w = carve_work(&q, N, T, cv);
+  q.qs_hi = cv.take<uint16_t>((size_t)q.rows_pad * q.ld_out);
+  q.qs_lo = cv.take<uint16_t>((size_t)q.rows_pad * q.ld_out);
+  q.qs_f16 = cv.take<uint16_t>((size_t)q.rows_pad * q.ld_out);
+  q.qa_hi = cv.take<uint16_t>((size_t)q.cols_pad * q.ld_in);
+  q.qa_lo = cv.take<uint16_t>((size_t)q.cols_pad * q.ld_in);
+  q.qa_f16 = cv.take<uint16_t>((size_t)q.cols_pad * q.ld_in);
+  int* list = cv.take<int>((size_t)std::max(d_in, d_out));
+  basis_panels(Q_S, d_out, q.rows_pad, q.ld_out, list, q.qs_hi, q.qs_lo, q.qs_f16, s);
+  basis_panels(Q_A, d_in, q.cols_pad, q.ld_in, list, q.qa_hi, q.qa_lo, q.qa_f16, s);
+  EOGP_LAUNCH_CHECK("ekfac panels");
+  eogp_status st = rotate_tokens(&q, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, w, s);
+  if (st != EOGP_OK) return st;
+  const int nbj = (int)ceil_div(d_out, 32), nbk = (int)ceil_div(d_in, 32);
+  timing::Scope ts(EOGP_KT_EKFAC, s);
+  hipLaunchKernelGGL(k_ekfac_sq, dim3((unsigned)ceil_div(nbk, 4), (unsigned)nbj), dim3(256), 0, s,
+                     w.St, q.rows_pad, w.At, q.cols_pad, w.cnt, N, nbk, (int)d_out, (int)d_in, sq,
+                     accumulate);
+  EOGP_LAUNCH_CHECK("ekfac squares");
   return EOGP_OK;
 }
 

@@ -322,6 +322,20 @@ inline unsigned grid_for(int64_t n, int per) {
 
 }  // namespace
 
+namespace {
+__global__ void k_iota(int* __restrict__ v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) v[i] = (int)i;
+}
+}  // namespace
+
+void basis_panels(const float* Q, int64_t d, int64_t rows_pad, int64_t ld, int* list,
+                  uint16_t* hi, uint16_t* lo, uint16_t* h16, hipStream_t s) {
+  hipLaunchKernelGGL(k_iota, dim3(grid_for(d, 256)), dim3(256), 0, s, list, d);
+  hipLaunchKernelGGL(k_gather_panel, dim3((unsigned)(rows_pad / 32), grid_for(ld, 32)), dim3(256),
+                     0, s, Q, d, list, (int)d, rows_pad, ld, hi, lo, h16);
+}
+
 void free_plan(eogp_plan* p) {
   if (!p) return;
   if (p->mem) (void)hipFree(p->mem);

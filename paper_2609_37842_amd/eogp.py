@@ -47,6 +47,7 @@ EXPORTED = (
     "eogp_rotate_retain_oneshot_workspace_size", "eogp_rotate_retain",
     "eogp_pca_project_workspace_size", "eogp_pca_project",
     "eogp_sign_pack", "eogp_srht_project",
+    "eogp_ekfac_workspace_size", "eogp_ekfac_eigenvalues",
     "eogp_score_topk_workspace_size", "eogp_score_topk",
     "eogp_timing_enable", "eogp_timing_read",
     "eogp_status_string", "eogp_last_error", "eogp_version",
@@ -81,6 +82,10 @@ def load(path: str | None = None):
         "eogp_pca_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i32, c_i64, c_i64, c_vp,
                                      c_i64, c_i32, c_vp, c_sz, c_vp]),
         "eogp_sign_pack": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp]),
+        "eogp_ekfac_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64]),
+        "eogp_ekfac_eigenvalues": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64,
+                                           c_i64, c_i64, c_vp, c_vp, c_i32, c_vp, c_i32, c_vp,
+                                           c_sz, c_vp]),
         "eogp_srht_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_vp, c_i64, c_vp, c_i64,
                                       c_vp]),
         "eogp_score_topk_workspace_size": (c_sz, [c_i64, c_i64, c_i32, ctypes.POINTER(c_i64),
@@ -282,6 +287,35 @@ def eogp_pca_project(Z, Pt, X=None, prec=PREC_FAST, ws=None, stream=None):
     return X
 
 
+def eogp_ekfac_workspace_size(N: int, T: int, d_in: int, d_out: int) -> int:
+    """Bytes of workspace eogp_ekfac_eigenvalues needs for these sizes."""
+    return int(load().eogp_ekfac_workspace_size(N, T, d_in, d_out))
+
+
+def eogp_ekfac_eigenvalues(acts, out_grads, token_mask, Q_A, Q_S, sq_sum=None, accumulate=False,
+                           prec=PREC_ACCURATE, ws=None, stream=None):
+    """Sum over the batch of the squared rotated gradients (Q_S^T G_i Q_A)^2,
+    [d_out, d_in] float32 (divide by the total number of examples for the
+    corrected eigenvalues); see eogp_ekfac_eigenvalues in eogp.h."""
+    L = load()
+    _need_cuda(acts, out_grads, token_mask, Q_A, Q_S, sq_sum)
+    N, T, d_in = acts.shape
+    d_out = out_grads.shape[2]
+    ld_a, ld_g = _token_stride(acts, "acts"), _token_stride(out_grads, "out_grads")
+    if sq_sum is None:
+        sq_sum = torch.empty((d_out, d_in), dtype=torch.float32, device=acts.device)
+        accumulate = False
+    if sq_sum.dtype != torch.float32 or tuple(sq_sum.shape) != (d_out, d_in) or not sq_sum.is_contiguous():
+        raise ValueError("sq_sum must be contiguous float32 [d_out, d_in]")
+    need = int(L.eogp_ekfac_workspace_size(N, T, d_in, d_out))
+    ws, wsb = _workspace(need, acts.device, ws)
+    _check(L.eogp_ekfac_eigenvalues(_ptr(acts), ld_a, _ptr(out_grads), ld_g,
+                                    _acts_dtype(acts, out_grads), _ptr(token_mask), N, T, d_in,
+                                    d_out, _ptr(Q_A), _ptr(Q_S), prec, _ptr(sq_sum),
+                                    1 if accumulate else 0, _ptr(ws), wsb, _stream(stream)))
+    return sq_sum
+
+
 def eogp_srht_project(Z, signs, rows, X=None, stream=None):
     """X [N, k] = the SRHT of each row of Z [N, m] (float32) with random signs
     [m] (int8) and kept rows [k] (int32); see eogp_srht_project in eogp.h."""
@@ -356,10 +390,10 @@ def eogp_version() -> int:
 # ---------------------------------------------------------------------------
 KT_ROTATION_GEMM, KT_RETAINED, KT_PCA_GEMM, KT_SIGN_PACK = 0, 1, 2, 3
 KT_SCORE_PASS, KT_SCORE_MERGE, KT_SCORE_PREP, KT_COMPACTION = 4, 5, 6, 7
-KT_SRHT = 8
+KT_SRHT, KT_EKFAC = 8, 9
 KERNEL_CLASSES = {"rotation_gemm": 0, "retained": 1, "pca_gemm": 2, "sign_pack": 3,
                   "score_pass": 4, "score_merge": 5, "score_prep": 6, "compaction": 7,
-                  "srht": 8}
+                  "srht": 8, "ekfac": 9}
 
 
 def eogp_timing_enable(on: bool = True):

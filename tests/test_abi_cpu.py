@@ -62,6 +62,15 @@ def test_encode_and_score_argument_validation_without_device():
     # pca: k > m, ld too small
     assert L.eogp_pca_project(fake, 8, 2, 8, fake, 2, 8, 9, fake, 9, 0, None, 0, None) == -1
     assert L.eogp_pca_project(fake, 4, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -1
+    # ekfac: bad sizes, NULL bases, bad precision
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 0, 4, fake, fake, 1, fake, 0,
+                                    fake, 1 << 30, None) == -1
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, None, fake, 1, fake, 0,
+                                    fake, 1 << 30, None) == -1
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, fake, fake, 7, fake, 0,
+                                    fake, 1 << 30, None) == -1
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, fake, fake, 1, fake, 0,
+                                    fake, 16, None) == -4
     # srht: k > p, m too large, ld too small
     assert L.eogp_srht_project(fake, 100, 2, 100, fake, fake, 129, fake, 129, None) == -1
     assert L.eogp_srht_project(fake, 40000, 2, 40000, fake, fake, 8, fake, 8, None) == -2

@@ -375,6 +375,65 @@ def test_rotate_retain_deterministic():
 
 
 # ---------------------------------------------------------------------------
+# EK-FAC corrected eigenvalues (the fitting pass before selection)
+# ---------------------------------------------------------------------------
+def rel_fro(a, b):
+    a = np.asarray(a, np.float64)
+    b = np.asarray(b, np.float64)
+    return np.linalg.norm(a - b) / np.linalg.norm(b)
+
+
+def test_ekfac_eigenvalues_tiny_workload(tiny_fit):
+    """Mean over the 256 tiny examples of the squared rotated gradients, in
+    the oracle-fitted eigenbases, against the oracle's fitting pass."""
+    raw, f = tiny_fit["raw"], tiny_fit["fit"]
+    QA = f["Q_A"].astype(np.float32)
+    QS = f["Q_S"].astype(np.float32)
+    sq = E.eogp_ekfac_eigenvalues(d(raw["a"]), d(raw["ds"]), d(raw["mask"]), d(QA), d(QS))
+    torch.cuda.synchronize()
+    lam = sq.cpu().numpy() / raw["a"].shape[0]
+    ref = O.ekfac_eigenvalues(raw["a"], raw["ds"], raw["mask"], QA, QS)
+    rel = np.abs(lam - ref) / np.maximum(np.abs(ref), 1e-30)
+    say(f"[ekfac] tiny: fro {rel_fro(lam, ref):.2e}, max entry rel {rel.max():.2e}")
+    assert rel_fro(lam, ref) <= 1e-4
+    assert np.all(rel <= 1e-3)
+
+
+def test_ekfac_ragged_batches_accumulate():
+    """Odd widths, ragged masks with an empty example, NaN in masked tokens;
+    two accumulated batches equal one batch of all examples."""
+    N, T, d_in, d_out, m = 9, 37, 97, 130, 10
+    a, ds, mask, QA, QS, _ = random_problem(71, N, T, d_in, d_out, m, lens_lo=0)
+    mask[3, :] = 0
+    a = S.fill_masked(a, mask)
+    ds = S.fill_masked(ds, mask)
+    ref = O.ekfac_eigenvalues(a, ds, mask, QA, QS) * N
+    one = E.eogp_ekfac_eigenvalues(d(a), d(ds), d(mask), d(QA), d(QS))
+    two = E.eogp_ekfac_eigenvalues(d(a[:4]), d(ds[:4]), d(mask[:4]), d(QA), d(QS))
+    E.eogp_ekfac_eigenvalues(d(a[4:]), d(ds[4:]), d(mask[4:]), d(QA), d(QS), sq_sum=two,
+                             accumulate=True)
+    again = E.eogp_ekfac_eigenvalues(d(a), d(ds), d(mask), d(QA), d(QS))
+    torch.cuda.synchronize()
+    say(f"[ekfac] ragged: fro {rel_fro(one.cpu().numpy(), ref):.2e}")
+    assert rel_fro(one.cpu().numpy(), ref) <= 1e-4
+    assert rel_fro(two.cpu().numpy(), ref) <= 1e-4
+    assert torch.equal(one, again)                       # fixed summation order
+
+
+def test_ekfac_bf16_inputs():
+    N, T, d_in, d_out = 4, 64, 256, 192
+    a, ds, mask, QA, QS, _ = random_problem(72, N, T, d_in, d_out, 10, lens_lo=8)
+    at, dt = d(a, torch.bfloat16), d(ds, torch.bfloat16)
+    ref = O.ekfac_eigenvalues(at.float().cpu().numpy(), dt.float().cpu().numpy(), mask, QA, QS) * N
+    for prec, tol in ((E.PREC_FAST, 2e-2), (E.PREC_ACCURATE, 1e-4)):
+        sq = E.eogp_ekfac_eigenvalues(at, dt, d(mask), d(QA), d(QS), prec=prec)
+        torch.cuda.synchronize()
+        err = rel_fro(sq.cpu().numpy(), ref)
+        say(f"[ekfac] bf16 prec={prec}: fro {err:.2e}")
+        assert err <= tol
+
+
+# ---------------------------------------------------------------------------
 # Random second stage (EOGP-R)
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("N,m,k", [
