@@ -26,6 +26,17 @@ struct GemmArgs {
   bool b_padded = false;
   float* C = nullptr;
   int64_t ldc = 0;
+  // Optional fp16 output instead of C, in MFMA-fragment order: product entry
+  // (row, col) is stored, rounded to nearest even, at
+  //   CT[((col / 32) * (ldct / 16) + row / 16) * 512 + (col % 32) * 16 + row % 16],
+  // i.e. for every 32 columns and 16 rows one contiguous 1 KB block holding
+  // the 32 x 16 fp16 operand of one v_mfma_*_32x32x16 (columns as MFMA rows,
+  // rows as the 16-deep reduction). Every row and column of every output
+  // tile is written (no bounds checks), so CT must hold round_up(N, 256)
+  // columns of ldct >= round_up(M, 256) rows; ldct is a multiple of 256.
+  // Single-pass products without split-K only.
+  uint16_t* CT = nullptr;
+  int64_t ldct = 0;
   int64_t M = 0;                   // rows (upper bound if M_dev is set)
   const int32_t* M_dev = nullptr;  // device-side row count (<= M), or null
   int64_t N = 0, K = 0;

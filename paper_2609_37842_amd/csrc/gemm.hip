@@ -1,29 +1,40 @@
 // MFMA contraction core for gfx950: C = A * B^T, K-contiguous operands.
 //
-// Tiling. A 512-thread workgroup (8 wave64s, two per SIMD, so one wave's LDS
-// waits and barrier are covered by the other's MFMAs) owns a 256 x BN output
-// tile (BN = 256 or 128, whichever pads N less); the waves form a 2 x 4 grid
-// and each computes 128 x BN/4 with v_mfma_f32_32x32x16 blocks whose
-// accumulators live in the accumulation registers, so every fragment read
-// from LDS feeds BN/128 (A) or 4 (B) MFMAs. K advances 32 at a time through two
-// LDS stages. LDS rows are 64 bytes (32 halves) without padding; the four
-// 16-byte chunks of a row are XOR-swizzled by (row / 4) so that 16 lanes
-// reading one chunk of 16 consecutive rows touch distinct banks.
+// Two kernels share the staging conventions below.
 //
-// Pipeline. Slice k+1 sits in registers while slice k is multiplied from LDS;
-// right after the multiplies it is converted and written to the other stage
-// and slice k+2 is requested, then one barrier. The steady-state loop has no
-// branches: rows beyond M read a copy of a valid row (their products land in
-// output rows that are never stored), and a
-// ragged last K-slice is processed first, in the prologue, by the only
-// bounds-checked load. B operands are padded panels (rows to 256, K to a
-// multiple of 32, zero-filled) or, for general caller layouts, checked loads.
+// k_gemm_p (single-pass products without split-K: the rotations). A 256-thread
+// workgroup (4 wave64s, one per SIMD) owns a 256 x 256 output tile; each wave
+// computes 128 x 128 with v_mfma_f32_32x32x16 blocks accumulating in the
+// accumulation registers. K advances 32 at a time through two LDS stages. One
+// iteration per slice, one block barrier: the second half-slice's fragments
+// are read and the first half's 16 MFMAs issue beside the staging of the next
+// slice (B, then A converted while it is written) and the global requests for
+// later slices; after the barrier the next slice's first-half fragments are
+// read while the second half's MFMAs issue. A is requested two slices before
+// it is staged (two register buffers), B one slice before.
+//
+// k_gemm (everything else: bf16x3 products, split-K, unaligned or
+// bounds-checked operands). A 512-thread workgroup (8 waves, two per SIMD)
+// owns a 256 x BN tile (BN = 256 or 128, whichever pads N less); each wave
+// computes 128 x BN/4. Slice k+1 sits in registers while slice k is multiplied
+// from LDS; then it is converted and written to the other stage and slice k+2
+// is requested, then one barrier.
+//
+// Common conventions. LDS rows are 64 bytes (32 halves) without padding; the
+// four 16-byte chunks of row r are XOR-swizzled by (r / 4) % 4, which makes the
+// MFMA fragment reads (32 consecutive rows, two chunks) and the staging writes
+// (whole rows, 4 or 8 lanes per row) free of bank conflicts. Rows beyond M
+// read a copy of a valid row (their products land in output rows that are
+// never stored, or in fp16 output rows nobody reads), and a ragged last
+// K-slice is processed first, by the only bounds-checked load. B operands are
+// padded panels (rows to 256, K to a multiple of 32, zero-filled) or, for
+// general caller layouts, checked loads.
 //
 // Precision. fp32 A is converted while it is staged: rounded to the MFMA type,
 // or split into high and low parts (accurate mode), whose cross terms
 // (A_lo*B_hi, A_hi*B_lo, A_hi*B_hi) accumulate into the same fp32 registers.
 //
-// Schedule. The grid is persistent, one workgroup per CU. Work units
+// Schedule. Grids are persistent, one workgroup per CU. Work units
 // (tile, K-split) are dealt out in contiguous ranges per XCD (workgroup b runs
 // on XCD b % 8), so workgroups sharing an A row-block (rotations) or a B
 // column-block (PCA, n_major) run together on one XCD and hit the same L2.
@@ -79,12 +90,12 @@ __device__ __forceinline__ f32x16 mfma32(const v4u& a, const v4u& b, f32x16 c) {
   }
 }
 
-// Offset (in halves) of 16-byte chunk `c` (0..3) of LDS row `r`. The XOR key
-// ((r >> 1) ^ (r >> 3)) & 3 spreads 8 (or 16) consecutive rows read at one
-// chunk over distinct 16-byte bank groups of a 128-byte (or 256-byte) bank
-// window, so 16-byte fragment reads and staging writes are conflict-free.
+// Offset (in halves) of 16-byte chunk `c` (0..3) of LDS row `r`. With the key
+// (r >> 2) & 3, the 16-byte fragment reads of 32 consecutive rows at one chunk
+// are conflict-free (measured with the LDS bank-conflict counter; the key
+// (r >> 1) ^ (r >> 3) spent half of the read cycles in conflicts).
 __device__ __forceinline__ int swz(int r, int c) {
-  return r * BK + ((c ^ (((r >> 1) ^ (r >> 3)) & 3)) << 3);
+  return r * BK + ((c ^ ((r >> 2) & 3)) << 3);
 }
 
 typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
@@ -111,6 +122,49 @@ __device__ __forceinline__ f32x2v uncvt_pair(uint32_t p) {
     r.y = __uint_as_float(p & 0xFFFF0000u);
     return r;
   }
+}
+
+typedef unsigned int v2u __attribute__((ext_vector_type(2)));
+
+// Epilogue of one wave's WI x WJ blocks of 32 x 32 (rows r0.., columns c0..;
+// r0 and c0 multiples of 32). Lane l holds column (l & 31) and rows
+// 8 (r / 4) + 4 (l / 32) + r % 4 of each block. fp32 C: bounds-checked stores.
+// fp16 CT (fragment order, see GemmArgs): four consecutive rows of one column
+// are 8 contiguous bytes; no checks.
+template <int WI, int WJ>
+__device__ __forceinline__ void store_tile(const GemmArgs& g, float* C, int64_t ldc, int64_t M,
+                                           int64_t N, int64_t r0, int64_t c0, int lane,
+                                           const f32x16 (&acc)[WI][WJ]) {
+  if (g.CT) {
+    const int64_t groups = g.ldct / 16;
+#pragma unroll
+    for (int i = 0; i < WI; ++i)
+#pragma unroll
+      for (int j = 0; j < WJ; ++j) {
+        const int64_t cb = (c0 + 32 * j) / 32;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int64_t row = r0 + 32 * i + 8 * q + 4 * (lane >> 5);
+          uint16_t* dst = g.CT + ((cb * groups + row / 16) * 32 + (lane & 31)) * 16 + row % 16;
+          v2u h;
+          h.x = cvt_pair<true>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
+          h.y = cvt_pair<true>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
+          *reinterpret_cast<v2u*>(dst) = h;
+        }
+      }
+    return;
+  }
+#pragma unroll
+  for (int i = 0; i < WI; ++i)
+#pragma unroll
+    for (int j = 0; j < WJ; ++j) {
+      const int64_t col = c0 + 32 * j + (lane & 31);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = r0 + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (row < M && col < N) C[row * ldc + col] = acc[i][j][r];
+      }
+    }
 }
 
 // AT: 0 = fp32 A, 1 = 16-bit A. AV: A rows allow 16-byte loads (else fp32 A is
@@ -319,7 +373,6 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
             v4f x = ra[q];
             if constexpr (F16) x *= a_scale;
             const uint32_t h0 = cvt_pair<F16>(x.x, x.y), h1 = cvt_pair<F16>(x.z, x.w);
-            typedef unsigned int v2u __attribute__((ext_vector_type(2)));
             v2u hv;
             hv.x = h0;
             hv.y = h1;
@@ -408,10 +461,13 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
     }
     stage(0, A0, RB);
     if constexpr (AV || AT == 1) {
-      // slice 1 into A1 and RB, slice 2 requested into A0
-      load_a(clamp(1), A1);
-      load_b(clamp(1), RB);
-      load_a(clamp(2), A0);
+      // slice 1 into A1 and RB, slice 2 requested into A0 (with a single
+      // slice there is nothing to request: clamp would name the ragged slice)
+      if (nk > 1) {
+        load_a(clamp(1), A1);
+        load_b(clamp(1), RB);
+        load_a(clamp(2), A0);
+      }
       __syncthreads();
       // Steady state, two slices per trip, branch-free: on entry slice p is in
       // LDS stage 0, slice p+1 in A1 and RB, slice p+2 in flight into A0.
@@ -436,8 +492,10 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
       }
     } else {
       // element path: one register slice, requested one slice ahead
-      load_a(clamp(1), A0);
-      load_b(clamp(1), RB);
+      if (nk > 1) {
+        load_a(clamp(1), A0);
+        load_b(clamp(1), RB);
+      }
       __syncthreads();
       for (int64_t kt = 0; kt + 1 < nk; ++kt) {
         const int st = (int)(kt & 1);
@@ -457,17 +515,272 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
       C = g.partial + (int64_t)split * M * N;
       ldc = N;
     }
+    store_tile<WI, WJ>(g, C, ldc, M, N, m0 + wm, n0 + wn, lane, acc);
+  }
+}
+
+constexpr int PT = 256;   // k_gemm_p: threads per workgroup
+
+// AT: 0 = fp32 A, 1 = 16-bit A (both with 16-byte aligned rows); B is a padded
+// panel; one part each; no split-K.
+template <int AT, bool F16>
+__global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_gemm_p(KParams kp) {
+  constexpr int BNP = 256;
+  constexpr int WI = 4, WJ = 4;          // 128 x 128 per wave
+  const GemmArgs& g = kp.g;
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BNP * BK];
+  __shared__ int64_t sOff[BM];
+
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int64_t M = g.M_dev ? (int64_t)(*g.M_dev) : g.M;
+  const int64_t N = g.N, K = g.K;
+  const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BNP - 1) / BNP;
+  const int64_t n_units = tiles_m * tiles_n;
+
+  const int G = gridDim.x, b = blockIdx.x;
+  int64_t t_begin, t_end, t_step;
+  if (G >= kXcds && G % kXcds == 0) {
+    const int xcd = b % kXcds;
+    const int64_t per = G / kXcds, chunk = (n_units + kXcds - 1) / kXcds;
+    t_begin = xcd * chunk + b / kXcds;
+    t_end = std::min<int64_t>((int64_t)(xcd + 1) * chunk, n_units);
+    t_step = per;
+  } else {
+    t_begin = b;
+    t_end = n_units;
+    t_step = G;
+  }
+
+  const int wm = (wid >> 1) * 128, wn = (wid & 1) * 128;
+  const float a_scale = g.a_scale;
+  // Staging: fp32 A 8 lanes per row (rows (tid >> 3) + 32 q, q < 8); 16-bit A
+  // 4 lanes per row (rows (tid >> 2) + 64 q, q < 4); B 4 lanes per row.
+  constexpr int AQ = AT == 0 ? 8 : 4;
+  constexpr int BQ = BNP / 64;
+  const int a_r0 = AT == 0 ? (tid >> 3) : (tid >> 2);
+  constexpr int a_rs = AT == 0 ? PT / 8 : PT / 4;
+  const int a_pc = AT == 0 ? (tid & 7) : (tid & 3);
+  const int b_r0 = tid >> 2, b_pc = tid & 3;
+
+  for (int64_t u = t_begin; u < t_end; u += t_step) {
+    int64_t tm, tn;
+    if (g.n_major) { tn = u / tiles_m; tm = u % tiles_m; }
+    else { tm = u / tiles_n; tn = u % tiles_n; }
+    const int64_t m0 = tm * BM, n0 = tn * BNP;
+    const int64_t kend = K;
+    const int64_t nk = (K + BK - 1) / BK;
+    const bool ragged = (K % BK) != 0;
+
+    __syncthreads();                     // previous unit's readers of sOff / stages are done
+    {
+      const int64_t row = m0 + tid;
+      const bool ok = row < M;
+      const int64_t src = g.a_rows ? (int64_t)g.a_rows[ok ? row : m0] : (ok ? row : m0);
+      sOff[tid] = src * g.lda;
+    }
+    __syncthreads();
+    int64_t a_off[AQ];
+#pragma unroll
+    for (int q = 0; q < AQ; ++q) a_off[q] = sOff[a_r0 + a_rs * q];
+    int64_t b_off[BQ];
+#pragma unroll
+    for (int q = 0; q < BQ; ++q) {
+      const int64_t brow = n0 + b_r0 + 64 * q;
+      b_off[q] = (brow < N ? brow : 0) * g.ldb + 8 * b_pc;
+    }
+    // Slice order: a ragged last slice first, then the full slices in order.
+    auto slice_k0 = [&](int64_t i) -> int64_t {
+      const int64_t s = ragged ? (i == 0 ? nk - 1 : i - 1) : i;
+      return s * BK;
+    };
+    auto clamp = [&](int64_t i) { return slice_k0(std::min<int64_t>(i, nk - 1)); };
+
+    struct ARegs {
+      v4f ra[AT == 0 ? AQ : 1];
+      v4u ra16[AT == 0 ? 1 : AQ];
+    };
+    struct BRegs { v4u rb[BQ]; };
+    struct Frag { v4u a[WI]; v4u b[WJ]; };
+    ARegs A0, A1;
+    BRegs RB;
+    Frag F0, F1;
+
+    auto load_a = [&](int64_t k0, ARegs& R) {
+      if constexpr (AT == 0) {
+        const float* A = static_cast<const float*>(g.A);
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) R.ra[q] = *reinterpret_cast<const v4f*>(A + a_off[q] + k0 + 4 * a_pc);
+      } else {
+        const uint16_t* A = static_cast<const uint16_t*>(g.A);
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) R.ra16[q] = *reinterpret_cast<const v4u*>(A + a_off[q] + k0 + 8 * a_pc);
+      }
+    };
+    auto load_b = [&](int64_t k0, BRegs& R) {
+#pragma unroll
+      for (int q = 0; q < BQ; ++q)
+        R.rb[q] = *(const __attribute__((address_space(1))) v4u*)(g.B_hi + b_off[q] + k0);
+    };
+    // The ragged slice: element-wise, bounds-checked (B is a padded panel, so
+    // its columns up to round_up(K, 32) are readable and zero beyond K).
+    auto load_tail = [&](int64_t k0, ARegs& RA, BRegs& R) {
+      if constexpr (AT == 0) {
+        const float* A = static_cast<const float*>(g.A);
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) {
+          const int64_t kk = k0 + 4 * a_pc;
+          v4f x;
+          x.x = (kk + 0 < kend) ? A[a_off[q] + kk + 0] : 0.f;
+          x.y = (kk + 1 < kend) ? A[a_off[q] + kk + 1] : 0.f;
+          x.z = (kk + 2 < kend) ? A[a_off[q] + kk + 2] : 0.f;
+          x.w = (kk + 3 < kend) ? A[a_off[q] + kk + 3] : 0.f;
+          RA.ra[q] = x;
+        }
+      } else {
+        const uint16_t* A = static_cast<const uint16_t*>(g.A);
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) {
+          uint32_t h[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int64_t kk = k0 + 8 * a_pc + e;
+            h[e] = kk < kend ? (uint32_t)A[a_off[q] + kk] : 0u;
+          }
+          RA.ra16[q] = mk4(pack2(h[0], h[1]), pack2(h[2], h[3]), pack2(h[4], h[5]), pack2(h[6], h[7]));
+        }
+      }
+      load_b(k0, R);
+    };
+    auto stage_a = [&](int st, const ARegs& RA) {
+      if constexpr (AT == 0) {
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) {
+          const int r = a_r0 + a_rs * q;
+          const int o = swz(r, a_pc >> 1) + 4 * (a_pc & 1);
+          v4f x = RA.ra[q];
+          if constexpr (F16) x *= a_scale;
+          v2u hv;
+          hv.x = cvt_pair<F16>(x.x, x.y);
+          hv.y = cvt_pair<F16>(x.z, x.w);
+          *reinterpret_cast<v2u*>(&sA[st][o]) = hv;
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < AQ; ++q)
+          *reinterpret_cast<v4u*>(&sA[st][swz(a_r0 + a_rs * q, a_pc)]) = RA.ra16[q];
+      }
+    };
+    auto stage_b = [&](int st, const BRegs& R) {
+#pragma unroll
+      for (int q = 0; q < BQ; ++q)
+        *reinterpret_cast<v4u*>(&sB[st][swz(b_r0 + 64 * q, b_pc)]) = R.rb[q];
+    };
+    auto read_frag = [&](int st, int ks, Frag& F) {
+      const int ch = 2 * ks + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < WI; ++i)
+        F.a[i] = *reinterpret_cast<const v4u*>(&sA[st][swz(wm + 32 * i + (lane & 31), ch)]);
+#pragma unroll
+      for (int j = 0; j < WJ; ++j)
+        F.b[j] = *reinterpret_cast<const v4u*>(&sB[st][swz(wn + 32 * j + (lane & 31), ch)]);
+    };
+
+    f32x16 acc[WI][WJ];
 #pragma unroll
     for (int i = 0; i < WI; ++i)
 #pragma unroll
-      for (int j = 0; j < WJ; ++j) {
-        const int64_t col = n0 + wn + 32 * j + (lane & 31);
+      for (int j = 0; j < WJ; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int64_t row = m0 + wm + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (row < M && col < N) C[row * ldc + col] = acc[i][j][r];
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    constexpr int NM = WI * WJ;               // MFMAs per half slice
+    constexpr int NMB = NM / 4;               // of those, issued beside the B work
+    // MFMAs with index < lim (from = 0) or >= lim (from = 1) of a half slice.
+    auto mma_part = [&](const Frag& F, int from, int lim) {
+#pragma unroll
+      for (int j = 0; j < WJ; ++j)
+#pragma unroll
+        for (int i = 0; i < WI; ++i) {
+          const int m = j * WI + i;
+          if ((from == 0 && m < lim) || (from == 1 && m >= lim))
+            acc[i][j] = mfma32<F16>(F.a[i], F.b[j], acc[i][j]);
         }
+    };
+    auto mma = [&](const Frag& F) { mma_part(F, 1, 0); };
+
+    // prologue: slice 0 staged, slice 1 in A1 and RB, slice 2 in flight into A0
+    if (ragged) load_tail(slice_k0(0), A0, RB);
+    else {
+      load_a(slice_k0(0), A0);
+      load_b(slice_k0(0), RB);
+    }
+    stage_a(0, A0);
+    stage_b(0, RB);
+    if (nk > 1) {
+      load_b(clamp(1), RB);
+      load_a(clamp(1), A1);
+      load_a(clamp(2), A0);
+    }
+    __syncthreads();
+    read_frag(0, 0, F0);
+
+    // One slice i in stage st (F0 holds its first half; the registers hold
+    // slice i+1, A and B, and slice i+2, A). Scheduling hints keep the three
+    // regions apart and spread each region's MFMAs over its other work.
+    auto iter = [&](int st, int64_t i, ARegs& Anext) {
+      const int64_t kb2 = clamp(i + 2), ka3 = clamp(i + 3);
+      // region 1a: second-half fragment reads; B of slice i+1 to LDS; B of
+      // slice i+2 requested before A of slice i+3, so that a wait for B never
+      // waits for the A request behind it
+      __builtin_amdgcn_sched_barrier(0);
+      read_frag(st, 1, F1);
+      stage_b(st ^ 1, RB);
+      load_b(kb2, RB);
+      mma_part(F0, 0, NMB);
+#pragma unroll
+      for (int m = 0; m < NMB; ++m) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                     // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, (WI + WJ + NMB - 1) / NMB, 0);   // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x200, (BQ + NMB - 1) / NMB, 0);   // LDS write
+        __builtin_amdgcn_sched_group_barrier(0x020, (BQ + NMB - 1) / NMB, 0);   // global load
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);                     // VALU
       }
+      __builtin_amdgcn_sched_barrier(0);
+      // region 1b: the rest of the first half beside A of slice i+1 (convert,
+      // LDS) and the request of A of slice i+3
+      mma_part(F0, 1, NMB);
+      stage_a(st ^ 1, Anext);
+      load_a(ka3, Anext);
+#pragma unroll
+      for (int m = 0; m < NM - NMB; ++m) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(0x002, 5, 1);
+        if (m < AQ) __builtin_amdgcn_sched_group_barrier(0x200, 1, 1);
+        if (m >= NM - NMB - AQ) __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      // region 2: next slice's first-half fragments in flight under this
+      // slice's second-half MFMAs
+      read_frag(st ^ 1, 0, F0);
+      mma(F1);
+      __builtin_amdgcn_sched_group_barrier(0x100, WI + WJ, 2);
+      __builtin_amdgcn_sched_group_barrier(0x008, WI * WJ, 2);
+      __builtin_amdgcn_sched_barrier(0);
+    };
+    int64_t p = 0;
+    for (; p + 2 <= nk; p += 2) {
+      iter(0, p, A1);
+      iter(1, p + 1, A0);
+    }
+    if (p < nk) {                            // odd count: the last slice is in stage 0
+      read_frag(0, 1, F1);
+      mma(F0);
+      mma(F1);
+    }
+    store_tile<WI, WJ>(g, g.C, g.ldc, M, N, m0 + wm, n0 + wn, lane, acc);
   }
 }
 
@@ -516,6 +829,19 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
       kp.splits = (int)((nk_all * BK + kp.kc - 1) / kp.kc);
     }
   }
+  if constexpr (AP == 1 && BP == 1) {
+    if (av && !bc && kp.splits == 1) {
+      // single-pass product: the pipelined 4-wave kernel, 256 x 256 tiles
+      const int64_t tiles_p = ((g.M + BM - 1) / BM) * ((g.N + 255) / 256);
+      int64_t grid = std::min<int64_t>(tiles_p, kCus);
+      if (grid >= kXcds) grid = grid / kXcds * kXcds;
+      timing::Scope ts(g.timing_class, s);
+      hipLaunchKernelGGL((k_gemm_p<AT, F16>), dim3((unsigned)grid), dim3(PT), 0, s, kp);
+      EOGP_LAUNCH_CHECK("gemm launch");
+      return EOGP_OK;
+    }
+  }
+  if (g.CT && kp.splits > 1) return fail(EOGP_ERR_UNSUPPORTED, "gemm: fp16 transposed output without split-K only");
   int64_t grid = std::min<int64_t>(tiles * kp.splits, kCus);
   if (grid >= kXcds) grid = grid / kXcds * kXcds;
   timing::Scope ts(g.timing_class, s);

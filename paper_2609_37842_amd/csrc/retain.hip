@@ -8,9 +8,18 @@
 //    columns the retained axes use: S~ = DS_valid Q_S[:, J], A~ = A_valid Q_A[:, K].
 // 3. Retained products: for every example and every 32 x 32 block of
 //    (row, column) pairs that holds retained axes, the block of sums
-//    sum_t S~[t, j] A~[t, k] over the example's tokens is formed (fp32 MFMA)
+//    sum_t S~[t, j] A~[t, k] over the example's tokens is formed (MFMA)
 //    and the retained entries are scaled by w_r and written to their
 //    canonical positions in Z.
+//
+// Intermediates. FAST and ACCURATE keep S~ and A~ in fp32, token-major, and
+// form the sums with exact fp32 products. The fp16 mode stores them as fp16
+// in MFMA-fragment order (1 KB blocks of 32 rows x 16 tokens), with every
+// example's token run starting at a multiple of 8, and forms the sums with
+// fp16 MFMA over 16 tokens at a time: half the bytes written and read, whole
+// 1 KB blocks per load, and 16x the MFMA rate. The extra rounding
+// of S~ and A~ adds about 1e-4 to the relative error of a row of Z in the
+// GPT-2-shaped workload (4.1e-4 -> 5.1e-4, against 1e-3).
 #include <algorithm>
 #include <cmath>
 
@@ -23,17 +32,26 @@ namespace eogp {
 namespace {
 
 // ---- token compaction ---------------------------------------------------------
+// len[i] = valid tokens of example i; cnt[i] = len[i] rounded up to `align`
+// (the run length the compacted list reserves; scanned into offsets later).
 __global__ __launch_bounds__(256) void k_count_valid(const uint8_t* __restrict__ mask, int64_t N,
-                                                     int64_t T, int32_t* __restrict__ cnt) {
+                                                     int64_t T, int align, int32_t* __restrict__ cnt,
+                                                     int32_t* __restrict__ len) {
   const int64_t i = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (i >= N) return;
   int c = 0;
   for (int64_t t = lane; t < T; t += 64) c += mask ? (mask[i * T + t] != 0) : 1;
   for (int off = 32; off > 0; off >>= 1) c += __shfl_xor(c, off);
-  if (lane == 0) cnt[i] = c;
+  if (lane == 0) {
+    cnt[i] = (c + align - 1) / align * align;
+    if (len) len[i] = c;
+  }
 }
 
+// Token list: example i's valid tokens (global index i * T + t) from off[i]
+// on; the run is padded to off[i + 1] with token i * T (a readable row whose
+// products land in padding columns that the retained products skip).
 __global__ __launch_bounds__(256) void k_write_tokens(const uint8_t* __restrict__ mask, int64_t N,
                                                       int64_t T, const int32_t* __restrict__ off,
                                                       int32_t* __restrict__ tok) {
@@ -49,6 +67,7 @@ __global__ __launch_bounds__(256) void k_write_tokens(const uint8_t* __restrict_
     if (v) tok[pos + pre] = (int32_t)(i * T + t);
     pos += __popcll(bm);
   }
+  for (int32_t q = pos + lane; q < off[i + 1]; q += 64) tok[q] = (int32_t)(i * T);
 }
 
 // ---- retained products --------------------------------------------------------
@@ -113,19 +132,110 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
   }
 }
 
+// fp16 intermediates: S~ and A~ in MFMA-fragment order (for every 32 rows j
+// and 16 tokens t one contiguous 1 KB block, j-major, 16 tokens per j; token
+// capacity ldt); example i's tokens are t = off[i] .. off[i] + len[i] - 1,
+// off[i] a multiple of 8. One wave per (active block, example) as above; each
+// v_mfma_f32_32x32x16_f16 takes 16 tokens: lane l feeds row l % 32 and tokens
+// 8 (l / 32) .. +7 of each operand with one 16-byte load (the wave reads one
+// whole 1 KB block, or two halves of neighbouring blocks when the run starts
+// at an odd multiple of 8). Tokens past the example's last one (padding, or
+// the next example) are zeroed in both operands before they reach the MFMA.
+constexpr int kRet16Unroll = 4;
+
+__global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__ St,
+                                                    const uint16_t* __restrict__ At, int64_t ldt,
+                                                    const int32_t* __restrict__ ex_off,
+                                                    const int32_t* __restrict__ ex_len,
+                                                    const int32_t* __restrict__ tiles, int n_tiles,
+                                                    const int32_t* __restrict__ ent_r,
+                                                    const uint16_t* __restrict__ ent_loc,
+                                                    const float* __restrict__ w, float out_scale,
+                                                    float* __restrict__ Z, int64_t ldz, int64_t ex0) {
+  typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+  __shared__ float blk[kRetWaves][32][33];
+  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int tile = blockIdx.x * kRetWaves + wid;
+  if (tile >= n_tiles) return;                 // whole wave leaves; no block barrier below
+  const int64_t i = ex0 + blockIdx.y;
+  const int jb = tiles[4 * tile + 0], kb = tiles[4 * tile + 1];
+  const int e0 = tiles[4 * tile + 2], e1 = tiles[4 * tile + 3];
+  const int64_t t0 = ex_off[i] + 8 * (lane >> 5);   // this lane's first token
+  const int n = ex_len[i];
+  const int half = lane >> 5, col = lane & 31;
+  const int64_t groups = ldt / 16;
+  // element offset of (row block b, this lane's row, token t), t a multiple of 8
+  auto at_tok = [&](int64_t b, int64_t t) { return ((b * groups + (t >> 4)) * 32 + col) * 16 + (t & 15); };
+  const uint16_t* sp = St + at_tok(jb, t0);
+  const uint16_t* ap = At + at_tok(kb, t0);
+  // Advancing 16 tokens moves a lane one block (512 elements) on.
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  int t = 0;
+  for (; t + 16 * kRet16Unroll <= n; t += 16 * kRet16Unroll) {
+    v4u a[kRet16Unroll], b[kRet16Unroll];
+#pragma unroll
+    for (int u = 0; u < kRet16Unroll; ++u) {
+      a[u] = *reinterpret_cast<const v4u*>(sp + (int64_t)(t / 16 + u) * 512);
+      b[u] = *reinterpret_cast<const v4u*>(ap + (int64_t)(t / 16 + u) * 512);
+    }
+#pragma unroll
+    for (int u = 0; u < kRet16Unroll; ++u)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a[u]),
+                                                   __builtin_bit_cast(f16x8, b[u]), acc, 0, 0, 0);
+  }
+  for (; t < n; t += 16) {
+    v4u a = *reinterpret_cast<const v4u*>(sp + (int64_t)(t / 16) * 512);
+    v4u b = *reinterpret_cast<const v4u*>(ap + (int64_t)(t / 16) * 512);
+    const int rem = n - t - 8 * half;          // valid tokens among this lane's eight
+    if (rem < 8) {
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const uint32_t keep = (2 * d < rem ? 0x0000FFFFu : 0u) | (2 * d + 1 < rem ? 0xFFFF0000u : 0u);
+        a[d] &= keep;
+        b[d] &= keep;
+      }
+    }
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                 __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
+  }
+  // acc[r] holds C[8 (r / 4) + 4 half + r % 4][col]
+#pragma unroll
+  for (int r = 0; r < 16; ++r) blk[wid][8 * (r >> 2) + 4 * half + (r & 3)][col] = acc[r];
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  for (int e = e0 + lane; e < e1; e += 64) {
+    const int r = ent_r[e];
+    const int loc = ent_loc[e];
+    Z[i * ldz + r] = w[r] * (out_scale * blk[wid][loc >> 5][loc & 31]);
+  }
+}
+
 struct Work {
-  int32_t* cnt;   // [N + 1] per-example valid-token counts, scanned in place
-  int32_t* tok;   // [N*T] global token index of each valid token
-  float* St;      // [N*T][rows_pad]
+  int32_t* cnt;   // [N + 1] per-example run lengths, scanned in place into offsets
+  int32_t* len;   // [N] valid tokens per example (aligned runs only)
+  int32_t* tok;   // [N*T + 8N] global token index of each listed token
+  float* St;      // [N*T][rows_pad] (fp32 intermediates)
   float* At;      // [N*T][cols_pad]
+  uint16_t* St16; // rows_pad x ldt entries, MFMA-fragment order (fp16 intermediates)
+  uint16_t* At16; // cols_pad x ldt entries
+  int64_t ldt = 0;
 };
+
+// Token capacity of the fp16 layout: runs padded to multiples of 8, the
+// 256-row output tiles of the rotation, and 16 columns read past the last run.
+int64_t f16_ldt(int64_t N, int64_t T) { return round_up(N * T + 8 * N + 256, 256); }
 
 size_t work_bytes(const eogp_plan* p, int64_t N, int64_t T) {
   size_t b = 0;
   b += align256((N + 1) * 4);
-  b += align256((size_t)N * T * 4);
-  b += align256((size_t)N * T * p->rows_pad * 4);
-  b += align256((size_t)N * T * p->cols_pad * 4);
+  b += align256((size_t)N * 4);
+  b += align256((size_t)(N * T + 8 * N) * 4);
+  const size_t f32b = align256((size_t)N * T * p->rows_pad * 4) + align256((size_t)N * T * p->cols_pad * 4);
+  const int64_t ldt = f16_ldt(N, T);
+  const size_t f16b = align256((size_t)ldt * p->rows_pad * 2) + align256((size_t)ldt * p->cols_pad * 2);
+  b += std::max(f32b, f16b);
   return b;
 }
 
@@ -136,21 +246,24 @@ size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T) { return work_
 namespace {
 
 // Steps 1 and 2: compaction of the valid tokens and the two rotations onto
-// the plan's eigenvector panels; fills w (carved from ws).
+// the plan's eigenvector panels; fills w (carved from ws). t16: fp16
+// transposed intermediates with runs aligned to 8 tokens (else fp32,
+// token-major, runs packed).
 eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
                           const void* grads, int64_t ld_grads, bool bf16_in, const uint8_t* mask,
-                          int64_t N, int64_t T, int prec, Work& w, hipStream_t s) {
+                          int64_t N, int64_t T, int prec, bool t16, Work& w, hipStream_t s) {
   // 1. compaction
   const unsigned g4 = (unsigned)ceil_div(N, 4);
   {
     timing::Scope ts(EOGP_KT_COMPACTION, s);
-    hipLaunchKernelGGL(k_count_valid, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt);
+    hipLaunchKernelGGL(k_count_valid, dim3(g4), dim3(256), 0, s, mask, N, T, t16 ? 8 : 1, w.cnt,
+                       t16 ? w.len : nullptr);
     EOGP_HIP(scan_exclusive(w.cnt, N, s));
     hipLaunchKernelGGL(k_write_tokens, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt, w.tok);
   }
   EOGP_LAUNCH_CHECK("token compaction");
 
-  // 2. rotations onto the used eigenvectors (rows = valid tokens; count on device)
+  // 2. rotations onto the used eigenvectors (rows = listed tokens; count on device)
   // FAST: bf16 operands; ACCURATE: bf16 high+low splits (three products);
   // F16: fp32 inputs scaled by 2^e and rounded once to fp16, fp16 bases.
   const bool accurate = prec == EOGP_PREC_ACCURATE;
@@ -167,12 +280,17 @@ eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
   gs.B_lo = p->qs_lo;
   gs.ldb = p->ld_out;
   gs.b_padded = true;
-  gs.C = w.St;
-  gs.ldc = p->rows_pad;
-  gs.M = N * T;
+  if (t16) {
+    gs.CT = w.St16;
+    gs.ldct = w.ldt;
+  } else {
+    gs.C = w.St;
+    gs.ldc = p->rows_pad;
+  }
+  gs.M = t16 ? N * T + 7 * N : N * T;
   gs.M_dev = w.cnt + N;
-  // Columns n_rows..rows_pad-1 of S~ are left unwritten: they only feed
-  // block outputs that are never read.
+  // Columns n_rows..rows_pad-1 of S~ are left unwritten (fp32) or hold
+  // zeros (fp16, zero panel rows): they only feed block outputs never read.
   gs.N = p->n_rows;
   gs.K = p->d_out;
   eogp_status st = gemm_nt(gs, at, a_parts, b_parts, f16, s);
@@ -184,8 +302,12 @@ eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
   ga.B_hi = f16 ? p->qa_f16 : p->qa_hi;
   ga.B_lo = p->qa_lo;
   ga.ldb = p->ld_in;
-  ga.C = w.At;
-  ga.ldc = p->cols_pad;
+  if (t16) {
+    ga.CT = w.At16;
+  } else {
+    ga.C = w.At;
+    ga.ldc = p->cols_pad;
+  }
   ga.N = p->n_cols;
   ga.K = p->d_in;
   return gemm_nt(ga, at, a_parts, b_parts, f16, s);
@@ -194,9 +316,17 @@ eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
 Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
   Work w;
   w.cnt = cv.take<int32_t>(N + 1);
-  w.tok = cv.take<int32_t>((size_t)N * T);
-  w.St = cv.take<float>((size_t)N * T * p->rows_pad);
-  w.At = cv.take<float>((size_t)N * T * p->cols_pad);
+  w.len = cv.take<int32_t>(N);
+  w.tok = cv.take<int32_t>((size_t)(N * T + 8 * N));
+  // the fp32 and fp16 layouts share one region
+  const size_t f32b = align256((size_t)N * T * p->rows_pad * 4) + align256((size_t)N * T * p->cols_pad * 4);
+  w.ldt = f16_ldt(N, T);
+  const size_t f16b = align256((size_t)w.ldt * p->rows_pad * 2) + align256((size_t)w.ldt * p->cols_pad * 2);
+  char* base = cv.take<char>(std::max(f32b, f16b));
+  w.St = reinterpret_cast<float*>(base);
+  w.At = reinterpret_cast<float*>(base + align256((size_t)N * T * p->rows_pad * 4));
+  w.St16 = reinterpret_cast<uint16_t*>(base);
+  w.At16 = reinterpret_cast<uint16_t*>(base + align256((size_t)w.ldt * p->rows_pad * 2));
   return w;
 }
 
@@ -209,9 +339,10 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   if (ws_bytes < work_bytes(p, N, T)) return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
   Carve cv(ws, ws_bytes);
   Work w = carve_work(p, N, T, cv);
-  eogp_status st = rotate_tokens(p, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, w, s);
-  if (st != EOGP_OK) return st;
   const bool f16 = prec == EOGP_PREC_F16;
+  eogp_status st = rotate_tokens(p, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, f16,
+                                 w, s);
+  if (st != EOGP_OK) return st;
 
   // 3. retained products, half-whitened, in canonical order
   const float out_scale = f16 ? std::ldexp(1.f, -(p->e_acts + p->e_grads)) : 1.f;
@@ -219,9 +350,15 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
     const int64_t nex = std::min<int64_t>(65535, N - ex0);
     timing::Scope ts(EOGP_KT_RETAINED, s);
     const unsigned gx = (unsigned)ceil_div(p->n_tiles, (int64_t)kRetWaves);
-    hipLaunchKernelGGL(k_retained, dim3(gx, (unsigned)nex), dim3(256), 0, s,
-                       w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,
-                       p->ent_r, p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
+    if (f16) {
+      hipLaunchKernelGGL(k_retained16, dim3(gx, (unsigned)nex), dim3(256), 0, s,
+                         w.St16, w.At16, w.ldt, w.cnt, w.len, p->tiles, (int)p->n_tiles,
+                         p->ent_r, p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
+    } else {
+      hipLaunchKernelGGL(k_retained, dim3(gx, (unsigned)nex), dim3(256), 0, s,
+                         w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,
+                         p->ent_r, p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
+    }
     EOGP_LAUNCH_CHECK("retained products");
   }
   return EOGP_OK;
@@ -328,7 +465,8 @@ eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int
   basis_panels(Q_S, d_out, q.rows_pad, q.ld_out, list, q.qs_hi, q.qs_lo, q.qs_f16, s);
   basis_panels(Q_A, d_in, q.cols_pad, q.ld_in, list, q.qa_hi, q.qa_lo, q.qa_f16, s);
   EOGP_LAUNCH_CHECK("ekfac panels");
-  eogp_status st = rotate_tokens(&q, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, w, s);
+  eogp_status st = rotate_tokens(&q, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, false,
+                                 w, s);
   if (st != EOGP_OK) return st;
   const int nbj = (int)ceil_div(d_out, 32), nbk = (int)ceil_div(d_in, 32);
   timing::Scope ts(EOGP_KT_EKFAC, s);
