@@ -523,7 +523,7 @@ constexpr int PT = 256;   // k_gemm_p: threads per workgroup
 
 // AT: 0 = fp32 A, 1 = 16-bit A (both with 16-byte aligned rows); B is a padded
 // panel; one part each; no split-K.
-template <int AT, bool F16>
+template <int AT, bool F16, bool SC>
 __global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_gemm_p(KParams kp) {
   constexpr int BNP = 256;
@@ -584,11 +584,21 @@ void k_gemm_p(KParams kp) {
     int64_t a_off[AQ];
 #pragma unroll
     for (int q = 0; q < AQ; ++q) a_off[q] = sOff[a_r0 + a_rs * q];
+    // per-piece base pointers: a slice's load is base + k0
+    const float* pa32[AT == 0 ? AQ : 1];
+    const uint16_t* pa16[AT == 0 ? 1 : AQ];
+#pragma unroll
+    for (int q = 0; q < AQ; ++q) {
+      if constexpr (AT == 0) pa32[q] = static_cast<const float*>(g.A) + a_off[q] + 4 * a_pc;
+      else pa16[q] = static_cast<const uint16_t*>(g.A) + a_off[q] + 8 * a_pc;
+    }
     int64_t b_off[BQ];
+    const uint16_t* pb[BQ];
 #pragma unroll
     for (int q = 0; q < BQ; ++q) {
       const int64_t brow = n0 + b_r0 + 64 * q;
       b_off[q] = (brow < N ? brow : 0) * g.ldb + 8 * b_pc;
+      pb[q] = g.B_hi + b_off[q];
     }
     // Slice order: a ragged last slice first, then the full slices in order.
     auto slice_k0 = [&](int64_t i) -> int64_t {
@@ -609,19 +619,17 @@ void k_gemm_p(KParams kp) {
 
     auto load_a = [&](int64_t k0, ARegs& R) {
       if constexpr (AT == 0) {
-        const float* A = static_cast<const float*>(g.A);
 #pragma unroll
-        for (int q = 0; q < AQ; ++q) R.ra[q] = *reinterpret_cast<const v4f*>(A + a_off[q] + k0 + 4 * a_pc);
+        for (int q = 0; q < AQ; ++q) R.ra[q] = *reinterpret_cast<const v4f*>(pa32[q] + k0);
       } else {
-        const uint16_t* A = static_cast<const uint16_t*>(g.A);
 #pragma unroll
-        for (int q = 0; q < AQ; ++q) R.ra16[q] = *reinterpret_cast<const v4u*>(A + a_off[q] + k0 + 8 * a_pc);
+        for (int q = 0; q < AQ; ++q) R.ra16[q] = *reinterpret_cast<const v4u*>(pa16[q] + k0);
       }
     };
     auto load_b = [&](int64_t k0, BRegs& R) {
 #pragma unroll
       for (int q = 0; q < BQ; ++q)
-        R.rb[q] = *(const __attribute__((address_space(1))) v4u*)(g.B_hi + b_off[q] + k0);
+        R.rb[q] = *(const __attribute__((address_space(1))) v4u*)(pb[q] + k0);
     };
     // The ragged slice: element-wise, bounds-checked (B is a padded panel, so
     // its columns up to round_up(K, 32) are readable and zero beyond K).
@@ -660,7 +668,7 @@ void k_gemm_p(KParams kp) {
           const int r = a_r0 + a_rs * q;
           const int o = swz(r, a_pc >> 1) + 4 * (a_pc & 1);
           v4f x = RA.ra[q];
-          if constexpr (F16) x *= a_scale;
+          if constexpr (F16 && SC) x *= a_scale;
           v2u hv;
           hv.x = cvt_pair<F16>(x.x, x.y);
           hv.y = cvt_pair<F16>(x.z, x.w);
@@ -836,7 +844,10 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
       int64_t grid = std::min<int64_t>(tiles_p, kCus);
       if (grid >= kXcds) grid = grid / kXcds * kXcds;
       timing::Scope ts(g.timing_class, s);
-      hipLaunchKernelGGL((k_gemm_p<AT, F16>), dim3((unsigned)grid), dim3(PT), 0, s, kp);
+      if (F16 && g.a_scale != 1.f)
+        hipLaunchKernelGGL((k_gemm_p<AT, F16, true>), dim3((unsigned)grid), dim3(PT), 0, s, kp);
+      else
+        hipLaunchKernelGGL((k_gemm_p<AT, F16, false>), dim3((unsigned)grid), dim3(PT), 0, s, kp);
       EOGP_LAUNCH_CHECK("gemm launch");
       return EOGP_OK;
     }
