@@ -136,20 +136,30 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, float* C, int64_t 
                                            int64_t N, int64_t r0, int64_t c0, int lane,
                                            const f32x16 (&acc)[WI][WJ]) {
   if (g.CT) {
+    // Rows 16p .. 16p+15 of a block are one 16-token group: lanes l < 32 hold
+    // rows +0..3 (q = 2p) and +8..11 (q = 2p+1), lanes l >= 32 rows +4..7 and
+    // +12..15. One swap between lane l and lane l + 32 gives lane l tokens
+    // 0..7 and lane l + 32 tokens 8..15 of column l % 32, so each wave store
+    // writes one whole 1 KB block.
     const int64_t groups = g.ldct / 16;
+    const int half = lane >> 5;
 #pragma unroll
     for (int i = 0; i < WI; ++i)
 #pragma unroll
       for (int j = 0; j < WJ; ++j) {
         const int64_t cb = (c0 + 32 * j) / 32;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int64_t row = r0 + 32 * i + 8 * q + 4 * (lane >> 5);
-          uint16_t* dst = g.CT + ((cb * groups + row / 16) * 32 + (lane & 31)) * 16 + row % 16;
-          v2u h;
-          h.x = cvt_pair<true>(acc[i][j][4 * q + 0], acc[i][j][4 * q + 1]);
-          h.y = cvt_pair<true>(acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]);
-          *reinterpret_cast<v2u*>(dst) = h;
+        for (int p = 0; p < 2; ++p) {
+          const f32x16& a = acc[i][j];
+          const uint32_t x0 = cvt_pair<true>(a[8 * p + 0], a[8 * p + 1]);
+          const uint32_t x1 = cvt_pair<true>(a[8 * p + 2], a[8 * p + 3]);
+          const uint32_t y0 = cvt_pair<true>(a[8 * p + 4], a[8 * p + 5]);
+          const uint32_t y1 = cvt_pair<true>(a[8 * p + 6], a[8 * p + 7]);
+          const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
+          const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
+          const int64_t grp = (r0 + 32 * i + 16 * p) / 16;
+          uint16_t* dst = g.CT + ((cb * groups + grp) * 32 + (lane & 31)) * 16 + 8 * half;
+          *reinterpret_cast<v4u*>(dst) = mk4(s0[0], s1[0], s0[1], s1[1]);
         }
       }
     return;

@@ -134,14 +134,15 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
 
 // fp16 intermediates: S~ and A~ in MFMA-fragment order (for every 32 rows j
 // and 16 tokens t one contiguous 1 KB block, j-major, 16 tokens per j; token
-// capacity ldt); example i's tokens are t = off[i] .. off[i] + len[i] - 1,
+// capacity ldt, at least 16 kRet16Unroll + 16 tokens past the last run);
+// example i's tokens are t = off[i] .. off[i] + len[i] - 1,
 // off[i] a multiple of 8. One wave per (active block, example) as above; each
 // v_mfma_f32_32x32x16_f16 takes 16 tokens: lane l feeds row l % 32 and tokens
 // 8 (l / 32) .. +7 of each operand with one 16-byte load (the wave reads one
 // whole 1 KB block, or two halves of neighbouring blocks when the run starts
 // at an odd multiple of 8). Tokens past the example's last one (padding, or
 // the next example) are zeroed in both operands before they reach the MFMA.
-constexpr int kRet16Unroll = 4;
+constexpr int kRet16Unroll = 8;
 
 __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__ St,
                                                     const uint16_t* __restrict__ At, int64_t ldt,
@@ -172,8 +173,11 @@ __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__
   f32x16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-  int t = 0;
-  for (; t + 16 * kRet16Unroll <= n; t += 16 * kRet16Unroll) {
+  // Batches of kRet16Unroll steps: all loads of a batch are issued first (a
+  // batch may read up to 16 kRet16Unroll tokens past the run, inside the
+  // buffer's slack), then the steps that hold tokens of the run are
+  // multiplied, the last one with the tokens past the run zeroed.
+  for (int t = 0; t < n; t += 16 * kRet16Unroll) {
     v4u a[kRet16Unroll], b[kRet16Unroll];
 #pragma unroll
     for (int u = 0; u < kRet16Unroll; ++u) {
@@ -181,24 +185,21 @@ __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__
       b[u] = *reinterpret_cast<const v4u*>(ap + (int64_t)(t / 16 + u) * 512);
     }
 #pragma unroll
-    for (int u = 0; u < kRet16Unroll; ++u)
+    for (int u = 0; u < kRet16Unroll; ++u) {
+      const int tu = t + 16 * u;
+      if (tu >= n) break;
+      const int rem = n - tu - 8 * half;       // valid tokens among this lane's eight
+      if (tu + 16 > n) {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const uint32_t keep = (2 * d < rem ? 0x0000FFFFu : 0u) | (2 * d + 1 < rem ? 0xFFFF0000u : 0u);
+          a[u][d] &= keep;
+          b[u][d] &= keep;
+        }
+      }
       acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a[u]),
                                                    __builtin_bit_cast(f16x8, b[u]), acc, 0, 0, 0);
-  }
-  for (; t < n; t += 16) {
-    v4u a = *reinterpret_cast<const v4u*>(sp + (int64_t)(t / 16) * 512);
-    v4u b = *reinterpret_cast<const v4u*>(ap + (int64_t)(t / 16) * 512);
-    const int rem = n - t - 8 * half;          // valid tokens among this lane's eight
-    if (rem < 8) {
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        const uint32_t keep = (2 * d < rem ? 0x0000FFFFu : 0u) | (2 * d + 1 < rem ? 0xFFFF0000u : 0u);
-        a[d] &= keep;
-        b[d] &= keep;
-      }
     }
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
-                                                 __builtin_bit_cast(f16x8, b), acc, 0, 0, 0);
   }
   // acc[r] holds C[8 (r / 4) + 4 half + r % 4][col]
 #pragma unroll
@@ -224,7 +225,8 @@ struct Work {
 };
 
 // Token capacity of the fp16 layout: runs padded to multiples of 8, the
-// 256-row output tiles of the rotation, and 16 columns read past the last run.
+// 256-row output tiles of the rotation, and the up to 16 kRet16Unroll + 8
+// tokens a batch of the retained products reads past the last run.
 int64_t f16_ldt(int64_t N, int64_t T) { return round_up(N * T + 8 * N + 256, 256); }
 
 size_t work_bytes(const eogp_plan* p, int64_t N, int64_t T) {
