@@ -2,7 +2,8 @@
 //
 // Two kernels share the staging conventions below.
 //
-// k_gemm_p (single-pass products without split-K: the rotations). A 256-thread
+// k_gemm_p (single-pass products on aligned operands: the rotations, and the
+// PCA projection with split-K). A 256-thread
 // workgroup (4 wave64s, one per SIMD) owns a 256 x 256 output tile; each wave
 // computes 128 x 128 with v_mfma_f32_32x32x16 blocks accumulating in the
 // accumulation registers. K advances 32 at a time through two LDS stages. One
@@ -13,8 +14,8 @@
 // read while the second half's MFMAs issue. A is requested two slices before
 // it is staged (two register buffers), B one slice before.
 //
-// k_gemm (everything else: bf16x3 products, split-K, unaligned or
-// bounds-checked operands). A 512-thread workgroup (8 waves, two per SIMD)
+// k_gemm (everything else: bf16x3 products, unaligned or bounds-checked
+// operands). A 512-thread workgroup (8 waves, two per SIMD)
 // owns a 256 x BN tile (BN = 256 or 128, whichever pads N less); each wave
 // computes 128 x BN/4. Slice k+1 sits in registers while slice k is multiplied
 // from LDS; then it is converted and written to the other stage and slice k+2
@@ -547,7 +548,7 @@ void k_gemm_p(KParams kp) {
   const int64_t M = g.M_dev ? (int64_t)(*g.M_dev) : g.M;
   const int64_t N = g.N, K = g.K;
   const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BNP - 1) / BNP;
-  const int64_t n_units = tiles_m * tiles_n;
+  const int64_t n_units = tiles_m * tiles_n * kp.splits;
 
   const int G = gridDim.x, b = blockIdx.x;
   int64_t t_begin, t_end, t_step;
@@ -575,13 +576,16 @@ void k_gemm_p(KParams kp) {
   const int b_r0 = tid >> 2, b_pc = tid & 3;
 
   for (int64_t u = t_begin; u < t_end; u += t_step) {
+    const int64_t t = u / kp.splits;
+    const int split = (int)(u % kp.splits);
     int64_t tm, tn;
-    if (g.n_major) { tn = u / tiles_m; tm = u % tiles_m; }
-    else { tm = u / tiles_n; tn = u % tiles_n; }
+    if (g.n_major) { tn = t / tiles_m; tm = t % tiles_m; }
+    else { tm = t / tiles_n; tn = t % tiles_n; }
     const int64_t m0 = tm * BM, n0 = tn * BNP;
-    const int64_t kend = K;
-    const int64_t nk = (K + BK - 1) / BK;
-    const bool ragged = (K % BK) != 0;
+    const int64_t kbeg = split * kp.kc;
+    const int64_t kend = std::min<int64_t>(K, kbeg + kp.kc);
+    const int64_t nk = (kend - kbeg + BK - 1) / BK;
+    const bool ragged = ((kend - kbeg) % BK) != 0;
 
     __syncthreads();                     // previous unit's readers of sOff / stages are done
     {
@@ -613,7 +617,7 @@ void k_gemm_p(KParams kp) {
     // Slice order: a ragged last slice first, then the full slices in order.
     auto slice_k0 = [&](int64_t i) -> int64_t {
       const int64_t s = ragged ? (i == 0 ? nk - 1 : i - 1) : i;
-      return s * BK;
+      return kbeg + s * BK;
     };
     auto clamp = [&](int64_t i) { return slice_k0(std::min<int64_t>(i, nk - 1)); };
 
@@ -798,7 +802,13 @@ void k_gemm_p(KParams kp) {
       mma(F0);
       mma(F1);
     }
-    store_tile<WI, WJ>(g, g.C, g.ldc, M, N, m0 + wm, n0 + wn, lane, acc);
+    float* C = g.C;
+    int64_t ldc = g.ldc;
+    if (kp.splits > 1) {
+      C = g.partial + (int64_t)split * M * N;
+      ldc = N;
+    }
+    store_tile<WI, WJ>(g, C, ldc, M, N, m0 + wm, n0 + wn, lane, acc);
   }
 }
 
@@ -848,17 +858,43 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
     }
   }
   if constexpr (AP == 1 && BP == 1) {
-    if (av && !bc && kp.splits == 1) {
-      // single-pass product: the pipelined 4-wave kernel, 256 x 256 tiles
+    if (av && !bc) {
+      // single-pass product: the pipelined 4-wave kernel, 256 x 256 tiles.
+      // Split K (host-known M, scratch given) when that shortens the
+      // estimated time: rounds of units x slices per unit, plus the partial
+      // sums (one slice of a 256 x 256 tile ~ 1.4 us; partials at ~5 TB/s).
       const int64_t tiles_p = ((g.M + BM - 1) / BM) * ((g.N + 255) / 256);
-      int64_t grid = std::min<int64_t>(tiles_p, kCus);
+      KParams kq = kp;
+      kq.splits = 1;
+      kq.kc = nk_all * BK;
+      if (!g.M_dev && g.partial && !g.CT && tiles_p < kCus) {
+        double best = 1e30;
+        for (int sp = 1; sp <= g.max_splits && sp <= std::max<int64_t>(1, nk_all / 16); ++sp) {
+          const int64_t kc = ceil_div(nk_all, sp);
+          const int64_t units = tiles_p * ceil_div(nk_all, kc);
+          const double t_us = (double)ceil_div(units, kCus) * kc * 1.4 +
+                              (sp > 1 ? (double)sp * g.M * g.N * 4 / 5e6 : 0.0);
+          if (t_us < best) {
+            best = t_us;
+            kq.kc = kc * BK;
+            kq.splits = (int)ceil_div(nk_all, kc);
+          }
+        }
+      }
+      int64_t grid = std::min<int64_t>(tiles_p * kq.splits, kCus);
       if (grid >= kXcds) grid = grid / kXcds * kXcds;
       timing::Scope ts(g.timing_class, s);
       if (F16 && g.a_scale != 1.f)
-        hipLaunchKernelGGL((k_gemm_p<AT, F16, true>), dim3((unsigned)grid), dim3(PT), 0, s, kp);
+        hipLaunchKernelGGL((k_gemm_p<AT, F16, true>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
       else
-        hipLaunchKernelGGL((k_gemm_p<AT, F16, false>), dim3((unsigned)grid), dim3(PT), 0, s, kp);
+        hipLaunchKernelGGL((k_gemm_p<AT, F16, false>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
       EOGP_LAUNCH_CHECK("gemm launch");
+      if (kq.splits > 1) {
+        const int64_t total = g.M * g.N;
+        hipLaunchKernelGGL(k_split_sum, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                           g.partial, kq.splits, g.M, g.N, g.C, g.ldc);
+        EOGP_LAUNCH_CHECK("gemm split sum");
+      }
       return EOGP_OK;
     }
   }
