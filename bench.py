@@ -235,11 +235,13 @@ class Gpt2Step:
 
     def rotation_bytes_per_step(self):
         """Algorithmic HBM bytes of the rotation contractions: each valid token
-        row read once (fp32), the rotated rows written once (fp32)."""
+        row read once (fp32), the rotated rows written once (fp16 in the fp16
+        mode, else fp32)."""
+        out_b = 2 if self.prec == self.E.PREC_F16 else 4
         tot = 0
         for u, (name, di, do) in enumerate(self.modules):
             p = self.plans[u]
-            tot += 4 * (di + do + p.n_rows + p.n_cols) * (self.valid_tokens + self.valid_q_tokens)
+            tot += (4 * (di + do) + out_b * (p.n_rows + p.n_cols)) * (self.valid_tokens + self.valid_q_tokens)
         return tot
 
 
@@ -429,7 +431,7 @@ def main(argv=None):
                        "topk": st.topk, "pca": f"fp16 P, {args.pca_prec}",
                        "first_stage": args.prec},
             "roofline": {
-                "kernel": "first-stage rotation contraction (k_gemm)",
+                "kernel": "first-stage rotation contraction (k_gemm_p)",
                 "bound": "mfma",
                 "achieved": achieved,
                 "peak": BF16_PEAK_TFLOPS,

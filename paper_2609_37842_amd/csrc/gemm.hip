@@ -11,8 +11,8 @@
 // are read and the first half's 16 MFMAs issue beside the staging of the next
 // slice (B, then A converted while it is written) and the global requests for
 // later slices; after the barrier the next slice's first-half fragments are
-// read while the second half's MFMAs issue. A is requested two slices before
-// it is staged (two register buffers), B one slice before.
+// read while the second half's MFMAs issue. A and B are requested two slices
+// before they are staged (two register buffers each).
 //
 // k_gemm (everything else: bf16x3 products, unaligned or bounds-checked
 // operands). A 512-thread workgroup (8 waves, two per SIMD)
@@ -628,7 +628,7 @@ void k_gemm_p(KParams kp) {
     struct BRegs { v4u rb[BQ]; };
     struct Frag { v4u a[WI]; v4u b[WJ]; };
     ARegs A0, A1;
-    BRegs RB;
+    BRegs RB, RB2;
     Frag F0, F1;
 
     auto load_a = [&](int64_t k0, ARegs& R) {
@@ -731,7 +731,8 @@ void k_gemm_p(KParams kp) {
     };
     auto mma = [&](const Frag& F) { mma_part(F, 1, 0); };
 
-    // prologue: slice 0 staged, slice 1 in A1 and RB, slice 2 in flight into A0
+    // prologue: slice 0 staged; slices 1 and 2 requested (A into A1 and A0,
+    // B into RB and RB2)
     if (ragged) load_tail(slice_k0(0), A0, RB);
     else {
       load_a(slice_k0(0), A0);
@@ -741,6 +742,7 @@ void k_gemm_p(KParams kp) {
     stage_b(0, RB);
     if (nk > 1) {
       load_b(clamp(1), RB);
+      load_b(clamp(2), RB2);
       load_a(clamp(1), A1);
       load_a(clamp(2), A0);
     }
@@ -748,17 +750,18 @@ void k_gemm_p(KParams kp) {
     read_frag(0, 0, F0);
 
     // One slice i in stage st (F0 holds its first half; the registers hold
-    // slice i+1, A and B, and slice i+2, A). Scheduling hints keep the three
-    // regions apart and spread each region's MFMAs over its other work.
-    auto iter = [&](int st, int64_t i, ARegs& Anext) {
-      const int64_t kb2 = clamp(i + 2), ka3 = clamp(i + 3);
+    // slices i+1 and i+2 of A and B; RB is the B buffer holding slice i+1).
+    // Scheduling hints keep the three regions apart and spread each region's
+    // MFMAs over its other work.
+    auto iter = [&](int st, int64_t i, ARegs& Anext, BRegs& RB) {
+      const int64_t k3 = clamp(i + 3);
       // region 1a: second-half fragment reads; B of slice i+1 to LDS; B of
-      // slice i+2 requested before A of slice i+3, so that a wait for B never
+      // slice i+3 requested before A of slice i+3, so that a wait for B never
       // waits for the A request behind it
       __builtin_amdgcn_sched_barrier(0);
       read_frag(st, 1, F1);
       stage_b(st ^ 1, RB);
-      load_b(kb2, RB);
+      load_b(k3, RB);
       mma_part(F0, 0, NMB);
 #pragma unroll
       for (int m = 0; m < NMB; ++m) {
@@ -773,7 +776,7 @@ void k_gemm_p(KParams kp) {
       // LDS) and the request of A of slice i+3
       mma_part(F0, 1, NMB);
       stage_a(st ^ 1, Anext);
-      load_a(ka3, Anext);
+      load_a(k3, Anext);
 #pragma unroll
       for (int m = 0; m < NM - NMB; ++m) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
@@ -794,8 +797,8 @@ void k_gemm_p(KParams kp) {
     };
     int64_t p = 0;
     for (; p + 2 <= nk; p += 2) {
-      iter(0, p, A1);
-      iter(1, p + 1, A0);
+      iter(0, p, A1, RB);
+      iter(1, p + 1, A0, RB2);
     }
     if (p < nk) {                            // odd count: the last slice is in stage 0
       read_frag(0, 1, F1);
