@@ -153,9 +153,10 @@ eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
 
 /* One-shot form with the paper's arguments: builds a plan from
  * (eigvals, damping, m, Q_A, Q_S), runs the first stage, releases the plan.
- * Synchronises `stream`. Workspace: eogp_rotate_retain_oneshot_workspace_size. */
+ * Synchronises `stream`. Workspace: eogp_rotate_retain_oneshot_workspace_size
+ * (an upper bound for any plan of these shapes; 0 for invalid sizes). */
 size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d_in,
-                                                 int64_t d_out);
+                                                 int64_t d_out, int64_t m);
 eogp_status eogp_rotate_retain(const void* acts, int64_t ld_acts, const void* out_grads,
                                int64_t ld_grads, eogp_dtype in_dtype,
                                const uint8_t* token_mask,

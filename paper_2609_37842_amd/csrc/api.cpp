@@ -189,11 +189,12 @@ eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
 }
 
 size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d_in,
-                                                 int64_t d_out) {
-  if (N < 0 || T < 0 || d_in < 1 || d_out < 1) return 0;
+                                                 int64_t d_out, int64_t m) {
+  if (N < 0 || T < 0 || d_in < 1 || d_out < 1 || m < 1) return 0;
   eogp_plan probe;
   probe.rows_pad = round_up(d_out, kPanelTile);
   probe.cols_pad = round_up(d_in, kPanelTile);
+  probe.m = m;
   return rotate_retain_ws(&probe, N, T);
 }
 
@@ -207,7 +208,7 @@ eogp_status eogp_rotate_retain(const void* acts, int64_t ld_acts, const void* ou
   eogp_status st = check_plan_args(eigvals, d_out, d_in, damping, m, Q_A, Q_S);
   if (st != EOGP_OK) return st;
   if (ldz < m) return fail(EOGP_ERR_INVALID, "rotate_retain: ldz < m");
-  if (ws_bytes < eogp_rotate_retain_oneshot_workspace_size(N, T, d_in, d_out) || (!ws && N > 0))
+  if (ws_bytes < eogp_rotate_retain_oneshot_workspace_size(N, T, d_in, d_out, m) || (!ws && N > 0))
     return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
   eogp_plan* plan = nullptr;
   st = build_plan(eigvals, d_out, d_in, damping, m, Q_A, Q_S, S(stream), &plan);

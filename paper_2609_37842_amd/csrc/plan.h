@@ -21,6 +21,7 @@ struct eogp_plan {
   int32_t* tiles = nullptr;      // [n_tiles][4] = {row block, col block, entry begin, entry end}
   int32_t* ent_r = nullptr;      // [m]   retained position of each entry, grouped by tile
   uint16_t* ent_loc = nullptr;   // [m]   (row in block) * 32 + (col in block)
+  int32_t* ent_pos = nullptr;    // [m]   entry index of each retained position (inverse of ent_r)
   uint16_t* qs_hi = nullptr;     // [rows_pad][ld_out] bf16: Q_S[:, J[p]] high part
   uint16_t* qs_lo = nullptr;     // [rows_pad][ld_out] bf16: low part
   uint16_t* qa_hi = nullptr;     // [cols_pad][ld_in]  bf16: Q_A[:, K[p]] high part

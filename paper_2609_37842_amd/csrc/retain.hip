@@ -9,8 +9,9 @@
 // 3. Retained products: for every example and every 32 x 32 block of
 //    (row, column) pairs that holds retained axes, the block of sums
 //    sum_t S~[t, j] A~[t, k] over the example's tokens is formed (MFMA)
-//    and the retained entries are scaled by w_r and written to their
-//    canonical positions in Z.
+//    and the retained entries are written, tile by tile, to a contiguous
+//    row; a gather then scales them by w_r into their canonical positions
+//    in Z.
 //
 // Intermediates. FAST and ACCURATE keep S~ and A~ in fp32, token-major, and
 // form the sums with exact fp32 products. The fp16 mode stores them as fp16
@@ -86,12 +87,9 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
                                                   const float* __restrict__ At, int64_t ldA,
                                                   const int32_t* __restrict__ ex_off,
                                                   const int32_t* __restrict__ tiles, int n_tiles,
-                                                  const int32_t* __restrict__ ent_r,
                                                   const uint16_t* __restrict__ ent_loc,
-                                                  const float* __restrict__ w,
-                                                  float out_scale,
-                                                  float* __restrict__ Z, int64_t ldz,
-                                                  int64_t ex0) {
+                                                  float out_scale, float* __restrict__ Zt,
+                                                  int64_t m, int64_t ex0) {
   __shared__ float blk[kRetWaves][32][33];
   const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int tile = blockIdx.x * kRetWaves + wid;
@@ -126,9 +124,8 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
   for (int e = e0 + lane; e < e1; e += 64) {
-    const int r = ent_r[e];
     const int loc = ent_loc[e];
-    Z[i * ldz + r] = w[r] * (out_scale * blk[wid][loc >> 5][loc & 31]);
+    Zt[i * m + e] = out_scale * blk[wid][loc >> 5][loc & 31];
   }
 }
 
@@ -149,10 +146,9 @@ __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__
                                                     const int32_t* __restrict__ ex_off,
                                                     const int32_t* __restrict__ ex_len,
                                                     const int32_t* __restrict__ tiles, int n_tiles,
-                                                    const int32_t* __restrict__ ent_r,
                                                     const uint16_t* __restrict__ ent_loc,
-                                                    const float* __restrict__ w, float out_scale,
-                                                    float* __restrict__ Z, int64_t ldz, int64_t ex0) {
+                                                    float out_scale, float* __restrict__ Zt,
+                                                    int64_t m, int64_t ex0) {
   typedef unsigned int v4u __attribute__((ext_vector_type(4)));
   __shared__ float blk[kRetWaves][32][33];
   const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -207,9 +203,37 @@ __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
   for (int e = e0 + lane; e < e1; e += 64) {
-    const int r = ent_r[e];
     const int loc = ent_loc[e];
-    Z[i * ldz + r] = w[r] * (out_scale * blk[wid][loc >> 5][loc & 31]);
+    Zt[i * m + e] = out_scale * blk[wid][loc >> 5][loc & 31];
+  }
+}
+
+// Coordinates in canonical order: the retained kernels write each example's
+// block sums in entry (tile) order, contiguously, to Zt; one workgroup per
+// example then gathers them into canonical order and applies the weights:
+//   Z[i, r] = w_r * Zt[i, pos(r)].
+// (Writing canonical positions straight from the blocks scatters 4-byte
+// stores over the whole row, which cost as much as the products themselves.)
+// Grid: (coordinate chunks of 2048, examples).
+constexpr int kZpermPer = 8;    // coordinates per thread (independent gathers in flight)
+
+__global__ __launch_bounds__(256) void k_zperm(const float* __restrict__ Zt, int64_t m,
+                                               const int32_t* __restrict__ ent_pos,
+                                               const float* __restrict__ w,
+                                               float* __restrict__ Z, int64_t ldz, int64_t ex0) {
+  const int64_t i = ex0 + blockIdx.y;
+  const float* src = Zt + i * m;
+  const int64_t r0 = (int64_t)blockIdx.x * 256 * kZpermPer + threadIdx.x;
+  float v[kZpermPer];
+#pragma unroll
+  for (int e = 0; e < kZpermPer; ++e) {
+    const int64_t r = r0 + 256 * e;
+    v[e] = r < m ? src[ent_pos[r]] : 0.f;
+  }
+#pragma unroll
+  for (int e = 0; e < kZpermPer; ++e) {
+    const int64_t r = r0 + 256 * e;
+    if (r < m) Z[i * ldz + r] = w[r] * v[e];
   }
 }
 
@@ -222,6 +246,7 @@ struct Work {
   uint16_t* St16; // rows_pad x ldt entries, MFMA-fragment order (fp16 intermediates)
   uint16_t* At16; // cols_pad x ldt entries
   int64_t ldt = 0;
+  float* Zt;      // [N][m] block sums in entry order (retained products only)
 };
 
 // Token capacity of the fp16 layout: runs padded to multiples of 8, the
@@ -238,6 +263,7 @@ size_t work_bytes(const eogp_plan* p, int64_t N, int64_t T) {
   const int64_t ldt = f16_ldt(N, T);
   const size_t f16b = align256((size_t)ldt * p->rows_pad * 2) + align256((size_t)ldt * p->cols_pad * 2);
   b += std::max(f32b, f16b);
+  b += align256((size_t)N * p->m * 4);
   return b;
 }
 
@@ -329,6 +355,7 @@ Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
   w.At = reinterpret_cast<float*>(base + align256((size_t)N * T * p->rows_pad * 4));
   w.St16 = reinterpret_cast<uint16_t*>(base);
   w.At16 = reinterpret_cast<uint16_t*>(base + align256((size_t)w.ldt * p->rows_pad * 2));
+  w.Zt = cv.take<float>((size_t)N * p->m);
   return w;
 }
 
@@ -355,12 +382,14 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
     if (f16) {
       hipLaunchKernelGGL(k_retained16, dim3(gx, (unsigned)nex), dim3(256), 0, s,
                          w.St16, w.At16, w.ldt, w.cnt, w.len, p->tiles, (int)p->n_tiles,
-                         p->ent_r, p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
+                         p->ent_loc, out_scale, w.Zt, p->m, ex0);
     } else {
       hipLaunchKernelGGL(k_retained, dim3(gx, (unsigned)nex), dim3(256), 0, s,
                          w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,
-                         p->ent_r, p->ent_loc, p->ret_w, out_scale, Z, ldz, ex0);
+                         p->ent_loc, out_scale, w.Zt, p->m, ex0);
     }
+    hipLaunchKernelGGL(k_zperm, dim3((unsigned)ceil_div(p->m, 256 * kZpermPer), (unsigned)nex),
+                       dim3(256), 0, s, w.Zt, p->m, p->ent_pos, p->ret_w, Z, ldz, ex0);
     EOGP_LAUNCH_CHECK("retained products");
   }
   return EOGP_OK;

@@ -263,7 +263,7 @@ __global__ void k_tile_prep(const int* tcount, int64_t nt, long long* toff, long
 __global__ void k_tile_place(const int32_t* __restrict__ ret, int64_t m, int64_t d_in,
                              const int* __restrict__ jpos, const int* __restrict__ kpos,
                              const int* __restrict__ rtile, const long long* toff, int* cursor,
-                             int32_t* ent_r, uint16_t* ent_loc) {
+                             int32_t* ent_r, uint16_t* ent_loc, int32_t* ent_pos) {
   int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= m) return;
   int32_t f = ret[r];
@@ -272,6 +272,7 @@ __global__ void k_tile_place(const int32_t* __restrict__ ret, int64_t m, int64_t
   long long p = toff[tile] + atomicAdd(&cursor[tile], 1);
   ent_r[p] = (int32_t)r;
   ent_loc[p] = (uint16_t)(((jp & 31) << 5) | (kp & 31));
+  ent_pos[r] = (int32_t)p;
 }
 
 __global__ void k_tile_desc(const int* tcount, int64_t nt, int n_kt, const long long* toff,
@@ -434,7 +435,7 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   size_t pb = 0;
   auto padd = [&](size_t b) { size_t o = pb; pb = align256(pb + b); return o; };
   size_t q_ret = padd(m * 4), q_w = padd(m * 4), q_tiles = padd(std::max<int64_t>(n_active, 1) * 16);
-  size_t q_er = padd(m * 4), q_el = padd(m * 2);
+  size_t q_er = padd(m * 4), q_el = padd(m * 2), q_ep = padd(m * 4);
   size_t q_sh = padd(p->rows_pad * p->ld_out * 2), q_sl = padd(p->rows_pad * p->ld_out * 2);
   size_t q_ah = padd(p->cols_pad * p->ld_in * 2), q_al = padd(p->cols_pad * p->ld_in * 2);
   size_t q_s16 = padd(p->rows_pad * p->ld_out * 2), q_a16 = padd(p->cols_pad * p->ld_in * 2);
@@ -449,6 +450,7 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   p->tiles = (int32_t*)(base + q_tiles);
   p->ent_r = (int32_t*)(base + q_er);
   p->ent_loc = (uint16_t*)(base + q_el);
+  p->ent_pos = (int32_t*)(base + q_ep);
   p->qs_hi = (uint16_t*)(base + q_sh);
   p->qs_lo = (uint16_t*)(base + q_sl);
   p->qa_hi = (uint16_t*)(base + q_ah);
@@ -462,7 +464,7 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
     return fail(EOGP_ERR_DEVICE, "plan build: copy failed");
   }
   hipLaunchKernelGGL(k_tile_place, dim3(grid_for(m, 256)), dim3(256), 0, s, ret, m, d_in, jpos,
-                     kpos, rt, toff, cur, p->ent_r, p->ent_loc);
+                     kpos, rt, toff, cur, p->ent_r, p->ent_loc, p->ent_pos);
   hipLaunchKernelGGL(k_tile_desc, dim3(grid_for(nt, 256)), dim3(256), 0, s, tc, nt, n_kt, toff,
                      flag, p->tiles);
   hipLaunchKernelGGL(k_gather_panel, dim3((unsigned)(p->rows_pad / 32), grid_for(p->ld_out, 32)),

@@ -74,7 +74,7 @@ def load(path: str | None = None):
         "eogp_rotate_retain_workspace_size": (c_sz, [c_vp, c_i64, c_i64]),
         "eogp_rotate_retain_planned": (c_i32, [c_vp, c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64,
                                                c_i64, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
-        "eogp_rotate_retain_oneshot_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64]),
+        "eogp_rotate_retain_oneshot_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64, c_i64]),
         "eogp_rotate_retain": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64, c_i64,
                                        c_i64, c_vp, c_vp, c_vp, ctypes.c_double, c_i64, c_vp, c_i64,
                                        c_i32, c_vp, c_sz, c_vp]),
@@ -249,7 +249,7 @@ def eogp_rotate_retain(acts, out_grads, token_mask, Q_A, Q_S, eigvals, damping, 
     ld_a, ld_g = _token_stride(acts, "acts"), _token_stride(out_grads, "out_grads")
     if Z is None:
         Z = torch.empty((N, m), dtype=torch.float32, device=acts.device)
-    need = int(L.eogp_rotate_retain_oneshot_workspace_size(N, T, d_in, d_out))
+    need = int(L.eogp_rotate_retain_oneshot_workspace_size(N, T, d_in, d_out, int(m)))
     ws, wsb = _workspace(need, acts.device, ws)
     _check(L.eogp_rotate_retain(_ptr(acts), ld_a, _ptr(out_grads), ld_g, _acts_dtype(acts, out_grads),
                                 _ptr(token_mask), N, T, d_in, d_out, _ptr(Q_A), _ptr(Q_S),

@@ -97,9 +97,11 @@ def test_workspace_size_queries_are_consistent():
     big = E.eogp_score_topk_workspace_size(100000, 40, ks, 10)
     assert 0 < small < big
     L = E.load()
-    a = L.eogp_rotate_retain_oneshot_workspace_size(4, 16, 64, 64)
-    b = L.eogp_rotate_retain_oneshot_workspace_size(8, 16, 64, 64)
-    assert 0 < a < b
+    a = L.eogp_rotate_retain_oneshot_workspace_size(4, 16, 64, 64, 500)
+    b = L.eogp_rotate_retain_oneshot_workspace_size(8, 16, 64, 64, 500)
+    c = L.eogp_rotate_retain_oneshot_workspace_size(8, 16, 64, 64, 4000)
+    assert 0 < a < b < c
+    assert L.eogp_rotate_retain_oneshot_workspace_size(8, 16, 64, 64, 0) == 0
     f16 = L.eogp_pca_project_workspace_size(100, 512, 128, 2, 0)     # fp16 P: split-K scratch
     f32 = L.eogp_pca_project_workspace_size(100, 512, 128, 0, 1)     # fp32 P: + split copy
     assert 0 < f16 < f32
