@@ -815,7 +815,8 @@ void k_gemm_p(KParams kp) {
   }
 }
 
-// C[row, col] = sum over splits, in split order, of the partial tiles.
+// C[row, col] = sum over splits, in split order, of the partial tiles. Four
+// consecutive columns per thread (16-byte loads) when N and ldc allow it.
 __global__ void k_split_sum(const float* __restrict__ part, int splits, int64_t M, int64_t N,
                             float* __restrict__ C, int64_t ldc) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -824,6 +825,24 @@ __global__ void k_split_sum(const float* __restrict__ part, int splits, int64_t 
   float s = 0.f;
   for (int p = 0; p < splits; ++p) s += part[(int64_t)p * M * N + idx];
   C[row * ldc + col] = s;
+}
+__global__ void k_split_sum4(const float* __restrict__ part, int splits, int64_t M, int64_t N,
+                             float* __restrict__ C, int64_t ldc) {
+  const int64_t idx = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+  if (idx >= M * N) return;
+  const int64_t row = idx / N, col = idx % N;
+  v4f s = {0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < splits; ++p) s += *reinterpret_cast<const v4f*>(part + (int64_t)p * M * N + idx);
+  *reinterpret_cast<v4f*>(C + row * ldc + col) = s;
+}
+void split_sum(const GemmArgs& g, int splits, hipStream_t s) {
+  const int64_t total = g.M * g.N;
+  if (g.N % 4 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.C % 16 == 0)
+    hipLaunchKernelGGL(k_split_sum4, dim3((unsigned)((total / 4 + 255) / 256)), dim3(256), 0, s,
+                       g.partial, splits, g.M, g.N, g.C, g.ldc);
+  else
+    hipLaunchKernelGGL(k_split_sum, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                       g.partial, splits, g.M, g.N, g.C, g.ldc);
 }
 
 template <int AT, int AP, int BP, bool F16, int BN>
@@ -893,9 +912,7 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
         hipLaunchKernelGGL((k_gemm_p<AT, F16, false>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
       EOGP_LAUNCH_CHECK("gemm launch");
       if (kq.splits > 1) {
-        const int64_t total = g.M * g.N;
-        hipLaunchKernelGGL(k_split_sum, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
-                           g.partial, kq.splits, g.M, g.N, g.C, g.ldc);
+        split_sum(g, kq.splits, s);
         EOGP_LAUNCH_CHECK("gemm split sum");
       }
       return EOGP_OK;
@@ -909,9 +926,7 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
   else pick<AT, AP, BP, F16, 128>(kp, av, bc, (unsigned)grid, s);
   EOGP_LAUNCH_CHECK("gemm launch");
   if (kp.splits > 1) {
-    const int64_t total = g.M * g.N;
-    hipLaunchKernelGGL(k_split_sum, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
-                       g.partial, kp.splits, g.M, g.N, g.C, g.ldc);
+    split_sum(g, kp.splits, s);
     EOGP_LAUNCH_CHECK("gemm split sum");
   }
   return EOGP_OK;
