@@ -202,6 +202,32 @@ def test_pca_directions_orthonormal_and_eigen(tiny_fit):
     assert np.all(np.diff(mu) <= 1e-15)
 
 
+def test_pca_fit_equals_svd_and_gram_routes():
+    # PCA fitting (appendix on PCA fitting): the columns of P are the top-k
+    # right singular vectors of Z, equivalently eigenvectors of Z^T Z / n, and
+    # they follow from the n x n Gram matrix Z Z^T as Z^T v / sqrt(lambda).
+    # Both routes (an SVD, and the Gram eigendecomposition) must give the
+    # oracle's P up to the sign rule, for n < m and n > m.
+    g = np.random.default_rng(31)
+    for n, m, k in ((40, 64, 12), (90, 30, 10)):
+        U, _ = np.linalg.qr(g.standard_normal((n, min(n, m))))
+        W, _ = np.linalg.qr(g.standard_normal((m, min(n, m))))
+        s = 2.0 ** -np.arange(min(n, m)) * 10.0          # well separated
+        Z = (U * s) @ W.T
+        P, mu = O.pca_fit(Z, k)
+        _, sv, Vt = np.linalg.svd(Z, full_matrices=False)
+        V = Vt[:k].T
+        assert np.allclose(np.abs(np.sum(P * V, axis=0)), 1.0, atol=1e-10)
+        assert np.allclose(mu[:k], sv[:k] ** 2 / n, rtol=1e-10)
+        lam, Vg = np.linalg.eigh(Z @ Z.T)
+        lam, Vg = lam[::-1][:k], Vg[:, ::-1][:, :k]
+        Pg = Z.T @ Vg / np.sqrt(lam)[None, :]
+        assert np.allclose(np.abs(np.sum(P * Pg, axis=0)), 1.0, atol=1e-10)
+        # sign rule: the largest-magnitude entry of every column is positive
+        piv = np.argmax(np.abs(P), axis=0)
+        assert np.all(P[piv, np.arange(k)] > 0)
+
+
 def test_proposition1_optimal_value(tiny_fit):
     # Within the first-stage span, the PCA reconstruction error equals the sum
     # of the trailing eigenvalues (eq. app_optimal_value) and beats random
