@@ -263,6 +263,36 @@ eogp_status eogp_ekfac_eigenvalues(const void* acts, int64_t ld_acts, const void
                                    int32_t accumulate, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
+ * PCA fit (appendix on PCA fitting; Proposition rayleigh_ritz): the shared
+ * projection P of one module from cached first-stage coordinates Z [n, m],
+ * uncentered. The columns of P are the top-k right singular vectors of Z,
+ * i.e. the eigenvectors of Z^T Z / n with the largest eigenvalues, recovered
+ * from the n x n Gram matrix: Z Z^T v_c = lambda_c v_c (descending),
+ * p_c = Z^T v_c / sqrt(lambda_c), mu_c = lambda_c / n.
+ *
+ *   Z    [n, ldz] fp32, ldz >= m (device).
+ *   Pt   [k, ldp] fp32, ldp >= m: row c = p_c, the layout eogp_pca_project
+ *        takes; each row is signed so that its largest-magnitude entry (the
+ *        first such on ties) is positive; columns m..ldp-1 are not written.
+ *   mu   [k] fp32: the eigenvalues of Z^T Z / n, descending.
+ * The Gram matrix and Z^T V are formed in fp64 (exact products of the fp32
+ * inputs); the symmetric eigendecomposition is rocSOLVER's dsyevdx in the
+ * caller's workspace. Cost: 2 n^2 m + 2 n m k flops plus the eigensolver.
+ * Errors: EOGP_ERR_INVALID for bad sizes or NULL pointers (need
+ * 1 <= k <= min(n, m), n < 2^31) or when Z has fewer than k nonzero
+ * singular values (eigenvalues at or below 1e-12 of the largest count as
+ * zero); EOGP_ERR_DEVICE if the eigensolver fails; on an error Pt and mu
+ * hold unspecified values;
+ * EOGP_ERR_WORKSPACE if ws is too small. Synchronises `stream` (the
+ * eigensolver's status is read back). The workspace size query needs a GPU
+ * (it asks rocSOLVER) and returns 0 if none is usable.
+ * ------------------------------------------------------------------------ */
+size_t eogp_pca_fit_workspace_size(int64_t n, int64_t m, int64_t k);
+eogp_status eogp_pca_fit(const float* Z, int64_t ldz, int64_t n, int64_t m, int64_t k,
+                         float* Pt, int64_t ldp, float* mu, void* ws, size_t ws_bytes,
+                         void* stream);
+
+/* ------------------------------------------------------------------------
  * Random second stage, EOGP-R (Appendix B.2, eq. app_srht_definition): the
  * subsampled randomized Hadamard transform x = sqrt(p/k) R H_p D J z in place
  * of the PCA projection, for every row z of Z:
@@ -304,7 +334,8 @@ typedef enum {
   EOGP_KT_COMPACTION = 7,     /* valid-token compaction                          */
   EOGP_KT_SRHT = 8,           /* random second stage (EOGP-R)                    */
   EOGP_KT_EKFAC = 9,          /* EK-FAC squared rotated gradients                */
-  EOGP_KT_COUNT = 10
+  EOGP_KT_PCA_FIT = 10,       /* PCA fit: Gram and projection contractions       */
+  EOGP_KT_COUNT = 11
 } eogp_kernel_class;
 eogp_status eogp_timing_enable(int32_t enable);
 eogp_status eogp_timing_read(int32_t kernel_class, double* total_ms, int64_t* launches);

@@ -24,6 +24,9 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
                         bool accurate, void* ws, size_t ws_bytes, hipStream_t s);
 int32_t score_max_topk();
 int srht_max_log();
+size_t pca_fit_ws(int64_t n, int64_t m, int64_t k);
+eogp_status pca_fit(const float* Z, int64_t ldz, int64_t n, int64_t m, int64_t k, float* Pt,
+                    int64_t ldp, float* mu, void* ws, size_t ws_bytes, hipStream_t s);
 size_t ekfac_ws(int64_t N, int64_t T, int64_t d_in, int64_t d_out);
 eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int64_t ld_grads,
                        bool bf16_in, const uint8_t* mask, int64_t N, int64_t T, int64_t d_in,
@@ -305,6 +308,24 @@ eogp_status eogp_srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m,
   if (ldz < m || ldx < k) return fail(EOGP_ERR_INVALID, "srht_project: leading dimension too small");
   if (N > 0 && (!Z || !signs || !rows || !X)) return fail(EOGP_ERR_INVALID, "srht_project: NULL pointer");
   return srht_project(Z, ldz, N, m, signs, rows, k, X, ldx, S(stream));
+}
+
+size_t eogp_pca_fit_workspace_size(int64_t n, int64_t m, int64_t k) {
+  if (n < 1 || m < 1 || k < 1 || k > std::min(n, m) || n >= kMaxFlat) {
+    (void)fail(EOGP_ERR_INVALID, "pca_fit: need 1 <= k <= min(n, m) and n < 2^31");
+    return 0;
+  }
+  return pca_fit_ws(n, m, k);
+}
+
+eogp_status eogp_pca_fit(const float* Z, int64_t ldz, int64_t n, int64_t m, int64_t k, float* Pt,
+                         int64_t ldp, float* mu, void* ws, size_t ws_bytes, void* stream) {
+  if (n < 1 || m < 1 || k < 1) return fail(EOGP_ERR_INVALID, "pca_fit: bad sizes");
+  if (k > std::min(n, m)) return fail(EOGP_ERR_INVALID, "pca_fit: need k <= min(n, m)");
+  if (n >= kMaxFlat) return fail(EOGP_ERR_INVALID, "pca_fit: n must be < 2^31");
+  if (ldz < m || ldp < m) return fail(EOGP_ERR_INVALID, "pca_fit: leading dimension too small");
+  if (!Z || !Pt || !mu || !ws) return fail(EOGP_ERR_INVALID, "pca_fit: NULL pointer");
+  return pca_fit(Z, ldz, n, m, k, Pt, ldp, mu, ws, ws_bytes, S(stream));
 }
 
 size_t eogp_score_topk_workspace_size(int64_t N, int64_t Q, int32_t U, const int64_t* k_per_module,

@@ -47,6 +47,7 @@ EXPORTED = (
     "eogp_rotate_retain_oneshot_workspace_size", "eogp_rotate_retain",
     "eogp_pca_project_workspace_size", "eogp_pca_project",
     "eogp_sign_pack", "eogp_srht_project",
+    "eogp_pca_fit_workspace_size", "eogp_pca_fit",
     "eogp_ekfac_workspace_size", "eogp_ekfac_eigenvalues",
     "eogp_score_topk_workspace_size", "eogp_score_topk",
     "eogp_timing_enable", "eogp_timing_read",
@@ -88,6 +89,9 @@ def load(path: str | None = None):
                                            c_sz, c_vp]),
         "eogp_srht_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_vp, c_i64, c_vp, c_i64,
                                       c_vp]),
+        "eogp_pca_fit_workspace_size": (c_sz, [c_i64, c_i64, c_i64]),
+        "eogp_pca_fit": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_vp, c_sz,
+                                 c_vp]),
         "eogp_score_topk_workspace_size": (c_sz, [c_i64, c_i64, c_i32, ctypes.POINTER(c_i64),
                                                   c_i32]),
         "eogp_score_topk": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64), c_vp,
@@ -336,6 +340,33 @@ def eogp_srht_project(Z, signs, rows, X=None, stream=None):
     return X
 
 
+def eogp_pca_fit_workspace_size(n: int, m: int, k: int) -> int:
+    return int(load().eogp_pca_fit_workspace_size(n, m, k))
+
+
+def eogp_pca_fit(Z, k, Pt=None, mu=None, ws=None, stream=None):
+    """Fit the PCA projection from first-stage coordinates Z [n, m] (float32):
+    returns (Pt [k, m] float32, mu [k] float32); see eogp_pca_fit in eogp.h.
+    Synchronises the stream."""
+    L = load()
+    _need_cuda(Z, Pt, mu)
+    n, m = Z.shape
+    if Z.dtype != torch.float32 or Z.stride(1) != 1:
+        raise ValueError("Z must be float32 [n, m] with unit column stride")
+    if Pt is None:
+        Pt = torch.empty((k, m), dtype=torch.float32, device=Z.device)
+    if mu is None:
+        mu = torch.empty((k,), dtype=torch.float32, device=Z.device)
+    need = int(L.eogp_pca_fit_workspace_size(n, m, k))
+    if need == 0:
+        bad_sizes = not (1 <= k <= min(n, m))
+        raise EogpError(-1 if bad_sizes else -3, L.eogp_last_error().decode())
+    ws, wsb = _workspace(need, Z.device, ws)
+    _check(L.eogp_pca_fit(_ptr(Z), max(Z.stride(0), m), n, m, k, _ptr(Pt), Pt.stride(0), _ptr(mu),
+                          _ptr(ws), wsb, _stream(stream)))
+    return Pt, mu
+
+
 def eogp_sign_pack(X, codes=None, scales=None, stream=None):
     """Packed sign bits [N, ceil(k/8)] (uint8) and fp16 scales [N] (uint16 bits)."""
     L = load()
@@ -390,10 +421,10 @@ def eogp_version() -> int:
 # ---------------------------------------------------------------------------
 KT_ROTATION_GEMM, KT_RETAINED, KT_PCA_GEMM, KT_SIGN_PACK = 0, 1, 2, 3
 KT_SCORE_PASS, KT_SCORE_MERGE, KT_SCORE_PREP, KT_COMPACTION = 4, 5, 6, 7
-KT_SRHT, KT_EKFAC = 8, 9
+KT_SRHT, KT_EKFAC, KT_PCA_FIT = 8, 9, 10
 KERNEL_CLASSES = {"rotation_gemm": 0, "retained": 1, "pca_gemm": 2, "sign_pack": 3,
                   "score_pass": 4, "score_merge": 5, "score_prep": 6, "compaction": 7,
-                  "srht": 8, "ekfac": 9}
+                  "srht": 8, "ekfac": 9, "pca_fit": 10}
 
 
 def eogp_timing_enable(on: bool = True):

@@ -75,6 +75,15 @@ def test_encode_and_score_argument_validation_without_device():
     assert L.eogp_srht_project(fake, 100, 2, 100, fake, fake, 129, fake, 129, None) == -1
     assert L.eogp_srht_project(fake, 40000, 2, 40000, fake, fake, 8, fake, 8, None) == -2
     assert L.eogp_srht_project(fake, 50, 2, 100, fake, fake, 8, fake, 8, None) == -1
+    # pca fit: k > min(n, m), ld too small, NULL workspace; the size query
+    # rejects bad sizes
+    assert L.eogp_pca_fit(fake, 8, 4, 8, 5, fake, 8, fake, fake, 1 << 20, None) == -1
+    assert L.eogp_pca_fit(fake, 8, 10, 8, 9, fake, 8, fake, fake, 1 << 20, None) == -1
+    assert L.eogp_pca_fit(fake, 6, 10, 8, 4, fake, 8, fake, fake, 1 << 20, None) == -1
+    assert L.eogp_pca_fit(fake, 8, 10, 8, 4, fake, 7, fake, fake, 1 << 20, None) == -1
+    assert L.eogp_pca_fit(fake, 8, 10, 8, 4, fake, 8, fake, None, 1 << 20, None) == -1
+    assert L.eogp_pca_fit_workspace_size(10, 8, 9) == 0
+    assert L.eogp_pca_fit_workspace_size(10, 8, 0) == 0
     # score: k_u not a multiple of 64, topk out of range, misaligned stride
     ks = (ctypes.c_int64 * 2)(64, 100)
     assert L.eogp_score_topk(fake, 32, fake, 4, 2, ks, fake, 164, 1, 3, fake, fake, None,
