@@ -245,6 +245,46 @@ class Gpt2Step:
         return tot
 
 
+FP64_PEAK_TFLOPS = 78.6
+
+
+def pca_fit_measurement(st, dev, n=10000):
+    """One module's PCA fit (m = 16,384 first-stage coordinates, k = 8,192
+    directions) from n cached coordinate rows, the fitting-set size of the
+    paper's OLMo runs. The rows are synthetic: N(0, 1) entries times a slowly
+    decaying per-coordinate profile, so the spectrum has no exact ties."""
+    import torch
+    E = st.E
+    m, k = st.m, st.k
+    g = torch.Generator(device=dev)
+    g.manual_seed(st.w.config_id * 1000 + 17)
+    Z = torch.randn((n, m), device=dev, generator=g)
+    Z *= (0.9995 ** torch.arange(m, device=dev, dtype=torch.float32))[None, :]
+    ws = torch.empty(E.eogp_pca_fit_workspace_size(n, m, k), dtype=torch.uint8, device=dev)
+    Pt = torch.empty((k, m), dtype=torch.float32, device=dev)
+    mu = torch.empty((k,), dtype=torch.float32, device=dev)
+    E.eogp_pca_fit(Z, k, Pt=Pt, mu=mu, ws=ws)            # warm-up: loads the solver's kernels
+    torch.cuda.synchronize()
+    E.eogp_timing_read(E.KT_PCA_FIT)
+    E.eogp_timing_enable(True)
+    t0 = time.perf_counter()
+    E.eogp_pca_fit(Z, k, Pt=Pt, mu=mu, ws=ws)
+    torch.cuda.synchronize()
+    secs = time.perf_counter() - t0
+    c_ms, _ = E.eogp_timing_read(E.KT_PCA_FIT)
+    E.eogp_timing_enable(False)
+    flops = 2.0 * n * n * m + 2.0 * n * m * k
+    tf = flops / (c_ms * 1e-3) / 1e12
+    del Z, ws, Pt, mu
+    torch.cuda.empty_cache()
+    return {"metric": "PCA fit time for one module from cached first-stage coordinates",
+            "seconds": secs, "n": n, "m": m, "k": k, "data": "synthetic",
+            "contractions_ms": c_ms, "eigensolver_and_rest_ms": 1000.0 * secs - c_ms,
+            "contraction_roofline": {"bound": "mfma", "achieved": tf, "peak": FP64_PEAK_TFLOPS,
+                                     "unit": "TFLOP/s (fp64)", "frac": tf / FP64_PEAK_TFLOPS,
+                                     "alg_flops": flops}}
+
+
 # ---------------------------------------------------------------------------
 # Oracle CPU baseline on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
@@ -515,6 +555,8 @@ def main(argv=None):
         }
         log(f"ekfac: {ek_ms:.1f} ms per batch over all modules")
         del sq
+        out["pca_fit"] = pca_fit_measurement(st, dev)
+        log(f"pca fit: {out['pca_fit']['seconds']:.2f} s per module")
         if not args.no_cpu_baseline:
             t0 = time.time()
             out["cpu_baseline"] = cpu_baseline(st)
