@@ -309,12 +309,16 @@ eogp_status eogp_pca_fit(const float* Z, int64_t ldz, int64_t n, int64_t m, int6
  *          column; repeated rows repeat the coordinate.
  *   X      [N, ldx] fp32, ldx >= k; columns k..ldx-1 are not written.
  * Errors: EOGP_ERR_INVALID for bad sizes or NULL pointers, k > p, or
- * ldz < m / ldx < k; EOGP_ERR_UNSUPPORTED for p > 32768 (m > 32768).
- * Enqueued on `stream`; needs no workspace.
+ * ldz < m / ldx < k; EOGP_ERR_UNSUPPORTED for p > 2^20 (m > 1,048,576);
+ * EOGP_ERR_WORKSPACE if ws is too small.
+ * p <= 32768 needs no workspace (ws may be NULL); larger p are transformed in
+ * two stages through ws (eogp_srht_project_workspace_size bytes: one padded
+ * fp32 row per example). Enqueued on `stream`.
  * ------------------------------------------------------------------------ */
+size_t eogp_srht_project_workspace_size(int64_t N, int64_t m);
 eogp_status eogp_srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m,
                               const int8_t* signs, const int32_t* rows, int64_t k, float* X,
-                              int64_t ldx, void* stream);
+                              int64_t ldx, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing, for measurement harnesses. While enabled, each launch of a

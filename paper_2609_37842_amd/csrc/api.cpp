@@ -24,6 +24,7 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
                         bool accurate, void* ws, size_t ws_bytes, hipStream_t s);
 int32_t score_max_topk();
 int srht_max_log();
+size_t srht_ws(int64_t N, int64_t m);
 size_t pca_fit_ws(int64_t n, int64_t m, int64_t k);
 eogp_status pca_fit(const float* Z, int64_t ldz, int64_t n, int64_t m, int64_t k, float* Pt,
                     int64_t ldp, float* mu, void* ws, size_t ws_bytes, hipStream_t s);
@@ -33,7 +34,8 @@ eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int
                        int64_t d_out, const float* Q_A, const float* Q_S, int prec, float* sq,
                        int accumulate, void* ws, size_t ws_bytes, hipStream_t s);
 eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const int8_t* signs,
-                         const int32_t* rows, int64_t k, float* X, int64_t ldx, hipStream_t s);
+                         const int32_t* rows, int64_t k, float* X, int64_t ldx, void* ws,
+                         size_t ws_bytes, hipStream_t s);
 const char* last_error_cstr();
 size_t score_ws(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t topk);
 eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* scales, int64_t N,
@@ -295,19 +297,26 @@ eogp_status eogp_ekfac_eigenvalues(const void* acts, int64_t ld_acts, const void
                     d_in, d_out, Q_A, Q_S, (int)prec, sq_sum, accumulate, ws, ws_bytes, S(stream));
 }
 
+size_t eogp_srht_project_workspace_size(int64_t N, int64_t m) {
+  if (N < 0 || m < 1 || m > ((int64_t)1 << srht_max_log())) return 0;
+  return srht_ws(N, m);
+}
+
 eogp_status eogp_srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m,
                               const int8_t* signs, const int32_t* rows, int64_t k, float* X,
-                              int64_t ldx, void* stream) {
+                              int64_t ldx, void* ws, size_t ws_bytes, void* stream) {
   if (N < 0 || m < 1 || k < 1) return fail(EOGP_ERR_INVALID, "srht_project: bad sizes");
   if (N >= kMaxFlat) return fail(EOGP_ERR_INVALID, "srht_project: N must be < 2^31");
   if (m > ((int64_t)1 << srht_max_log()))
-    return fail(EOGP_ERR_UNSUPPORTED, "srht_project: m > 32768 is not supported");
+    return fail(EOGP_ERR_UNSUPPORTED, "srht_project: m > 2^20 is not supported");
   int64_t p = 1;
   while (p < m) p <<= 1;
   if (k > p) return fail(EOGP_ERR_INVALID, "srht_project: need k <= p = 2^ceil(log2 m)");
   if (ldz < m || ldx < k) return fail(EOGP_ERR_INVALID, "srht_project: leading dimension too small");
   if (N > 0 && (!Z || !signs || !rows || !X)) return fail(EOGP_ERR_INVALID, "srht_project: NULL pointer");
-  return srht_project(Z, ldz, N, m, signs, rows, k, X, ldx, S(stream));
+  if (ws_bytes < srht_ws(N, m) || (srht_ws(N, m) > 0 && !ws))
+    return fail(EOGP_ERR_WORKSPACE, "srht_project: workspace too small");
+  return srht_project(Z, ldz, N, m, signs, rows, k, X, ldx, ws, ws_bytes, S(stream));
 }
 
 size_t eogp_pca_fit_workspace_size(int64_t n, int64_t m, int64_t k) {

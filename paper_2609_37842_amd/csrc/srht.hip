@@ -4,11 +4,20 @@
 // transform in Sylvester order (entry (r, i) = (-1)^popcount(r & i)),
 //   x_c = W(D J z)[rows[c]] / sqrt(k).
 //
-// One workgroup per row. The row is read once (coalesced), multiplied by the
-// random signs and zero-padded into LDS; the butterfly stages run in LDS two
-// at a time (radix 4: each thread combines four elements h apart), one radix-2
-// stage first when log2 p is odd; the kept rows are then gathered and scaled.
-// Cost: p log2 p additions per row, HBM traffic m + k floats per row.
+// p <= 32768: one workgroup per row. The row is read once (coalesced),
+// multiplied by the random signs and zero-padded into LDS; the butterfly
+// stages run in LDS two at a time (radix 4: each thread combines four elements
+// h apart), one radix-2 stage first when log2 p is odd; the kept rows are then
+// gathered and scaled. Cost: p log2 p additions per row, HBM traffic m + k
+// floats per row.
+//
+// p > 32768 (up to 2^20): W_p = W_p1 (x) W_p2 in Sylvester order (index
+// i = i1 p2 + i2, p2 = 32768, p1 = p / p2 <= 32). One workgroup per (row,
+// chunk i1) transforms its 32768 entries along i2 in LDS as above and writes
+// them to the workspace; the gather then forms each kept coordinate
+// r = r1 p2 + r2 as the length-p1 transform along i1 of that column,
+//   x_c = sum_j (-1)^popcount(r1 & j) S[j p2 + r2] / sqrt(k).
+// Extra HBM traffic: p floats written and k p1 read per row.
 #include <cmath>
 
 #include "common.h"
@@ -17,23 +26,13 @@
 namespace eogp {
 namespace {
 
-constexpr int kSrhtMaxLog = 15;   // p <= 32768: the padded row fits the LDS (128 KB)
+constexpr int kSrhtMaxLog = 15;      // one stage: the padded row fits the LDS (128 KB)
+constexpr int kSrhtMaxLogTwo = 20;   // two stages: p1 = p / 2^15 <= 32
 
-__global__ __launch_bounds__(1024) void k_srht(const float* __restrict__ Z, int64_t ldz, int m,
-                                               int logp, const int8_t* __restrict__ signs,
-                                               const int32_t* __restrict__ rows, int k,
-                                               float scale, float* __restrict__ X, int64_t ldx) {
-  extern __shared__ float L[];
-  const int64_t i = blockIdx.x;
+// In-LDS unnormalised Walsh-Hadamard transform of L[0 .. 2^logp).
+__device__ __forceinline__ void fwht_lds(float* L, int logp) {
   const int tid = threadIdx.x, nt = blockDim.x;
   const int p = 1 << logp;
-  const float* z = Z + i * ldz;
-  for (int c = tid; c < p; c += nt) {
-    float v = 0.f;
-    if (c < m) v = signs[c] < 0 ? -z[c] : z[c];
-    L[c] = v;
-  }
-  __syncthreads();
   int h = 1;
   if (logp & 1) {                                   // one radix-2 stage (h = 1)
     for (int b = tid; b < p / 2; b += nt) {
@@ -58,6 +57,24 @@ __global__ __launch_bounds__(1024) void k_srht(const float* __restrict__ Z, int6
     }
     __syncthreads();
   }
+}
+
+__global__ __launch_bounds__(1024) void k_srht(const float* __restrict__ Z, int64_t ldz, int m,
+                                               int logp, const int8_t* __restrict__ signs,
+                                               const int32_t* __restrict__ rows, int k,
+                                               float scale, float* __restrict__ X, int64_t ldx) {
+  extern __shared__ float L[];
+  const int64_t i = blockIdx.x;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int p = 1 << logp;
+  const float* z = Z + i * ldz;
+  for (int c = tid; c < p; c += nt) {
+    float v = 0.f;
+    if (c < m) v = signs[c] < 0 ? -z[c] : z[c];
+    L[c] = v;
+  }
+  __syncthreads();
+  fwht_lds(L, logp);
   float* x = X + i * ldx;
   for (int c = tid; c < k; c += nt) {
     const int r = rows[c];
@@ -65,31 +82,110 @@ __global__ __launch_bounds__(1024) void k_srht(const float* __restrict__ Z, int6
   }
 }
 
+// Two-stage form, first stage: grid (p1, N); chunk i1 of row i, signed and
+// zero-padded, transformed along i2 into S[i][i1 p2 ..].
+__global__ __launch_bounds__(1024) void k_srht_chunk(const float* __restrict__ Z, int64_t ldz,
+                                                     int m, const int8_t* __restrict__ signs,
+                                                     float* __restrict__ S, int64_t lds_row) {
+  extern __shared__ float L[];
+  const int64_t i = blockIdx.y;
+  const int64_t c0 = (int64_t)blockIdx.x << kSrhtMaxLog;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const float* z = Z + i * ldz;
+  for (int c = tid; c < (1 << kSrhtMaxLog); c += nt) {
+    const int64_t g = c0 + c;
+    float v = 0.f;
+    if (g < m) v = signs[g] < 0 ? -z[g] : z[g];
+    L[c] = v;
+  }
+  __syncthreads();
+  fwht_lds(L, kSrhtMaxLog);
+  float* out = S + i * lds_row + c0;
+  for (int c = tid; c < (1 << kSrhtMaxLog); c += nt) out[c] = L[c];
+}
+
+// Second stage fused with the gather: grid (ceil(k / 256), N).
+__global__ __launch_bounds__(256) void k_srht_cross(const float* __restrict__ S, int64_t lds_row,
+                                                    int logp, const int32_t* __restrict__ rows,
+                                                    int k, float scale, float* __restrict__ X,
+                                                    int64_t ldx) {
+  const int64_t i = blockIdx.y;
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= k) return;
+  const int p = 1 << logp, p1 = 1 << (logp - kSrhtMaxLog);
+  const int r = rows[c];
+  if (r < 0 || r >= p) {
+    X[i * ldx + c] = __builtin_nanf("");
+    return;
+  }
+  const int r1 = r >> kSrhtMaxLog, r2 = r & ((1 << kSrhtMaxLog) - 1);
+  const float* col = S + i * lds_row + r2;
+  float acc = 0.f;
+  for (int j = 0; j < p1; ++j) {
+    const float v = col[(int64_t)j << kSrhtMaxLog];
+    acc += (__popc(r1 & j) & 1) ? -v : v;
+  }
+  X[i * ldx + c] = acc * scale;
+}
+
 }  // namespace
 
-int srht_max_log() { return kSrhtMaxLog; }
+int srht_max_log() { return kSrhtMaxLogTwo; }
 
-eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const int8_t* signs,
-                         const int32_t* rows, int64_t k, float* X, int64_t ldx, hipStream_t s) {
-  if (N == 0) return EOGP_OK;
+namespace {
+int srht_log(int64_t m) {
   int logp = 0;
   while ((int64_t(1) << logp) < m) ++logp;
-  const int p = 1 << logp;
-  const size_t lds = (size_t)p * sizeof(float);
-  static bool attr_set = false;     // the attribute is per kernel, not per device
+  return logp;
+}
+}  // namespace
+
+size_t srht_ws(int64_t N, int64_t m) {
+  const int logp = srht_log(m);
+  if (logp <= kSrhtMaxLog) return 0;
+  return align256((size_t)N * ((size_t)1 << logp) * sizeof(float));
+}
+
+eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const int8_t* signs,
+                         const int32_t* rows, int64_t k, float* X, int64_t ldx, void* ws,
+                         size_t ws_bytes, hipStream_t s) {
+  if (N == 0) return EOGP_OK;
+  const int logp = srht_log(m);
+  static bool attr_set = false;     // the attributes are per kernel, not per device
   if (!attr_set) {
     EOGP_HIP(hipFuncSetAttribute((const void*)k_srht, hipFuncAttributeMaxDynamicSharedMemorySize,
                                  (int)(sizeof(float) << kSrhtMaxLog)));
+    EOGP_HIP(hipFuncSetAttribute((const void*)k_srht_chunk,
+                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)(sizeof(float) << kSrhtMaxLog)));
     attr_set = true;
   }
-  const int nt = std::max(64, std::min(1024, p / 4));
   const float scale = (float)(1.0 / std::sqrt((double)k));
   timing::Scope ts(EOGP_KT_SRHT, s);
-  for (int64_t r0 = 0; r0 < N; r0 += 0x7FFFFFFF) {
-    const int64_t nr = std::min<int64_t>(N - r0, 0x7FFFFFFF);
-    hipLaunchKernelGGL(k_srht, dim3((unsigned)nr), dim3(nt), lds, s, Z + r0 * ldz, ldz, (int)m,
-                       logp, signs, rows, (int)k, scale, X + r0 * ldx, ldx);
-    EOGP_LAUNCH_CHECK("srht_project");
+  if (logp <= kSrhtMaxLog) {
+    const int p = 1 << logp;
+    const size_t lds = (size_t)p * sizeof(float);
+    const int nt = std::max(64, std::min(1024, p / 4));
+    for (int64_t r0 = 0; r0 < N; r0 += 0x7FFFFFFF) {
+      const int64_t nr = std::min<int64_t>(N - r0, 0x7FFFFFFF);
+      hipLaunchKernelGGL(k_srht, dim3((unsigned)nr), dim3(nt), lds, s, Z + r0 * ldz, ldz, (int)m,
+                         logp, signs, rows, (int)k, scale, X + r0 * ldx, ldx);
+      EOGP_LAUNCH_CHECK("srht_project");
+    }
+    return EOGP_OK;
+  }
+  if (ws_bytes < srht_ws(N, m) || !ws) return fail(EOGP_ERR_WORKSPACE, "srht_project: workspace too small");
+  float* S = static_cast<float*>(ws);
+  const int64_t p = int64_t(1) << logp;
+  const int p1 = 1 << (logp - kSrhtMaxLog);
+  for (int64_t r0 = 0; r0 < N; r0 += 65535) {
+    const int64_t nr = std::min<int64_t>(N - r0, 65535);
+    hipLaunchKernelGGL(k_srht_chunk, dim3((unsigned)p1, (unsigned)nr), dim3(1024),
+                       sizeof(float) << kSrhtMaxLog, s, Z + r0 * ldz, ldz, (int)m, signs,
+                       S + r0 * p, p);
+    hipLaunchKernelGGL(k_srht_cross, dim3((unsigned)ceil_div(k, 256), (unsigned)nr), dim3(256), 0,
+                       s, S + r0 * p, p, logp, rows, (int)k, scale, X + r0 * ldx, ldx);
+    EOGP_LAUNCH_CHECK("srht_project (two stages)");
   }
   return EOGP_OK;
 }

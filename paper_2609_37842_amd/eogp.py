@@ -46,7 +46,7 @@ EXPORTED = (
     "eogp_rotate_retain_workspace_size", "eogp_rotate_retain_planned",
     "eogp_rotate_retain_oneshot_workspace_size", "eogp_rotate_retain",
     "eogp_pca_project_workspace_size", "eogp_pca_project",
-    "eogp_sign_pack", "eogp_srht_project",
+    "eogp_sign_pack", "eogp_srht_project_workspace_size", "eogp_srht_project",
     "eogp_pca_fit_workspace_size", "eogp_pca_fit",
     "eogp_ekfac_workspace_size", "eogp_ekfac_eigenvalues",
     "eogp_score_topk_workspace_size", "eogp_score_topk",
@@ -87,8 +87,9 @@ def load(path: str | None = None):
         "eogp_ekfac_eigenvalues": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64,
                                            c_i64, c_i64, c_vp, c_vp, c_i32, c_vp, c_i32, c_vp,
                                            c_sz, c_vp]),
+        "eogp_srht_project_workspace_size": (c_sz, [c_i64, c_i64]),
         "eogp_srht_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_vp, c_i64, c_vp, c_i64,
-                                      c_vp]),
+                                      c_vp, c_sz, c_vp]),
         "eogp_pca_fit_workspace_size": (c_sz, [c_i64, c_i64, c_i64]),
         "eogp_pca_fit": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_vp, c_sz,
                                  c_vp]),
@@ -320,7 +321,11 @@ def eogp_ekfac_eigenvalues(acts, out_grads, token_mask, Q_A, Q_S, sq_sum=None, a
     return sq_sum
 
 
-def eogp_srht_project(Z, signs, rows, X=None, stream=None):
+def eogp_srht_project_workspace_size(N: int, m: int) -> int:
+    return int(load().eogp_srht_project_workspace_size(N, m))
+
+
+def eogp_srht_project(Z, signs, rows, X=None, ws=None, stream=None):
     """X [N, k] = the SRHT of each row of Z [N, m] (float32) with random signs
     [m] (int8) and kept rows [k] (int32); see eogp_srht_project in eogp.h."""
     L = load()
@@ -335,8 +340,9 @@ def eogp_srht_project(Z, signs, rows, X=None, stream=None):
         raise ValueError("rows must be contiguous int32 [k]")
     if X is None:
         X = torch.empty((N, k), dtype=torch.float32, device=Z.device)
+    ws, wsb = _workspace(int(L.eogp_srht_project_workspace_size(N, m)), Z.device, ws)
     _check(L.eogp_srht_project(_ptr(Z), max(Z.stride(0), m), N, m, _ptr(signs), _ptr(rows), k,
-                               _ptr(X), max(X.stride(0), k), _stream(stream)))
+                               _ptr(X), max(X.stride(0), k), _ptr(ws), wsb, _stream(stream)))
     return X
 
 

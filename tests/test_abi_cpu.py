@@ -71,10 +71,14 @@ def test_encode_and_score_argument_validation_without_device():
                                     fake, 1 << 30, None) == -1
     assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, fake, fake, 1, fake, 0,
                                     fake, 16, None) == -4
-    # srht: k > p, m too large, ld too small
-    assert L.eogp_srht_project(fake, 100, 2, 100, fake, fake, 129, fake, 129, None) == -1
-    assert L.eogp_srht_project(fake, 40000, 2, 40000, fake, fake, 8, fake, 8, None) == -2
-    assert L.eogp_srht_project(fake, 50, 2, 100, fake, fake, 8, fake, 8, None) == -1
+    # srht: k > p, m too large, ld too small, two-stage form without workspace
+    assert L.eogp_srht_project(fake, 100, 2, 100, fake, fake, 129, fake, 129, None, 0, None) == -1
+    assert L.eogp_srht_project(fake, (1 << 20) + 1, 2, (1 << 20) + 1, fake, fake, 8, fake, 8,
+                               None, 0, None) == -2
+    assert L.eogp_srht_project(fake, 50, 2, 100, fake, fake, 8, fake, 8, None, 0, None) == -1
+    assert L.eogp_srht_project(fake, 40000, 2, 40000, fake, fake, 8, fake, 8, None, 0, None) == -4
+    assert L.eogp_srht_project_workspace_size(2, 32768) == 0
+    assert L.eogp_srht_project_workspace_size(2, 40000) == 2 * 65536 * 4
     # pca fit: k > min(n, m), ld too small, NULL workspace; the size query
     # rejects bad sizes
     assert L.eogp_pca_fit(fake, 8, 4, 8, 5, fake, 8, fake, fake, 1 << 20, None) == -1

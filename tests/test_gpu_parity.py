@@ -439,6 +439,10 @@ def test_ekfac_bf16_inputs():
 @pytest.mark.parametrize("N,m,k", [
     (5, 1, 1), (7, 3, 4), (9, 512, 128), (4, 700, 300), (3, 16384, 8192), (2, 32768, 16384),
     (0, 64, 8),
+    # two-stage form (p > 32768): padded 40000 -> 65536, the OLMo-2-32B-shaped
+    # module (m = 65,536, k = 32,768), the paper's timing configuration
+    # (m = 262,144, k = 2,048), and the largest supported width
+    (3, 40000, 8192), (2, 65536, 32768), (2, 262144, 2048), (1, 1 << 20, 4096), (0, 70000, 8),
 ])
 def test_srht_project(N, m, k):
     """Against the fp64 oracle; fp32 butterflies keep about 1e-6 relative."""
@@ -457,8 +461,9 @@ def test_srht_project(N, m, k):
     assert err.max() <= 1e-5
 
 
-def test_srht_project_strides_and_bad_rows():
-    m, k = 1000, 64
+@pytest.mark.parametrize("m", [1000, 40000])
+def test_srht_project_strides_and_bad_rows(m):
+    k = 64
     p = O.srht_width(m)
     signs, rows = S.srht_draws(9, 1, m, p, k)
     rows[5] = p                                  # outside the transform
