@@ -142,6 +142,8 @@ eogp_status eogp_plan_set_input_exponents(eogp_plan* plan, int32_t e_acts, int32
  *              (about 3e-3 for fp32 inputs; the natural mode for bf16 inputs).
  *              EOGP_ERR_UNSUPPORTED for EOGP_PREC_F16 with bf16 inputs.
  *   ws         workspace of at least eogp_rotate_retain_workspace_size bytes.
+ * Sizes: N*T + 8N + 256 < 2^31 (the compacted token list is indexed in
+ * 32 bits), else EOGP_ERR_INVALID.
  * ------------------------------------------------------------------------ */
 size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64_t T);
 eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
@@ -246,21 +248,28 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride,
  * incremented by (accumulate != 0) the sum over its N examples of that
  * square; after all batches the caller divides by the total number of
  * examples. Inputs, strides, mask, dtypes and precision modes are those of
- * eogp_rotate_retain (the fp16 mode takes no input exponents here).
+ * eogp_rotate_retain.
  *
  *   Q_A, Q_S  [d_in, d_in] and [d_out, d_out] fp32 K-FAC eigenbases.
+ *   e_acts, e_grads  power-of-two input scaling of the fp16 mode, as set by
+ *             eogp_plan_set_input_exponents for the first stage (in
+ *             [-60, 60]; ignored by the other modes). In the fp16 mode the
+ *             rotated tokens are also kept in fp16 (relative error of
+ *             sq_sum about 1e-3) and the squares are fp16 MFMA products.
  *   sq_sum    [d_out, d_in] fp32, row-major (the layout of eigvals).
  *   ws        at least eogp_ekfac_workspace_size bytes.
- * Errors as for eogp_rotate_retain. The sum over examples is formed in a
- * fixed order, so repeated calls give identical results.
+ * Errors as for eogp_rotate_retain; EOGP_ERR_INVALID for an exponent outside
+ * [-60, 60]. The sum over examples is formed in a fixed order, so repeated
+ * calls give identical results.
  * ------------------------------------------------------------------------ */
 size_t eogp_ekfac_workspace_size(int64_t N, int64_t T, int64_t d_in, int64_t d_out);
 eogp_status eogp_ekfac_eigenvalues(const void* acts, int64_t ld_acts, const void* out_grads,
                                    int64_t ld_grads, eogp_dtype in_dtype,
                                    const uint8_t* token_mask, int64_t N, int64_t T,
                                    int64_t d_in, int64_t d_out, const float* Q_A,
-                                   const float* Q_S, eogp_prec prec, float* sq_sum,
-                                   int32_t accumulate, void* ws, size_t ws_bytes, void* stream);
+                                   const float* Q_S, eogp_prec prec, int32_t e_acts,
+                                   int32_t e_grads, float* sq_sum, int32_t accumulate, void* ws,
+                                   size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * PCA fit (appendix on PCA fitting; Proposition rayleigh_ritz): the shared

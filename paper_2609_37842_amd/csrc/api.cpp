@@ -31,8 +31,9 @@ eogp_status pca_fit(const float* Z, int64_t ldz, int64_t n, int64_t m, int64_t k
 size_t ekfac_ws(int64_t N, int64_t T, int64_t d_in, int64_t d_out);
 eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int64_t ld_grads,
                        bool bf16_in, const uint8_t* mask, int64_t N, int64_t T, int64_t d_in,
-                       int64_t d_out, const float* Q_A, const float* Q_S, int prec, float* sq,
-                       int accumulate, void* ws, size_t ws_bytes, hipStream_t s);
+                       int64_t d_out, const float* Q_A, const float* Q_S, int prec,
+                       int32_t e_acts, int32_t e_grads, float* sq, int accumulate, void* ws,
+                       size_t ws_bytes, hipStream_t s);
 eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const int8_t* signs,
                          const int32_t* rows, int64_t k, float* X, int64_t ldx, void* ws,
                          size_t ws_bytes, hipStream_t s);
@@ -94,7 +95,8 @@ eogp_status check_first_stage(const eogp_plan* p, const void* acts, const void* 
     return fail(EOGP_ERR_INVALID, "rotate_retain: unknown precision mode");
   if (prec == EOGP_PREC_F16 && dt != EOGP_F32)
     return fail(EOGP_ERR_UNSUPPORTED, "rotate_retain: the fp16 mode takes fp32 inputs");
-  if (N * T >= kMaxFlat) return fail(EOGP_ERR_INVALID, "rotate_retain: N*T must be < 2^31");
+  if (N * T + 8 * N + 256 >= kMaxFlat)
+    return fail(EOGP_ERR_INVALID, "rotate_retain: N*T + 8N + 256 must be < 2^31");
   return EOGP_OK;
 }
 }  // namespace
@@ -271,11 +273,15 @@ eogp_status eogp_ekfac_eigenvalues(const void* acts, int64_t ld_acts, const void
                                    int64_t ld_grads, eogp_dtype in_dtype,
                                    const uint8_t* token_mask, int64_t N, int64_t T,
                                    int64_t d_in, int64_t d_out, const float* Q_A,
-                                   const float* Q_S, eogp_prec prec, float* sq_sum,
-                                   int32_t accumulate, void* ws, size_t ws_bytes, void* stream) {
+                                   const float* Q_S, eogp_prec prec, int32_t e_acts,
+                                   int32_t e_grads, float* sq_sum, int32_t accumulate, void* ws,
+                                   size_t ws_bytes, void* stream) {
   if (N < 0 || T < 0 || d_in < 1 || d_out < 1) return fail(EOGP_ERR_INVALID, "ekfac: bad sizes");
   if (d_out * d_in >= kMaxFlat) return fail(EOGP_ERR_INVALID, "ekfac: d_in*d_out must be < 2^31");
-  if (N * T >= kMaxFlat) return fail(EOGP_ERR_INVALID, "ekfac: N*T must be < 2^31");
+  if (N * T + 8 * N + 256 >= kMaxFlat)
+    return fail(EOGP_ERR_INVALID, "ekfac: N*T + 8N + 256 must be < 2^31");
+  if (e_acts < -60 || e_acts > 60 || e_grads < -60 || e_grads > 60)
+    return fail(EOGP_ERR_INVALID, "ekfac: input exponents must lie in [-60, 60]");
   if (!Q_A || !Q_S || !sq_sum) return fail(EOGP_ERR_INVALID, "ekfac: NULL pointer");
   if (N > 0 && T > 0 && (!acts || !out_grads)) return fail(EOGP_ERR_INVALID, "ekfac: NULL pointer");
   if (in_dtype != EOGP_F32 && in_dtype != EOGP_BF16)
@@ -294,7 +300,8 @@ eogp_status eogp_ekfac_eigenvalues(const void* acts, int64_t ld_acts, const void
   if (ws_bytes < ekfac_ws(N, T, d_in, d_out) || !ws)
     return fail(EOGP_ERR_WORKSPACE, "ekfac: workspace too small");
   return ekfac_pass(acts, ld_acts, out_grads, ld_grads, in_dtype == EOGP_BF16, token_mask, N, T,
-                    d_in, d_out, Q_A, Q_S, (int)prec, sq_sum, accumulate, ws, ws_bytes, S(stream));
+                    d_in, d_out, Q_A, Q_S, (int)prec, e_acts, e_grads, sq_sum, accumulate, ws,
+                    ws_bytes, S(stream));
 }
 
 size_t eogp_srht_project_workspace_size(int64_t N, int64_t m) {

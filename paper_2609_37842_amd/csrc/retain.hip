@@ -399,10 +399,12 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
 // Lambda[j, k] = mean over examples of (Q_S^T G_i Q_A)[j, k]^2 (Section 2.2,
 // eq. ekfac_eigendecompose; corrected eigenvalues over examples from
 // sequence-level gradients, Appendix C.2). After the rotations onto every
-// eigenvector, one wave per 32 x 32 block (j, k) walks the examples in order:
-// the block of sums C = sum_t S~[t, j] A~[t, k] over the example's valid
-// tokens is formed with fp32 MFMA and C * C is added to the block's running
-// sum of squares in registers, so the result does not depend on scheduling.
+// eigenvector, the examples are walked in order: the block of sums
+// C = sum_t S~[t, j] A~[t, k] over the example's valid tokens is formed with
+// MFMA and C * C is added to a running sum of squares in registers, so the
+// result does not depend on scheduling. FAST and ACCURATE: fp32 token-major
+// intermediates, one wave per 32 x 32 block, fp32 MFMA (exact products).
+// fp16 mode: fp16 fragment-order intermediates, fp16 MFMA (k_ekfac_sq16).
 namespace {
 
 __global__ __launch_bounds__(256) void k_ekfac_sq(const float* __restrict__ St, int64_t ldS,
@@ -452,6 +454,123 @@ __global__ __launch_bounds__(256) void k_ekfac_sq(const float* __restrict__ St, 
   }
 }
 
+// fp16 mode: S~ and A~ in the fp16 fragment order of the first stage (runs
+// aligned to 8 tokens). A wave owns one 32-row block jb and KQ = 4 32-column
+// blocks kb .. kb+3 (32 x 128 entries); per 16 tokens it loads one S~ block
+// and four A~ blocks (1 KB each) and issues four v_mfma_f32_32x32x16_f16, so
+// each loaded block feeds 0.8 MFMAs; the four waves of a
+// workgroup take neighbouring row blocks and the same column blocks, whose
+// loads they share through the L1. Example by example the block sums C are
+// formed over the example's tokens (tokens past its run zeroed) and C * C is
+// added to the running sums. Small modules split the examples into ranges
+// (grid z) so that the grid still fills the chip; each range writes its own
+// partial sums, which k_ekfac_sum adds in range order (deterministic).
+constexpr int kSq16Unroll = 4;     // 16-token steps loaded per batch
+constexpr int kSq16Cols = 4;       // 32-column blocks per wave (measured best of 1, 2, 4, 8)
+
+template <int KQ>
+__global__ __launch_bounds__(256) void k_ekfac_sq16(const uint16_t* __restrict__ St,
+                                                    const uint16_t* __restrict__ At, int64_t ldt,
+                                                    const int32_t* __restrict__ ex_off,
+                                                    const int32_t* __restrict__ ex_len, int64_t N,
+                                                    int splits, int d_out, int d_in,
+                                                    float* __restrict__ part) {
+  typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int jb = blockIdx.y * 4 + wid;
+  const int kb0 = blockIdx.x * KQ;
+  if (jb * 32 >= d_out) return;                // whole wave leaves; no block barrier below
+  const int split = blockIdx.z;
+  const int64_t i_beg = split * N / splits, i_end = (split + 1) * N / splits;
+  const int half = lane >> 5, col = lane & 31;
+  const int64_t groups = ldt / 16;
+  auto at_tok = [&](int64_t b, int64_t t) { return ((b * groups + (t >> 4)) * 32 + col) * 16 + (t & 15); };
+  f32x16 acc2[KQ];
+#pragma unroll
+  for (int q = 0; q < KQ; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc2[q][r] = 0.f;
+  for (int64_t i = i_beg; i < i_end; ++i) {
+    const int n = ex_len[i];
+    if (n == 0) continue;
+    const int64_t t0 = ex_off[i] + 8 * half;
+    const uint16_t* sp = St + at_tok(jb, t0);
+    const uint16_t* ap = At + at_tok(kb0, t0);
+    const int64_t bstride = groups * 512;      // elements from one column block to the next
+    f32x16 c[KQ];
+#pragma unroll
+    for (int q = 0; q < KQ; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) c[q][r] = 0.f;
+    for (int t = 0; t < n; t += 16 * kSq16Unroll) {
+      v4u a[kSq16Unroll], b[kSq16Unroll][KQ];
+#pragma unroll
+      for (int u = 0; u < kSq16Unroll; ++u) {
+        const int64_t o = (int64_t)(t / 16 + u) * 512;
+        a[u] = *reinterpret_cast<const v4u*>(sp + o);
+#pragma unroll
+        for (int q = 0; q < KQ; ++q) b[u][q] = *reinterpret_cast<const v4u*>(ap + q * bstride + o);
+      }
+#pragma unroll
+      for (int u = 0; u < kSq16Unroll; ++u) {
+        const int tu = t + 16 * u;
+        if (tu >= n) break;
+        if (tu + 16 > n) {
+          const int rem = n - tu - 8 * half;     // valid tokens among this lane's eight
+#pragma unroll
+          for (int d = 0; d < 4; ++d) {
+            const uint32_t keep = (2 * d < rem ? 0x0000FFFFu : 0u) | (2 * d + 1 < rem ? 0xFFFF0000u : 0u);
+            a[u][d] &= keep;
+#pragma unroll
+            for (int q = 0; q < KQ; ++q) b[u][q][d] &= keep;
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < KQ; ++q)
+          c[q] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a[u]),
+                                                        __builtin_bit_cast(f16x8, b[u][q]), c[q], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < KQ; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc2[q][r] = fmaf(c[q][r], c[q][r], acc2[q][r]);
+  }
+  // acc2[q][r] holds entry (32 jb + 8 (r / 4) + 4 half + r % 4, 32 (kb0 + q) + col)
+  float* o = part + (int64_t)split * d_out * d_in;
+#pragma unroll
+  for (int q = 0; q < KQ; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int j = jb * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+      const int k = (kb0 + q) * 32 + col;
+      if (j < d_out && k < d_in) o[(int64_t)j * d_in + k] = acc2[q][r];
+    }
+}
+
+// sq[e] = (accumulate ? sq[e] : 0) + h^2 * sum over ranges, in order, of part[s][e]
+// (h = 2^-(e_acts + e_grads) undoes the input scaling of both factors; applied
+// twice so that the factor itself neither overflows nor underflows).
+__global__ __launch_bounds__(256) void k_ekfac_sum(const float* __restrict__ part, int splits,
+                                                   int64_t n, float h, float* __restrict__ sq,
+                                                   int accumulate) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= n) return;
+  float v = 0.f;
+  for (int s = 0; s < splits; ++s) v += part[s * n + e];
+  v = (v * h) * h;
+  sq[e] = accumulate ? sq[e] + v : v;
+}
+
+// Example ranges of the fp16 squares: enough workgroups for two per CU, at
+// least 4 examples per range, at most 32 ranges.
+int sq16_splits(int64_t N, int64_t d_in, int64_t d_out) {
+  const int64_t groups = ceil_div(d_in, 32 * kSq16Cols) * ceil_div(d_out, 128);
+  int64_t sp = ceil_div(2 * kCus, groups);
+  sp = std::min<int64_t>(sp, std::max<int64_t>(1, N / 4));
+  return (int)std::max<int64_t>(1, std::min<int64_t>(sp, 32));
+}
+
 eogp_plan basis_plan(int64_t d_in, int64_t d_out) {
   eogp_plan q;
   q.d_out = d_out;
@@ -474,16 +593,19 @@ size_t panel_bytes(const eogp_plan& q) {
 
 size_t ekfac_ws(int64_t N, int64_t T, int64_t d_in, int64_t d_out) {
   const eogp_plan q = basis_plan(d_in, d_out);
-  return work_bytes(&q, N, T) + panel_bytes(q);
+  return work_bytes(&q, N, T) + panel_bytes(q) +
+         align256((size_t)sq16_splits(N, d_in, d_out) * d_out * d_in * 4);
 }
 
 eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int64_t ld_grads,
                        bool bf16_in, const uint8_t* mask, int64_t N, int64_t T, int64_t d_in,
-                       int64_t d_out, const float* Q_A, const float* Q_S, int prec, float* sq,
-                       int accumulate, void* ws, size_t ws_bytes, hipStream_t s) {
+                       int64_t d_out, const float* Q_A, const float* Q_S, int prec,
+                       int32_t e_acts, int32_t e_grads, float* sq, int accumulate, void* ws,
+                       size_t ws_bytes, hipStream_t s) {
   eogp_plan q = basis_plan(d_in, d_out);
-  if (ws_bytes < work_bytes(&q, N, T) + panel_bytes(q))
-    return fail(EOGP_ERR_WORKSPACE, "ekfac: workspace too small");
+  if (ws_bytes < ekfac_ws(N, T, d_in, d_out)) return fail(EOGP_ERR_WORKSPACE, "ekfac: workspace too small");
+  q.e_acts = e_acts;
+  q.e_grads = e_grads;
   Carve cv(ws, ws_bytes);
   Work w = carve_work(&q, N, T, cv);
   q.qs_hi = cv.take<uint16_t>((size_t)q.rows_pad * q.ld_out);
@@ -496,11 +618,26 @@ eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int
   basis_panels(Q_S, d_out, q.rows_pad, q.ld_out, list, q.qs_hi, q.qs_lo, q.qs_f16, s);
   basis_panels(Q_A, d_in, q.cols_pad, q.ld_in, list, q.qa_hi, q.qa_lo, q.qa_f16, s);
   EOGP_LAUNCH_CHECK("ekfac panels");
-  eogp_status st = rotate_tokens(&q, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, false,
+  float* part = cv.take<float>((size_t)sq16_splits(N, d_in, d_out) * d_out * d_in);
+  const bool f16 = prec == EOGP_PREC_F16;
+  eogp_status st = rotate_tokens(&q, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, f16,
                                  w, s);
   if (st != EOGP_OK) return st;
-  const int nbj = (int)ceil_div(d_out, 32), nbk = (int)ceil_div(d_in, 32);
   timing::Scope ts(EOGP_KT_EKFAC, s);
+  if (f16) {
+    const int sp = sq16_splits(N, d_in, d_out);
+    hipLaunchKernelGGL(k_ekfac_sq16<kSq16Cols>, dim3((unsigned)ceil_div(d_in, 32 * kSq16Cols), (unsigned)ceil_div(d_out, 128),
+                                          (unsigned)sp),
+                       dim3(256), 0, s, w.St16, w.At16, w.ldt, w.cnt, w.len, N, sp, (int)d_out,
+                       (int)d_in, part);
+    const int64_t n = d_out * d_in;
+    const float h = std::ldexp(1.f, -(e_acts + e_grads));
+    hipLaunchKernelGGL(k_ekfac_sum, dim3((unsigned)ceil_div(n, 256)), dim3(256), 0, s, part, sp, n,
+                       h, sq, accumulate);
+    EOGP_LAUNCH_CHECK("ekfac squares");
+    return EOGP_OK;
+  }
+  const int nbj = (int)ceil_div(d_out, 32), nbk = (int)ceil_div(d_in, 32);
   hipLaunchKernelGGL(k_ekfac_sq, dim3((unsigned)ceil_div(nbk, 4), (unsigned)nbj), dim3(256), 0, s,
                      w.St, q.rows_pad, w.At, q.cols_pad, w.cnt, N, nbk, (int)d_out, (int)d_in, sq,
                      accumulate);

@@ -85,8 +85,8 @@ def load(path: str | None = None):
         "eogp_sign_pack": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp]),
         "eogp_ekfac_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64]),
         "eogp_ekfac_eigenvalues": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64,
-                                           c_i64, c_i64, c_vp, c_vp, c_i32, c_vp, c_i32, c_vp,
-                                           c_sz, c_vp]),
+                                           c_i64, c_i64, c_vp, c_vp, c_i32, c_i32, c_i32, c_vp,
+                                           c_i32, c_vp, c_sz, c_vp]),
         "eogp_srht_project_workspace_size": (c_sz, [c_i64, c_i64]),
         "eogp_srht_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_vp, c_i64, c_vp, c_i64,
                                       c_vp, c_sz, c_vp]),
@@ -298,10 +298,11 @@ def eogp_ekfac_workspace_size(N: int, T: int, d_in: int, d_out: int) -> int:
 
 
 def eogp_ekfac_eigenvalues(acts, out_grads, token_mask, Q_A, Q_S, sq_sum=None, accumulate=False,
-                           prec=PREC_ACCURATE, ws=None, stream=None):
+                           prec=PREC_ACCURATE, exponents=(0, 0), ws=None, stream=None):
     """Sum over the batch of the squared rotated gradients (Q_S^T G_i Q_A)^2,
     [d_out, d_in] float32 (divide by the total number of examples for the
-    corrected eigenvalues); see eogp_ekfac_eigenvalues in eogp.h."""
+    corrected eigenvalues). exponents = (e_acts, e_grads), the power-of-two
+    input scaling of the fp16 mode; see eogp_ekfac_eigenvalues in eogp.h."""
     L = load()
     _need_cuda(acts, out_grads, token_mask, Q_A, Q_S, sq_sum)
     N, T, d_in = acts.shape
@@ -316,8 +317,9 @@ def eogp_ekfac_eigenvalues(acts, out_grads, token_mask, Q_A, Q_S, sq_sum=None, a
     ws, wsb = _workspace(need, acts.device, ws)
     _check(L.eogp_ekfac_eigenvalues(_ptr(acts), ld_a, _ptr(out_grads), ld_g,
                                     _acts_dtype(acts, out_grads), _ptr(token_mask), N, T, d_in,
-                                    d_out, _ptr(Q_A), _ptr(Q_S), prec, _ptr(sq_sum),
-                                    1 if accumulate else 0, _ptr(ws), wsb, _stream(stream)))
+                                    d_out, _ptr(Q_A), _ptr(Q_S), prec, int(exponents[0]),
+                                    int(exponents[1]), _ptr(sq_sum), 1 if accumulate else 0,
+                                    _ptr(ws), wsb, _stream(stream)))
     return sq_sum
 
 

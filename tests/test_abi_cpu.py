@@ -62,15 +62,20 @@ def test_encode_and_score_argument_validation_without_device():
     # pca: k > m, ld too small
     assert L.eogp_pca_project(fake, 8, 2, 8, fake, 2, 8, 9, fake, 9, 0, None, 0, None) == -1
     assert L.eogp_pca_project(fake, 4, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -1
-    # ekfac: bad sizes, NULL bases, bad precision
-    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 0, 4, fake, fake, 1, fake, 0,
-                                    fake, 1 << 30, None) == -1
-    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, None, fake, 1, fake, 0,
-                                    fake, 1 << 30, None) == -1
-    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, fake, fake, 7, fake, 0,
-                                    fake, 1 << 30, None) == -1
-    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, fake, fake, 1, fake, 0,
-                                    fake, 16, None) == -4
+    # ekfac: bad sizes, NULL bases, bad precision, exponent out of range, small workspace
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 0, 4, fake, fake, 1, 0, 0,
+                                    fake, 0, fake, 1 << 30, None) == -1
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, None, fake, 1, 0, 0,
+                                    fake, 0, fake, 1 << 30, None) == -1
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, fake, fake, 7, 0, 0,
+                                    fake, 0, fake, 1 << 30, None) == -1
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, fake, fake, 2, 61, 0,
+                                    fake, 0, fake, 1 << 30, None) == -1
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 4, 4, fake, fake, 1, 0, 0,
+                                    fake, 0, fake, 16, None) == -4
+    # the compacted token list is indexed in 32 bits
+    assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 1 << 20, (1 << 11) - 8, 4, 4, fake,
+                                    fake, 1, 0, 0, fake, 0, fake, 1 << 30, None) == -1
     # srht: k > p, m too large, ld too small, two-stage form without workspace
     assert L.eogp_srht_project(fake, 100, 2, 100, fake, fake, 129, fake, 129, None, 0, None) == -1
     assert L.eogp_srht_project(fake, (1 << 20) + 1, 2, (1 << 20) + 1, fake, fake, 8, fake, 8,

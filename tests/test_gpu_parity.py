@@ -433,6 +433,80 @@ def test_ekfac_bf16_inputs():
         assert err <= tol
 
 
+# fp16 mode: inputs, bases and the rotated tokens are each rounded once to
+# fp16 (unit roundoff u = 2^-11 ~ 4.9e-4), products and sums in fp32. A block
+# sum C = sum_t S~ A~ then carries a relative error of a few u (the rounding
+# of both input factors, of both bases and of both rotated factors), and C^2
+# twice that; over the whole matrix the errors are independent, so the
+# Frobenius-relative error of sq_sum stays near 2u ~ 1e-3: the tolerance
+# below is 3e-3.
+F16_EKFAC_TOL = 3e-3
+
+
+@pytest.mark.parametrize("N,T,d_in,d_out,lens_lo", [
+    (9, 37, 97, 130, 0),          # odd widths, ragged runs, an empty example
+    (40, 64, 384, 320, 1),        # several column groups, example ranges split
+    (3, 200, 256, 128, 150),      # few examples: one range
+])
+def test_ekfac_fp16_mode_matches_oracle(N, T, d_in, d_out, lens_lo):
+    say(f"[ekfac fp16] N={N} T={T} d_in={d_in} d_out={d_out}")
+    a, ds, mask, QA, QS, _ = random_problem(73 + N, N, T, d_in, d_out, 10, lens_lo=lens_lo)
+    if N == 9:
+        mask[3, :] = 0
+        a = S.fill_masked(a, mask)
+        ds = S.fill_masked(ds, mask)
+    ref = O.ekfac_eigenvalues(a, ds, mask, QA, QS) * N
+    ex = (0, 7)                                         # gradients are of order 1e-2
+    sq = E.eogp_ekfac_eigenvalues(d(a), d(ds), d(mask), d(QA), d(QS), prec=E.PREC_F16, exponents=ex)
+    again = E.eogp_ekfac_eigenvalues(d(a), d(ds), d(mask), d(QA), d(QS), prec=E.PREC_F16, exponents=ex)
+    torch.cuda.synchronize()
+    err = rel_fro(sq.cpu().numpy(), ref)
+    say(f"   fro {err:.2e}")
+    assert err <= F16_EKFAC_TOL
+    assert torch.equal(sq, again)                       # fixed summation order
+    # two accumulated batches give the one-batch result
+    h = N // 2
+    two = E.eogp_ekfac_eigenvalues(d(a[:h]), d(ds[:h]), d(mask[:h]), d(QA), d(QS), prec=E.PREC_F16,
+                                   exponents=ex)
+    E.eogp_ekfac_eigenvalues(d(a[h:]), d(ds[h:]), d(mask[h:]), d(QA), d(QS), sq_sum=two,
+                             accumulate=True, prec=E.PREC_F16, exponents=ex)
+    torch.cuda.synchronize()
+    assert rel_fro(two.cpu().numpy(), ref) <= F16_EKFAC_TOL
+
+
+def test_ekfac_fp16_mode_tiny_workload(tiny_fit):
+    raw, f = tiny_fit["raw"], tiny_fit["fit"]
+    QA = f["Q_A"].astype(np.float32)
+    QS = f["Q_S"].astype(np.float32)
+    sq = E.eogp_ekfac_eigenvalues(d(raw["a"]), d(raw["ds"]), d(raw["mask"]), d(QA), d(QS),
+                                  prec=E.PREC_F16)
+    torch.cuda.synchronize()
+    lam = sq.cpu().numpy() / raw["a"].shape[0]
+    ref = O.ekfac_eigenvalues(raw["a"], raw["ds"], raw["mask"], QA, QS)
+    say(f"[ekfac fp16] tiny: fro {rel_fro(lam, ref):.2e}")
+    assert rel_fro(lam, ref) <= F16_EKFAC_TOL
+
+
+def test_ekfac_fp16_mode_input_exponents():
+    """Gradients of order 1e-7 leave fp16's normal range; the exponents bring
+    them back, and the result is scaled back exactly."""
+    N, T, d_in, d_out = 6, 48, 160, 96
+    a, ds, mask, QA, QS, _ = random_problem(74, N, T, d_in, d_out, 10, lens_lo=20)
+    ds = (ds * 1e-5).astype(np.float32)
+    ref = O.ekfac_eigenvalues(a, ds, mask, QA, QS) * N
+    plain = E.eogp_ekfac_eigenvalues(d(a), d(ds), d(mask), d(QA), d(QS), prec=E.PREC_F16)
+    scaled = E.eogp_ekfac_eigenvalues(d(a), d(ds), d(mask), d(QA), d(QS), prec=E.PREC_F16,
+                                      exponents=(-1, 24))
+    torch.cuda.synchronize()
+    e0, e1 = rel_fro(plain.cpu().numpy(), ref), rel_fro(scaled.cpu().numpy(), ref)
+    say(f"[ekfac fp16] without exponents {e0:.2e}, with {e1:.2e}")
+    assert e1 <= F16_EKFAC_TOL
+    assert e0 > 10 * e1
+    with pytest.raises(E.EogpError):
+        E.eogp_ekfac_eigenvalues(d(a), d(ds), d(mask), d(QA), d(QS), prec=E.PREC_F16,
+                                 exponents=(0, 61))
+
+
 # ---------------------------------------------------------------------------
 # Random second stage (EOGP-R)
 # ---------------------------------------------------------------------------
