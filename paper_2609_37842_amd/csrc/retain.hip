@@ -237,6 +237,30 @@ __global__ __launch_bounds__(256) void k_zperm(const float* __restrict__ Zt, int
   }
 }
 
+// Rows of up to kZpermLdsMax coordinates: one workgroup per example copies
+// the row of block sums into LDS with 16-byte loads, then gathers from LDS and
+// writes Z coalesced (the random reads stay on chip).
+constexpr int kZpermLdsMax = 32768;
+
+__global__ __launch_bounds__(1024) void k_zperm_lds(const float* __restrict__ Zt, int m,
+                                                    const int32_t* __restrict__ ent_pos,
+                                                    const float* __restrict__ w,
+                                                    float* __restrict__ Z, int64_t ldz, int64_t ex0) {
+  extern __shared__ float L[];
+  const int64_t i = ex0 + blockIdx.x;
+  const float* src = Zt + i * (int64_t)m;
+  const int tid = threadIdx.x, nt = blockDim.x;
+  if ((m & 3) == 0) {                          // rows start on 16-byte boundaries
+    for (int c = tid; c < m / 4; c += nt)
+      reinterpret_cast<float4*>(L)[c] = reinterpret_cast<const float4*>(src)[c];
+  } else {
+    for (int c = tid; c < m; c += nt) L[c] = src[c];
+  }
+  __syncthreads();
+  float* dst = Z + i * ldz;
+  for (int r = tid; r < m; r += nt) dst[r] = w[r] * L[ent_pos[r]];
+}
+
 struct Work {
   int32_t* cnt;   // [N + 1] per-example run lengths, scanned in place into offsets
   int32_t* len;   // [N] valid tokens per example (aligned runs only)
@@ -375,6 +399,12 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
 
   // 3. retained products, half-whitened, in canonical order
   const float out_scale = f16 ? std::ldexp(1.f, -(p->e_acts + p->e_grads)) : 1.f;
+  static bool attr_set = false;     // the attribute is per kernel, not per device
+  if (!attr_set) {
+    EOGP_HIP(hipFuncSetAttribute((const void*)k_zperm_lds, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                 (int)(sizeof(float) * kZpermLdsMax)));
+    attr_set = true;
+  }
   for (int64_t ex0 = 0; p->n_tiles > 0 && ex0 < N; ex0 += 65535) {
     const int64_t nex = std::min<int64_t>(65535, N - ex0);
     timing::Scope ts(EOGP_KT_RETAINED, s);
@@ -388,8 +418,13 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
                          w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,
                          p->ent_loc, out_scale, w.Zt, p->m, ex0);
     }
-    hipLaunchKernelGGL(k_zperm, dim3((unsigned)ceil_div(p->m, 256 * kZpermPer), (unsigned)nex),
-                       dim3(256), 0, s, w.Zt, p->m, p->ent_pos, p->ret_w, Z, ldz, ex0);
+    if (p->m <= kZpermLdsMax) {
+      hipLaunchKernelGGL(k_zperm_lds, dim3((unsigned)nex), dim3(1024), (size_t)p->m * 4, s, w.Zt,
+                         (int)p->m, p->ent_pos, p->ret_w, Z, ldz, ex0);
+    } else {
+      hipLaunchKernelGGL(k_zperm, dim3((unsigned)ceil_div(p->m, 256 * kZpermPer), (unsigned)nex),
+                         dim3(256), 0, s, w.Zt, p->m, p->ent_pos, p->ret_w, Z, ldz, ex0);
+    }
     EOGP_LAUNCH_CHECK("retained products");
   }
   return EOGP_OK;
