@@ -181,6 +181,34 @@ def test_half_whitened_second_moment_matches_proxy_diagonal(tiny_fit):
     assert np.max(np.abs(lhs - rhs)) < 1e-12
 
 
+def test_ekfac_eigenvalues_parseval_identity_basis_and_symmetries():
+    """Corrected eigenvalues (Section 2.2, eq. ekfac_eigendecompose) against
+    gradients summed by explicit loops: with identity bases Lambda is the mean of
+    the squared gradient entries; for any orthogonal bases the entries sum to the
+    mean squared Frobenius norm (the rotation preserves it); permuting or
+    negating basis columns permutes Lambda and leaves it unchanged otherwise."""
+    a, ds, mask, QA, QS, _ = small_problem(81, N=4, T=6, d_in=5, d_out=3)
+    mask[1, 4:] = 0
+    mask[2, :] = 0
+    N, T = mask.shape
+    G = np.zeros((N, 3, 5))
+    for i in range(N):
+        for t in range(T):
+            if mask[i, t]:
+                for j in range(3):
+                    for k in range(5):
+                        G[i, j, k] += ds[i, t, j] * a[i, t, k]
+    lam_id = O.ekfac_eigenvalues(a, ds, mask, np.eye(5), np.eye(3))
+    assert np.allclose(lam_id, (G * G).mean(axis=0), rtol=1e-13, atol=0)
+    lam = O.ekfac_eigenvalues(a, ds, mask, QA, QS)
+    assert np.isclose(lam.sum(), (G * G).sum(axis=(1, 2)).mean(), rtol=1e-12)
+    assert np.all(lam >= 0)
+    pa, ps = np.array([3, 0, 4, 1, 2]), np.array([2, 0, 1])
+    sa, ss = np.array([1, -1, 1, -1, -1]), np.array([-1, 1, 1])
+    lam_p = O.ekfac_eigenvalues(a, ds, mask, QA[:, pa] * sa, QS[:, ps] * ss)
+    assert np.allclose(lam_p, lam[np.ix_(ps, pa)], rtol=1e-12, atol=0)
+
+
 def test_kfac_eigenbasis_diagonalises_factors(tiny_fit):
     f = tiny_fit["fit"]
     for F, Q in ((f["A"], f["Q_A"]), (f["S"], f["Q_S"])):
