@@ -107,7 +107,12 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
   g.M = N;
   g.N = k;
   g.K = m;
+  // Units run split by split (each XCD's contiguous range is then one K
+  // range), column tile by column tile with the row tiles of a column tile
+  // together: each P slice is fetched once and shared by the row tiles, and
+  // the Z slices of the K range stay in that XCD's L2.
   g.n_major = true;
+  g.split_major = true;
   g.timing_class = EOGP_KT_PCA_GEMM;
   const size_t copy = pca_split_copy_bytes(m, k, p_dtype);
   if (ws_bytes < copy) return fail(EOGP_ERR_WORKSPACE, "pca_project: workspace too small");

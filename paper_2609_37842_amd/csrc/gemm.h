@@ -40,7 +40,10 @@ struct GemmArgs {
   int64_t M = 0;                   // rows (upper bound if M_dev is set)
   const int32_t* M_dev = nullptr;  // device-side row count (<= M), or null
   int64_t N = 0, K = 0;
-  bool n_major = false;            // unit order: N-tiles outer (PCA: share B across M)
+  bool n_major = false;            // unit order: N-tiles outer (share B across M)
+  // Split-K unit order: splits outermost, then tiles (M or N outer per n_major),
+  // so that the units running together share one K range of one operand.
+  bool split_major = false;
   // Split-K scratch (host-known M only): max_splits partial [M][N] fp32 tiles.
   float* partial = nullptr;
   int max_splits = 1;

@@ -226,8 +226,15 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
   const int sc = tid & 31, sr = tid >> 5;   // element A path: column, first row (rows sr + 16e)
 
   for (int64_t u = t_begin; u < t_end; u += t_step) {
-    const int64_t t = u / kp.splits;
-    const int split = (int)(u % kp.splits);
+    int64_t t;
+    int split;
+    if (g.split_major) {
+      split = (int)(u / (tiles_m * tiles_n));
+      t = u % (tiles_m * tiles_n);
+    } else {
+      t = u / kp.splits;
+      split = (int)(u % kp.splits);
+    }
     int64_t tm, tn;
     if (g.n_major) { tn = t / tiles_m; tm = t % tiles_m; }
     else { tm = t / tiles_n; tn = t % tiles_n; }
@@ -576,8 +583,15 @@ void k_gemm_p(KParams kp) {
   const int b_r0 = tid >> 2, b_pc = tid & 3;
 
   for (int64_t u = t_begin; u < t_end; u += t_step) {
-    const int64_t t = u / kp.splits;
-    const int split = (int)(u % kp.splits);
+    int64_t t;
+    int split;
+    if (g.split_major) {
+      split = (int)(u / (tiles_m * tiles_n));
+      t = u % (tiles_m * tiles_n);
+    } else {
+      t = u / kp.splits;
+      split = (int)(u % kp.splits);
+    }
     int64_t tm, tn;
     if (g.n_major) { tn = t / tiles_m; tm = t % tiles_m; }
     else { tm = t / tiles_n; tn = t % tiles_n; }
