@@ -597,6 +597,11 @@ __global__ __launch_bounds__(256) void k_ekfac_sum(const float* __restrict__ par
   sq[e] = accumulate ? sq[e] + v : v;
 }
 
+__global__ __launch_bounds__(256) void k_fill_zero(float* __restrict__ x, int64_t n) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < n) x[e] = 0.f;
+}
+
 // Example ranges of the fp16 squares: enough workgroups for two per CU, at
 // least 4 examples per range, at most 32 ranges.
 int sq16_splits(int64_t N, int64_t d_in, int64_t d_out) {
@@ -639,6 +644,14 @@ eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int
                        size_t ws_bytes, hipStream_t s) {
   eogp_plan q = basis_plan(d_in, d_out);
   if (ws_bytes < ekfac_ws(N, T, d_in, d_out)) return fail(EOGP_ERR_WORKSPACE, "ekfac: workspace too small");
+  if (N == 0) {                                  // an empty batch adds nothing
+    if (!accumulate) {
+      hipLaunchKernelGGL(k_fill_zero, dim3((unsigned)ceil_div(d_out * d_in, 256)), dim3(256), 0, s,
+                         sq, d_out * d_in);
+      EOGP_LAUNCH_CHECK("ekfac (empty batch)");
+    }
+    return EOGP_OK;
+  }
   q.e_acts = e_acts;
   q.e_grads = e_grads;
   Carve cv(ws, ws_bytes);

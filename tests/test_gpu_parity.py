@@ -474,6 +474,22 @@ def test_ekfac_fp16_mode_matches_oracle(N, T, d_in, d_out, lens_lo):
     assert rel_fro(two.cpu().numpy(), ref) <= F16_EKFAC_TOL
 
 
+@pytest.mark.parametrize("prec", [0, 1, 2])
+def test_ekfac_empty_batches(prec):
+    """No examples, or every token masked: the sums are zero (accumulate=False)
+    or left unchanged (accumulate=True), in every precision mode."""
+    d_in, d_out = 96, 64
+    a, ds, mask, QA, QS, _ = random_problem(75, 3, 16, d_in, d_out, 10)
+    for n, msk in ((0, mask[:0]), (3, np.zeros_like(mask))):
+        sq = E.eogp_ekfac_eigenvalues(d(a[:n]), d(ds[:n]), d(msk), d(QA), d(QS), prec=prec)
+        prev = torch.full((d_out, d_in), 2.5, dtype=torch.float32, device=DEV)
+        E.eogp_ekfac_eigenvalues(d(a[:n]), d(ds[:n]), d(msk), d(QA), d(QS), sq_sum=prev,
+                                 accumulate=True, prec=prec)
+        torch.cuda.synchronize()
+        assert torch.all(sq == 0)
+        assert torch.all(prev == 2.5)
+
+
 def test_ekfac_fp16_mode_tiny_workload(tiny_fit):
     raw, f = tiny_fit["raw"], tiny_fit["fit"]
     QA = f["Q_A"].astype(np.float32)
