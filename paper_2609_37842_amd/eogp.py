@@ -414,9 +414,12 @@ def eogp_score_topk(codes, scales, k_per_module, Y, topk, full_scores=False, out
     full = torch.empty((Q, N), dtype=torch.float32, device=Y.device) if full_scores else None
     need = int(L.eogp_score_topk_workspace_size(N, Q, U, ks, topk))
     ws, wsb = _workspace(need, Y.device, ws)
-    _check(L.eogp_score_topk(_ptr(codes), codes.stride(0), _ptr(scales), N, U, ks, _ptr(Y),
-                             Y.stride(0), Q, topk, _ptr(out_idx), _ptr(out_score), _ptr(full),
-                             _ptr(ws), wsb, _stream(stream)))
+    # an empty tensor may report stride 0; with no rows any valid stride will do
+    cstride = codes.stride(0) if N > 0 else sum(int(k) for k in k_per_module) // 8
+    ldy = Y.stride(0) if Q > 0 else sum(int(k) for k in k_per_module)
+    _check(L.eogp_score_topk(_ptr(codes), cstride, _ptr(scales), N, U, ks, _ptr(Y), ldy, Q,
+                             topk, _ptr(out_idx), _ptr(out_score), _ptr(full), _ptr(ws), wsb,
+                             _stream(stream)))
     return out_idx, out_score, full
 
 

@@ -620,6 +620,22 @@ def test_score_topk_bit_exact_large_stores(N, ks, Q, topk):
     assert np.array_equal(sc.cpu().numpy(), ov)
 
 
+def test_score_empty_store_and_no_queries():
+    """An empty store pads every query's list (index -1, score -inf); no
+    queries is a no-op."""
+    ks = [128, 64]
+    codes, scales, Y = random_store(23, 0, ks, 4)
+    idx, sc, _ = E.eogp_score_topk(d(codes), d(scales.view(np.int16)), ks, d(Y), 10)
+    torch.cuda.synchronize()
+    assert torch.all(idx == -1)
+    assert torch.all(sc == float("-inf"))
+    codes, scales, _ = random_store(24, 50, ks, 1)
+    idx, sc, _ = E.eogp_score_topk(d(codes), d(scales.view(np.int16)), ks,
+                                   torch.empty((0, 192), device=DEV), 10)
+    torch.cuda.synchronize()
+    assert idx.shape == (0, 10) and sc.shape == (0, 10)
+
+
 def test_score_integral_queries_give_exact_real_scores():
     g = np.random.default_rng(21)
     ks = [256, 128]
