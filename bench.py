@@ -288,7 +288,7 @@ def pca_fit_measurement(st, dev, n=10000):
 # ---------------------------------------------------------------------------
 # Oracle CPU baseline on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
-def cpu_baseline(st: Gpt2Step, budget_s=25.0):
+def cpu_baseline(st: Gpt2Step):
     import numpy as np
     import torch
 
@@ -298,7 +298,7 @@ def cpu_baseline(st: Gpt2Step, budget_s=25.0):
         threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    n_ex = 24
+    n_ex = 48                                     # about 10 s of oracle work on 16 threads
     per_shape = {}
     for si, (name, di, do) in enumerate(st.shapes):
         u = si                                     # block 0 module of this shape
