@@ -3,7 +3,10 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <mutex>
+#include <set>
 #include <string>
+#include <tuple>
 
 #include "common.h"
 #include "plan.h"
@@ -61,6 +64,18 @@ eogp_status check_hip(hipError_t e, const char* what) {
   if (e == hipSuccess) return EOGP_OK;
   g_last_error = std::string(what) + ": " + hipGetErrorString(e);
   return EOGP_ERR_DEVICE;
+}
+
+eogp_status ensure_dynamic_lds(const void* fn, int bytes) {
+  static std::mutex mu;
+  static std::set<std::tuple<const void*, int, int>> done;   // (kernel, device, bytes)
+  int dev = 0;
+  EOGP_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> g(mu);
+  if (done.count({fn, dev, bytes})) return EOGP_OK;
+  EOGP_HIP(hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes));
+  done.insert({fn, dev, bytes});
+  return EOGP_OK;
 }
 
 }  // namespace eogp

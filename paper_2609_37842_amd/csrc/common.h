@@ -26,6 +26,10 @@ eogp_status check_hip(hipError_t e, const char* what);
     if (e_ != hipSuccess) return ::eogp::check_hip(e_, what);   \
   } while (0)
 
+// Raises kernel `fn`'s dynamic-LDS limit to `bytes` on the current device, once
+// per (kernel, device); safe to call from several host threads.
+eogp_status ensure_dynamic_lds(const void* fn, int bytes);
+
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }

@@ -399,11 +399,9 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
 
   // 3. retained products, half-whitened, in canonical order
   const float out_scale = f16 ? std::ldexp(1.f, -(p->e_acts + p->e_grads)) : 1.f;
-  static bool attr_set = false;     // the attribute is per kernel, not per device
-  if (!attr_set) {
-    EOGP_HIP(hipFuncSetAttribute((const void*)k_zperm_lds, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)(sizeof(float) * kZpermLdsMax)));
-    attr_set = true;
+  if (p->m <= kZpermLdsMax) {
+    const eogp_status st_lds = ensure_dynamic_lds((const void*)k_zperm_lds, (int)(sizeof(float) * kZpermLdsMax));
+    if (st_lds != EOGP_OK) return st_lds;
   }
   for (int64_t ex0 = 0; p->n_tiles > 0 && ex0 < N; ex0 += 65535) {
     const int64_t nex = std::min<int64_t>(65535, N - ex0);

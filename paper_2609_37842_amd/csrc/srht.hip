@@ -151,14 +151,9 @@ eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, cons
                          size_t ws_bytes, hipStream_t s) {
   if (N == 0) return EOGP_OK;
   const int logp = srht_log(m);
-  static bool attr_set = false;     // the attributes are per kernel, not per device
-  if (!attr_set) {
-    EOGP_HIP(hipFuncSetAttribute((const void*)k_srht, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)(sizeof(float) << kSrhtMaxLog)));
-    EOGP_HIP(hipFuncSetAttribute((const void*)k_srht_chunk,
-                                 hipFuncAttributeMaxDynamicSharedMemorySize,
-                                 (int)(sizeof(float) << kSrhtMaxLog)));
-    attr_set = true;
+  for (const void* fn : {(const void*)k_srht, (const void*)k_srht_chunk}) {
+    const eogp_status st = ensure_dynamic_lds(fn, (int)(sizeof(float) << kSrhtMaxLog));
+    if (st != EOGP_OK) return st;
   }
   const float scale = (float)(1.0 / std::sqrt((double)k));
   timing::Scope ts(EOGP_KT_SRHT, s);
