@@ -44,6 +44,10 @@ struct GemmArgs {
   // Split-K unit order: splits outermost, then tiles (M or N outer per n_major),
   // so that the units running together share one K range of one operand.
   bool split_major = false;
+  // Optional kXcds int32 work counters (device memory; the launch zeroes them):
+  // when given, each XCD's workgroups take their units from a shared counter
+  // (longest units first) instead of a fixed stride.
+  int32_t* sched = nullptr;
   // Split-K scratch (host-known M only): max_splits partial [M][N] fp32 tiles.
   float* partial = nullptr;
   int max_splits = 1;
@@ -55,6 +59,14 @@ struct GemmArgs {
 // (2 needs B_lo); f16: MFMA operands are fp16 (else bf16).
 eogp_status gemm_nt(const GemmArgs& g, AType a_type, int a_parts, int b_parts, bool f16,
                     hipStream_t s);
+
+// Two independent products in one launch (same operand types and timing
+// class; put the one with the longer K first): their units share the grid, so
+// the second fills the first one's last round. Applies to single-pass products
+// on aligned operands without split-K, with g1.sched given (the work
+// counters); anything else runs as two ordinary launches.
+eogp_status gemm_nt2(const GemmArgs& g1, const GemmArgs& g2, AType a_type, int a_parts,
+                     int b_parts, bool f16, hipStream_t s);
 
 // Bytes of split-K scratch for an M x N product with up to max_splits splits.
 size_t gemm_partial_bytes(int64_t M, int64_t N, int max_splits);

@@ -39,6 +39,11 @@
 // (tile, K-split) are dealt out in contiguous ranges per XCD (workgroup b runs
 // on XCD b % 8), so workgroups sharing an A row-block (rotations) or a B
 // column-block (PCA, n_major) run together on one XCD and hit the same L2.
+// k_gemm_p can run two independent products in one launch (the two rotations
+// of a module): each XCD's range then holds its share of the first product's
+// units followed by its share of the second's, and the XCD's workgroups take
+// positions from a per-XCD atomic counter, so the short units of the second
+// product fill the last round of the first instead of leaving CUs idle.
 // Small-M problems split K; each split writes its own fp32 partial tile and a
 // second kernel adds the partials in split order (deterministic).
 #include <algorithm>
@@ -55,7 +60,15 @@ struct KParams {
   GemmArgs g;
   int64_t kc;       // K per split (multiple of BK)
   int splits;
+  // k_gemm_p only: an optional second product in the same launch (one split)
+  GemmArgs g2;
+  int64_t kc2 = 0;
+  int nprob = 1;
 };
+
+__global__ void k_zero_sched(int32_t* __restrict__ c) {
+  if (threadIdx.x < kXcds) c[threadIdx.x] = 0;
+}
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
@@ -546,33 +559,42 @@ __global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_gemm_p(KParams kp) {
   constexpr int BNP = 256;
   constexpr int WI = 4, WJ = 4;          // 128 x 128 per wave
-  const GemmArgs& g = kp.g;
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][BNP * BK];
   __shared__ int64_t sOff[BM];
+  __shared__ int sPos;
 
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int64_t M = g.M_dev ? (int64_t)(*g.M_dev) : g.M;
-  const int64_t N = g.N, K = g.K;
-  const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BNP - 1) / BNP;
-  const int64_t n_units = tiles_m * tiles_n * kp.splits;
-
+  // Units of each product: tiles x splits (M from the device count when given).
+  auto units_of = [&](int pi) -> int64_t {
+    const GemmArgs& q = pi ? kp.g2 : kp.g;
+    const int64_t Mq = q.M_dev ? (int64_t)(*q.M_dev) : q.M;
+    return ((Mq + BM - 1) / BM) * ((q.N + BNP - 1) / BNP) * (pi ? 1 : kp.splits);
+  };
+  const int64_t nu0 = units_of(0), nu1 = kp.nprob > 1 ? units_of(1) : 0;
+  // One queue per XCD (workgroup b runs on XCD b % kXcds): the queue holds a
+  // contiguous range of each product's units, the first product's before the
+  // second's, so the workgroups of an XCD work on neighbouring tiles (shared
+  // operand rows in that XCD's L2). Positions are taken at a fixed stride, or
+  // from the XCD's counter when kp.g.sched is given.
   const int G = gridDim.x, b = blockIdx.x;
-  int64_t t_begin, t_end, t_step;
-  if (G >= kXcds && G % kXcds == 0) {
-    const int xcd = b % kXcds;
-    const int64_t per = G / kXcds, chunk = (n_units + kXcds - 1) / kXcds;
-    t_begin = xcd * chunk + b / kXcds;
-    t_end = std::min<int64_t>((int64_t)(xcd + 1) * chunk, n_units);
-    t_step = per;
-  } else {
-    t_begin = b;
-    t_end = n_units;
-    t_step = G;
+  const bool xq = G >= kXcds && G % kXcds == 0;
+  const int nq = xq ? kXcds : 1, x = xq ? b % kXcds : 0;
+  const int64_t c0 = (nu0 + nq - 1) / nq, c1 = (nu1 + nq - 1) / nq;
+  const int64_t beg0 = std::min<int64_t>(x * c0, nu0);
+  const int64_t len0 = std::min<int64_t>((x + 1) * c0, nu0) - beg0;
+  const int64_t beg1 = std::min<int64_t>(x * c1, nu1);
+  const int64_t len1 = std::min<int64_t>((x + 1) * c1, nu1) - beg1;
+  const int64_t qlen = len0 + len1;
+  int32_t* const sched = kp.g.sched;
+  int64_t pos = b / nq;
+  if (sched) {
+    if (tid == 0) sPos = atomicAdd(&sched[x], 1);
+    __syncthreads();
+    pos = sPos;
   }
 
   const int wm = (wid >> 1) * 128, wn = (wid & 1) * 128;
-  const float a_scale = g.a_scale;
   // Staging: fp32 A 8 lanes per row (rows (tid >> 3) + 32 q, q < 8); 16-bit A
   // 4 lanes per row (rows (tid >> 2) + 64 q, q < 4); B 4 lanes per row.
   constexpr int AQ = AT == 0 ? 8 : 4;
@@ -582,22 +604,35 @@ void k_gemm_p(KParams kp) {
   const int a_pc = AT == 0 ? (tid & 7) : (tid & 3);
   const int b_r0 = tid >> 2, b_pc = tid & 3;
 
-  for (int64_t u = t_begin; u < t_end; u += t_step) {
+  while (pos < qlen) {
+    const int pi = pos < len0 ? 0 : 1;
+    const int64_t u = pi ? beg1 + (pos - len0) : beg0 + pos;
+    if (sched) {
+      __syncthreads();                   // every thread has read sPos
+      if (tid == 0) sPos = atomicAdd(&sched[x], 1);   // next position, fetched ahead
+    }
+    const GemmArgs& g = pi ? kp.g2 : kp.g;
+    const int splits = pi ? 1 : kp.splits;
+    const int64_t kc = pi ? kp.kc2 : kp.kc;
+    const int64_t M = g.M_dev ? (int64_t)(*g.M_dev) : g.M;
+    const int64_t N = g.N, K = g.K;
+    const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BNP - 1) / BNP;
+    const float a_scale = g.a_scale;
     int64_t t;
     int split;
     if (g.split_major) {
       split = (int)(u / (tiles_m * tiles_n));
       t = u % (tiles_m * tiles_n);
     } else {
-      t = u / kp.splits;
-      split = (int)(u % kp.splits);
+      t = u / splits;
+      split = (int)(u % splits);
     }
     int64_t tm, tn;
     if (g.n_major) { tn = t / tiles_m; tm = t % tiles_m; }
     else { tm = t / tiles_n; tn = t % tiles_n; }
     const int64_t m0 = tm * BM, n0 = tn * BNP;
-    const int64_t kbeg = split * kp.kc;
-    const int64_t kend = std::min<int64_t>(K, kbeg + kp.kc);
+    const int64_t kbeg = split * kc;
+    const int64_t kend = std::min<int64_t>(K, kbeg + kc);
     const int64_t nk = (kend - kbeg + BK - 1) / BK;
     const bool ragged = ((kend - kbeg) % BK) != 0;
 
@@ -821,11 +856,17 @@ void k_gemm_p(KParams kp) {
     }
     float* C = g.C;
     int64_t ldc = g.ldc;
-    if (kp.splits > 1) {
+    if (splits > 1) {
       C = g.partial + (int64_t)split * M * N;
       ldc = N;
     }
     store_tile<WI, WJ>(g, C, ldc, M, N, m0 + wm, n0 + wn, lane, acc);
+    if (sched) {
+      __syncthreads();                   // sPos (written before the unit's first barrier)
+      pos = sPos;
+    } else {
+      pos += G / nq;
+    }
   }
 }
 
@@ -919,6 +960,7 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
       }
       int64_t grid = std::min<int64_t>(tiles_p * kq.splits, kCus);
       if (grid >= kXcds) grid = grid / kXcds * kXcds;
+      if (g.sched) hipLaunchKernelGGL(k_zero_sched, dim3(1), dim3(64), 0, s, g.sched);
       timing::Scope ts(g.timing_class, s);
       if (F16 && g.a_scale != 1.f)
         hipLaunchKernelGGL((k_gemm_p<AT, F16, true>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
@@ -950,6 +992,53 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
 
 size_t gemm_partial_bytes(int64_t M, int64_t N, int max_splits) {
   return (size_t)M * N * 4 * (size_t)std::max(1, max_splits);
+}
+
+namespace {
+// The pipelined kernel applies: single-pass product, 16-byte aligned A rows,
+// B a padded panel on 16-byte boundaries.
+bool pipelined(const GemmArgs& g, AType a_type) {
+  const int a_align = a_type == AType::F32 ? 4 : 8;
+  const bool av = (g.lda % a_align == 0) && ((uintptr_t)g.A % 16 == 0);
+  const bool bc = !(g.b_padded && (g.ldb % 8 == 0) && ((uintptr_t)g.B_hi % 16 == 0) &&
+                    (g.B_lo == nullptr || (uintptr_t)g.B_lo % 16 == 0));
+  return av && !bc && !g.partial;
+}
+}  // namespace
+
+eogp_status gemm_nt2(const GemmArgs& g1, const GemmArgs& g2, AType a_type, int a_parts,
+                     int b_parts, bool f16, hipStream_t s) {
+  const bool empty1 = g1.M == 0 || g1.N == 0, empty2 = g2.M == 0 || g2.N == 0;
+  if (a_parts != 1 || b_parts != 1 || !g1.sched || empty1 || empty2 || !pipelined(g1, a_type) ||
+      !pipelined(g2, a_type) || g1.timing_class != g2.timing_class) {
+    const eogp_status st = gemm_nt(g1, a_type, a_parts, b_parts, f16, s);
+    if (st != EOGP_OK) return st;
+    return gemm_nt(g2, a_type, a_parts, b_parts, f16, s);
+  }
+  KParams kq;
+  kq.g = g1;
+  kq.splits = 1;
+  kq.kc = round_up(g1.K, BK);
+  kq.g2 = g2;
+  kq.kc2 = round_up(g2.K, BK);
+  kq.nprob = 2;
+  const int64_t tiles = ceil_div(g1.M, BM) * ceil_div(g1.N, 256) + ceil_div(g2.M, BM) * ceil_div(g2.N, 256);
+  int64_t grid = std::min<int64_t>(tiles, kCus);
+  if (grid >= kXcds) grid = grid / kXcds * kXcds;
+  const bool sc = f16 && (g1.a_scale != 1.f || g2.a_scale != 1.f);
+  hipLaunchKernelGGL(k_zero_sched, dim3(1), dim3(64), 0, s, g1.sched);
+  timing::Scope ts(g1.timing_class, s);
+  const dim3 gd((unsigned)grid), bd(PT);
+  if (a_type == AType::F32) {
+    if (f16 && sc) hipLaunchKernelGGL((k_gemm_p<0, true, true>), gd, bd, 0, s, kq);
+    else if (f16) hipLaunchKernelGGL((k_gemm_p<0, true, false>), gd, bd, 0, s, kq);
+    else hipLaunchKernelGGL((k_gemm_p<0, false, false>), gd, bd, 0, s, kq);
+  } else {
+    if (f16) hipLaunchKernelGGL((k_gemm_p<1, true, false>), gd, bd, 0, s, kq);
+    else hipLaunchKernelGGL((k_gemm_p<1, false, false>), gd, bd, 0, s, kq);
+  }
+  EOGP_LAUNCH_CHECK("gemm launch (two products)");
+  return EOGP_OK;
 }
 
 eogp_status gemm_nt(const GemmArgs& g, AType a_type, int a_parts, int b_parts, bool f16,

@@ -271,6 +271,7 @@ struct Work {
   uint16_t* At16; // cols_pad x ldt entries
   int64_t ldt = 0;
   float* Zt;      // [N][m] block sums in entry order (retained products only)
+  int32_t* sched; // [kXcds] work counters of the rotation launch
 };
 
 // Token capacity of the fp16 layout: runs padded to multiples of 8, the
@@ -288,6 +289,7 @@ size_t work_bytes(const eogp_plan* p, int64_t N, int64_t T) {
   const size_t f16b = align256((size_t)ldt * p->rows_pad * 2) + align256((size_t)ldt * p->cols_pad * 2);
   b += std::max(f32b, f16b);
   b += align256((size_t)N * p->m * 4);
+  b += align256(kXcds * 4);
   return b;
 }
 
@@ -345,8 +347,6 @@ eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
   // zeros (fp16, zero panel rows): they only feed block outputs never read.
   gs.N = p->n_rows;
   gs.K = p->d_out;
-  eogp_status st = gemm_nt(gs, at, a_parts, b_parts, f16, s);
-  if (st != EOGP_OK) return st;
   GemmArgs ga = gs;
   ga.A = acts;
   ga.lda = ld_acts;
@@ -362,7 +362,12 @@ eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
   }
   ga.N = p->n_cols;
   ga.K = p->d_in;
-  return gemm_nt(ga, at, a_parts, b_parts, f16, s);
+  // One launch for both rotations, the longer contraction first.
+  GemmArgs& first = gs.K >= ga.K ? gs : ga;
+  GemmArgs& second = gs.K >= ga.K ? ga : gs;
+  first.sched = w.sched;
+  second.sched = nullptr;
+  return gemm_nt2(first, second, at, a_parts, b_parts, f16, s);
 }
 
 Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
@@ -380,6 +385,7 @@ Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
   w.St16 = reinterpret_cast<uint16_t*>(base);
   w.At16 = reinterpret_cast<uint16_t*>(base + align256((size_t)w.ldt * p->rows_pad * 2));
   w.Zt = cv.take<float>((size_t)N * p->m);
+  w.sched = cv.take<int32_t>(kXcds);
   return w;
 }
 
