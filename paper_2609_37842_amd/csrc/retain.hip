@@ -148,13 +148,20 @@ __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__
                                                     const int32_t* __restrict__ tiles, int n_tiles,
                                                     const uint16_t* __restrict__ ent_loc,
                                                     float out_scale, float* __restrict__ Zt,
-                                                    int64_t m, int64_t ex0) {
+                                                    int64_t m, int64_t ex0, int64_t nex) {
   typedef unsigned int v4u __attribute__((ext_vector_type(4)));
   __shared__ float blk[kRetWaves][32][33];
   const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int tile = blockIdx.x * kRetWaves + wid;
-  if (tile >= n_tiles) return;                 // whole wave leaves; no block barrier below
-  const int64_t i = ex0 + blockIdx.y;
+  // Workgroup b runs on XCD b % kXcds: the tile groups of one example all go
+  // to one XCD (examples dealt round-robin over the XCDs), so the example's S~
+  // and A~ blocks are fetched into one L2.
+  const int gx = (n_tiles + kRetWaves - 1) / kRetWaves;
+  const int xb = blockIdx.x % kXcds, rb = blockIdx.x / kXcds;
+  const int64_t ex_local = xb + (int64_t)kXcds * (rb / gx);
+  if (ex_local >= nex) return;                 // whole workgroup leaves; no block barrier below
+  const int tile = (rb % gx) * kRetWaves + wid;
+  if (tile >= n_tiles) return;                 // whole wave leaves
+  const int64_t i = ex0 + ex_local;
   const int jb = tiles[4 * tile + 0], kb = tiles[4 * tile + 1];
   const int e0 = tiles[4 * tile + 2], e1 = tiles[4 * tile + 3];
   const int64_t t0 = ex_off[i] + 8 * (lane >> 5);   // this lane's first token
@@ -409,14 +416,20 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
     const eogp_status st_lds = ensure_dynamic_lds((const void*)k_zperm_lds, (int)(sizeof(float) * kZpermLdsMax));
     if (st_lds != EOGP_OK) return st_lds;
   }
-  for (int64_t ex0 = 0; p->n_tiles > 0 && ex0 < N; ex0 += 65535) {
-    const int64_t nex = std::min<int64_t>(65535, N - ex0);
+  // examples per launch: the 2-D grid's y limit, and the 1-D grid of the fp16
+  // kernel (kXcds x ceil(nex / kXcds) x tile groups) below 2^31
+  const int64_t gx64 = ceil_div(p->n_tiles, (int64_t)kRetWaves);
+  const int64_t ex_chunk = std::max<int64_t>(
+      kXcds, std::min<int64_t>(65535 / kXcds * kXcds,
+                               (((int64_t)1 << 31) - 1) / (kXcds * std::max<int64_t>(1, gx64)) * kXcds));
+  for (int64_t ex0 = 0; p->n_tiles > 0 && ex0 < N; ex0 += ex_chunk) {
+    const int64_t nex = std::min<int64_t>(ex_chunk, N - ex0);
     timing::Scope ts(EOGP_KT_RETAINED, s);
-    const unsigned gx = (unsigned)ceil_div(p->n_tiles, (int64_t)kRetWaves);
+    const unsigned gx = (unsigned)gx64;
     if (f16) {
-      hipLaunchKernelGGL(k_retained16, dim3(gx, (unsigned)nex), dim3(256), 0, s,
-                         w.St16, w.At16, w.ldt, w.cnt, w.len, p->tiles, (int)p->n_tiles,
-                         p->ent_loc, out_scale, w.Zt, p->m, ex0);
+      hipLaunchKernelGGL(k_retained16, dim3((unsigned)(kXcds * ceil_div(nex, kXcds) * gx)),
+                         dim3(256), 0, s, w.St16, w.At16, w.ldt, w.cnt, w.len, p->tiles,
+                         (int)p->n_tiles, p->ent_loc, out_scale, w.Zt, p->m, ex0, nex);
     } else {
       hipLaunchKernelGGL(k_retained, dim3(gx, (unsigned)nex), dim3(256), 0, s,
                          w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,
