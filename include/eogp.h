@@ -219,7 +219,7 @@ eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k,
  *   codes        [N, code_row_stride] bytes; module u occupies bytes
  *                sum_{v<u} k_v/8 .. + k_u/8 of each row (eogp_sign_pack layout).
  *   scales       [N, U] fp16 bit patterns.
- *   k_per_module HOST [U]; each k_u must be a positive multiple of 64.
+ *   k_per_module HOST [U]; each k_u a positive multiple of 64, at most 2^22.
  *   Y            [Q, ldy] fp32 query coordinates (modules concatenated),
  *                ldy >= sum_u k_u.
  *   out_idx      [Q, topk] int64 example indices; out_score [Q, topk] fp32

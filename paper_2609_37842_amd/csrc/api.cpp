@@ -377,6 +377,8 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride, const
   for (int u = 0; u < U; ++u) {
     if (k_per_module[u] < 64 || k_per_module[u] % 64 != 0)
       return fail(EOGP_ERR_INVALID, "score_topk: every k_u must be a positive multiple of 64");
+    if (k_per_module[u] > ((int64_t)1 << 22))
+      return fail(EOGP_ERR_INVALID, "score_topk: k_u must be at most 2^22");
     ksum += k_per_module[u];
   }
   if (ksum >= kMaxFlat) return fail(EOGP_ERR_INVALID, "score_topk: sum of k_u too large");

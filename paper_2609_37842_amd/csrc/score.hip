@@ -4,29 +4,41 @@
 // Arithmetic. Each query module vector y is taken in fixed point,
 // y_int = rint(y 2^f) with f = 14 - e for max|y| = mu 2^e (|y_int| <= 2^14), and
 // split into two int8 planes y_int = 256 h + l (h in [-64, 64], l in
-// [-128, 127]). With b in {0, 1} the MFMA computes n1 = sum_{b=1} y_int exactly
-// in int32, and <y_int, 2b - 1> = 2 n1 - sum(y_int). Each module term
+// [-128, 127]). With b in {0, 1} the MFMAs compute n1 = sum_{b=1} y_int exactly
+// in integers, and <y_int, 2b - 1> = 2 n1 - sum(y_int). Each module term
 // s * (2 n1 - sum) * 2^-f is exact in fp64 and the terms are added in module
 // order, so the score is reproducible bit for bit.
 //
-// Data flow. A pass streams every stored code once for a group of 16 queries
-// (the 16 columns of v_mfma_i32_16x16x64_i8). A 512-thread workgroup (8
-// waves) owns 1024 consecutive examples at a time, each wave 8 tiles of 16
-// rows. The pass walks the modules in 512-bit steps; per step the workgroup
-// stages the query planes (16 KB) in LDS once for its 1024 rows,
-// double-buffered, and each wave multiplies its 128 rows against them (each
-// plane fragment read from LDS feeds 8 MFMAs) with its code words for that
-// step, which it requested one step earlier (16-byte loads). Bits are
-// expanded without reordering the stored layout: the 32-bit code word w
-// yields the int8 operand dwords (w >> d) & 0x01010101 (bits d, d+8, d+16,
-// d+24), and the query planes are laid out in that same permuted order when
-// they are prepared.
+// Data flow. A pass streams every stored code once for a group of 16
+// queries. v_mfma_i32_32x32x32_i8 takes the 32 plane rows (16 queries x
+// {h, l}) as its A operand and 32 stored rows as B, so one instruction
+// serves both planes and each lane ends with 8 queries of one stored row
+// (the h and l sums of a query land in the same lane). A 512-thread
+// workgroup (8 waves, 2 per SIMD) owns 512 consecutive rows at a time, each
+// wave two tiles of 32 rows. The modules are walked in steps of 512 bits;
+// per step each lane holds 32 bytes of its row (two 16-byte loads, requested
+// D steps ahead in a register ring), the workgroup stages the step's plane
+// fragments (16 KB) in LDS once, double-buffered, and every fragment read
+// from LDS feeds both tiles.
+//
+// Bit expansion. The 16 bytes c of a lane feed 8 MFMAs, one per bit
+// position t of a byte. The operand of MFMA t is (c >> s) & (0x01010101 <<
+// w) with t = s + w, w = t mod NCLS: its bytes are 0 or 2^w, so the MFMA adds
+// 2^w times the wanted sum into accumulator class w, and n1 = sum_w acc_w /
+// 2^w (exact shifts: every term of acc_w is a multiple of 2^w). One shift
+// serves NCLS masks, so the expansion costs (1 + NCLS) / NCLS ... 1 VALU op
+// per 4 bits instead of 2. The query planes are prepared in exactly that
+// order: byte j of lane (M, g) of MFMA (u, t) in step s of a module holds
+// coordinate 8 (64 s + 32 g + 16 u + j) + t.
+//
 // After the last module the workgroup's scores are filtered against a
 // per-query threshold into an LDS candidate list (score desc, index asc). A
 // list that fills up is pruned to the top-k (bitonic sort) and the entries
 // that did not fit are inserted again, so no qualifying row is lost. Finally
 // each workgroup writes its top-k per query and a merge kernel reduces them.
 #include <algorithm>
+#include <type_traits>
+#include <utility>
 #include <vector>
 
 #include "common.h"
@@ -35,18 +47,32 @@
 namespace eogp {
 namespace {
 
-constexpr int QB = 16;          // queries per pass
-constexpr int NW = 8;           // waves per workgroup
+constexpr int QB = 16;                 // queries per pass
+constexpr int NW = 8;                  // waves per workgroup
 constexpr int NTHR = NW * 64;
-constexpr int KSTEP = 8;        // MFMA k-steps (64 bits each) per 512-bit step
-constexpr int MCAP = 512;       // candidate slots per query in the merge
+constexpr int MCAP = 512;              // candidate slots per query in the merge
 constexpr int MAX_TOPK = 256;
+
+// A step covers SB bytes (8 SB bits) of a module in every row: lane (row,
+// g) holds SB / 2 of them as NU = SB / 32 16-byte words, which feed FR = 8 NU
+// MFMAs per tile, whose plane fragments take PU = 64 FR 16-byte slots (FR KB).
+template <int SB>
+struct StepShape {
+  static constexpr int NU = SB / 32;
+  static constexpr int FR = 8 * NU;
+  static constexpr int PU = 64 * FR;
+  static constexpr int PV = PU / NTHR;   // plane words staged per thread
+};
+
+typedef __attribute__((__vector_size__(16 * sizeof(int)))) int i32x16;
+template <typename T>
+using cptr = const __attribute__((address_space(4))) T*;   // read-only, scalar loads
 
 struct ModInfo {
   int32_t k;       // bits of the module
   int32_t coff;    // first coordinate of the module in a query row
   int32_t boff;    // first byte of the module in a code row
-  int32_t ksbase;  // first k-step of the module in the plane buffer
+  int32_t sbase;   // first step of the module
 };
 
 __device__ __forceinline__ uint64_t order_key(double x) {
@@ -62,15 +88,25 @@ __device__ __forceinline__ bool before(uint64_t ka, uint32_t ia, uint64_t kb, ui
 }
 
 // ---- query preparation --------------------------------------------------------
-// grid (Q, U): per (query, module) the exponent f and sum of y_int.
+// grid (16 * groups, U): per (query, module) the exponent f and the sum of
+// y_int, stored [group][U][16]; queries past Q get f = 0 and sum 0.
 __global__ __launch_bounds__(256) void k_query_stats(const float* __restrict__ Y, int64_t ldy,
-                                                     int U, const ModInfo* __restrict__ mods,
+                                                     int64_t Q, int U,
+                                                     const ModInfo* __restrict__ mods,
                                                      int32_t* __restrict__ fq,
                                                      int32_t* __restrict__ ysum) {
   __shared__ float smax[4];
   __shared__ int ssum[4];
   const int64_t q = blockIdx.x;
   const int u = blockIdx.y;
+  const int64_t o = ((q / QB) * U + u) * QB + (q % QB);
+  if (q >= Q) {
+    if (threadIdx.x == 0) {
+      fq[o] = 0;
+      ysum[o] = 0;
+    }
+    return;
+  }
   const ModInfo md = mods[u];
   const float* y = Y + q * ldy + md.coff;
   float mx = 0.f;
@@ -92,40 +128,54 @@ __global__ __launch_bounds__(256) void k_query_stats(const float* __restrict__ Y
   if ((threadIdx.x & 63) == 0) ssum[threadIdx.x >> 6] = s;
   __syncthreads();
   if (threadIdx.x == 0) {
-    fq[q * U + u] = f;
-    ysum[q * U + u] = ssum[0] + ssum[1] + ssum[2] + ssum[3];
+    fq[o] = f;
+    ysum[o] = ssum[0] + ssum[1] + ssum[2] + ssum[3];
   }
 }
 
-// One thread per plane byte: (group, k-step, lane, slot) -> coordinate c of the
-// lane's row/column mapping; writes h and l of y_int (0 outside the module).
+// One thread per plane byte, laid out [group][step][MFMA f][lane][j] with
+// f = 8 u + t: lane (M, g) = (lane % 32, lane / 32) is plane M / 16 (0: h,
+// 1: l) of query M % 16, byte j holds coordinate
+// 8 (sb s + sb / 2 g + 16 u + j) + t of the step's module (0 past the module),
+// sb = bytes per row and step.
 __global__ void k_query_planes(const float* __restrict__ Y, int64_t ldy, int64_t Q, int U,
                                const ModInfo* __restrict__ mods, const int32_t* __restrict__ fq,
-                               int64_t KS, int64_t n_groups, int8_t* __restrict__ ph,
-                               int8_t* __restrict__ pl) {
+                               int64_t n_steps, int64_t n_groups, int sb,
+                               int8_t* __restrict__ planes) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t total = n_groups * KS * 64 * 16;
+  const int64_t step_bytes = (int64_t)sb * 256;          // sb / 4 KB
+  const int64_t total = n_groups * n_steps * step_bytes;
   if (idx >= total) return;
-  const int slot = (int)(idx & 15);
+  const int j = (int)(idx & 15);
   const int lane = (int)((idx >> 4) & 63);
-  const int64_t K = (idx >> 10) % KS;
-  const int64_t grp = (idx >> 10) / KS;
-  int u = 0;
-  while (u + 1 < U && mods[u + 1].ksbase <= K) ++u;
-  const ModInfo md = mods[u];
-  const int64_t Ku = K - md.ksbase;
-  const int64_t ms = Ku / KSTEP;
-  const int s = (int)(Ku % KSTEP);
-  const int g = lane >> 4, n = lane & 15;
-  const int e = slot >> 2, b = slot & 3;
-  const int64_t c = 32 * (16 * ms + 4 * g + (s >> 1)) + 4 * (s & 1) + e + 8 * b;
-  const int64_t q = grp * QB + n;
+  const int fr = (int)((idx >> 10) % (sb / 4));
+  const int64_t gs = idx / step_bytes;
+  const int64_t step = gs % n_steps;
+  const int64_t grp = gs / n_steps;
+  int lo = 0, hi = U - 1;                    // last module whose first step <= step
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (mods[mid].sbase <= step) lo = mid; else hi = mid - 1;
+  }
+  const ModInfo md = mods[lo];
+  const int64_t sl = step - md.sbase;
+  const int uc = fr >> 3, t = fr & 7;
+  const int M = lane & 31, g = lane >> 5;
+  const int qn = M & 15;
+  const int64_t c = 8 * (sb * sl + (sb / 2) * g + 16 * uc + j) + t;
+  const int64_t q = grp * QB + qn;
   int yi = 0;
-  if (q < Q && c < md.k) yi = (int)rintf(ldexpf(Y[q * ldy + md.coff + c], fq[q * U + u]));
+  if (q < Q && c < md.k)
+    yi = (int)rintf(ldexpf(Y[q * ldy + md.coff + c], fq[(grp * U + lo) * QB + qn]));
   const int h = (yi + 128) >> 8;   // floor division (arithmetic shift)
   const int l = yi - 256 * h;
-  ph[idx] = (int8_t)h;
-  pl[idx] = (int8_t)l;
+  planes[idx] = (int8_t)((M >> 4) ? l : h);
+}
+
+// Copies a store of n < 16 bytes into a zero-padded 16-byte slot.
+__global__ void k_pad16(const uint8_t* __restrict__ src, int n, uint8_t* __restrict__ dst) {
+  const int i = threadIdx.x;
+  dst[i] = i < n ? src[i] : (uint8_t)0;
 }
 
 // ---- candidate lists in LDS ---------------------------------------------------
@@ -175,14 +225,6 @@ __device__ void prune(Cand<CAP>& cd, int n, int topk) {
   __syncthreads();
 }
 
-// One step of the pass (one or two 512-bit halves of one module): module,
-// first code byte of the step within a row, first k-step of its query
-// planes, valid code bytes, whether it is the module's last step, and its
-// number of halves.
-struct Step {
-  int32_t u, boff, kbase, bytes, last, halves, pad0, pad1;
-};
-
 struct ScoreArgs {
   const uint8_t* codes;
   int64_t cstride;
@@ -190,14 +232,11 @@ struct ScoreArgs {
   int64_t N;
   int U;
   const ModInfo* mods;
-  const int8_t* ph;
-  const int8_t* pl;
-  const Step* steps;
+  const uint4* planes;
   int n_steps;
-  int64_t KS;
   int64_t grp;
-  const int32_t* fq;
-  const int32_t* ysum;
+  const int32_t* fq;     // [groups][U][16]
+  const int32_t* ysum;   // [groups][U][16]
   int64_t Q;
   int topk;
   float* full;
@@ -205,23 +244,36 @@ struct ScoreArgs {
   uint32_t* cidx;
 };
 
-// RT: 16-row tiles per wave (rows per block: NW * RT * 16). MULTI: several
-// modules, whose fp64 terms are summed in module order as each ends; else
-// one module, whose term is formed after its last step. HS: 512-bit halves per
-// step; with HS = 2 a lane reads both 64-byte halves of each 128-byte line of
-// its rows in the same step.
-template <int CAP, int RT, bool MULTI, int HS>
+// Calls f(integral_constant<I>) for I = 0 .. sizeof...(I) - 1 in order.
+template <typename F, int... I>
+__device__ __forceinline__ void for_each_index(std::integer_sequence<int, I...>, F&& f) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+
+// Walks the steps of the modules in order (uniform, scalar registers).
+struct Cursor {
+  int u, sl, nst, kbytes, boff;
+};
+
+// NCLS: accumulator classes of the bit expansion (1, 2 or 4). D: steps
+// requested ahead. MULTI: several modules, whose fp64 terms are summed in
+// module order as each ends; else one module, whose term is formed after its
+// last step. CAP: candidate slots per query. SB: bytes per row and step. RT:
+// 32-row tiles per wave (each plane fragment read from LDS feeds RT MFMAs).
+template <int NCLS, int D, bool MULTI, int CAP, int SB, int RT>
 __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
-  constexpr int ROWS = NW * RT * 16;
-  constexpr int PU = 2 * HS * KSTEP * 64;            // plane uint4 per step
-  constexpr int PV = PU / NTHR;                      // staged per thread
-  __shared__ __attribute__((aligned(16))) uint4 sP[2][2][HS * KSTEP][64];
+  constexpr int ROWS = NW * RT * 32;   // rows per block
+  static_assert(NCLS == 1 || NCLS == 2 || NCLS == 4, "bit-weight classes");
+  static_assert(D >= 2 && D <= 8, "ring depth");
+  using SS = StepShape<SB>;
+  constexpr int NU = SS::NU, FR = SS::FR, PU = SS::PU, PV = SS::PV;
+  __shared__ __attribute__((aligned(16))) uint4 sP[2][PU];
   __shared__ Cand<CAP> cd;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int n = lane & 15;           // query column of this lane
-  const int g = lane >> 4;           // k-group of this lane
-  const int64_t q = a.grp * QB + n;
-  const bool q_ok = q < a.Q;
+  const int r32 = lane & 31, hg = lane >> 5;
+  const cptr<int32_t> cmods = (cptr<int32_t>)(a.mods);   // ModInfo fields, 4 per module
+  const cptr<int32_t> cfq = (cptr<int32_t>)(a.fq);
+  const cptr<int32_t> cys = (cptr<int32_t>)(a.ysum);
   if (tid < QB) {
     cd.cnt[tid] = 0;
     cd.thr[tid] = 0ull;
@@ -229,172 +281,264 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
   if (tid == 0) cd.overflow = 0;
   __syncthreads();
   const int64_t n_blocks = (a.N + ROWS - 1) / ROWS;
-  const uint4* phv = reinterpret_cast<const uint4*>(a.ph);
-  const uint4* plv = reinterpret_cast<const uint4*>(a.pl);
+  const int n = a.n_steps;
+  const uint4* pl_grp = a.planes + (int64_t)a.grp * n * PU;
   const uint32_t M1 = 0x01010101u;
-  // plane staging: uint4 number f = tid + NTHR v of the step is (plane,
-  // k-step, lane) = (f / (HS KSTEP 64), (f / 64) % (HS KSTEP), f % 64), so
-  // consecutive lanes move consecutive 16 bytes; k-steps past the step's
-  // valid halves are staged as zero
-  auto plane_src = [&](const Step& st, int f) -> uint4 {
-    const int plane = f / (HS * KSTEP * 64), ks = (f >> 6) % (HS * KSTEP), ln = f & 63;
-    if (ks >= st.halves * KSTEP) return make_uint4(0u, 0u, 0u, 0u);
-    const int64_t o = (a.grp * a.KS + st.kbase + ks) * 64 + ln;
-    return (plane ? plv : phv)[o];
+
+  auto start = [&](Cursor& c) __attribute__((always_inline)) {
+    const int k = cmods[0];
+    c.u = 0;
+    c.sl = 0;
+    c.nst = (k + 8 * SB - 1) / (8 * SB);
+    c.kbytes = k >> 3;
+    c.boff = cmods[2];
   };
-  auto plane_dst = [&](int buf, int f, const uint4& v) {
-    sP[buf][f / (HS * KSTEP * 64)][(f >> 6) % (HS * KSTEP)][f & 63] = v;
+  auto advance = [&](Cursor& c) __attribute__((always_inline)) {
+    if (++c.sl == c.nst) {
+      c.sl = 0;
+      if (++c.u < a.U) {
+        const int k = cmods[4 * c.u];
+        c.nst = (k + 8 * SB - 1) / (8 * SB);
+        c.kbytes = k >> 3;
+        c.boff = cmods[4 * c.u + 2];
+      }
+    }
   };
 
   for (int64_t blk = blockIdx.x; blk < n_blocks; blk += gridDim.x) {
-    const int64_t row0 = blk * ROWS + (int64_t)wid * (RT * 16);
-    // this lane's code row of tile rt is row0 + 16 rt + n; rows past N read
-    // row N - 1 and are never reported
-    auto load_codes = [&](const Step& st, uint4 (*cw)[HS]) {
+    int64_t row[RT], rowc[RT];
+    const uint8_t* rowp[RT];
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-        const int64_t row = std::min<int64_t>(row0 + rt * 16 + n, a.N - 1);
-        const uint8_t* src = a.codes + row * a.cstride + st.boff + 16 * g;
-#pragma unroll
-        for (int h = 0; h < HS; ++h) {
-          const int have = st.bytes - 64 * h - 16 * g;   // valid bytes of this lane's 16
-          uint4 v = make_uint4(0u, 0u, 0u, 0u);
-          if (have >= 16) {
-            v = *reinterpret_cast<const uint4*>(src + 64 * h);
-          } else if (have >= 8) {
-            const uint2 hv = *reinterpret_cast<const uint2*>(src + 64 * h);
-            v.x = hv.x;
-            v.y = hv.y;
-          }
-          cw[rt][h] = v;
-        }
-      }
-    };
+    for (int rt = 0; rt < RT; ++rt) {
+      row[rt] = blk * ROWS + (int64_t)(wid * RT + rt) * 32 + r32;   // this lane's stored row
+      rowc[rt] = std::min<int64_t>(row[rt], a.N - 1);                // rows past N: never reported
+      rowp[rt] = a.codes + rowc[rt] * a.cstride + (SB / 2) * hg;
+    }
 
-    double sc[RT][4];
+    i32x16 acc[RT][NCLS];
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sc[rt][r] = 0.0;
-    i32x4 acc_h[RT], acc_l[RT];
+      for (int w = 0; w < NCLS; ++w)
 #pragma unroll
-    for (int rt = 0; rt < RT; ++rt) {
-      acc_h[rt] = i32x4{0, 0, 0, 0};
-      acc_l[rt] = i32x4{0, 0, 0, 0};
-    }
+        for (int r = 0; r < 16; ++r) acc[rt][w][r] = 0;
+    double sc[RT][8];   // [tile][i]: query 8 (i / 4) + 4 (lane / 32) + i % 4 of the group
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int i = 0; i < 8; ++i) sc[rt][i] = 0.0;
 
-    // module term: s * (2 n1 - sum y_int) * 2^-f, added in module order
-    auto fold = [&](int u) {
-      const int f = q_ok ? a.fq[q * a.U + u] : 0;
-      const int ys = q_ok ? a.ysum[q * a.U + u] : 0;
+    // ring slot: [rt][0, NU) the lane's code words of tile rt, [RT][0, PV)
+    // the thread's share of the step's plane fragments
+    constexpr int RW = NU > PV ? NU : PV;
+    uint4 ring[D][RT + 1][RW];
+    uint32_t scl[D][RT];   // several modules: the rows' scales for the slot's module
+    uint32_t s16[RT];      // one module: the rows' scales, requested before the codes
+    if (!MULTI) {
 #pragma unroll
-      for (int rt = 0; rt < RT; ++rt) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t row = row0 + rt * 16 + 4 * g + r;
-          const uint16_t s16 = row < a.N ? a.scales[row * a.U + u] : (uint16_t)0;
-          const int n1 = 256 * acc_h[rt][r] + acc_l[rt][r];
-          const int nn = 2 * n1 - ys;
-          sc[rt][r] += ldexp((double)f16_bits_to_f32(s16) * (double)nn, -f);
-        }
-        acc_h[rt] = i32x4{0, 0, 0, 0};
-        acc_l[rt] = i32x4{0, 0, 0, 0};
-      }
-    };
-
-    // prologue: step 0 staged, its code words in registers
-    uint4 cw[RT][HS], cwn[RT][HS];
-    {
-      const Step st = a.steps[0];
-#pragma unroll
-      for (int v = 0; v < PV; ++v) plane_dst(0, tid + NTHR * v, plane_src(st, tid + NTHR * v));
-      load_codes(st, cw);
+      for (int rt = 0; rt < RT; ++rt) s16[rt] = a.scales[rowc[rt]];
     }
-    __syncthreads();
-    for (int sidx = 0; sidx < a.n_steps; ++sidx) {
-      const int buf = sidx & 1;
-      const Step st = a.steps[sidx];
-      const bool more = sidx + 1 < a.n_steps;
-      uint4 pv[PV];
-      if (more) {
-        const Step nx = a.steps[sidx + 1];
+    Cursor cc, cl;
+    start(cc);
+    start(cl);
+
+    // plane fragments and code words of step `target` (the load cursor's)
+    // into ring slot SL, D steps ahead. Every step issues the same loads in
+    // the order they are consumed, so the in-order load counter never makes
+    // a step wait for a later step's data, and the number of requests in
+    // flight never depends on the step or the lane. In a partial step (the
+    // last of a module whose k is not a multiple of 8 SB, or a step past the
+    // end) a lane whose 16 bytes are not all inside the module reads 16
+    // readable bytes instead: the 8 bytes before its 8 valid ones (the valid
+    // half is then the upper one), or the store's first 16 bytes; `fixup`
+    // keeps the valid bytes when the step is used.
+    int64_t voff[D];
+    int vbytes[D];
+    auto load_step = [&](auto slot_c, int target) __attribute__((always_inline)) {
+      constexpr int SL = decltype(slot_c)::value;
+      const bool live = target < n;
+      const uint4* psrc = pl_grp + (int64_t)(live ? target : n - 1) * PU + tid;
 #pragma unroll
-        for (int v = 0; v < PV; ++v) pv[v] = plane_src(nx, tid + NTHR * v);
-        load_codes(nx, cwn);
-      }
-#pragma unroll
-      for (int h = 0; h < HS; ++h) {
-        if (h < st.halves) {                          // uniform
-          // plane fragments of k-step s + 1 are read while k-step s multiplies
-          i32x4 fbh = __builtin_bit_cast(i32x4, sP[buf][0][h * KSTEP][lane]);
-          i32x4 fbl = __builtin_bit_cast(i32x4, sP[buf][1][h * KSTEP][lane]);
-#pragma unroll
-          for (int s = 0; s < KSTEP; ++s) {
-            const i32x4 bh = fbh, bl = fbl;
-            if (s + 1 < KSTEP) {
-              fbh = __builtin_bit_cast(i32x4, sP[buf][0][h * KSTEP + s + 1][lane]);
-              fbl = __builtin_bit_cast(i32x4, sP[buf][1][h * KSTEP + s + 1][lane]);
-            }
-            const int d0 = 4 * (s & 1);
-#pragma unroll
-            for (int rt = 0; rt < RT; ++rt) {
-              const uint4& c = cw[rt][h];
-              const uint32_t w = (s >> 1) == 0 ? c.x : (s >> 1) == 1 ? c.y : (s >> 1) == 2 ? c.z : c.w;
-              i32x4 av;
-              av[0] = (int)((w >> (d0 + 0)) & M1);
-              av[1] = (int)((w >> (d0 + 1)) & M1);
-              av[2] = (int)((w >> (d0 + 2)) & M1);
-              av[3] = (int)((w >> (d0 + 3)) & M1);
-              acc_h[rt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bh, acc_h[rt], 0, 0, 0);
-              acc_l[rt] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av, bl, acc_l[rt], 0, 0, 0);
-              // expand the next operand while these two multiply
-              __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);   // VALU
-              __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
-            }
-          }
-        }
-      }
-      if (MULTI && st.last) fold(st.u);
-      if (more) {
-#pragma unroll
-        for (int v = 0; v < PV; ++v) plane_dst(buf ^ 1, tid + NTHR * v, pv[v]);
+      for (int v = 0; v < PV; ++v) ring[SL][RT][v] = psrc[v * NTHR];
+      const int64_t off = (int64_t)cl.boff + SB * cl.sl;
+      const int valid = live ? min(SB, cl.kbytes - SB * cl.sl) : 0;   // multiple of 8
+      voff[SL] = off;
+      vbytes[SL] = valid;
+      if (valid == SB) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-          for (int h = 0; h < HS; ++h) cw[rt][h] = cwn[rt][h];
+          for (int uc = 0; uc < NU; ++uc)
+            ring[SL][rt][uc] = *reinterpret_cast<const uint4*>(rowp[rt] + off + 16 * uc);
+      } else {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int uc = 0; uc < NU; ++uc) {
+            const int have = valid - (SB / 2) * hg - 16 * uc;
+            const int64_t pos = off + (SB / 2) * hg + 16 * uc;   // within the row
+            const bool at0 = rowc[rt] == 0 && pos == 0;          // the store's first byte
+            const uint8_t* src = rowp[rt] + off + 16 * uc;
+            const uint8_t* p = have >= 16 ? src : (have >= 8 && !at0) ? src - 8 : a.codes;
+            ring[SL][rt][uc] = *reinterpret_cast<const uint4*>(p);
+          }
       }
+      if (MULTI) {
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) scl[SL][rt] = a.scales[rowc[rt] * a.U + min(cl.u, a.U - 1)];
+      }
+    };
+    // keeps the valid bytes of a partial step (branch-free selects)
+    auto fixup = [&](auto slot_c) __attribute__((always_inline)) {
+      constexpr int SL = decltype(slot_c)::value;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int uc = 0; uc < NU; ++uc) {
+          const int have = vbytes[SL] - (SB / 2) * hg - 16 * uc;
+          const bool at0 = rowc[rt] == 0 && voff[SL] + (SB / 2) * hg + 16 * uc == 0;
+          const uint4 v = ring[SL][rt][uc];
+          const uint32_t full = have >= 16 ? ~0u : 0u;
+          const uint32_t half = (have >= 8 && have < 16) ? ~0u : 0u;
+          const uint32_t lo0 = at0 ? v.x : v.z, lo1 = at0 ? v.y : v.w;
+          ring[SL][rt][uc] = make_uint4((v.x & full) | (lo0 & half), (v.y & full) | (lo1 & half),
+                                        v.z & full, v.w & full);
+        }
+    };
+
+    // module term s * (2 n1 - sum y_int) * 2^-f, added in module order
+    auto fold = [&](int u, const uint32_t (&s16v)[RT]) __attribute__((always_inline)) {
+      const int64_t mo = (a.grp * a.U + u) * QB;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        int H[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          int v = acc[rt][0][r];
+#pragma unroll
+          for (int w = 1; w < NCLS; ++w) v += acc[rt][w][r] >> w;
+          H[r] = v;
+        }
+        const double sv = (double)f16_bits_to_f32((uint16_t)s16v[rt]);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int i0 = 8 * (i >> 2) + (i & 3);
+          const int f = hg ? cfq[mo + i0 + 4] : cfq[mo + i0];
+          const int ys = hg ? cys[mo + i0 + 4] : cys[mo + i0];
+          const int64_t n1 = 256 * (int64_t)H[i] + (int64_t)H[i + 8];
+          const int64_t nn = 2 * n1 - ys;
+          const double term = ldexp(sv * (double)nn, -f);
+          sc[rt][i] = MULTI ? sc[rt][i] + term : term;
+        }
+#pragma unroll
+        for (int w = 0; w < NCLS; ++w)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) acc[rt][w][r] = 0;
+      }
+    };
+
+    auto step = [&](auto slot_c, int s) __attribute__((always_inline)) {
+      constexpr int SL = decltype(slot_c)::value;
+      constexpr int NX = (SL + 1) % D;   // slot of step s + 1
+      const int buf = s & 1;
+      if (vbytes[SL] < SB) fixup(slot_c);
+      // fragment f = 8 uc + t of the step, read from LDS two rounds ahead of
+      // its use so the LDS latency stays hidden; each feeds the RT tiles
+      const uint4* frag = &sP[buf][lane];
+      i32x4 fr[3];
+      fr[0] = __builtin_bit_cast(i32x4, frag[0]);
+      fr[1] = __builtin_bit_cast(i32x4, frag[64]);
+#pragma unroll
+      for (int f = 0; f < FR; ++f) {
+        if (f + 2 < FR) fr[(f + 2) % 3] = __builtin_bit_cast(i32x4, frag[(f + 2) * 64]);
+        const int uc = f >> 3, t = f & 7;
+        const int w = t % NCLS, sh = t - w;
+        const uint32_t mk = M1 << w;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          const uint4 c = ring[SL][rt][uc];
+          i32x4 av;
+          av[0] = (int)((c.x >> sh) & mk);
+          av[1] = (int)((c.y >> sh) & mk);
+          av[2] = (int)((c.z >> sh) & mk);
+          av[3] = (int)((c.w >> sh) & mk);
+          acc[rt][w] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fr[f % 3], av, acc[rt][w], 0, 0, 0);
+        }
+        // per round: the read two rounds ahead, then each tile's expansion and MFMA
+        if (f + 2 < FR) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt) {
+          __builtin_amdgcn_sched_group_barrier(0x002, NCLS == 1 ? 8 : NCLS == 2 ? 6 : 5, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // MFMA
+        }
+      }
+      if (MULTI) {
+        if (cc.sl == cc.nst - 1) fold(cc.u, scl[SL]);
+        advance(cc);
+      }
+      load_step(slot_c, s + D);
+      advance(cl);
+#pragma unroll
+      for (int v = 0; v < PV; ++v) sP[buf ^ 1][tid + v * NTHR] = ring[NX][RT][v];
       __syncthreads();
+    };
+
+    // prologue: the first D steps requested, step 0's planes staged
+    for_each_index(std::make_integer_sequence<int, D>{}, [&](auto i_c) __attribute__((always_inline)) {
+      load_step(i_c, decltype(i_c)::value);
+      advance(cl);
+    });
+#pragma unroll
+    for (int v = 0; v < PV; ++v) sP[0][tid + v * NTHR] = ring[0][RT][v];
+    __syncthreads();
+    // whole rounds of D steps (every step of a round runs, so the loads in
+    // flight are the same on every path around the loop), then the rest
+    int s0 = 0;
+    for (; s0 + D <= n; s0 += D) {
+      for_each_index(std::make_integer_sequence<int, D>{}, [&](auto i_c) __attribute__((always_inline)) {
+        step(i_c, s0 + decltype(i_c)::value);
+      });
     }
-    if (!MULTI) fold(0);
+    for_each_index(std::make_integer_sequence<int, D - 1>{}, [&](auto i_c) __attribute__((always_inline)) {
+      if (s0 + decltype(i_c)::value < n) step(i_c, s0 + decltype(i_c)::value);
+    });
+
+    if (!MULTI) fold(0, s16);
 
     // candidates of this block; a full list is pruned and the entries that
-    // did not fit are offered again (the loop condition is uniform)
+    // did not fit are offered again (the loop condition is uniform). The
+    // opaque copy of the lane half keeps the list addresses from being
+    // computed once before the block loop and held through it.
+    int hq = hg;
+    asm volatile("" : "+v"(hq));
+    auto qsel = [&](int i) { return 8 * (i >> 2) + 4 * hq + (i & 3); };
     uint32_t pend = 0;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t row = row0 + rt * 16 + 4 * g + r;
-        if (row < a.N && q_ok) {
-          if (a.full) a.full[q * a.N + row] = (float)sc[rt][r];
-          pend |= 1u << (4 * rt + r);
+      for (int i = 0; i < 8; ++i) {
+        const int64_t q = a.grp * QB + qsel(i);
+        if (row[rt] < a.N && q < a.Q) {
+          if (a.full) a.full[q * a.N + row[rt]] = (float)sc[rt][i];
+          pend |= 1u << (8 * rt + i);
         }
       }
     for (;;) {
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const uint32_t bit = 1u << (4 * rt + r);
+        for (int i = 0; i < 8; ++i) {
+          const uint32_t bit = 1u << (8 * rt + i);
           if (pend & bit) {
-            const uint64_t key = order_key(sc[rt][r]);
-            if (key < cd.thr[n]) {
+            const int qn = qsel(i);
+            const uint64_t key = order_key(sc[rt][i]);
+            if (key < cd.thr[qn]) {
               pend &= ~bit;
             } else {
-              const int pos = atomicAdd(&cd.cnt[n], 1);
+              const int pos = atomicAdd(&cd.cnt[qn], 1);
               if (pos < CAP) {
-                cd.key[n][pos] = key;
-                cd.idx[n][pos] = (uint32_t)(row0 + rt * 16 + 4 * g + r);
+                cd.key[qn][pos] = key;
+                cd.idx[qn][pos] = (uint32_t)row[rt];
                 pend &= ~bit;
               } else {
                 cd.overflow = 1;
@@ -464,55 +608,65 @@ __global__ __launch_bounds__(256, 1) void k_merge(const uint64_t* __restrict__ c
 }
 
 // Pass configuration: candidate slots per query (256 when that leaves room
-// for at least 128 new entries after a prune, else 512), 512-bit halves per
-// step (two when the LDS holds both), 16-row tiles per wave and whether
-// several modules are summed. One workgroup per CU either way (LDS).
+// for at least 128 new entries after a prune, else 512), bytes per row and
+// step, 32-row tiles per wave and steps requested ahead. One workgroup runs
+// per CU (LDS).
 struct PassCfg {
-  int cap, hs, rt;
-  bool multi;
+  int cap, sb, rt, d;
 };
-inline PassCfg pass_cfg(int32_t U, int32_t topk) {
+inline PassCfg pass_cfg(int32_t topk) {
   PassCfg c;
   c.cap = topk <= 128 ? 256 : 512;
-  c.hs = c.cap == 256 ? 2 : 1;
-  c.rt = (c.hs == 1 && U == 1) ? 8 : 4;
-  c.multi = U > 1;
+  c.sb = 64;
+  c.rt = 2;
+  c.d = 3;
   return c;
 }
 
 struct Layout {
-  int64_t KS = 0;        // k-steps per query group over all modules
-  int64_t n_steps = 0;   // 512-bit steps over all modules
+  int64_t n_steps = 0;   // steps over all modules
   int64_t n_groups = 0;
   int64_t grid = 0;      // workgroups of the scoring pass
-  size_t o_mods = 0, o_steps = 0, o_fq = 0, o_ys = 0, o_ph = 0, o_pl = 0, o_ck = 0, o_ci = 0,
-         total = 0;
+  int64_t step_bytes = 0;
+  size_t o_mods = 0, o_fq = 0, o_ys = 0, o_pl = 0, o_ck = 0, o_ci = 0, o_pad = 0, total = 0;
 };
 
 Layout layout(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t topk) {
   Layout L;
-  const PassCfg c = pass_cfg(U, topk);
-  for (int u = 0; u < U; ++u) {
-    const int64_t nms = (kmod[u] + 511) / 512;
-    L.KS += KSTEP * nms;
-    L.n_steps += (nms + c.hs - 1) / c.hs;
-  }
+  const PassCfg c = pass_cfg(topk);
+  for (int u = 0; u < U; ++u) L.n_steps += (kmod[u] + 8 * c.sb - 1) / (8 * c.sb);
   L.n_groups = (Q + QB - 1) / QB;
-  const int64_t rows = (int64_t)NW * c.rt * 16;
-  const int64_t n_blocks = (N + rows - 1) / rows;
+  L.step_bytes = 256 * (int64_t)c.sb;
+  const int64_t n_blocks = (N + NW * 32 * c.rt - 1) / (NW * 32 * c.rt);
   L.grid = std::max<int64_t>(1, std::min<int64_t>(n_blocks, kCus));
   size_t b = 0;
   auto add = [&](size_t x) { size_t o = b; b = align256(b + x); return o; };
   L.o_mods = add(sizeof(ModInfo) * U);
-  L.o_steps = add(sizeof(Step) * L.n_steps);
-  L.o_fq = add(4 * Q * U);
-  L.o_ys = add(4 * Q * U);
-  L.o_ph = add((size_t)L.n_groups * L.KS * 1024);
-  L.o_pl = add((size_t)L.n_groups * L.KS * 1024);
+  L.o_fq = add(4 * (size_t)L.n_groups * U * QB);
+  L.o_ys = add(4 * (size_t)L.n_groups * U * QB);
+  L.o_pl = add((size_t)(L.n_groups * L.n_steps * L.step_bytes));
   L.o_ck = add((size_t)L.grid * QB * topk * 8);
   L.o_ci = add((size_t)L.grid * QB * topk * 4);
+  L.o_pad = add(16);   // a store of fewer than 16 bytes is copied here (see score_topk)
   L.total = b;
   return L;
+}
+
+template <int NCLS, bool MULTI, int CAP>
+eogp_status launch_pass(const PassCfg& c, dim3 gd, const ScoreArgs& a, hipStream_t s) {
+#define EOGP_SCORE_CFG(SB, RT, D)                                                      \
+  if (c.sb == SB && c.rt == RT && c.d == D) {                                          \
+    hipLaunchKernelGGL((k_score<NCLS, D, MULTI, CAP, SB, RT>), gd, dim3(NTHR), 0, s, a); \
+    return EOGP_OK;                                                                    \
+  }
+  EOGP_SCORE_CFG(64, 2, 3)
+#undef EOGP_SCORE_CFG
+  return fail(EOGP_ERR_UNSUPPORTED, "score_topk: no kernel for this pass configuration");
+}
+
+template <bool MULTI>
+eogp_status launch_pass(const PassCfg& c, dim3 gd, const ScoreArgs& a, hipStream_t s) {
+  return c.cap == 256 ? launch_pass<2, MULTI, 256>(c, gd, a, s) : launch_pass<2, MULTI, 512>(c, gd, a, s);
 }
 
 }  // namespace
@@ -534,47 +688,43 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
   ModInfo* mods = reinterpret_cast<ModInfo*>(base + L.o_mods);
   int32_t* fq = reinterpret_cast<int32_t*>(base + L.o_fq);
   int32_t* ys = reinterpret_cast<int32_t*>(base + L.o_ys);
-  int8_t* ph = reinterpret_cast<int8_t*>(base + L.o_ph);
-  int8_t* pl = reinterpret_cast<int8_t*>(base + L.o_pl);
+  int8_t* planes = reinterpret_cast<int8_t*>(base + L.o_pl);
   uint64_t* ck = reinterpret_cast<uint64_t*>(base + L.o_ck);
   uint32_t* ci = reinterpret_cast<uint32_t*>(base + L.o_ci);
 
-  Step* steps = reinterpret_cast<Step*>(base + L.o_steps);
-  const PassCfg cfg = pass_cfg(U, topk);
+  // The pass reads 16 bytes at the store's start in place of bytes past a
+  // module's end; a store with fewer readable bytes is copied into a zeroed
+  // 16-byte slot of the workspace first.
+  int64_t ksum = 0;
+  for (int u = 0; u < U; ++u) ksum += kmod[u];
+  if (N > 0 && (N - 1) * cstride + ksum / 8 < 16) {
+    uint8_t* pad = reinterpret_cast<uint8_t*>(base + L.o_pad);
+    hipLaunchKernelGGL(k_pad16, dim3(1), dim3(16), 0, s, codes,
+                       (int)((N - 1) * cstride + ksum / 8), pad);
+    EOGP_LAUNCH_CHECK("small-store copy");
+    codes = pad;
+  }
+  const PassCfg cfg = pass_cfg(topk);
   std::vector<ModInfo> hm(U);
-  std::vector<Step> hs;
-  hs.reserve(L.n_steps);
-  int64_t coff = 0, boff = 0, ks = 0;
+  int64_t coff = 0, boff = 0, sbase = 0;
   for (int u = 0; u < U; ++u) {
     hm[u].k = (int32_t)kmod[u];
     hm[u].coff = (int32_t)coff;
     hm[u].boff = (int32_t)boff;
-    hm[u].ksbase = (int32_t)ks;
-    const int64_t nms = (kmod[u] + 511) / 512, mbytes = kmod[u] / 8;
-    for (int64_t ms = 0; ms < nms; ms += cfg.hs) {
-      Step st{};
-      st.u = u;
-      st.boff = (int32_t)(boff + 64 * ms);
-      st.kbase = (int32_t)(ks + KSTEP * ms);
-      st.bytes = (int32_t)std::min<int64_t>(64 * cfg.hs, mbytes - 64 * ms);
-      st.halves = (int32_t)std::min<int64_t>(cfg.hs, nms - ms);
-      st.last = ms + cfg.hs >= nms;
-      hs.push_back(st);
-    }
+    hm[u].sbase = (int32_t)sbase;
     coff += kmod[u];
     boff += kmod[u] / 8;
-    ks += KSTEP * nms;
+    sbase += (kmod[u] + 8 * cfg.sb - 1) / (8 * cfg.sb);
   }
-  // the tables are small; copy them synchronously so the host vectors may go
+  // the table is small; copy it synchronously so the host vector may go
   EOGP_HIP(hipMemcpyAsync(mods, hm.data(), sizeof(ModInfo) * U, hipMemcpyHostToDevice, s));
-  EOGP_HIP(hipMemcpyAsync(steps, hs.data(), sizeof(Step) * hs.size(), hipMemcpyHostToDevice, s));
   EOGP_HIP(hipStreamSynchronize(s));
   timing::Scope tprep(EOGP_KT_SCORE_PREP, s);
-  hipLaunchKernelGGL(k_query_stats, dim3((unsigned)Q, (unsigned)U), dim3(256), 0, s, Y, ldy, U,
-                     mods, fq, ys);
-  const int64_t pbytes = L.n_groups * L.KS * 1024;
+  hipLaunchKernelGGL(k_query_stats, dim3((unsigned)(L.n_groups * QB), (unsigned)U), dim3(256), 0,
+                     s, Y, ldy, Q, U, mods, fq, ys);
+  const int64_t pbytes = L.n_groups * L.n_steps * L.step_bytes;
   hipLaunchKernelGGL(k_query_planes, dim3((unsigned)ceil_div(pbytes, 256)), dim3(256), 0, s, Y,
-                     ldy, Q, U, mods, fq, L.KS, L.n_groups, ph, pl);
+                     ldy, Q, U, mods, fq, L.n_steps, L.n_groups, cfg.sb, planes);
   EOGP_LAUNCH_CHECK("query preparation");
   timing::end(tprep.slot, s);
   tprep.slot = -1;
@@ -586,11 +736,8 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     a.N = N;
     a.U = U;
     a.mods = mods;
-    a.ph = ph;
-    a.pl = pl;
-    a.steps = steps;
+    a.planes = reinterpret_cast<const uint4*>(planes);
     a.n_steps = (int)L.n_steps;
-    a.KS = L.KS;
     a.grp = grp;
     a.fq = fq;
     a.ysum = ys;
@@ -601,14 +748,10 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     a.cidx = ci;
     {
       timing::Scope tp(EOGP_KT_SCORE_PASS, s);
-      const dim3 gd((unsigned)L.grid), bd(NTHR);
-      if (cfg.cap == 256) {
-        if (cfg.multi) hipLaunchKernelGGL((k_score<256, 4, true, 2>), gd, bd, 0, s, a);
-        else hipLaunchKernelGGL((k_score<256, 4, false, 2>), gd, bd, 0, s, a);
-      } else {
-        if (cfg.multi) hipLaunchKernelGGL((k_score<512, 4, true, 1>), gd, bd, 0, s, a);
-        else hipLaunchKernelGGL((k_score<512, 8, false, 1>), gd, bd, 0, s, a);
-      }
+      const dim3 gd((unsigned)L.grid);
+      const eogp_status st = U > 1 ? launch_pass<true>(cfg, gd, a, s)
+                                   : launch_pass<false>(cfg, gd, a, s);
+      if (st != EOGP_OK) return st;
     }
     timing::Scope tm(EOGP_KT_SCORE_MERGE, s);
     hipLaunchKernelGGL(k_merge, dim3(QB), dim3(256), 0, s, ck, ci, (int)L.grid, grp, Q, topk,
