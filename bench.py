@@ -18,8 +18,10 @@ artifacts and the store are resident in device memory before timing starts.
 
 Printed: one JSON line with the metric, the roofline of the dominant kernel
 (the first-stage rotation contraction, timed live with HIP events on its
-stream), the oracle CPU baseline, and the scoring-at-scale measurement
-(8,388,608 codes x 16,384 bits, 512 queries, top-100).
+stream), the oracle CPU baseline, one transformer block of the OLMo-2-1B- and
+OLMo-2-32B-shaped workloads (bf16 inputs; batches of 256 and 64 examples; the
+full-model rate at the same per-block cost), and the scoring-at-scale
+measurement (8,388,608 codes x 16,384 bits, 512 queries, top-100).
 """
 from __future__ import annotations
 
@@ -56,6 +58,9 @@ def parse(argv=None):
     ap.add_argument("--scoring-queries", type=int, default=512)
     ap.add_argument("--scoring-codes", type=int, default=8 * 1024 * 1024)
     ap.add_argument("--only-scoring", action="store_true")
+    ap.add_argument("--no-olmo", action="store_true",
+                    help="skip the OLMo-2-1B and OLMo-2-32B per-block measurements")
+    ap.add_argument("--only-olmo", action="store_true")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB 4 times (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters against known traffic)")
@@ -346,6 +351,90 @@ def cpu_baseline(st: Gpt2Step):
 # ---------------------------------------------------------------------------
 # Scoring at scale: 8M codes x 16384 bits, 512 queries, top-100
 # ---------------------------------------------------------------------------
+def olmo_block(w, B, n_model_blocks, dev, reps=3):
+    """One transformer block of an OLMo-2-shaped model (its 7 linears, bf16
+    activations and output-gradients) through the whole compression path:
+    first stage (bf16 MFMA, fp32 accumulation), PCA with the module's fp16 P,
+    sign packing. Throughput per block, and for the whole model at the same
+    per-block cost (every block has the same shapes)."""
+    import torch
+    from paper_2609_37842_amd import eogp as E
+    from paper_2609_37842_amd import synth as S
+    t0 = time.time()
+    inputs = {}
+    for si, (name, di, do) in enumerate(w.block):
+        if (di, do) not in inputs:   # linears of one shape share the batch's inputs
+            inputs[(di, do)] = S.torch_inputs(w, si, B, w.T, di, do, dev, torch.bfloat16)
+    cache, mods = {}, []
+    for si, (name, di, do) in enumerate(w.block):
+        art = S.torch_module_artifacts(w, si, di, do, dev, torch.float16, cache)
+        plan = E.eogp_plan_create(art["eigvals"], art["damping"], w.m, art["Q_A"], art["Q_S"])
+        mods.append((name, di, do, plan, art["Pt"]))
+        del art
+    del cache
+    torch.cuda.synchronize()
+    log(f"{w.name}: block ready ({time.time() - t0:.1f}s)")
+    U = len(mods)
+    Z = torch.empty((B, w.m), dtype=torch.float32, device=dev)
+    X = torch.empty((B, w.k), dtype=torch.float32, device=dev)
+    codes = torch.empty((B, U * (w.k // 8)), dtype=torch.uint8, device=dev)
+    scales = torch.empty((B, U), dtype=torch.int16, device=dev)
+    ws = torch.empty(max(E.eogp_rotate_retain_workspace_size(p, B, w.T) for (_, _, _, p, _) in mods),
+                     dtype=torch.uint8, device=dev)
+    pws = torch.empty(E.eogp_pca_project_workspace_size(B, w.m, w.k, E.F16, E.PREC_FAST),
+                      dtype=torch.uint8, device=dev)
+    kb = w.k // 8
+
+    def run():
+        for u, (name, di, do, plan, Pt) in enumerate(mods):
+            a, ds, mk = inputs[(di, do)]
+            E.eogp_rotate_retain_planned(plan, a, ds, mk, Z=Z, prec=E.PREC_FAST, ws=ws)
+            E.eogp_pca_project(Z, Pt, X=X, prec=E.PREC_FAST, ws=pws)
+            E.eogp_sign_pack(X, codes[:, u * kb:(u + 1) * kb], scales[:, u:u + 1])
+
+    run()
+    torch.cuda.synchronize()
+    for c in range(len(E.KERNEL_CLASSES)):
+        E.eogp_timing_read(c)
+    E.eogp_timing_enable(True)
+    t1 = time.perf_counter()
+    for _ in range(reps):
+        run()
+    torch.cuda.synchronize()
+    el = (time.perf_counter() - t1) / reps
+    kt = {name: E.eogp_timing_read(c) for name, c in E.KERNEL_CLASSES.items()}
+    E.eogp_timing_enable(False)
+    rot_ms, rot_n = kt["rotation_gemm"]
+    flops = 0.0
+    valid = {}
+    for (name, di, do, plan, _) in mods:
+        vt = valid.setdefault((di, do), int(inputs[(di, do)][2].sum().item()))
+        flops += 2.0 * vt * (do * plan.n_rows + di * plan.n_cols)
+    rot_tflops = flops * reps / (rot_ms * 1e-3) / 1e12
+    pca_ms, _ = kt["pca_gemm"]
+    out = {
+        "workload": w.name, "block": [n for (n, _, _) in w.block], "batch": B, "T": w.T,
+        "valid_tokens_per_example": sum(v for v in valid.values()) / len(valid) / B,
+        "m": w.m, "k": w.k, "first_stage": "bf16 inputs, bf16 MFMA, fp32 accumulation",
+        "pca": "fp16 P, fp32 accumulation",
+        "ms_per_block": 1000.0 * el,
+        "examples_per_s_per_block": B / el,
+        "model_blocks": n_model_blocks,
+        "examples_per_s_full_model": B / (el * n_model_blocks),
+        "kernel_ms_per_block": {name: ms / reps for name, (ms, n) in kt.items() if n},
+        "rotation_roofline": {"bound": "mfma", "achieved": rot_tflops, "peak": BF16_PEAK_TFLOPS,
+                              "unit": "TFLOP/s", "frac": rot_tflops / BF16_PEAK_TFLOPS,
+                              "alg_flops_per_block": flops},
+        "pca_ms_per_block": pca_ms / reps,
+        "retained_axes": {n: {"J": p.n_rows, "K": p.n_cols} for (n, _, _, p, _) in mods},
+    }
+    for (_, _, _, plan, _) in mods:
+        plan.close()
+    del mods, inputs, Z, X, codes, scales, ws, pws
+    torch.cuda.empty_cache()
+    return out
+
+
 def scoring_at_scale(args, dev):
     import torch
     from paper_2609_37842_amd import eogp as E
@@ -423,7 +512,7 @@ def main(argv=None):
         return 0
 
     out = {}
-    if not args.only_scoring:
+    if not args.only_scoring and not args.only_olmo:
         st = Gpt2Step(args, dev)
         for s in range(args.warmup):
             st.step(s)
@@ -563,7 +652,15 @@ def main(argv=None):
             log(f"cpu baseline done ({time.time() - t0:.1f}s)")
         del st
         torch.cuda.empty_cache()
-    if not args.no_scoring:
+    if not args.no_olmo and not args.only_scoring:
+        from paper_2609_37842_amd import synth as S
+        for key, w, B, nb in (("olmo2_1b", S.OLMO2_1B, 256, 16), ("olmo2_32b", S.OLMO2_32B, 64, 64)):
+            o = olmo_block(w, B, nb, dev)
+            log(f"{w.name}: {o['ms_per_block']:.1f} ms per block of {B}, "
+                f"{o['examples_per_s_full_model']:.2f} ex/s full model, rotation "
+                f"{o['rotation_roofline']['achieved']:.0f} TFLOP/s")
+            out[key] = o
+    if not args.no_scoring and not args.only_olmo:
         sc = scoring_at_scale(args, dev)
         log(f"scoring: {sc['ms_per_pass']:.3f} ms/pass, {sc['hbm_GBps']:.0f} GB/s")
         if args.only_scoring:
