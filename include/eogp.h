@@ -139,7 +139,8 @@ eogp_status eogp_plan_set_input_exponents(eogp_plan* plan, int32_t e_acts, int32
  *              EOGP_PREC_F16 (fp32 inputs only) rounds inputs and bases once to
  *              fp16 (relative error of a row of Z about 4e-4 for inputs inside
  *              fp16's normal range); EOGP_PREC_FAST rounds operands to bf16
- *              (about 3e-3 for fp32 inputs; the natural mode for bf16 inputs).
+ *              and keeps the rotated tokens in bf16 (about 3e-3 for fp32
+ *              inputs; the natural mode for bf16 inputs).
  *              EOGP_ERR_UNSUPPORTED for EOGP_PREC_F16 with bf16 inputs.
  *   ws         workspace of at least eogp_rotate_retain_workspace_size bytes.
  * Sizes: N*T + 8N + 256 < 2^31 (the compacted token list is indexed in

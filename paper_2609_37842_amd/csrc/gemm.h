@@ -37,6 +37,7 @@ struct GemmArgs {
   // Single-pass products without split-K only.
   uint16_t* CT = nullptr;
   int64_t ldct = 0;
+  bool ct_bf16 = false;            // CT entries are bf16 (else fp16)
   int64_t M = 0;                   // rows (upper bound if M_dev is set)
   const int32_t* M_dev = nullptr;  // device-side row count (<= M), or null
   int64_t N = 0, K = 0;

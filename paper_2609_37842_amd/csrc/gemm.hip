@@ -143,8 +143,8 @@ typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 // Epilogue of one wave's WI x WJ blocks of 32 x 32 (rows r0.., columns c0..;
 // r0 and c0 multiples of 32). Lane l holds column (l & 31) and rows
 // 8 (r / 4) + 4 (l / 32) + r % 4 of each block. fp32 C: bounds-checked stores.
-// fp16 CT (fragment order, see GemmArgs): four consecutive rows of one column
-// are 8 contiguous bytes; no checks.
+// 16-bit CT (fragment order, see GemmArgs; fp16 or bf16): four consecutive
+// rows of one column are 8 contiguous bytes; no checks.
 template <int WI, int WJ>
 __device__ __forceinline__ void store_tile(const GemmArgs& g, float* C, int64_t ldc, int64_t M,
                                            int64_t N, int64_t r0, int64_t c0, int lane,
@@ -165,10 +165,13 @@ __device__ __forceinline__ void store_tile(const GemmArgs& g, float* C, int64_t 
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
           const f32x16& a = acc[i][j];
-          const uint32_t x0 = cvt_pair<true>(a[8 * p + 0], a[8 * p + 1]);
-          const uint32_t x1 = cvt_pair<true>(a[8 * p + 2], a[8 * p + 3]);
-          const uint32_t y0 = cvt_pair<true>(a[8 * p + 4], a[8 * p + 5]);
-          const uint32_t y1 = cvt_pair<true>(a[8 * p + 6], a[8 * p + 7]);
+          auto cvt = [&](float u, float v) {
+            return g.ct_bf16 ? cvt_pair<false>(u, v) : cvt_pair<true>(u, v);
+          };
+          const uint32_t x0 = cvt(a[8 * p + 0], a[8 * p + 1]);
+          const uint32_t x1 = cvt(a[8 * p + 2], a[8 * p + 3]);
+          const uint32_t y0 = cvt(a[8 * p + 4], a[8 * p + 5]);
+          const uint32_t y1 = cvt(a[8 * p + 6], a[8 * p + 7]);
           const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
           const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
           const int64_t grp = (r0 + 32 * i + 16 * p) / 16;

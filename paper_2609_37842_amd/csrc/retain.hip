@@ -129,7 +129,7 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
   }
 }
 
-// fp16 intermediates: S~ and A~ in MFMA-fragment order (for every 32 rows j
+// 16-bit intermediates (fp16, or bf16 with BF): S~ and A~ in MFMA-fragment order (for every 32 rows j
 // and 16 tokens t one contiguous 1 KB block, j-major, 16 tokens per j; token
 // capacity ldt, at least 16 kRet16Unroll + 16 tokens past the last run);
 // example i's tokens are t = off[i] .. off[i] + len[i] - 1,
@@ -141,6 +141,7 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
 // the next example) are zeroed in both operands before they reach the MFMA.
 constexpr int kRet16Unroll = 8;
 
+template <bool BF>
 __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__ St,
                                                     const uint16_t* __restrict__ At, int64_t ldt,
                                                     const int32_t* __restrict__ ex_off,
@@ -200,8 +201,12 @@ __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__
           b[u][d] &= keep;
         }
       }
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a[u]),
-                                                   __builtin_bit_cast(f16x8, b[u]), acc, 0, 0, 0);
+      if constexpr (BF)
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[u]),
+                                                      __builtin_bit_cast(bf16x8, b[u]), acc, 0, 0, 0);
+      else
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a[u]),
+                                                     __builtin_bit_cast(f16x8, b[u]), acc, 0, 0, 0);
     }
   }
   // acc[r] holds C[8 (r / 4) + 4 half + r % 4][col]
@@ -344,6 +349,7 @@ eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
   if (t16) {
     gs.CT = w.St16;
     gs.ldct = w.ldt;
+    gs.ct_bf16 = !f16;   // FAST: bf16 intermediates (fp32's range); F16: fp16
   } else {
     gs.C = w.St;
     gs.ldc = p->rows_pad;
@@ -406,7 +412,10 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   Carve cv(ws, ws_bytes);
   Work w = carve_work(p, N, T, cv);
   const bool f16 = prec == EOGP_PREC_F16;
-  eogp_status st = rotate_tokens(p, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, f16,
+  // 16-bit fragment-order intermediates in the F16 (fp16) and FAST (bf16)
+  // modes; fp32 token-major ones in the ACCURATE mode
+  const bool t16 = prec != EOGP_PREC_ACCURATE;
+  eogp_status st = rotate_tokens(p, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, t16,
                                  w, s);
   if (st != EOGP_OK) return st;
 
@@ -426,10 +435,16 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
     const int64_t nex = std::min<int64_t>(ex_chunk, N - ex0);
     timing::Scope ts(EOGP_KT_RETAINED, s);
     const unsigned gx = (unsigned)gx64;
-    if (f16) {
-      hipLaunchKernelGGL(k_retained16, dim3((unsigned)(kXcds * ceil_div(nex, kXcds) * gx)),
-                         dim3(256), 0, s, w.St16, w.At16, w.ldt, w.cnt, w.len, p->tiles,
-                         (int)p->n_tiles, p->ent_loc, out_scale, w.Zt, p->m, ex0, nex);
+    if (t16) {
+      const dim3 grid16((unsigned)(kXcds * ceil_div(nex, kXcds) * gx));
+      if (f16)
+        hipLaunchKernelGGL(k_retained16<false>, grid16, dim3(256), 0, s, w.St16, w.At16, w.ldt,
+                           w.cnt, w.len, p->tiles, (int)p->n_tiles, p->ent_loc, out_scale, w.Zt,
+                           p->m, ex0, nex);
+      else
+        hipLaunchKernelGGL(k_retained16<true>, grid16, dim3(256), 0, s, w.St16, w.At16, w.ldt,
+                           w.cnt, w.len, p->tiles, (int)p->n_tiles, p->ent_loc, out_scale, w.Zt,
+                           p->m, ex0, nex);
     } else {
       hipLaunchKernelGGL(k_retained, dim3(gx, (unsigned)nex), dim3(256), 0, s,
                          w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,
