@@ -8,12 +8,13 @@ lengths ~ U{64..512}, m = 16384 retained coordinates and k = 8192 code bits per
 module, a store of 20,000 examples and 256 queries.
 
 One step is one pass of the whole hot path over one batch:
-  * store B = 625 training examples: for every module, first stage (valid-token
-    compaction, MFMA rotations, retained products, half-whitening), PCA
-    projection with the module's fp16 P, sign packing into the store;
-  * project 8 queries through every module (unquantized);
-  * score those 8 queries against all 20,000 stored codes with top-100.
-32 steps are the whole job (20,000 examples, 256 queries). Inputs, shared
+  * store B = 1,250 training examples: for every module, first stage
+    (valid-token compaction, MFMA rotations, retained products,
+    half-whitening), PCA projection with the module's fp16 P, sign packing
+    into the store;
+  * project 16 queries through every module (unquantized);
+  * score those 16 queries against all 20,000 stored codes with top-100.
+16 steps are the whole job (20,000 examples, 256 queries). Inputs, shared
 artifacts and the store are resident in device memory before timing starts.
 
 Printed: one JSON line with the metric, the roofline of the dominant kernel
@@ -43,10 +44,10 @@ BF16_PEAK_TFLOPS = 2516.6    # dense MFMA bf16/fp16, 256 CU x 2.4 GHz x 4096 flo
 def parse(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--steps", type=int, default=16)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--batch", type=int, default=625)
-    ap.add_argument("--queries-per-step", type=int, default=8)
+    ap.add_argument("--batch", type=int, default=1250)
+    ap.add_argument("--queries-per-step", type=int, default=16)
     ap.add_argument("--blocks", type=int, default=12)
     ap.add_argument("--prec", choices=["f16", "accurate", "fast"], default="f16",
                     help="first-stage contractions: f16 = fp32 inputs rounded once to fp16 "
@@ -303,7 +304,7 @@ def cpu_baseline(st: Gpt2Step):
         threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
-    n_ex = 48                                     # about 10 s of oracle work on 16 threads
+    n_ex = 64                                     # about 10-15 s of oracle work on 16 threads
     per_shape = {}
     for si, (name, di, do) in enumerate(st.shapes):
         u = si                                     # block 0 module of this shape

@@ -104,6 +104,10 @@ def test_encode_and_score_argument_validation_without_device():
                              fake, 1 << 20, None) == -1
     assert L.eogp_score_topk(fake, 12, fake, 4, 1, ks, fake, 64, 1, 5, fake, fake, None,
                              fake, 1 << 20, None) == -1
+    # a module longer than 2^22 bits (its integer sums could overflow)
+    big = (ctypes.c_int64 * 1)((1 << 22) + 64)
+    assert L.eogp_score_topk(fake, (1 << 19) + 8, fake, 4, 1, big, fake, (1 << 22) + 64, 1, 5,
+                             fake, fake, None, fake, 1 << 20, None) == -1
     # workspace too small
     assert L.eogp_score_topk(fake, 8, fake, 4, 1, ks, fake, 64, 1, 5, fake, fake, None,
                              fake, 16, None) == -4

@@ -2,7 +2,7 @@
 
 The oracle cannot evaluate whole full-size problems in seconds, so each test
 runs the HIP path at the real shape (for the GPT-2-small-shaped workload in
-the launch configuration bench.py times: 633 examples x 512 tokens per call)
+the launch configuration bench.py times: 1,266 examples x 512 tokens per call)
 and checks
 
 * sampled examples, or sampled retained coordinates, of the first stage
@@ -106,14 +106,14 @@ def first_stage_sampled(w, si, name, d_in, d_out, N, T, dtype, precs, examples, 
 
 
 def test_gpt2_small_c_fc_full_step_shape():
-    """GPT-2-small-shaped c_fc (769 -> 3072) at 633 examples x 512 tokens,
+    """GPT-2-small-shaped c_fc (769 -> 3072) at 1,266 examples x 512 tokens,
     fp32 inputs; fp16 and bf16x3 first stages, then PCA with the fp16 P,
     sign bits and scales on three sampled examples."""
     w = S.GPT2_SMALL
     si = 2
     name, d_in, d_out = w.block[si]
-    N, T = 633, w.T
-    examples = [0, 316, 632]
+    N, T = 1266, w.T
+    examples = [0, 633, 1265]
     say(f"[full size] gpt2 {name}")
     Zs, zref, art = first_stage_sampled(w, si, name, d_in, d_out, N, T, torch.float32,
                                         [(E.PREC_F16, 1e-3), (E.PREC_ACCURATE, 1e-3)], examples)

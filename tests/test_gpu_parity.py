@@ -620,6 +620,30 @@ def test_score_topk_bit_exact_large_stores(N, ks, Q, topk):
     assert np.array_equal(sc.cpu().numpy(), ov)
 
 
+@pytest.mark.parametrize("N,ks,stride", [
+    (1, [64], 8),            # an 8-byte store: the pass reads a zero-padded copy
+    (1, [64, 64], 16),       # exactly 16 readable bytes
+    (2, [64], 8),
+    (3, [192], 32),          # rows wider than their codes (stride > sum k_u / 8)
+])
+def test_score_tiny_stores(N, ks, stride):
+    """Stores of a few bytes: every lane's 16-byte reads stay inside the
+    store (or its padded copy) and the scores are exact."""
+    say(f"[score] tiny N={N} ks={ks} stride={stride}")
+    codes, scales, Y = random_store(N + 40, N, ks, 5)
+    wide = np.zeros((N, stride), np.uint8)
+    wide[:, :codes.shape[1]] = codes
+    ct = d(wide)[:, :codes.shape[1]] if stride > codes.shape[1] else d(wide)
+    idx, sc, full = E.eogp_score_topk(ct, d(scales.view(np.int16)), ks, d(Y), 3,
+                                      full_scores=True)
+    torch.cuda.synchronize()
+    ref = O.score(codes, scales, ks, Y)
+    assert np.array_equal(full.cpu().numpy(), ref.astype(np.float32))
+    oi, ov = O.topk(ref, 3)
+    assert np.array_equal(idx.cpu().numpy(), oi)
+    assert np.array_equal(sc.cpu().numpy(), ov)
+
+
 def test_score_empty_store_and_no_queries():
     """An empty store pads every query's list (index -1, score -inf); no
     queries is a no-op."""
