@@ -39,6 +39,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2516.6    # dense MFMA bf16/fp16, 256 CU x 2.4 GHz x 4096 flop/clk
+INT8_PEAK_TOPS = 5033.2      # dense MFMA int8, twice the bf16 rate
 
 
 def parse(argv=None):
@@ -472,6 +473,10 @@ def scoring_at_scale(args, dev):
     bytes_per_pass = N * (k // 8 + 2)
     avg = pass_ms / max(1, passes)
     gbs = bytes_per_pass / (avg * 1e-3) / 1e9
+    # whole job against its bound: every pass streams the store once at the HBM peak, or the
+    # int8 MFMA work (2 planes x 2 ops per query, code bit and row) at the dense int8 peak
+    hbm_bound_ms = passes * bytes_per_pass / (HBM_PEAK_GBS * 1e9) * 1e3
+    mfma_bound_ms = 4.0 * Q * N * k / (INT8_PEAK_TOPS * 1e12) * 1e3
     return {
         "workload": w.name,
         "codes": N, "bits": k, "queries": Q, "topk": topk,
@@ -483,6 +488,9 @@ def scoring_at_scale(args, dev):
         "frac": gbs / HBM_PEAK_GBS,
         "merge_ms_total": merge_ms, "prep_ms": prep_ms,
         "job_ms": 1000.0 * total_s,
+        "job_bound_ms": max(hbm_bound_ms, mfma_bound_ms),
+        "job_bound": {"hbm_ms": hbm_bound_ms, "int8_mfma_ms": mfma_bound_ms,
+                      "frac": max(hbm_bound_ms, mfma_bound_ms) / (1000.0 * total_s)},
     }
 
 
