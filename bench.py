@@ -163,7 +163,11 @@ class Gpt2Step:
         # coordinates of every module side by side; the query rows of Xall are
         # the unquantized query coordinates Y [Qb, U*k] that scoring reads
         f32 = torch.float32
+        # the PCA step takes the coordinates in fp16 (as the paper caches them; its
+        # fp16 P would round an fp32 Z to the same values); the SRHT takes fp32
         self.Z = torch.empty((Nt, self.m), dtype=f32, device=dev)
+        self.Z16 = (torch.empty((Nt, self.m), dtype=torch.float16, device=dev)
+                    if self.pca_prec == E.PREC_FAST else self.Z)
         self.Xall = torch.empty((Nt, U * self.k), dtype=f32, device=dev)
         self.Y = self.Xall[self.B:]
         g = S.torch_generator(w.config_id, 900001, dev)
@@ -195,9 +199,9 @@ class Gpt2Step:
         k = self.k
         for u, (name, di, do) in enumerate(self.modules):
             E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
-                                         Z=self.Z, prec=self.prec, ws=self.ws)
+                                         Z=self.Z16, prec=self.prec, ws=self.ws)
             X = self.Xall[:, u * k:(u + 1) * k]
-            E.eogp_pca_project(self.Z, self.Pt[u], X=X, prec=self.pca_prec, ws=self.pca_ws)
+            E.eogp_pca_project(self.Z16, self.Pt[u], X=X, prec=self.pca_prec, ws=self.pca_ws)
             E.eogp_sign_pack(X[:self.B], codes[:, u * self.kb:(u + 1) * self.kb],
                              scales[:, u:u + 1])
         E.eogp_score_topk(self.codes, self.scales, [k] * self.U, self.Y, self.topk,
@@ -377,7 +381,7 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3):
     torch.cuda.synchronize()
     log(f"{w.name}: block ready ({time.time() - t0:.1f}s)")
     U = len(mods)
-    Z = torch.empty((B, w.m), dtype=torch.float32, device=dev)
+    Z = torch.empty((B, w.m), dtype=torch.float16, device=dev)   # fp16 coordinates, fp16 P
     X = torch.empty((B, w.k), dtype=torch.float32, device=dev)
     codes = torch.empty((B, U * (w.k // 8)), dtype=torch.uint8, device=dev)
     scales = torch.empty((B, U), dtype=torch.int16, device=dev)
@@ -418,7 +422,7 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3):
         "workload": w.name, "block": [n for (n, _, _) in w.block], "batch": B, "T": w.T,
         "valid_tokens_per_example": sum(v for v in valid.values()) / len(valid) / B,
         "m": w.m, "k": w.k, "first_stage": "bf16 inputs, bf16 MFMA, fp32 accumulation",
-        "pca": "fp16 P, fp32 accumulation",
+        "pca": "fp16 coordinates and P, fp32 accumulation",
         "ms_per_block": 1000.0 * el,
         "examples_per_s_per_block": B / el,
         "model_blocks": n_model_blocks,
@@ -566,7 +570,9 @@ def main(argv=None):
             "config": {"workload": st.w.name, "modules": st.U, "batch_per_step": st.B,
                        "queries_per_step": st.Qb, "store": st.N_store, "T": st.T,
                        "valid_tokens_per_batch": st.valid_tokens, "m": st.m, "k": st.k,
-                       "topk": st.topk, "pca": f"fp16 P, {args.pca_prec}",
+                       "topk": st.topk,
+                       "pca": ("fp16 coordinates and P, fp32 accumulation" if args.pca_prec == "fast"
+                               else "fp32 coordinates split into two fp16 parts, fp16 P"),
                        "first_stage": args.prec},
             "roofline": {
                 "kernel": "first-stage rotation contraction (k_gemm_p)",

@@ -147,12 +147,18 @@ eogp_status eogp_plan_set_input_exponents(eogp_plan* plan, int32_t e_acts, int32
  * 32 bits), else EOGP_ERR_INVALID.
  * ------------------------------------------------------------------------ */
 size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64_t T);
+/* The planned call takes the plan built once per module (eogp_plan_create)
+ * and writes Z in `z_dtype`: EOGP_F32, or EOGP_F16, each coordinate rounded
+ * once to fp16 (nearest even; beyond fp16's range it becomes inf) -- the
+ * paper caches first-stage coordinates in FP16, and eogp_pca_project takes
+ * such a Z directly. Other z_dtype values give EOGP_ERR_INVALID. */
 eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
                                        int64_t ld_acts, const void* out_grads,
                                        int64_t ld_grads, eogp_dtype in_dtype,
                                        const uint8_t* token_mask, int64_t N, int64_t T,
-                                       float* Z, int64_t ldz, eogp_prec prec,
-                                       void* ws, size_t ws_bytes, void* stream);
+                                       void* Z, eogp_dtype z_dtype, int64_t ldz,
+                                       eogp_prec prec, void* ws, size_t ws_bytes,
+                                       void* stream);
 
 /* One-shot form with the paper's arguments: builds a plan from
  * (eigvals, damping, m, Q_A, Q_S), runs the first stage, releases the plan.
@@ -173,7 +179,10 @@ eogp_status eogp_rotate_retain(const void* acts, int64_t ld_acts, const void* ou
  * matrix applied to a whole batch of cached first-stage coordinates):
  *   X[i, c] = sum_r Z[i, r] P[r, c],  i.e. x_i = P^T z_i.
  *
- *   Z   [N, ldz] fp32 (first m columns used).
+ *   Z   [N, ldz] in `z_dtype` (first m columns used): EOGP_F32 with any P, or
+ *       16-bit Z of P's own type (EOGP_F16 with fp16 P, EOGP_BF16 with bf16 P;
+ *       rows on 16-byte boundaries: ldz % 8 == 0, Z 16-byte aligned), else
+ *       EOGP_ERR_UNSUPPORTED. A 16-bit Z enters one MFMA product as it is.
  *   P   the m x k PCA matrix stored COLUMN-major: direction c occupies
  *       P + c*ldp .. P + c*ldp + m - 1 (ldp >= m), in `p_dtype` (EOGP_F16 as
  *       the paper stores it, EOGP_BF16 or EOGP_F32).
@@ -188,9 +197,9 @@ eogp_status eogp_rotate_retain(const void* acts, int64_t ld_acts, const void* ou
  * ------------------------------------------------------------------------ */
 size_t eogp_pca_project_workspace_size(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype,
                                        eogp_prec prec);
-eogp_status eogp_pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m,
-                             const void* P, eogp_dtype p_dtype, int64_t ldp, int64_t k,
-                             float* X, int64_t ldx, eogp_prec prec, void* ws,
+eogp_status eogp_pca_project(const void* Z, eogp_dtype z_dtype, int64_t ldz, int64_t N,
+                             int64_t m, const void* P, eogp_dtype p_dtype, int64_t ldp,
+                             int64_t k, float* X, int64_t ldx, eogp_prec prec, void* ws,
                              size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------

@@ -16,13 +16,13 @@ namespace eogp {
 size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T);
 eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
                           int64_t ld_grads, bool bf16_in,
-                          const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
+                          const uint8_t* mask, int64_t N, int64_t T, void* Z, bool z16, int64_t ldz,
                           int prec, void* ws, size_t ws_bytes, hipStream_t s);
 eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t* codes,
                       int64_t cstride, uint16_t* scales, int64_t sstride, hipStream_t s);
 size_t pca_ws(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype);
 size_t pca_split_copy_bytes(int64_t m, int64_t k, eogp_dtype p_dtype);
-eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const void* P,
+eogp_status pca_project(const void* Z, eogp_dtype z_dtype, int64_t ldz, int64_t N, int64_t m, const void* P,
                         eogp_dtype p_dtype, int64_t ldp, int64_t k, float* X, int64_t ldx,
                         bool accurate, void* ws, size_t ws_bytes, hipStream_t s);
 int32_t score_max_topk();
@@ -97,7 +97,7 @@ eogp_status check_plan_args(const float* eigvals, int64_t d_out, int64_t d_in, d
 }
 
 eogp_status check_first_stage(const eogp_plan* p, const void* acts, const void* grads,
-                              eogp_dtype dt, int64_t N, int64_t T, const float* Z, int64_t ldz,
+                              eogp_dtype dt, int64_t N, int64_t T, const void* Z, int64_t ldz,
                               eogp_prec prec) {
   if (!p) return fail(EOGP_ERR_INVALID, "rotate_retain: NULL plan");
   if (N < 0 || T < 0) return fail(EOGP_ERR_INVALID, "rotate_retain: negative size");
@@ -186,10 +186,12 @@ size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64
 eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
                                        int64_t ld_acts, const void* out_grads, int64_t ld_grads,
                                        eogp_dtype in_dtype, const uint8_t* token_mask, int64_t N,
-                                       int64_t T, float* Z, int64_t ldz, eogp_prec prec, void* ws,
-                                       size_t ws_bytes, void* stream) {
+                                       int64_t T, void* Z, eogp_dtype z_dtype, int64_t ldz,
+                                       eogp_prec prec, void* ws, size_t ws_bytes, void* stream) {
   eogp_status st = check_first_stage(plan, acts, out_grads, in_dtype, N, T, Z, ldz, prec);
   if (st != EOGP_OK) return st;
+  if (z_dtype != EOGP_F32 && z_dtype != EOGP_F16)
+    return fail(EOGP_ERR_INVALID, "rotate_retain: Z must be fp32 or fp16");
   if (ld_acts == 0) ld_acts = plan->d_in;
   if (ld_grads == 0) ld_grads = plan->d_out;
   if (ld_acts < plan->d_in || ld_grads < plan->d_out)
@@ -207,7 +209,8 @@ eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
   if (hipGetDevice(&dev) == hipSuccess && dev != plan->device)
     return fail(EOGP_ERR_INVALID, "rotate_retain: plan belongs to another device");
   return rotate_retain(plan, acts, ld_acts, out_grads, ld_grads, in_dtype == EOGP_BF16,
-                       token_mask, N, T, Z, ldz, (int)prec, ws, ws_bytes, S(stream));
+                       token_mask, N, T, Z, z_dtype == EOGP_F16, ldz, (int)prec, ws, ws_bytes,
+                       S(stream));
 }
 
 size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d_in,
@@ -236,7 +239,7 @@ eogp_status eogp_rotate_retain(const void* acts, int64_t ld_acts, const void* ou
   st = build_plan(eigvals, d_out, d_in, damping, m, Q_A, Q_S, S(stream), &plan);
   if (st != EOGP_OK) return st;
   st = eogp_rotate_retain_planned(plan, acts, ld_acts, out_grads, ld_grads, in_dtype, token_mask,
-                                  N, T, Z, ldz, prec, ws, ws_bytes, stream);
+                                  N, T, Z, EOGP_F32, ldz, prec, ws, ws_bytes, stream);
   hipError_t e = hipStreamSynchronize(S(stream));
   free_plan(plan);
   if (st == EOGP_OK && e != hipSuccess) return check_hip(e, "rotate_retain");
@@ -250,9 +253,9 @@ size_t eogp_pca_project_workspace_size(int64_t N, int64_t m, int64_t k, eogp_dty
   return pca_ws(N, m, k, p_dtype);
 }
 
-eogp_status eogp_pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const void* P,
-                             eogp_dtype p_dtype, int64_t ldp, int64_t k, float* X, int64_t ldx,
-                             eogp_prec prec, void* ws, size_t ws_bytes, void* stream) {
+eogp_status eogp_pca_project(const void* Z, eogp_dtype z_dtype, int64_t ldz, int64_t N, int64_t m,
+                             const void* P, eogp_dtype p_dtype, int64_t ldp, int64_t k, float* X,
+                             int64_t ldx, eogp_prec prec, void* ws, size_t ws_bytes, void* stream) {
   if (N < 0 || m < 1 || k < 1) return fail(EOGP_ERR_INVALID, "pca_project: bad sizes");
   if (k > m) return fail(EOGP_ERR_INVALID, "pca_project: need k <= m");
   if (prec != EOGP_PREC_FAST && prec != EOGP_PREC_ACCURATE)
@@ -261,10 +264,16 @@ eogp_status eogp_pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, 
   if (ldz < m || ldp < m || ldx < k) return fail(EOGP_ERR_INVALID, "pca_project: leading dimension too small");
   if (p_dtype != EOGP_F32 && p_dtype != EOGP_BF16 && p_dtype != EOGP_F16)
     return fail(EOGP_ERR_INVALID, "pca_project: bad P dtype");
+  if (z_dtype != EOGP_F32 && z_dtype != EOGP_F16 && z_dtype != EOGP_BF16)
+    return fail(EOGP_ERR_INVALID, "pca_project: bad Z dtype");
+  if (z_dtype != EOGP_F32 && z_dtype != p_dtype)
+    return fail(EOGP_ERR_UNSUPPORTED, "pca_project: 16-bit Z needs P of the same type");
+  if (z_dtype != EOGP_F32 && N > 0 && (ldz % 8 || (uintptr_t)Z % 16))
+    return fail(EOGP_ERR_UNSUPPORTED, "pca_project: 16-bit Z rows must start on 16-byte boundaries");
   if (ws_bytes < pca_split_copy_bytes(m, k, p_dtype) || (p_dtype == EOGP_F32 && !ws))
     return fail(EOGP_ERR_WORKSPACE, "pca_project: workspace too small for fp32 P");
-  return pca_project(Z, ldz, N, m, P, p_dtype, ldp, k, X, ldx, prec == EOGP_PREC_ACCURATE, ws,
-                     ws_bytes, S(stream));
+  return pca_project(Z, z_dtype, ldz, N, m, P, p_dtype, ldp, k, X, ldx,
+                     prec == EOGP_PREC_ACCURATE, ws, ws_bytes, S(stream));
 }
 
 eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t* codes,

@@ -95,9 +95,9 @@ size_t pca_ws(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype) {
          align256(gemm_partial_bytes(N, k, kPcaMaxSplits));
 }
 
-eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const void* P,
-                        eogp_dtype p_dtype, int64_t ldp, int64_t k, float* X, int64_t ldx,
-                        bool accurate, void* ws, size_t ws_bytes, hipStream_t s) {
+eogp_status pca_project(const void* Z, eogp_dtype z_dtype, int64_t ldz, int64_t N, int64_t m,
+                        const void* P, eogp_dtype p_dtype, int64_t ldp, int64_t k, float* X,
+                        int64_t ldx, bool accurate, void* ws, size_t ws_bytes, hipStream_t s) {
   if (N == 0 || k == 0) return EOGP_OK;
   GemmArgs g;
   g.A = Z;
@@ -122,7 +122,7 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
     g.max_splits = (int)std::min<int64_t>(
         kPcaMaxSplits, (int64_t)((ws_bytes - copy) / gemm_partial_bytes(N, k, 1)));
   }
-  if (p_dtype == EOGP_F32) {
+  if (p_dtype == EOGP_F32) {   // (Z is fp32 here)
     const int64_t ldo = round_up(m, 32), rows = round_up(k, 256);
     Carve cv(ws, ws_bytes);
     uint16_t* hi = cv.take<uint16_t>((size_t)rows * ldo);
@@ -141,6 +141,8 @@ eogp_status pca_project(const float* Z, int64_t ldz, int64_t N, int64_t m, const
   g.ldb = ldp;
   // A caller's P needs no bounds checks when its shape already matches the tiles.
   g.b_padded = (m % 32 == 0) && (k % 256 == 0);
+  // 16-bit Z has P's type (checked by the caller): one product on that type's MFMA
+  if (z_dtype != EOGP_F32) return gemm_nt(g, AType::B16, 1, 1, p_dtype == EOGP_F16, s);
   return gemm_nt(g, AType::F32, accurate ? 2 : 1, 1, p_dtype == EOGP_F16, s);
 }
 

@@ -23,6 +23,7 @@
 // GPT-2-shaped workload (4.1e-4 -> 5.1e-4, against 1e-3).
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "gemm.h"
 #include "plan.h"
@@ -229,10 +230,21 @@ __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__
 // Grid: (coordinate chunks of 2048, examples).
 constexpr int kZpermPer = 8;    // coordinates per thread (independent gathers in flight)
 
+// OT: float, or _Float16: the fp32 coordinate rounded to fp16 (nearest even).
+// The opaque step keeps the product and the conversion apart (a fused
+// multiply-convert would round the exact product once), so an fp16 Z equals
+// the fp32 Z converted afterwards.
+template <typename OT>
+__device__ __forceinline__ OT coord_out(float v) {
+  if constexpr (!std::is_same<OT, float>::value) asm("" : "+v"(v));
+  return (OT)v;
+}
+
+template <typename OT>
 __global__ __launch_bounds__(256) void k_zperm(const float* __restrict__ Zt, int64_t m,
                                                const int32_t* __restrict__ ent_pos,
                                                const float* __restrict__ w,
-                                               float* __restrict__ Z, int64_t ldz, int64_t ex0) {
+                                               OT* __restrict__ Z, int64_t ldz, int64_t ex0) {
   const int64_t i = ex0 + blockIdx.y;
   const float* src = Zt + i * m;
   const int64_t r0 = (int64_t)blockIdx.x * 256 * kZpermPer + threadIdx.x;
@@ -245,7 +257,7 @@ __global__ __launch_bounds__(256) void k_zperm(const float* __restrict__ Zt, int
 #pragma unroll
   for (int e = 0; e < kZpermPer; ++e) {
     const int64_t r = r0 + 256 * e;
-    if (r < m) Z[i * ldz + r] = w[r] * v[e];
+    if (r < m) Z[i * ldz + r] = coord_out<OT>(w[r] * v[e]);
   }
 }
 
@@ -254,10 +266,11 @@ __global__ __launch_bounds__(256) void k_zperm(const float* __restrict__ Zt, int
 // writes Z coalesced (the random reads stay on chip).
 constexpr int kZpermLdsMax = 32768;
 
+template <typename OT>
 __global__ __launch_bounds__(1024) void k_zperm_lds(const float* __restrict__ Zt, int m,
                                                     const int32_t* __restrict__ ent_pos,
                                                     const float* __restrict__ w,
-                                                    float* __restrict__ Z, int64_t ldz, int64_t ex0) {
+                                                    OT* __restrict__ Z, int64_t ldz, int64_t ex0) {
   extern __shared__ float L[];
   const int64_t i = ex0 + blockIdx.x;
   const float* src = Zt + i * (int64_t)m;
@@ -269,8 +282,8 @@ __global__ __launch_bounds__(1024) void k_zperm_lds(const float* __restrict__ Zt
     for (int c = tid; c < m; c += nt) L[c] = src[c];
   }
   __syncthreads();
-  float* dst = Z + i * ldz;
-  for (int r = tid; r < m; r += nt) dst[r] = w[r] * L[ent_pos[r]];
+  OT* dst = Z + i * ldz;
+  for (int r = tid; r < m; r += nt) dst[r] = coord_out<OT>(w[r] * L[ent_pos[r]]);
 }
 
 struct Work {
@@ -406,8 +419,8 @@ Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
 
 eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
                           int64_t ld_grads, bool bf16_in,
-                          const uint8_t* mask, int64_t N, int64_t T, float* Z, int64_t ldz,
-                          int prec, void* ws, size_t ws_bytes, hipStream_t s) {
+                          const uint8_t* mask, int64_t N, int64_t T, void* Z, bool z16,
+                          int64_t ldz, int prec, void* ws, size_t ws_bytes, hipStream_t s) {
   if (ws_bytes < work_bytes(p, N, T)) return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
   Carve cv(ws, ws_bytes);
   Work w = carve_work(p, N, T, cv);
@@ -422,7 +435,8 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   // 3. retained products, half-whitened, in canonical order
   const float out_scale = f16 ? std::ldexp(1.f, -(p->e_acts + p->e_grads)) : 1.f;
   if (p->m <= kZpermLdsMax) {
-    const eogp_status st_lds = ensure_dynamic_lds((const void*)k_zperm_lds, (int)(sizeof(float) * kZpermLdsMax));
+    const void* fn = z16 ? (const void*)k_zperm_lds<_Float16> : (const void*)k_zperm_lds<float>;
+    const eogp_status st_lds = ensure_dynamic_lds(fn, (int)(sizeof(float) * kZpermLdsMax));
     if (st_lds != EOGP_OK) return st_lds;
   }
   // examples per launch: the 2-D grid's y limit, and the 1-D grid of the fp16
@@ -450,12 +464,20 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
                          w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,
                          p->ent_loc, out_scale, w.Zt, p->m, ex0);
     }
-    if (p->m <= kZpermLdsMax) {
-      hipLaunchKernelGGL(k_zperm_lds, dim3((unsigned)nex), dim3(1024), (size_t)p->m * 4, s, w.Zt,
-                         (int)p->m, p->ent_pos, p->ret_w, Z, ldz, ex0);
+    const dim3 gz((unsigned)ceil_div(p->m, 256 * kZpermPer), (unsigned)nex);
+    if (p->m <= kZpermLdsMax && z16) {
+      hipLaunchKernelGGL(k_zperm_lds<_Float16>, dim3((unsigned)nex), dim3(1024), (size_t)p->m * 4,
+                         s, w.Zt, (int)p->m, p->ent_pos, p->ret_w, static_cast<_Float16*>(Z), ldz,
+                         ex0);
+    } else if (p->m <= kZpermLdsMax) {
+      hipLaunchKernelGGL(k_zperm_lds<float>, dim3((unsigned)nex), dim3(1024), (size_t)p->m * 4, s,
+                         w.Zt, (int)p->m, p->ent_pos, p->ret_w, static_cast<float*>(Z), ldz, ex0);
+    } else if (z16) {
+      hipLaunchKernelGGL(k_zperm<_Float16>, gz, dim3(256), 0, s, w.Zt, p->m, p->ent_pos,
+                         p->ret_w, static_cast<_Float16*>(Z), ldz, ex0);
     } else {
-      hipLaunchKernelGGL(k_zperm, dim3((unsigned)ceil_div(p->m, 256 * kZpermPer), (unsigned)nex),
-                         dim3(256), 0, s, w.Zt, p->m, p->ent_pos, p->ret_w, Z, ldz, ex0);
+      hipLaunchKernelGGL(k_zperm<float>, gz, dim3(256), 0, s, w.Zt, p->m, p->ent_pos, p->ret_w,
+                         static_cast<float*>(Z), ldz, ex0);
     }
     EOGP_LAUNCH_CHECK("retained products");
   }

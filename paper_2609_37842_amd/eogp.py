@@ -74,14 +74,14 @@ def load(path: str | None = None):
         "eogp_plan_set_input_exponents": (c_i32, [c_vp, c_i32, c_i32]),
         "eogp_rotate_retain_workspace_size": (c_sz, [c_vp, c_i64, c_i64]),
         "eogp_rotate_retain_planned": (c_i32, [c_vp, c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64,
-                                               c_i64, c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
+                                               c_i64, c_vp, c_i32, c_i64, c_i32, c_vp, c_sz, c_vp]),
         "eogp_rotate_retain_oneshot_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64, c_i64]),
         "eogp_rotate_retain": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64, c_i64,
                                        c_i64, c_vp, c_vp, c_vp, ctypes.c_double, c_i64, c_vp, c_i64,
                                        c_i32, c_vp, c_sz, c_vp]),
         "eogp_pca_project_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i32, c_i32]),
-        "eogp_pca_project": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i32, c_i64, c_i64, c_vp,
-                                     c_i64, c_i32, c_vp, c_sz, c_vp]),
+        "eogp_pca_project": (c_i32, [c_vp, c_i32, c_i64, c_i64, c_i64, c_vp, c_i32, c_i64, c_i64,
+                                     c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
         "eogp_sign_pack": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp]),
         "eogp_ekfac_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64]),
         "eogp_ekfac_eigenvalues": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64,
@@ -234,13 +234,15 @@ def eogp_rotate_retain_planned(plan: eogp_plan, acts, out_grads, token_mask=None
         raise ValueError("token_mask must be contiguous uint8 [N, T]")
     if Z is None:
         Z = torch.empty((N, plan.m), dtype=torch.float32, device=acts.device)
-    if Z.dtype != torch.float32 or Z.dim() != 2 or Z.stride(1) != 1 or Z.shape[0] != N:
-        raise ValueError("Z must be float32 [N, >= m] with unit column stride")
+    if (Z.dtype not in (torch.float32, torch.float16) or Z.dim() != 2 or Z.stride(1) != 1
+            or Z.shape[0] != N):
+        raise ValueError("Z must be float32 or float16 [N, >= m] with unit column stride")
     need = eogp_rotate_retain_workspace_size(plan, N, T)
     ws, wsb = _workspace(need, acts.device, ws)
     _check(L.eogp_rotate_retain_planned(plan._h, _ptr(acts), ld_a, _ptr(out_grads), ld_g,
                                         _acts_dtype(acts, out_grads), _ptr(token_mask), N, T,
-                                        _ptr(Z), Z.stride(0), prec, _ptr(ws), wsb, _stream(stream)))
+                                        _ptr(Z), _DTYPE_CODE[Z.dtype], Z.stride(0), prec, _ptr(ws),
+                                        wsb, _stream(stream)))
     return Z
 
 
@@ -273,22 +275,24 @@ def eogp_pca_project_workspace_size(N: int, m: int, k: int, p_dtype: int, prec: 
 
 def eogp_pca_project(Z, Pt, X=None, prec=PREC_FAST, ws=None, stream=None):
     """X [N, k] = Z [N, m] @ P, with P given as Pt [k, m] (each direction
-    contiguous, i.e. P column-major) in float16, bfloat16 or float32."""
+    contiguous, i.e. P column-major) in float16, bfloat16 or float32; Z in
+    float32, or in P's own 16-bit type."""
     L = load()
     _need_cuda(Z, Pt, X)
     N, m = Z.shape
     k, m2 = Pt.shape
     if m2 != m or Pt.stride(1) != 1 or Z.stride(1) != 1:
         raise ValueError("Pt must be [k, m] with unit column stride; Z [N, m]")
-    if Z.dtype != torch.float32:
-        raise ValueError("Z must be float32")
+    if Z.dtype not in (torch.float32, torch.float16, torch.bfloat16):
+        raise ValueError("Z must be float32, float16 or bfloat16")
     if X is None:
         X = torch.empty((N, k), dtype=torch.float32, device=Z.device)
     pd = _DTYPE_CODE[Pt.dtype]
     need = int(L.eogp_pca_project_workspace_size(N, m, k, pd, prec))
     ws, wsb = _workspace(need, Z.device, ws)
-    _check(L.eogp_pca_project(_ptr(Z), Z.stride(0), N, m, _ptr(Pt), pd, Pt.stride(0), k, _ptr(X),
-                              X.stride(0), prec, _ptr(ws), wsb, _stream(stream)))
+    _check(L.eogp_pca_project(_ptr(Z), _DTYPE_CODE[Z.dtype], Z.stride(0), N, m, _ptr(Pt), pd,
+                              Pt.stride(0), k, _ptr(X), X.stride(0), prec, _ptr(ws), wsb,
+                              _stream(stream)))
     return X
 
 

@@ -60,8 +60,12 @@ def test_encode_and_score_argument_validation_without_device():
     assert L.eogp_sign_pack(fake, 8, 2, 16, fake, 2, fake, 1, None) == -1
     assert L.eogp_sign_pack(fake, 16, 2, 16, fake, 1, fake, 1, None) == -1
     # pca: k > m, ld too small
-    assert L.eogp_pca_project(fake, 8, 2, 8, fake, 2, 8, 9, fake, 9, 0, None, 0, None) == -1
-    assert L.eogp_pca_project(fake, 4, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -1
+    assert L.eogp_pca_project(fake, 0, 8, 2, 8, fake, 2, 8, 9, fake, 9, 0, None, 0, None) == -1
+    assert L.eogp_pca_project(fake, 0, 4, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -1
+    # 16-bit Z must have P's type and 16-byte rows; unknown Z dtype
+    assert L.eogp_pca_project(fake, 1, 8, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -2
+    assert L.eogp_pca_project(fake, 2, 12, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -2
+    assert L.eogp_pca_project(fake, 7, 8, 2, 8, fake, 2, 8, 4, fake, 4, 0, None, 0, None) == -1
     # ekfac: bad sizes, NULL bases, bad precision, exponent out of range, small workspace
     assert L.eogp_ekfac_eigenvalues(fake, 0, fake, 0, 0, None, 2, 3, 0, 4, fake, fake, 1, 0, 0,
                                     fake, 0, fake, 1 << 30, None) == -1

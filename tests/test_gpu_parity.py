@@ -267,6 +267,33 @@ def test_rotate_retain_bf16_inputs_fast_and_accurate():
     plan.close()
 
 
+def test_fp16_coordinates_feed_the_pca_unchanged():
+    """fp16 first-stage coordinates are the fp32 ones rounded once (nearest
+    even); the PCA projection of a 16-bit Z with a P of the same type equals,
+    bit for bit, the projection of the fp32 Z (which is rounded to P's type as
+    it is staged); mismatched 16-bit types are refused."""
+    say("[first stage] fp16 Z")
+    N, T, d_in, d_out, m, k = 40, 48, 96, 80, 1000, 200
+    a, ds, mask, QA, QS, lam = random_problem(31, N, T, d_in, d_out, m, lens_lo=5)
+    plan = E.eogp_plan_create(d(lam), 1e-3, m, d(QA), d(QS))
+    for prec in (E.PREC_F16, E.PREC_ACCURATE, E.PREC_FAST):
+        Z32 = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask), prec=prec)
+        Z16 = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask), prec=prec,
+                                           Z=torch.empty((N, m), dtype=torch.float16, device=DEV))
+        torch.cuda.synchronize()
+        assert torch.equal(Z16, Z32.half())
+    plan.close()
+    g = np.random.default_rng(32)
+    Pt = torch.from_numpy(np.ascontiguousarray(S.haar_orthogonal(g, m)[:, :k].T)).to(DEV)
+    for pt in (Pt.half(), Pt.bfloat16()):
+        X32 = E.eogp_pca_project(Z32, pt, prec=E.PREC_FAST)
+        X16 = E.eogp_pca_project(Z32.to(pt.dtype), pt, prec=E.PREC_FAST)
+        torch.cuda.synchronize()
+        assert torch.equal(X16, X32)
+    with pytest.raises(Exception):
+        E.eogp_pca_project(Z16, Pt.bfloat16(), prec=E.PREC_FAST)
+
+
 def test_rotate_retain_no_mask_and_ldz():
     N, T, d_in, d_out, m = 3, 20, 40, 50, 100
     a, ds, mask, QA, QS, lam = random_problem(12, N, T, d_in, d_out, m, nan_masked=False)
