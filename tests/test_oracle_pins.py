@@ -209,6 +209,72 @@ def test_ekfac_eigenvalues_parseval_identity_basis_and_symmetries():
     assert np.allclose(lam_p, lam[np.ix_(ps, pa)], rtol=1e-12, atol=0)
 
 
+def test_kfac_factors_loop_sum_over_valid_tokens():
+    """K-FAC factors (Section 2.2, eq. kfac_factorization; Appendix C.2: factor
+    statistics averaged over non-padding tokens) against outer products summed
+    token by token in pure Python and divided by the number of valid tokens.
+    Masked tokens hold NaN, so reading one poisons the result; the valid count
+    (11) differs from N*T (15) and from the per-example mean, so a wrong
+    normaliser fails too."""
+    g = np.random.default_rng(91)
+    N, T, d_in, d_out = 3, 5, 4, 3
+    a = g.standard_normal((N, T, d_in))
+    ds = g.standard_normal((N, T, d_out))
+    mask = np.array([[1, 1, 1, 0, 0], [1, 1, 1, 1, 1], [0, 1, 1, 1, 0]], dtype=np.uint8)
+    a[mask == 0] = np.nan
+    ds[mask == 0] = np.nan
+    n_valid = int(mask.sum())
+    assert n_valid == 11
+    A_ref = [[0.0] * d_in for _ in range(d_in)]
+    S_ref = [[0.0] * d_out for _ in range(d_out)]
+    for i in range(N):
+        for t in range(T):
+            if not mask[i, t]:
+                continue
+            for p in range(d_in):
+                for q in range(d_in):
+                    A_ref[p][q] += float(a[i, t, p]) * float(a[i, t, q])
+            for p in range(d_out):
+                for q in range(d_out):
+                    S_ref[p][q] += float(ds[i, t, p]) * float(ds[i, t, q])
+    A, Sf = O.kfac_factors(a, ds, mask)
+    assert np.all(np.isfinite(A)) and np.all(np.isfinite(Sf))
+    assert np.allclose(A, np.array(A_ref) / n_valid, rtol=1e-13, atol=0)
+    assert np.allclose(Sf, np.array(S_ref) / n_valid, rtol=1e-13, atol=0)
+
+
+def test_kfac_factors_closed_form_with_basis_vector_tokens():
+    """Closed form: when every valid activation token is a standard basis
+    vector e_c and every output-gradient token is 2 e_c', the factors are
+    diagonal with entries count_c / n_valid and 4 count_c' / n_valid."""
+    N, T, d = 2, 6, 3
+    a = np.full((N, T, d), np.nan)
+    ds = np.full((N, T, d), np.nan)
+    mask = np.zeros((N, T), dtype=np.uint8)
+    cols = {(0, 0): 0, (0, 1): 0, (0, 3): 2, (1, 0): 1, (1, 2): 0, (1, 5): 2}
+    for (i, t), c in cols.items():
+        mask[i, t] = 1
+        a[i, t] = np.eye(d)[c]
+        ds[i, t] = 2.0 * np.eye(d)[(c + 1) % d]
+    A, Sf = O.kfac_factors(a, ds, mask)
+    counts = np.bincount(list(cols.values()), minlength=d).astype(np.float64)
+    assert np.array_equal(A, np.diag(counts / 6.0))
+    assert np.array_equal(Sf, np.diag(4.0 * np.roll(counts, 1) / 6.0))
+
+
+def test_relative_damping_hand_computed():
+    """Appendix C.2 (eq. app_module_damping): lambda_u = 0.1 tr(Lambda_u) / d_u
+    over the module's full set of corrected eigenvalues. Hand-computed:
+    Lambda = [[1, 2, 3], [4, 5, 9]] has trace of the diagonal matrix 24 over
+    d_u = 6 parameters, so lambda_u = 0.4. The rule is linear in Lambda and
+    depends only on the multiset of eigenvalues (not their layout)."""
+    lam = np.array([[1.0, 2.0, 3.0], [4.0, 5.0, 9.0]])
+    assert O.relative_damping(lam) == pytest.approx(0.4, rel=1e-15)
+    assert O.relative_damping(7.0 * lam) == pytest.approx(2.8, rel=1e-15)
+    assert O.relative_damping(lam.T) == pytest.approx(0.4, rel=1e-15)
+    assert O.relative_damping(np.full((5, 7), 3.0)) == pytest.approx(0.3, rel=1e-15)
+
+
 def test_kfac_eigenbasis_diagonalises_factors(tiny_fit):
     f = tiny_fit["fit"]
     for F, Q in ((f["A"], f["Q_A"]), (f["S"], f["Q_S"])):
