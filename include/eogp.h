@@ -19,8 +19,10 @@
  *   - Arrays are row-major and contiguous unless a leading dimension ("ld",
  *     in elements) or a row stride is given.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream). Calls
- *     only enqueue work on it and return, except eogp_plan_create and the
- *     one-shot eogp_rotate_retain, which synchronise `stream` once.
+ *     only enqueue work on it and return, except eogp_plan_create, the
+ *     one-shot eogp_rotate_retain and eogp_pca_fit, which synchronise `stream`
+ *     once. Host arrays passed to an enqueuing call (such as k_per_module)
+ *     are read before the call returns and may be released at once.
  *   - Argument errors return EOGP_ERR_INVALID before anything is enqueued;
  *     EOGP_ERR_UNSUPPORTED marks a valid but unimplemented dtype/shape mix;
  *     EOGP_ERR_DEVICE a HIP launch or runtime error; EOGP_ERR_WORKSPACE a
@@ -60,17 +62,18 @@ typedef enum { EOGP_F32 = 0, EOGP_BF16 = 1, EOGP_F16 = 2 } eogp_dtype;
 typedef enum { EOGP_PREC_FAST = 0, EOGP_PREC_ACCURATE = 1, EOGP_PREC_F16 = 2 } eogp_prec;
 
 /* ------------------------------------------------------------------------
- * Fitting shared projections: retained-axis selection (Algorithm 1, first
- * block, "select Q_{u,m}, Lambda_{u,m} using the m_u largest corrected
- * eigenvalues"; Section 3.2 first stage and eq. sigma_ekfac, which makes the
- * m largest corrected eigenvalues the top-m PCA axes of Sigma_proxy).
+ * Fitting shared projections: retained-axis selection (Algorithm 1, fitting
+ * block: the axes with the m_u largest corrected eigenvalues are kept;
+ * Section 3.2 first stage and eq. sigma_ekfac, which makes the m largest
+ * corrected eigenvalues the top-m PCA axes of Sigma_proxy).
  *
  * A plan holds, for one module, the m retained axes in canonical order
  * (Lambda descending, then flat index j*d_in + k ascending), their
  * half-whitening weights (Lambda_r + lambda)^-1/2 (eq. first_stage), and the
  * eigenvector columns of Q_A and Q_S those axes use, gathered so the first
  * stage runs as dense contractions without forming Q_m (eq.
- * app_projection_maps, "Kronecker factors and retained-coordinate indices").
+ * app_projection_maps: the map is stored as its two Kronecker factors plus
+ * the indices of the kept coordinates).
  *
  *   eigvals  [d_out, d_in] fp32: corrected eigenvalue Lambda[j, k] of the
  *            axis Q_A[:, k] (x) Q_S[:, j] (eq. ekfac_eigendecompose).
@@ -175,8 +178,9 @@ eogp_status eogp_rotate_retain(const void* acts, int64_t ld_acts, const void* ou
                                eogp_prec prec, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * Second stage (eq. second_stage; appendix "Implementation": one correction
- * matrix applied to a whole batch of cached first-stage coordinates):
+ * Second stage (eq. second_stage; Appendix E.3, implementation and runtime:
+ * one correction matrix applied to a whole batch of cached first-stage
+ * coordinates):
  *   X[i, c] = sum_r Z[i, r] P[r, c],  i.e. x_i = P^T z_i.
  *
  *   Z   [N, ldz] in `z_dtype` (first m columns used): EOGP_F32 with any P, or
@@ -203,8 +207,8 @@ eogp_status eogp_pca_project(const void* Z, eogp_dtype z_dtype, int64_t ldz, int
                              size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * One-bit encoding (eq. onebit; Algorithm 1, "store packed binary signs and
- * s = FP16(||x||_1 / k)"; payload layout of eq. app_payload):
+ * One-bit encoding (eq. onebit; Algorithm 1, storing block: packed sign bits
+ * plus an fp16 scale ||x||_1 / k; payload layout of eq. app_payload):
  *   bit c of row i = (X[i, c] >= 0)  (so -0.0 -> 1, NaN -> 0), stored in byte
  *   c >> 3, bit c & 7 of codes + i*code_row_stride (ceil(k/8) bytes written);
  *   scales[i*scale_stride] = fp16 bits of ||X[i, :k]||_1 / k, summed in fp64 and
@@ -217,7 +221,7 @@ eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k,
 
 /* ------------------------------------------------------------------------
  * Scoring (eq. onebit_influence, eq. app_stored_influence; Algorithm 1,
- * "scoring a query") with a per-query top-k:
+ * query block) with a per-query top-k:
  *   score(q, i) = sum_{u = 0..U-1, ascending} s_{i,u} <y_{q,u}, b_{i,u}>,
  * b in {-1, +1}. Each query module vector y_{q,u} is taken in fixed point:
  * f = 14 - e for max_c |y_c| = mu 2^e (mu in [0.5, 1)), y_int = rint(y 2^f)
@@ -238,8 +242,13 @@ eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k,
  *   full_scores  [Q, N] fp32, or NULL to skip writing every score.
  *   topk         1..256.
  *   ws           eogp_score_topk_workspace_size(N, Q, U, k_per_module, topk) bytes.
+ *                With several modules it includes the exact per-(module,
+ *                query, row) integer dots of one 16-query pass, U*16*N*4
+ *                bytes (8 when some k_u > 2^16), which a second kernel
+ *                turns into fp64 terms summed in module order.
  * Requirements: code_row_stride a multiple of 8 and codes 8-byte aligned;
- * Y finite. The per-module table is copied to the device from host memory.
+ * Y finite. k_per_module is read on the host during the call (the module
+ * table travels in kernel arguments); the call only enqueues work.
  * ------------------------------------------------------------------------ */
 size_t eogp_score_topk_workspace_size(int64_t N, int64_t Q, int32_t U,
                                       const int64_t* k_per_module, int32_t topk);

@@ -89,14 +89,15 @@ __device__ __forceinline__ bool before(uint64_t ka, uint32_t ia, uint64_t kb, ui
 
 // ---- query preparation --------------------------------------------------------
 // grid (16 * groups, U): per (query, module) the exponent f and the sum of
-// y_int, stored [group][U][16]; queries past Q get f = 0 and sum 0.
+// y_int, stored [group][U][16]; queries past Q get f = 0 and sum 0. The sum is
+// carried in 64 bits: |y_int| <= 2^14 and k_u <= 2^22 bound it by 2^36.
 __global__ __launch_bounds__(256) void k_query_stats(const float* __restrict__ Y, int64_t ldy,
                                                      int64_t Q, int U,
                                                      const ModInfo* __restrict__ mods,
                                                      int32_t* __restrict__ fq,
-                                                     int32_t* __restrict__ ysum) {
+                                                     int64_t* __restrict__ ysum) {
   __shared__ float smax[4];
-  __shared__ int ssum[4];
+  __shared__ int64_t ssum[4];
   const int64_t q = blockIdx.x;
   const int u = blockIdx.y;
   const int64_t o = ((q / QB) * U + u) * QB + (q % QB);
@@ -121,9 +122,9 @@ __global__ __launch_bounds__(256) void k_query_stats(const float* __restrict__ Y
     (void)frexpf(mx, &e);
     f = 14 - e;
   }
-  int s = 0;
+  int64_t s = 0;
   if (mx > 0.f)
-    for (int c = threadIdx.x; c < md.k; c += 256) s += (int)rintf(ldexpf(y[c], f));
+    for (int c = threadIdx.x; c < md.k; c += 256) s += (int64_t)rintf(ldexpf(y[c], f));
   for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
   if ((threadIdx.x & 63) == 0) ssum[threadIdx.x >> 6] = s;
   __syncthreads();
@@ -131,6 +132,19 @@ __global__ __launch_bounds__(256) void k_query_stats(const float* __restrict__ Y
     fq[o] = f;
     ysum[o] = ssum[0] + ssum[1] + ssum[2] + ssum[3];
   }
+}
+
+// Writes entries first .. first + count - 1 of the module table. The table
+// travels in the kernel arguments (copied when the launch is enqueued), so
+// the call needs no host synchronisation and the host's copy may go at once.
+constexpr int MOD_CHUNK = 64;
+struct ModChunk {
+  ModInfo m[MOD_CHUNK];
+  int32_t first, count;
+};
+__global__ void k_mod_table(ModChunk c, ModInfo* __restrict__ mods) {
+  const int i = threadIdx.x;
+  if (i < c.count) mods[c.first + i] = c.m[i];
 }
 
 // One thread per plane byte, laid out [group][step][MFMA f][lane][j] with
@@ -225,6 +239,8 @@ __device__ void prune(Cand<CAP>& cd, int n, int topk) {
   __syncthreads();
 }
 
+constexpr int MAX_RNG = 64;   // module ranges of the multi-module pass
+
 struct ScoreArgs {
   const uint8_t* codes;
   int64_t cstride;
@@ -236,12 +252,17 @@ struct ScoreArgs {
   int n_steps;
   int64_t grp;
   const int32_t* fq;     // [groups][U][16]
-  const int32_t* ysum;   // [groups][U][16]
+  const int64_t* ysum;   // [groups][U][16]
   int64_t Q;
   int topk;
   float* full;
   uint64_t* ckey;   // [grid][QB][topk]
   uint32_t* cidx;
+  // multi-module pass: module ranges (range r = modules rng[r] .. rng[r+1]-1)
+  // and the per-(module, query, row) integer dots it writes, [U][QB][N]
+  int n_rng;
+  int32_t rng[MAX_RNG + 1];
+  void* part;
 };
 
 // Calls f(integral_constant<I>) for I = 0 .. sizeof...(I) - 1 in order.
@@ -256,47 +277,73 @@ struct Cursor {
 };
 
 // NCLS: accumulator classes of the bit expansion (1, 2 or 4). D: steps
-// requested ahead. MULTI: several modules, whose fp64 terms are summed in
-// module order as each ends; else one module, whose term is formed after its
-// last step. CAP: candidate slots per query. SB: bytes per row and step. RT:
-// 32-row tiles per wave (each plane fragment read from LDS feeds RT MFMAs).
-template <int NCLS, int D, bool MULTI, int CAP, int SB, int RT>
+// requested ahead. MODE 0: one module; its fp64 term is formed after the last
+// step and the rows are offered to the per-query candidate lists. MODE 1 / 2:
+// several modules; a work unit is (512-row block, range of modules), and at
+// the end of each module the exact dot <y_int, 2b - 1> of every (row, query)
+// is written to `part` as int32 (MODE 1, every k_u <= 2^16) or int64 (MODE 2);
+// k_score_fold then forms the fp64 terms and sums them in module order. CAP:
+// candidate slots per query (MODE 0). SB: bytes per row and step. RT: 32-row
+// tiles per wave (each plane fragment read from LDS feeds RT MFMAs).
+template <int NCLS, int D, int MODE, int CAP, int SB, int RT>
 __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
+  constexpr bool MULTI = MODE != 0;
   constexpr int ROWS = NW * RT * 32;   // rows per block
   static_assert(NCLS == 1 || NCLS == 2 || NCLS == 4, "bit-weight classes");
   static_assert(D >= 2 && D <= 8, "ring depth");
   using SS = StepShape<SB>;
   constexpr int NU = SS::NU, FR = SS::FR, PU = SS::PU, PV = SS::PV;
   __shared__ __attribute__((aligned(16))) uint4 sP[2][PU];
-  __shared__ Cand<CAP> cd;
+  __shared__ Cand<MULTI ? 1 : CAP> cd;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int r32 = lane & 31, hg = lane >> 5;
   const cptr<int32_t> cmods = (cptr<int32_t>)(a.mods);   // ModInfo fields, 4 per module
   const cptr<int32_t> cfq = (cptr<int32_t>)(a.fq);
-  const cptr<int32_t> cys = (cptr<int32_t>)(a.ysum);
-  if (tid < QB) {
-    cd.cnt[tid] = 0;
-    cd.thr[tid] = 0ull;
+  const cptr<int64_t> cys = (cptr<int64_t>)(a.ysum);
+  if (!MULTI) {
+    if (tid < QB) {
+      cd.cnt[tid] = 0;
+      cd.thr[tid] = 0ull;
+    }
+    if (tid == 0) cd.overflow = 0;
+    __syncthreads();
   }
-  if (tid == 0) cd.overflow = 0;
-  __syncthreads();
   const int64_t n_blocks = (a.N + ROWS - 1) / ROWS;
-  const int n = a.n_steps;
-  const uint4* pl_grp = a.planes + (int64_t)a.grp * n * PU;
   const uint32_t M1 = 0x01010101u;
 
+  // Work units. MODE 0: row blocks at a fixed stride. Multi-module: units
+  // (range, block) in range-major order, dealt to the XCDs in contiguous
+  // chunks (workgroup b runs on XCD b % 8), so the workgroups of one XCD share
+  // the plane fragments of few module ranges in their L2.
+  const int nrng = MULTI ? a.n_rng : 1;
+  const int64_t n_units = n_blocks * nrng;
+  const int G = gridDim.x, b = blockIdx.x;
+  const bool xq = MULTI && G >= kXcds && G % kXcds == 0;
+  const int nq = xq ? kXcds : 1, xcd = xq ? b % kXcds : 0;
+  const int64_t chunk = (n_units + nq - 1) / nq;
+  const int64_t q_end = std::min<int64_t>((int64_t)(xcd + 1) * chunk, n_units);
+  for (int64_t unit = (int64_t)xcd * chunk + b / nq; unit < q_end; unit += G / nq) {
+    const int rg = MULTI ? (int)(unit / n_blocks) : 0;
+    const int64_t blk = MULTI ? unit % n_blocks : unit;
+    const int u_lo = MULTI ? a.rng[rg] : 0;
+    const int u_hi = MULTI ? a.rng[rg + 1] : 1;
+    const int s_lo = MULTI ? cmods[4 * u_lo + 3] : 0;
+    const int s_hi = (MULTI && u_hi < a.U) ? cmods[4 * u_hi + 3] : a.n_steps;
+    const int n = s_hi - s_lo;
+    const uint4* pl_grp = a.planes + ((int64_t)a.grp * a.n_steps + s_lo) * PU;
+
   auto start = [&](Cursor& c) __attribute__((always_inline)) {
-    const int k = cmods[0];
-    c.u = 0;
+    const int k = cmods[4 * u_lo];
+    c.u = u_lo;
     c.sl = 0;
     c.nst = (k + 8 * SB - 1) / (8 * SB);
     c.kbytes = k >> 3;
-    c.boff = cmods[2];
+    c.boff = cmods[4 * u_lo + 2];
   };
   auto advance = [&](Cursor& c) __attribute__((always_inline)) {
     if (++c.sl == c.nst) {
       c.sl = 0;
-      if (++c.u < a.U) {
+      if (++c.u < u_hi) {
         const int k = cmods[4 * c.u];
         c.nst = (k + 8 * SB - 1) / (8 * SB);
         c.kbytes = k >> 3;
@@ -305,7 +352,6 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
     }
   };
 
-  for (int64_t blk = blockIdx.x; blk < n_blocks; blk += gridDim.x) {
     int64_t row[RT], rowc[RT];
     const uint8_t* rowp[RT];
 #pragma unroll
@@ -322,17 +368,12 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
       for (int w = 0; w < NCLS; ++w)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[rt][w][r] = 0;
-    double sc[RT][8];   // [tile][i]: query 8 (i / 4) + 4 (lane / 32) + i % 4 of the group
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) sc[rt][i] = 0.0;
+    double sc[MULTI ? 1 : RT][8];   // [tile][i]: query 8 (i / 4) + 4 (lane / 32) + i % 4 of the group
 
     // ring slot: [rt][0, NU) the lane's code words of tile rt, [RT][0, PV)
     // the thread's share of the step's plane fragments
     constexpr int RW = NU > PV ? NU : PV;
     uint4 ring[D][RT + 1][RW];
-    uint32_t scl[D][RT];   // several modules: the rows' scales for the slot's module
     uint32_t s16[RT];      // one module: the rows' scales, requested before the codes
     if (!MULTI) {
 #pragma unroll
@@ -383,10 +424,6 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
             ring[SL][rt][uc] = *reinterpret_cast<const uint4*>(p);
           }
       }
-      if (MULTI) {
-#pragma unroll
-        for (int rt = 0; rt < RT; ++rt) scl[SL][rt] = a.scales[rowc[rt] * a.U + min(cl.u, a.U - 1)];
-      }
     };
     // keeps the valid bytes of a partial step (branch-free selects)
     auto fixup = [&](auto slot_c) __attribute__((always_inline)) {
@@ -406,8 +443,9 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
         }
     };
 
-    // module term s * (2 n1 - sum y_int) * 2^-f, added in module order
-    auto fold = [&](int u, const uint32_t (&s16v)[RT]) __attribute__((always_inline)) {
+    // end of module u: the exact dot n = 2 n1 - sum y_int of every (row,
+    // query); one module: its term s * n * 2^-f; several: n to `part`
+    auto fold = [&](int u) __attribute__((always_inline)) {
       const int64_t mo = (a.grp * a.U + u) * QB;
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt) {
@@ -419,16 +457,23 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
           for (int w = 1; w < NCLS; ++w) v += acc[rt][w][r] >> w;
           H[r] = v;
         }
-        const double sv = (double)f16_bits_to_f32((uint16_t)s16v[rt]);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const int i0 = 8 * (i >> 2) + (i & 3);
-          const int f = hg ? cfq[mo + i0 + 4] : cfq[mo + i0];
-          const int ys = hg ? cys[mo + i0 + 4] : cys[mo + i0];
+          const int64_t ys = hg ? cys[mo + i0 + 4] : cys[mo + i0];
           const int64_t n1 = 256 * (int64_t)H[i] + (int64_t)H[i + 8];
           const int64_t nn = 2 * n1 - ys;
-          const double term = ldexp(sv * (double)nn, -f);
-          sc[rt][i] = MULTI ? sc[rt][i] + term : term;
+          if constexpr (MULTI) {
+            if (row[rt] < a.N) {
+              const int64_t o = ((int64_t)u * QB + i0 + 4 * hg) * a.N + row[rt];
+              if constexpr (MODE == 1) static_cast<int32_t*>(a.part)[o] = (int32_t)nn;
+              else static_cast<int64_t*>(a.part)[o] = nn;
+            }
+          } else {
+            const int f = hg ? cfq[mo + i0 + 4] : cfq[mo + i0];
+            const double sv = (double)f16_bits_to_f32((uint16_t)s16[rt]);
+            sc[rt][i] = ldexp(sv * (double)nn, -f);
+          }
         }
 #pragma unroll
         for (int w = 0; w < NCLS; ++w)
@@ -473,7 +518,7 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
         }
       }
       if (MULTI) {
-        if (cc.sl == cc.nst - 1) fold(cc.u, scl[SL]);
+        if (cc.sl == cc.nst - 1) fold(cc.u);
         advance(cc);
       }
       load_step(slot_c, s + D);
@@ -503,61 +548,164 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
       if (s0 + decltype(i_c)::value < n) step(i_c, s0 + decltype(i_c)::value);
     });
 
-    if (!MULTI) fold(0, s16);
+    if constexpr (!MULTI) {
+      fold(0);
 
-    // candidates of this block; a full list is pruned and the entries that
-    // did not fit are offered again (the loop condition is uniform). The
-    // opaque copy of the lane half keeps the list addresses from being
-    // computed once before the block loop and held through it.
-    int hq = hg;
-    asm volatile("" : "+v"(hq));
-    auto qsel = [&](int i) { return 8 * (i >> 2) + 4 * hq + (i & 3); };
-    uint32_t pend = 0;
-#pragma unroll
-    for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int64_t q = a.grp * QB + qsel(i);
-        if (row[rt] < a.N && q < a.Q) {
-          if (a.full) a.full[q * a.N + row[rt]] = (float)sc[rt][i];
-          pend |= 1u << (8 * rt + i);
-        }
-      }
-    for (;;) {
-#pragma unroll
+      // candidates of this block; a full list is pruned and the entries that
+      // did not fit are offered again (the loop condition is uniform). The
+      // opaque copy of the lane half keeps the list addresses from being
+      // computed once before the block loop and held through it.
+      int hq = hg;
+      asm volatile("" : "+v"(hq));
+      auto qsel = [&](int i) { return 8 * (i >> 2) + 4 * hq + (i & 3); };
+      uint32_t pend = 0;
+  #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
-#pragma unroll
+  #pragma unroll
         for (int i = 0; i < 8; ++i) {
-          const uint32_t bit = 1u << (8 * rt + i);
-          if (pend & bit) {
-            const int qn = qsel(i);
-            const uint64_t key = order_key(sc[rt][i]);
-            if (key < cd.thr[qn]) {
-              pend &= ~bit;
-            } else {
-              const int pos = atomicAdd(&cd.cnt[qn], 1);
-              if (pos < CAP) {
-                cd.key[qn][pos] = key;
-                cd.idx[qn][pos] = (uint32_t)row[rt];
+          const int64_t q = a.grp * QB + qsel(i);
+          if (row[rt] < a.N && q < a.Q) {
+            if (a.full) a.full[q * a.N + row[rt]] = (float)sc[rt][i];
+            pend |= 1u << (8 * rt + i);
+          }
+        }
+      for (;;) {
+  #pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+  #pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const uint32_t bit = 1u << (8 * rt + i);
+            if (pend & bit) {
+              const int qn = qsel(i);
+              const uint64_t key = order_key(sc[rt][i]);
+              if (key < cd.thr[qn]) {
                 pend &= ~bit;
               } else {
-                cd.overflow = 1;
+                const int pos = atomicAdd(&cd.cnt[qn], 1);
+                if (pos < CAP) {
+                  cd.key[qn][pos] = key;
+                  cd.idx[qn][pos] = (uint32_t)row[rt];
+                  pend &= ~bit;
+                } else {
+                  cd.overflow = 1;
+                }
               }
             }
           }
+        __syncthreads();
+        const int ov = cd.overflow;
+        __syncthreads();
+        if (!ov) break;
+        for (int qq = 0; qq < QB; ++qq)
+          if (cd.cnt[qq] >= CAP) prune<CAP, NTHR>(cd, qq, a.topk);
+        if (tid == 0) cd.overflow = 0;
+        __syncthreads();
+      }
+    }
+  }
+  if constexpr (!MULTI) {
+    for (int qq = 0; qq < QB; ++qq) prune<CAP, NTHR>(cd, qq, a.topk);
+    for (int i = tid; i < QB * a.topk; i += NTHR) {
+      const int qq = i / a.topk, e = i % a.topk;
+      const int64_t o = ((int64_t)blockIdx.x * QB + qq) * a.topk + e;
+      const bool have = e < cd.cnt[qq];
+      a.ckey[o] = have ? cd.key[qq][e] : 0ull;
+      a.cidx[o] = have ? cd.idx[qq][e] : 0xFFFFFFFFu;
+    }
+  }
+}
+
+// Multi-module scores from the exact per-module dots: one thread per stored
+// row, the 16 queries of the group in registers; for u = 0 .. U-1 in order,
+// score += s_{i,u} * n * 2^-f (each term exact in fp64), then the rows are
+// offered to the per-query candidate lists as in k_score. Workgroups walk
+// blocks of 256 rows at a fixed stride.
+struct FoldArgs {
+  const void* part;           // [U][QB][N] int32 or int64
+  const uint16_t* scales;     // [N][U] fp16 bits
+  int64_t N;
+  int U;
+  const int32_t* fq;          // [groups][U][16]
+  int64_t grp;
+  int64_t Q;
+  int topk;
+  float* full;
+  uint64_t* ckey;             // [grid][QB][topk]
+  uint32_t* cidx;
+};
+constexpr int FOLD_THR = 256;
+
+template <int CAP, bool N64>
+__global__ __launch_bounds__(FOLD_THR) void k_score_fold(FoldArgs a) {
+  __shared__ Cand<CAP> cd;
+  const int tid = threadIdx.x;
+  const cptr<int32_t> cfq = (cptr<int32_t>)(a.fq);
+  if (tid < QB) {
+    cd.cnt[tid] = 0;
+    cd.thr[tid] = 0ull;
+  }
+  if (tid == 0) cd.overflow = 0;
+  __syncthreads();
+  const int32_t* p32 = static_cast<const int32_t*>(a.part);
+  const int64_t* p64 = static_cast<const int64_t*>(a.part);
+  for (int64_t r0 = (int64_t)blockIdx.x * FOLD_THR; r0 < a.N; r0 += (int64_t)gridDim.x * FOLD_THR) {
+    const int64_t row = r0 + tid;
+    const bool ok = row < a.N;
+    const int64_t rowc = ok ? row : a.N - 1;
+    double sc[QB];
+#pragma unroll
+    for (int q = 0; q < QB; ++q) sc[q] = 0.0;
+    for (int u = 0; u < a.U; ++u) {
+      const double sv = (double)f16_bits_to_f32(a.scales[rowc * a.U + u]);
+      const int64_t mo = (a.grp * a.U + u) * QB;
+#pragma unroll
+      for (int q = 0; q < QB; ++q) {
+        const int64_t o = ((int64_t)u * QB + q) * a.N + rowc;
+        const int64_t nn = N64 ? p64[o] : (int64_t)p32[o];
+        sc[q] += ldexp(sv * (double)nn, -cfq[mo + q]);
+      }
+    }
+    uint32_t pend = 0;
+#pragma unroll
+    for (int q = 0; q < QB; ++q) {
+      const int64_t qg = a.grp * QB + q;
+      if (ok && qg < a.Q) {
+        if (a.full) a.full[qg * a.N + row] = (float)sc[q];
+        pend |= 1u << q;
+      }
+    }
+    for (;;) {
+#pragma unroll
+      for (int q = 0; q < QB; ++q) {
+        const uint32_t bit = 1u << q;
+        if (pend & bit) {
+          const uint64_t key = order_key(sc[q]);
+          if (key < cd.thr[q]) {
+            pend &= ~bit;
+          } else {
+            const int pos = atomicAdd(&cd.cnt[q], 1);
+            if (pos < CAP) {
+              cd.key[q][pos] = key;
+              cd.idx[q][pos] = (uint32_t)row;
+              pend &= ~bit;
+            } else {
+              cd.overflow = 1;
+            }
+          }
         }
+      }
       __syncthreads();
       const int ov = cd.overflow;
       __syncthreads();
       if (!ov) break;
       for (int qq = 0; qq < QB; ++qq)
-        if (cd.cnt[qq] >= CAP) prune<CAP, NTHR>(cd, qq, a.topk);
+        if (cd.cnt[qq] >= CAP) prune<CAP, FOLD_THR>(cd, qq, a.topk);
       if (tid == 0) cd.overflow = 0;
       __syncthreads();
     }
   }
-  for (int qq = 0; qq < QB; ++qq) prune<CAP, NTHR>(cd, qq, a.topk);
-  for (int i = tid; i < QB * a.topk; i += NTHR) {
+  for (int qq = 0; qq < QB; ++qq) prune<CAP, FOLD_THR>(cd, qq, a.topk);
+  for (int i = tid; i < QB * a.topk; i += FOLD_THR) {
     const int qq = i / a.topk, e = i % a.topk;
     const int64_t o = ((int64_t)blockIdx.x * QB + qq) * a.topk + e;
     const bool have = e < cd.cnt[qq];
@@ -627,46 +775,80 @@ struct Layout {
   int64_t n_steps = 0;   // steps over all modules
   int64_t n_groups = 0;
   int64_t grid = 0;      // workgroups of the scoring pass
+  int64_t fold_grid = 0; // workgroups of the multi-module fold (0: one module)
   int64_t step_bytes = 0;
-  size_t o_mods = 0, o_fq = 0, o_ys = 0, o_pl = 0, o_ck = 0, o_ci = 0, o_pad = 0, total = 0;
+  int n_rng = 1;         // module ranges of the multi-module pass
+  bool n64 = false;      // multi-module dots stored in 64 bits
+  size_t o_mods = 0, o_fq = 0, o_ys = 0, o_pl = 0, o_ck = 0, o_ci = 0, o_part = 0, o_pad = 0,
+         total = 0;
 };
 
 Layout layout(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t topk) {
   Layout L;
   const PassCfg c = pass_cfg(topk);
-  for (int u = 0; u < U; ++u) L.n_steps += (kmod[u] + 8 * c.sb - 1) / (8 * c.sb);
+  int64_t kmax = 0;
+  for (int u = 0; u < U; ++u) {
+    L.n_steps += (kmod[u] + 8 * c.sb - 1) / (8 * c.sb);
+    kmax = std::max<int64_t>(kmax, kmod[u]);
+  }
   L.n_groups = (Q + QB - 1) / QB;
   L.step_bytes = 256 * (int64_t)c.sb;
   const int64_t n_blocks = (N + NW * 32 * c.rt - 1) / (NW * 32 * c.rt);
-  L.grid = std::max<int64_t>(1, std::min<int64_t>(n_blocks, kCus));
+  int64_t lists = 0;
+  if (U == 1) {
+    L.grid = std::max<int64_t>(1, std::min<int64_t>(n_blocks, kCus));
+    lists = L.grid;
+  } else {
+    // about four units per CU when the row blocks alone are too few, each
+    // range at least one module; ranges are cut by step count
+    L.n_rng = (int)std::min<int64_t>({(int64_t)U, (int64_t)MAX_RNG,
+                                      std::max<int64_t>(1, ceil_div(4 * kCus, std::max<int64_t>(1, n_blocks)))});
+    const int64_t units = std::max<int64_t>(1, n_blocks * L.n_rng);
+    L.grid = std::min<int64_t>(units, kCus);
+    if (L.grid >= kXcds) L.grid = L.grid / kXcds * kXcds;
+    L.fold_grid = std::max<int64_t>(1, std::min<int64_t>(ceil_div(N, FOLD_THR), 2 * kCus));
+    lists = L.fold_grid;
+    L.n64 = kmax > (1 << 16);   // |n| <= k 2^14 fits 32 bits up to k = 2^16
+  }
   size_t b = 0;
   auto add = [&](size_t x) { size_t o = b; b = align256(b + x); return o; };
   L.o_mods = add(sizeof(ModInfo) * U);
   L.o_fq = add(4 * (size_t)L.n_groups * U * QB);
-  L.o_ys = add(4 * (size_t)L.n_groups * U * QB);
+  L.o_ys = add(8 * (size_t)L.n_groups * U * QB);
   L.o_pl = add((size_t)(L.n_groups * L.n_steps * L.step_bytes));
-  L.o_ck = add((size_t)L.grid * QB * topk * 8);
-  L.o_ci = add((size_t)L.grid * QB * topk * 4);
+  L.o_ck = add((size_t)lists * QB * topk * 8);
+  L.o_ci = add((size_t)lists * QB * topk * 4);
+  L.o_part = add(U > 1 ? (size_t)U * QB * (size_t)N * (L.n64 ? 8 : 4) : 0);
   L.o_pad = add(16);   // a store of fewer than 16 bytes is copied here (see score_topk)
   L.total = b;
   return L;
 }
 
-template <int NCLS, bool MULTI, int CAP>
+// Module ranges of the multi-module pass: n_rng consecutive ranges of
+// roughly equal step counts, each at least one module.
+void module_ranges(const std::vector<ModInfo>& hm, int64_t n_steps, int n_rng, int32_t* rng) {
+  const int U = (int)hm.size();
+  rng[0] = 0;
+  for (int r = 1; r < n_rng; ++r) {
+    const int64_t target = (n_steps * r + n_rng / 2) / n_rng;
+    const int v_max = U - (n_rng - r);     // leaves a module for each later range
+    int v = rng[r - 1] + 1;                // at least one module in range r - 1
+    while (v < v_max && hm[v].sbase < target) ++v;
+    rng[r] = v;
+  }
+  rng[n_rng] = U;
+}
+
+template <int MODE, int CAP>
 eogp_status launch_pass(const PassCfg& c, dim3 gd, const ScoreArgs& a, hipStream_t s) {
 #define EOGP_SCORE_CFG(SB, RT, D)                                                      \
   if (c.sb == SB && c.rt == RT && c.d == D) {                                          \
-    hipLaunchKernelGGL((k_score<NCLS, D, MULTI, CAP, SB, RT>), gd, dim3(NTHR), 0, s, a); \
+    hipLaunchKernelGGL((k_score<2, D, MODE, CAP, SB, RT>), gd, dim3(NTHR), 0, s, a);    \
     return EOGP_OK;                                                                    \
   }
   EOGP_SCORE_CFG(64, 2, 3)
 #undef EOGP_SCORE_CFG
   return fail(EOGP_ERR_UNSUPPORTED, "score_topk: no kernel for this pass configuration");
-}
-
-template <bool MULTI>
-eogp_status launch_pass(const PassCfg& c, dim3 gd, const ScoreArgs& a, hipStream_t s) {
-  return c.cap == 256 ? launch_pass<2, MULTI, 256>(c, gd, a, s) : launch_pass<2, MULTI, 512>(c, gd, a, s);
 }
 
 }  // namespace
@@ -687,7 +869,7 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
   char* base = static_cast<char*>(ws);
   ModInfo* mods = reinterpret_cast<ModInfo*>(base + L.o_mods);
   int32_t* fq = reinterpret_cast<int32_t*>(base + L.o_fq);
-  int32_t* ys = reinterpret_cast<int32_t*>(base + L.o_ys);
+  int64_t* ys = reinterpret_cast<int64_t*>(base + L.o_ys);
   int8_t* planes = reinterpret_cast<int8_t*>(base + L.o_pl);
   uint64_t* ck = reinterpret_cast<uint64_t*>(base + L.o_ck);
   uint32_t* ci = reinterpret_cast<uint32_t*>(base + L.o_ci);
@@ -716,9 +898,14 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     boff += kmod[u] / 8;
     sbase += (kmod[u] + 8 * cfg.sb - 1) / (8 * cfg.sb);
   }
-  // the table is small; copy it synchronously so the host vector may go
-  EOGP_HIP(hipMemcpyAsync(mods, hm.data(), sizeof(ModInfo) * U, hipMemcpyHostToDevice, s));
-  EOGP_HIP(hipStreamSynchronize(s));
+  for (int u0 = 0; u0 < U; u0 += MOD_CHUNK) {
+    ModChunk mc;
+    mc.first = u0;
+    mc.count = std::min(MOD_CHUNK, U - u0);
+    for (int i = 0; i < mc.count; ++i) mc.m[i] = hm[u0 + i];
+    hipLaunchKernelGGL(k_mod_table, dim3(1), dim3(MOD_CHUNK), 0, s, mc, mods);
+  }
+  EOGP_LAUNCH_CHECK("module table");
   timing::Scope tprep(EOGP_KT_SCORE_PREP, s);
   hipLaunchKernelGGL(k_query_stats, dim3((unsigned)(L.n_groups * QB), (unsigned)U), dim3(256), 0,
                      s, Y, ldy, Q, U, mods, fq, ys);
@@ -728,33 +915,65 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
   EOGP_LAUNCH_CHECK("query preparation");
   timing::end(tprep.slot, s);
   tprep.slot = -1;
+  ScoreArgs a;
+  a.codes = codes;
+  a.cstride = cstride;
+  a.scales = scales;
+  a.N = N;
+  a.U = U;
+  a.mods = mods;
+  a.planes = reinterpret_cast<const uint4*>(planes);
+  a.n_steps = (int)L.n_steps;
+  a.fq = fq;
+  a.ysum = ys;
+  a.Q = Q;
+  a.topk = topk;
+  a.full = full;
+  a.ckey = ck;
+  a.cidx = ci;
+  a.n_rng = L.n_rng;
+  a.part = base + L.o_part;
+  if (U > 1) module_ranges(hm, L.n_steps, L.n_rng, a.rng);
+  FoldArgs fa;
+  fa.part = a.part;
+  fa.scales = scales;
+  fa.N = N;
+  fa.U = U;
+  fa.fq = fq;
+  fa.Q = Q;
+  fa.topk = topk;
+  fa.full = full;
+  fa.ckey = ck;
+  fa.cidx = ci;
   for (int64_t grp = 0; grp < L.n_groups; ++grp) {
-    ScoreArgs a;
-    a.codes = codes;
-    a.cstride = cstride;
-    a.scales = scales;
-    a.N = N;
-    a.U = U;
-    a.mods = mods;
-    a.planes = reinterpret_cast<const uint4*>(planes);
-    a.n_steps = (int)L.n_steps;
     a.grp = grp;
-    a.fq = fq;
-    a.ysum = ys;
-    a.Q = Q;
-    a.topk = topk;
-    a.full = full;
-    a.ckey = ck;
-    a.cidx = ci;
+    fa.grp = grp;
     {
+      // one pass over the store: the streaming kernel, and for several
+      // modules the fold that adds their terms in order
       timing::Scope tp(EOGP_KT_SCORE_PASS, s);
       const dim3 gd((unsigned)L.grid);
-      const eogp_status st = U > 1 ? launch_pass<true>(cfg, gd, a, s)
-                                   : launch_pass<false>(cfg, gd, a, s);
+      eogp_status st;
+      if (U == 1) {
+        st = cfg.cap == 256 ? launch_pass<0, 256>(cfg, gd, a, s) : launch_pass<0, 512>(cfg, gd, a, s);
+      } else {
+        st = L.n64 ? launch_pass<2, 256>(cfg, gd, a, s) : launch_pass<1, 256>(cfg, gd, a, s);
+        if (st == EOGP_OK) {
+          const dim3 fg((unsigned)L.fold_grid), fb(FOLD_THR);
+          if (cfg.cap == 256) {
+            if (L.n64) hipLaunchKernelGGL((k_score_fold<256, true>), fg, fb, 0, s, fa);
+            else hipLaunchKernelGGL((k_score_fold<256, false>), fg, fb, 0, s, fa);
+          } else {
+            if (L.n64) hipLaunchKernelGGL((k_score_fold<512, true>), fg, fb, 0, s, fa);
+            else hipLaunchKernelGGL((k_score_fold<512, false>), fg, fb, 0, s, fa);
+          }
+        }
+      }
       if (st != EOGP_OK) return st;
     }
     timing::Scope tm(EOGP_KT_SCORE_MERGE, s);
-    hipLaunchKernelGGL(k_merge, dim3(QB), dim3(256), 0, s, ck, ci, (int)L.grid, grp, Q, topk,
+    const int lists = (int)(U == 1 ? L.grid : L.fold_grid);
+    hipLaunchKernelGGL(k_merge, dim3(QB), dim3(256), 0, s, ck, ci, lists, grp, Q, topk,
                        out_idx, out_score);
     EOGP_LAUNCH_CHECK("score pass");
   }

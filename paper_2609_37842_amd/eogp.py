@@ -404,13 +404,20 @@ def eogp_score_topk(codes, scales, k_per_module, Y, topk, full_scores=False, out
     """Per-query top-k (index int64 [Q, topk], score float32 [Q, topk]) and
     optionally every score (float32 [Q, N])."""
     L = load()
-    _need_cuda(codes, scales, Y)
-    N = codes.shape[0]
-    Q = Y.shape[0]
     U = len(k_per_module)
+    if codes.dtype != torch.uint8 or codes.dim() != 2 or (codes.shape[0] > 0 and codes.stride(1) != 1):
+        raise ValueError("codes must be uint8 [N, row bytes] with unit column stride")
+    N = codes.shape[0]
+    if scales.dtype not in (torch.int16, torch.float16):
+        raise ValueError("scales must hold fp16 bit patterns (int16 or float16)")
+    if not ((scales.dim() == 2 and tuple(scales.shape) == (N, U)) or
+            (scales.dim() == 1 and U == 1 and scales.shape[0] == N)) or not scales.is_contiguous():
+        raise ValueError("scales must be contiguous [N, U] (or [N] for one module)")
+    if Y.dtype != torch.float32 or Y.dim() != 2 or (Y.shape[0] > 0 and Y.stride(1) != 1):
+        raise ValueError("Y must be float32 [Q, sum k_u] with unit column stride")
+    _need_cuda(codes, scales, Y)
+    Q = Y.shape[0]
     ks = (c_i64 * U)(*[int(k) for k in k_per_module])
-    if scales.dtype not in (torch.int16, torch.float16) or scales.numel() != N * U:
-        raise ValueError("scales must be fp16 bits [N, U]")
     if out_idx is None:
         out_idx = torch.empty((Q, topk), dtype=torch.int64, device=Y.device)
     if out_score is None:

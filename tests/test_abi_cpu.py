@@ -132,3 +132,44 @@ def test_workspace_size_queries_are_consistent():
     f32 = L.eogp_pca_project_workspace_size(100, 512, 128, 0, 1)     # fp32 P: + split copy
     assert 0 < f16 < f32
     assert L.eogp_pca_project_workspace_size(1000, 512, 128, 2, 0) > f16
+
+
+def test_score_binding_rejects_bad_layouts():
+    """The Python binding checks dtypes and strides before anything reaches
+    the library: codes must be uint8 with unit column stride, scales
+    contiguous fp16 bit patterns [N, U], Y float32 with unit column stride."""
+    import pytest
+    import torch
+    codes = torch.zeros((4, 16), dtype=torch.uint8)
+    scales = torch.zeros((4, 2), dtype=torch.int16)
+    Y = torch.zeros((3, 128), dtype=torch.float32)
+    ks = [64, 64]
+    with pytest.raises(ValueError, match="codes"):
+        E.eogp_score_topk(codes.to(torch.int16), scales, ks, Y, 5)
+    with pytest.raises(ValueError, match="codes"):
+        E.eogp_score_topk(torch.zeros((16, 4), dtype=torch.uint8).t(), scales, ks, Y, 5)
+    with pytest.raises(ValueError, match="scales"):
+        E.eogp_score_topk(codes, scales.float(), ks, Y, 5)
+    with pytest.raises(ValueError, match="scales"):
+        E.eogp_score_topk(codes, torch.zeros((2, 4), dtype=torch.int16).t(), ks, Y, 5)
+    with pytest.raises(ValueError, match="scales"):
+        E.eogp_score_topk(codes, torch.zeros((4, 3), dtype=torch.int16), ks, Y, 5)
+    with pytest.raises(ValueError, match="Y"):
+        E.eogp_score_topk(codes, scales, ks, Y.half(), 5)
+    with pytest.raises(ValueError, match="Y"):
+        E.eogp_score_topk(codes, scales, ks, torch.zeros((128, 3)).t(), 5)
+    # well-formed host tensors reach the device check
+    with pytest.raises(ValueError, match="device"):
+        E.eogp_score_topk(codes, scales, ks, Y, 5)
+
+
+def test_multi_module_score_workspace_holds_the_exact_dots():
+    """With several modules the workspace carries one 16-query pass of
+    per-(module, query, row) integer dots: 4 bytes each while every k_u is at
+    most 2^16, 8 bytes beyond."""
+    N = 10000
+    one = E.eogp_score_topk_workspace_size(N, 16, [4096], 10)
+    two = E.eogp_score_topk_workspace_size(N, 16, [2048, 2048], 10)
+    assert two - one >= 2 * 16 * N * 4
+    wide = E.eogp_score_topk_workspace_size(N, 16, [1 << 17, 64], 10)
+    assert wide - E.eogp_score_topk_workspace_size(N, 16, [1 << 17], 10) >= 2 * 16 * N * 8

@@ -105,15 +105,35 @@ def first_stage_sampled(w, si, name, d_in, d_out, N, T, dtype, precs, examples, 
     return out, ref, art
 
 
-def test_gpt2_small_c_fc_full_step_shape():
-    """GPT-2-small-shaped c_fc (769 -> 3072) at 1,266 examples x 512 tokens,
-    fp32 inputs; fp16 and bf16x3 first stages, then PCA with the fp16 P,
-    sign bits and scales on three sampled examples."""
+SIGN_RECORD = {}
+
+
+def record_sign_mismatch(key, value):
+    """Keeps the measured sign-mismatch fractions and writes them to
+    gpurun_out/sign_mismatch_gpt2.json (a run record, not an input)."""
+    import json
+    import os
+    SIGN_RECORD[key] = value
+    out = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "gpurun_out")
+    os.makedirs(out, exist_ok=True)
+    with open(os.path.join(out, "sign_mismatch_gpt2.json"), "w") as f:
+        json.dump(SIGN_RECORD, f, indent=1, sort_keys=True)
+
+
+@pytest.mark.parametrize("si", [0, 1, 2, 3])   # c_attn, attn.c_proj, c_fc, mlp.c_proj
+def test_gpt2_small_full_step_shape(si):
+    """Each GPT-2-small-shaped linear at the bench's launch shape (1,266
+    examples x 512 tokens, fp32 inputs): the first stage in the bench's fp16
+    mode and in the accurate mode against the oracle on eight sampled
+    examples (all retained coordinates), then the PCA projection with the
+    module's fp16 P, sign bits and scales. The accurate path must keep every
+    sign outside the band |x| < 1e-3 rms (eq. onebit); the bench's fp16 path
+    (fp16 first stage, fp16 coordinates into the PCA) is held to a bound on
+    the fraction outside the band, and both fractions are recorded."""
     w = S.GPT2_SMALL
-    si = 2
     name, d_in, d_out = w.block[si]
     N, T = 1266, w.T
-    examples = [0, 633, 1265]
+    examples = [0, 181, 362, 633, 790, 1000, 1200, 1265]
     say(f"[full size] gpt2 {name}")
     Zs, zref, art = first_stage_sampled(w, si, name, d_in, d_out, N, T, torch.float32,
                                         [(E.PREC_F16, 1e-3), (E.PREC_ACCURATE, 1e-3)], examples)
@@ -122,21 +142,32 @@ def test_gpt2_small_c_fc_full_step_shape():
     rms = np.sqrt(np.mean(xref ** 2, axis=1, keepdims=True))
     so = O.onebit_scale(xref).view(np.float16)
     ei = torch.tensor(examples, device=DEV)
-    for prec, pca_prec in ((E.PREC_ACCURATE, E.PREC_ACCURATE), (E.PREC_F16, E.PREC_FAST)):
-        X = E.eogp_pca_project(Zs[prec], art["Pt"], prec=pca_prec)
+    band = np.abs(xref) < 1e-3 * rms
+    for prec, pca_prec, label in ((E.PREC_ACCURATE, E.PREC_ACCURATE, "accurate"),
+                                  (E.PREC_F16, E.PREC_FAST, "bench_f16")):
+        Zin = Zs[prec]
+        if label == "bench_f16":
+            Zin = Zin.half()                               # the bench keeps Z in fp16
+        X = E.eogp_pca_project(Zin, art["Pt"], prec=pca_prec)
         codes, scales = E.eogp_sign_pack(X)
         torch.cuda.synchronize()
         err = rel_rows(X[ei].cpu().numpy(), xref)
         bits_g = O.unpack_bits(codes[ei].cpu().numpy(), w.k)
         diff = bits_g != O.sign_bits(xref)
-        outside = diff & (np.abs(xref) >= 1e-3 * rms)
-        say(f"   prec={prec}: pca max rel {err.max():.2e}, sign mismatch fraction "
+        outside = diff & ~band
+        say(f"   {label}: pca max rel {err.max():.2e}, sign mismatch fraction "
             f"{diff.mean():.2e} ({outside.mean():.2e} outside the band)")
+        record_sign_mismatch(f"{name}/{label}", {
+            "bits": int(diff.size), "mismatch": int(diff.sum()),
+            "mismatch_outside_band": int(outside.sum()),
+            "fraction": float(diff.mean()), "fraction_outside_band": float(outside.mean()),
+            "in_band_fraction_of_bits": float(band.mean()),
+            "x_max_rel_err": float(err.max())})
         assert err.max() <= 1e-3
-        if prec == E.PREC_ACCURATE:
+        if label == "accurate":
             assert not np.any(outside)                   # strict in accurate mode
         else:
-            assert outside.mean() <= 1e-3                # reported, bounded
+            assert outside.mean() <= 1e-3                # bounded and recorded
         sg = scales[ei].cpu().numpy().view(np.float16)[:, 0]
         assert np.all(np.abs(sg.astype(np.float64) - so.astype(np.float64))
                       <= 2 * np.spacing(so).astype(np.float64))

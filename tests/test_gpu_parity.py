@@ -73,7 +73,7 @@ def oracle_Z(a, ds, mask, QA, QS, lam, damping, m):
 # ---------------------------------------------------------------------------
 # One-bit encoding
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("k", [64, 128, 100, 8192, 13])
+@pytest.mark.parametrize("k", [64, 128, 100, 8192, 13, 16384, 32768])
 def test_sign_pack_bit_exact(k):
     say(f"[sign_pack] k={k}")
     g = np.random.default_rng(k)
@@ -697,6 +697,71 @@ def test_score_integral_queries_give_exact_real_scores():
     torch.cuda.synchronize()
     real = O.score_real(codes, scales, ks, Y)
     assert np.array_equal(full.cpu().numpy(), real.astype(np.float32))
+
+
+@pytest.mark.parametrize("ks", [[1 << 18], [1 << 18, 64]])
+def test_score_long_modules_with_same_signed_queries(ks):
+    """k_u = 2^18 with every query coordinate positive: sum_c y_int reaches
+    about 3.2e9 > 2^31, so it must be carried in 64 bits (the one-module
+    kernel) and the per-module dots stored in 64 bits (several modules).
+    Scores of sampled rows are exact against the oracle (eq. onebit_influence)."""
+    N, Q = 1100, 3
+    say(f"[score] long modules ks={ks} N={N}")
+    g = np.random.default_rng(1 << 18)
+    nbytes = sum(k // 8 for k in ks)
+    codes = g.integers(0, 256, size=(N, nbytes), dtype=np.uint8)
+    scales = np.exp(g.standard_normal((N, len(ks)))).astype(np.float16).view(np.uint16)
+    Y = g.uniform(0.5, 1.0, size=(Q, sum(ks))).astype(np.float32)
+    fx = O.query_fixed_point(Y[0, :ks[0]])[0]
+    assert int(fx.sum()) > 2 ** 31                       # the case the 64-bit sums exist for
+    idx, sc, full = E.eogp_score_topk(d(codes), d(scales.view(np.int16)), ks, d(Y), 10,
+                                      full_scores=True)
+    torch.cuda.synchronize()
+    rows = np.sort(g.choice(N, 48, replace=False))
+    ref = O.score(codes[rows], scales[rows], ks, Y)
+    assert np.array_equal(full.cpu().numpy()[:, rows], ref.astype(np.float32))
+    f = full.double()
+    for q in range(Q):
+        assert torch.equal(sc[q], full[q, idx[q]])
+        rest = torch.ones(N, dtype=torch.bool, device=DEV)
+        rest[idx[q]] = False
+        assert float(f[q][rest].max()) <= float(sc[q, -1])
+
+
+def test_score_gpt2_store_layout_sampled_rows():
+    """The GPT-2-small-shaped store as the bench scores it: 20,000 rows of 48
+    modules x 8,192 bits (983 MB of codes), 16 queries, top-100. 256 sampled
+    rows are scored exactly against the oracle; the top-100 is checked by the
+    properties that define it on the full score vector."""
+    N, U, k, Q, topk = 20000, 48, 8192, 16, 100
+    say(f"[score] gpt2 store N={N} U={U} k={k}")
+    gen = torch.Generator(device=DEV)
+    gen.manual_seed(48)
+    codes = torch.randint(0, 256, (N, U * k // 8), dtype=torch.uint8, device=DEV, generator=gen)
+    scales = torch.exp(torch.randn((N, U), device=DEV, generator=gen)).half().view(torch.int16)
+    Y = torch.randn((Q, U * k), device=DEV, generator=gen)
+    idx, sc, full = E.eogp_score_topk(codes, scales, [k] * U, Y, topk, full_scores=True)
+    torch.cuda.synchronize()
+    rows = np.sort(np.random.default_rng(48).choice(N, 256, replace=False))
+    rows[-1] = N - 1
+    ri = torch.from_numpy(rows).to(DEV)
+    ref = O.score(codes[ri].cpu().numpy(), scales[ri].cpu().numpy().view(np.uint16), [k] * U,
+                  Y.cpu().numpy())
+    assert np.array_equal(full[:, ri].cpu().numpy(), ref.astype(np.float32))
+    f = full.double()
+    for q in range(Q):
+        iq = idx[q]
+        assert torch.equal(sc[q], full[q, iq])
+        assert bool(torch.all(sc[q, :-1] >= sc[q, 1:]))
+        rest = torch.ones(N, dtype=torch.bool, device=DEV)
+        rest[iq] = False
+        assert float(f[q][rest].max()) <= float(sc[q, -1])
+        ties = iq[sc[q] == sc[q, -1]]
+        # among equal scores the smaller index ranks first, and nothing left
+        # out ties the last entry with a smaller index
+        assert bool(torch.all(ties[:-1] < ties[1:]))
+        left = torch.nonzero(rest & (full[q] == sc[q, -1])).flatten()
+        assert left.numel() == 0 or int(left.min()) > int(ties.max())
 
 
 def test_score_ties_resolved_by_index():
