@@ -17,12 +17,19 @@ One step is one pass of the whole hot path over one batch:
 16 steps are the whole job (20,000 examples, 256 queries). Inputs, shared
 artifacts and the store are resident in device memory before timing starts.
 
-Printed: one JSON line with the metric, the roofline of the dominant kernel
+Printed: one JSON line with the metric (the plan build, once per module per
+job, amortised over the job's 16 steps), the roofline of the dominant kernel
 (the first-stage rotation contraction, timed live with HIP events on its
-stream), the oracle CPU baseline, one transformer block of the OLMo-2-1B- and
-OLMo-2-32B-shaped workloads (bf16 inputs; batches of 256 and 64 examples; the
-full-model rate at the same per-block cost), and the scoring-at-scale
-measurement (8,388,608 codes x 16,384 bits, 512 queries, top-100).
+stream) and of the step's scoring pass, the oracle CPU baseline on a bounded
+sample plus the parity of the bench's own codes and scores against the oracle
+on that sample, the other reading of the code length (8,192 bits per example
+in total, 192 per module), the EOGP-R, EK-FAC and PCA-fit legs, the
+OLMo-2-1B-shaped workload (one block of 256 examples, bf16 inputs, its oracle
+baseline and its 1,024-query scoring leg over 100,000 stored examples x 112
+modules x 16,384 bits), the OLMo-2-32B-shaped workload (4 blocks resident in
+HBM, 64 examples; the full-model rate at the same per-block cost), and the
+scoring-at-scale measurement (8,388,608 codes x 16,384 bits, 512 queries,
+top-100).
 """
 from __future__ import annotations
 
@@ -234,6 +241,43 @@ class Gpt2Step:
         E.eogp_score_topk(self.codes, self.scales, [k] * self.U, self.Y, self.topk,
                           out_idx=self.out_idx, out_score=self.out_score, ws=self.score_ws)
 
+    def prepare_total_bits(self):
+        """The other reading of the workload's code length: 8,192 bits per
+        example in total, split evenly over the 48 modules (k_u = 8192 / 48,
+        rounded to a multiple of 64 = 192 bits, 9,216 bits per example), with
+        each module's own fp16 P [16384, 192]."""
+        torch, S, E = self.torch, self.S, self.E
+        k2 = max(64, int(round(self.k / self.U / 64.0)) * 64)
+        self.k2 = k2
+        base = S.torch_pca_directions_t(S.rng(self.w.config_id, 600000 + self.m), self.m, k2,
+                                        self.dev).half()
+        self.Pt2 = [base.clone() for _ in range(self.U)]
+        Nt = self.B + self.Qb
+        self.X2 = torch.empty((Nt, self.U * k2), dtype=torch.float32, device=self.dev)
+        self.codes2 = torch.zeros((self.N_store, self.U * k2 // 8), dtype=torch.uint8, device=self.dev)
+        self.scales2 = torch.zeros((self.N_store, self.U), dtype=torch.int16, device=self.dev)
+        self.pca_ws2 = torch.empty(E.eogp_pca_project_workspace_size(Nt, self.m, k2, E.F16,
+                                                                     self.pca_prec),
+                                   dtype=torch.uint8, device=self.dev)
+        self.score_ws2 = torch.empty(
+            E.eogp_score_topk_workspace_size(self.N_store, self.Qb, [k2] * self.U, self.topk),
+            dtype=torch.uint8, device=self.dev)
+
+    def step_total_bits(self, s):
+        E = self.E
+        slot = s % self.n_slots
+        k2, kb2 = self.k2, self.k2 // 8
+        codes = self.codes2[slot * self.B:(slot + 1) * self.B]
+        scales = self.scales2[slot * self.B:(slot + 1) * self.B]
+        for u, (name, di, do) in enumerate(self.modules):
+            E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
+                                         Z=self.Z16, prec=self.prec, ws=self.ws)
+            X = self.X2[:, u * k2:(u + 1) * k2]
+            E.eogp_pca_project(self.Z16, self.Pt2[u], X=X, prec=self.pca_prec, ws=self.pca_ws2)
+            E.eogp_sign_pack(X[:self.B], codes[:, u * kb2:(u + 1) * kb2], scales[:, u:u + 1])
+        E.eogp_score_topk(self.codes2, self.scales2, [k2] * self.U, self.X2[self.B:], self.topk,
+                          out_idx=self.out_idx, out_score=self.out_score, ws=self.score_ws2)
+
     def rotation_flops_per_step(self):
         """Algorithmic flops of the rotation contractions in one step:
         2 * valid tokens * (d_out |J| + d_in |K|) per module, batch and queries."""
@@ -257,6 +301,19 @@ class Gpt2Step:
 
 
 FP64_PEAK_TFLOPS = 78.6
+
+
+def score_pass_roofline(st, kt_pass):
+    """HBM roofline of the step's scoring pass: every stored code byte and
+    scale read once per 16-query pass (N * sum_u (k_u/8 + 2) bytes)."""
+    ms, n = kt_pass
+    if not n:
+        return None
+    alg = st.N_store * st.U * (st.k // 8 + 2)
+    avg = ms / n
+    gbs = alg / (avg * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": gbs / HBM_PEAK_GBS, "alg_bytes_per_pass": alg, "avg_pass_ms": avg}
 
 
 def pca_fit_measurement(st, dev, n=10000):
@@ -299,18 +356,37 @@ def pca_fit_measurement(st, dev, n=10000):
 # ---------------------------------------------------------------------------
 # Oracle CPU baseline on a bounded sample of the same workload
 # ---------------------------------------------------------------------------
+def blas_threads():
+    """Threads numpy's BLAS runs with (the oracle's only parallel part)."""
+    try:
+        from threadpoolctl import threadpool_info
+        return max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+    except Exception:
+        return 1
+
+
+def sign_parity(bits_gpu, X_oracle):
+    """Sign bits of the GPU's codes against the oracle's x (eq. onebit): the
+    fraction that differ, and the fraction that differ outside the band
+    |x| < 1e-3 rms(x) of each oracle row."""
+    import numpy as np
+
+    import oracle as O
+    rms = np.sqrt(np.mean(X_oracle ** 2, axis=1, keepdims=True))
+    diff = bits_gpu != O.sign_bits(X_oracle)
+    outside = diff & (np.abs(X_oracle) >= 1e-3 * rms)
+    return {"bits": int(diff.size), "mismatch": int(diff.sum()),
+            "mismatch_outside_band": int(outside.sum())}
+
+
 def cpu_baseline(st: Gpt2Step):
     import numpy as np
     import torch
 
     import oracle as O
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count() or 1
+    threads = blas_threads()
     n_ex = 64                                     # about 10-15 s of oracle work on 16 threads
-    per_shape = {}
+    per_shape, parity = {}, {}
     for si, (name, di, do) in enumerate(st.shapes):
         u = si                                     # block 0 module of this shape
         S_ = st.S
@@ -326,8 +402,15 @@ def cpu_baseline(st: Gpt2Step):
         t0 = time.perf_counter()
         Z = np.stack([O.first_stage_tokens(a[i], ds[i], mk[i], QA, QS, ret) for i in range(n_ex)])
         X = O.pca_project(Z, P)
-        O.encode(X)
+        _, oscale = O.encode(X)
         per_shape[name] = (time.perf_counter() - t0) / n_ex
+        # the bench's own codes of these examples (store rows 0.., module u)
+        cg = st.codes[:n_ex, u * st.kb:(u + 1) * st.kb].cpu().numpy()
+        sg = st.scales[:n_ex, u].cpu().numpy().view(np.uint16).view(np.float16).astype(np.float64)
+        so = oscale.view(np.float16).astype(np.float64)
+        rec = sign_parity(O.unpack_bits(cg, st.k), X)
+        rec["scale_max_ulps"] = float(np.max(np.abs(sg - so) / np.spacing(so.astype(np.float16)).astype(np.float64)))
+        parity[name] = rec
         del P
     per_example = len(st.modules) // len(st.shapes) * sum(per_shape.values())
     # queries of one step: same first stage + PCA, plus scoring against the store
@@ -340,10 +423,39 @@ def cpu_baseline(st: Gpt2Step):
     O.topk(sc, st.topk)
     t_score = (time.perf_counter() - t0) * (st.N_store / n_codes)
     step_s = (st.B + st.Qb) * per_example + t_score
+    # the GPU's scores of the same rows and queries (one extra call outside the
+    # timed region, every score written)
+    E = st.E
+    idx, val, full = E.eogp_score_topk(st.codes, st.scales, [st.k] * st.U, st.Y, st.topk,
+                                       full_scores=True, ws=None)
+    torch.cuda.synchronize()
+    fg = full[:, :n_codes].cpu().numpy()
+    exact = int(np.sum(fg == sc.astype(np.float32)))
+    ff = full.double()
+    topk_ok = True
+    for q in range(st.Qb):
+        iq = idx[q]
+        rest = torch.ones(st.N_store, dtype=torch.bool, device=full.device)
+        rest[iq] = False
+        topk_ok &= bool(torch.equal(val[q], full[q, iq])) and \
+            float(ff[q][rest].max()) <= float(val[q, -1])
+    tot = {k_: sum(r[k_] for r in parity.values()) for k_ in ("bits", "mismatch", "mismatch_outside_band")}
+    st.parity = {
+        "sample": (f"codes of stored examples 0..{n_ex - 1} for the block-0 module of each shape "
+                   f"(the bench's own store) against the oracle's signs; the {st.Qb} step queries "
+                   f"scored against store rows 0..{n_codes - 1}"),
+        "per_shape": parity,
+        "sign_mismatch": tot["mismatch"] / tot["bits"],
+        "sign_mismatch_outside_band": tot["mismatch_outside_band"] / tot["bits"],
+        "scores_bit_exact": f"{exact} of {fg.size}",
+        "topk_consistent_with_scores": topk_ok,
+    }
     return {
         "value": st.B / step_s,
         "unit": "train examples/s",
         "cores": int(threads),
+        "host_cpus": os.cpu_count(),
+        "blas_threads": int(threads),
         "kind": "oracle",
         "sample": (f"first stage + PCA + encode of {n_ex} examples for one module of each of the "
                    f"4 GPT-2 linear shapes (x{len(st.modules) // len(st.shapes)} blocks), and "
@@ -357,12 +469,15 @@ def cpu_baseline(st: Gpt2Step):
 # ---------------------------------------------------------------------------
 # Scoring at scale: 8M codes x 16384 bits, 512 queries, top-100
 # ---------------------------------------------------------------------------
-def olmo_block(w, B, n_model_blocks, dev, reps=3):
-    """One transformer block of an OLMo-2-shaped model (its 7 linears, bf16
-    activations and output-gradients) through the whole compression path:
-    first stage (bf16 MFMA, fp32 accumulation), PCA with the module's fp16 P,
-    sign packing. Throughput per block, and for the whole model at the same
-    per-block cost (every block has the same shapes)."""
+def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False):
+    """`resident` transformer blocks of an OLMo-2-shaped model (7 linears
+    each, bf16 activations and output-gradients), each module with its own
+    plan (gathered eigenvector panels) and its own fp16 P held in HBM at the
+    same time, through the whole compression path: first stage (bf16 MFMA,
+    fp32 accumulation), PCA with the module's fp16 P, sign packing.
+    Throughput per block, and for the whole model at the same per-block cost
+    (every block has the same shapes). With cpu=True the oracle is timed on a
+    bounded sample and checked against this run's codes."""
     import torch
     from paper_2609_37842_amd import eogp as E
     from paper_2609_37842_amd import synth as S
@@ -372,14 +487,21 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3):
         if (di, do) not in inputs:   # linears of one shape share the batch's inputs
             inputs[(di, do)] = S.torch_inputs(w, si, B, w.T, di, do, dev, torch.bfloat16)
     cache, mods = {}, []
-    for si, (name, di, do) in enumerate(w.block):
-        art = S.torch_module_artifacts(w, si, di, do, dev, torch.float16, cache)
-        plan = E.eogp_plan_create(art["eigvals"], art["damping"], w.m, art["Q_A"], art["Q_S"])
-        mods.append((name, di, do, plan, art["Pt"]))
-        del art
+    t_plan = 0.0
+    for blk in range(resident):
+        for si, (name, di, do) in enumerate(w.block):
+            u = blk * len(w.block) + si
+            art = S.torch_module_artifacts(w, u, di, do, dev, torch.float16, cache)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            plan = E.eogp_plan_create(art["eigvals"], art["damping"], w.m, art["Q_A"], art["Q_S"])
+            t_plan += time.perf_counter() - t1
+            mods.append((f"{blk}.{name}", di, do, plan, art["Pt"]))
+            del art
     del cache
     torch.cuda.synchronize()
-    log(f"{w.name}: block ready ({time.time() - t0:.1f}s)")
+    log(f"{w.name}: {resident} block(s) resident ({time.time() - t0:.1f}s), "
+        f"HBM in use {torch.cuda.memory_allocated() / 2**30:.1f} GiB")
     U = len(mods)
     Z = torch.empty((B, w.m), dtype=torch.float16, device=dev)   # fp16 coordinates, fp16 P
     X = torch.empty((B, w.k), dtype=torch.float32, device=dev)
@@ -407,7 +529,7 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3):
     for _ in range(reps):
         run()
     torch.cuda.synchronize()
-    el = (time.perf_counter() - t1) / reps
+    el = (time.perf_counter() - t1) / reps / resident               # per block
     kt = {name: E.eogp_timing_read(c) for name, c in E.KERNEL_CLASSES.items()}
     E.eogp_timing_enable(False)
     rot_ms, rot_n = kt["rotation_gemm"]
@@ -418,25 +540,150 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3):
         flops += 2.0 * vt * (do * plan.n_rows + di * plan.n_cols)
     rot_tflops = flops * reps / (rot_ms * 1e-3) / 1e12
     pca_ms, _ = kt["pca_gemm"]
+    # plan build (selection and panel gathering, once per module per job) amortised
+    # over a job of w.N examples in batches of B
+    plan_ms_per_block = 1000.0 * t_plan / resident / (w.N / B)
+    el_job = el + plan_ms_per_block * 1e-3
     out = {
         "workload": w.name, "block": [n for (n, _, _) in w.block], "batch": B, "T": w.T,
+        "blocks_resident": resident, "modules_resident": U,
+        "hbm_resident_GiB": torch.cuda.memory_allocated() / 2**30,
         "valid_tokens_per_example": sum(v for v in valid.values()) / len(valid) / B,
         "m": w.m, "k": w.k, "first_stage": "bf16 inputs, bf16 MFMA, fp32 accumulation",
         "pca": "fp16 coordinates and P, fp32 accumulation",
-        "ms_per_block": 1000.0 * el,
-        "examples_per_s_per_block": B / el,
+        "ms_per_block": 1000.0 * el_job,
+        "ms_per_block_loop": 1000.0 * el,
+        "plan_ms_amortised_per_block": plan_ms_per_block,
+        "examples_per_s_per_block": B / el_job,
         "model_blocks": n_model_blocks,
-        "examples_per_s_full_model": B / (el * n_model_blocks),
-        "kernel_ms_per_block": {name: ms / reps for name, (ms, n) in kt.items() if n},
+        "examples_per_s_full_model": B / (el_job * n_model_blocks),
+        "kernel_ms_per_block": {name: ms / reps / resident for name, (ms, n) in kt.items() if n},
         "rotation_roofline": {"bound": "mfma", "achieved": rot_tflops, "peak": BF16_PEAK_TFLOPS,
                               "unit": "TFLOP/s", "frac": rot_tflops / BF16_PEAK_TFLOPS,
-                              "alg_flops_per_block": flops},
-        "pca_ms_per_block": pca_ms / reps,
-        "retained_axes": {n: {"J": p.n_rows, "K": p.n_cols} for (n, _, _, p, _) in mods},
+                              "alg_flops_per_block": flops / resident,
+                              "avg_launch_ms": rot_ms / max(1, rot_n)},
+        "pca_ms_per_block": pca_ms / reps / resident,
+        "retained_axes": {n: {"J": p.n_rows, "K": p.n_cols} for (n, _, _, p, _) in mods[:len(w.block)]},
     }
+    if cpu:
+        out["cpu_baseline"], out["parity"] = olmo_cpu_baseline(w, mods, inputs, codes, scales, B,
+                                                               n_model_blocks, out)
     for (_, _, _, plan, _) in mods:
         plan.close()
     del mods, inputs, Z, X, codes, scales, ws, pws
+    torch.cuda.empty_cache()
+    return out
+
+
+def olmo_cpu_baseline(w, mods, inputs, codes, scales, B, n_model_blocks, meas, n_ex=4):
+    """The oracle on a bounded sample of the OLMo-2 block: n_ex examples
+    through the first block's module of each distinct shape (first stage, PCA,
+    encoding), extrapolated to the whole model; and the sign bits of this
+    run's codes for those examples against the oracle's."""
+    import numpy as np
+
+    import oracle as O
+    from paper_2609_37842_amd import synth as S
+    import torch
+    threads = blas_threads()
+    per_shape, parity, seen = {}, {}, {}
+    kb = w.k // 8
+    for si, (name, di, do) in enumerate(w.block):
+        if (di, do) in seen:
+            continue
+        seen[(di, do)] = name
+        art = S.torch_module_artifacts(w, si, di, do, codes.device, torch.float16, {})
+        QA = art["Q_A"].double().cpu().numpy()
+        QS = art["Q_S"].double().cpu().numpy()
+        lam = art["eigvals"].cpu().numpy()
+        P = art["Pt"].cpu().numpy().astype(np.float64).T
+        del art
+        a, ds, mk = inputs[(di, do)]
+        a = a[:n_ex].float().double().cpu().numpy()
+        ds = ds[:n_ex].float().double().cpu().numpy()
+        mk = mk[:n_ex].cpu().numpy()
+        ret = O.select_retained(lam, float(S.recipe_damping(w)), w.m)
+        t0 = time.perf_counter()
+        Zo = np.stack([O.first_stage_tokens(a[i], ds[i], mk[i], QA, QS, ret) for i in range(n_ex)])
+        Xo = O.pca_project(Zo, P)
+        O.encode(Xo)
+        per_shape[name] = (time.perf_counter() - t0) / n_ex
+        cg = codes[:n_ex, si * kb:(si + 1) * kb].cpu().numpy()
+        parity[name] = sign_parity(O.unpack_bits(cg, w.k), Xo)
+        del P, QA, QS
+    shape_of = {}
+    for (name, di, do) in w.block:
+        shape_of[name] = seen[(di, do)]
+    per_example = n_model_blocks * sum(per_shape[shape_of[n]] for (n, _, _) in w.block)
+    tot = {k_: sum(r[k_] for r in parity.values()) for k_ in ("bits", "mismatch", "mismatch_outside_band")}
+    cpu = {"value": 1.0 / per_example, "unit": "train examples/s (full model)",
+           "cores": int(threads), "host_cpus": os.cpu_count(), "blas_threads": int(threads),
+           "kind": "oracle",
+           "sample": (f"first stage + PCA + encode of {n_ex} examples for the block-0 module of "
+                      f"each of the {len(per_shape)} distinct linear shapes, extrapolated to the "
+                      f"{len(w.block)} linears x {n_model_blocks} blocks"),
+           "seconds_per_example": per_example}
+    par = {"sample": f"codes of examples 0..{n_ex - 1}, block-0 module of each shape (bf16 inputs)",
+           "per_shape": parity,
+           "sign_mismatch": tot["mismatch"] / tot["bits"],
+           "sign_mismatch_outside_band": tot["mismatch_outside_band"] / tot["bits"]}
+    return cpu, par
+
+
+def olmo_scoring(w, dev, n_queries=None):
+    """The OLMo-2-1B-shaped scoring leg: n_queries (default the workload's
+    1,024) query projections over all 112 modules (16,384 coordinates each)
+    against a store of w.N examples x 112 modules x 16,384 bits with per-module
+    fp16 scales, top-100 per query. Synthetic store (random bits p = 0.5,
+    scales fp16(exp(N(0,1)))) and queries N(0, 1)."""
+    import torch
+    from paper_2609_37842_amd import eogp as E
+    from paper_2609_37842_amd import synth as S
+    U = len(w.block) * w.n_blocks
+    N, k, topk = w.N, w.k, w.topk
+    Q = w.Q if n_queries is None else n_queries
+    g = S.torch_generator(w.config_id, 910001, dev)
+    row = U * k // 8
+    codes = torch.empty((N, row), dtype=torch.uint8, device=dev)
+    step = max(1, (1 << 30) // row)
+    for i0 in range(0, N, step):
+        i1 = min(N, i0 + step)
+        codes[i0:i1] = torch.randint(0, 256, (i1 - i0, row), dtype=torch.uint8, device=dev,
+                                     generator=g)
+    scales = torch.exp(torch.randn((N, U), device=dev, generator=g)).half().view(torch.int16)
+    Y = torch.randn((Q, U * k), device=dev, generator=g)
+    ks = [k] * U
+    ws = torch.empty(E.eogp_score_topk_workspace_size(N, Q, ks, topk), dtype=torch.uint8, device=dev)
+    idx = torch.empty((Q, topk), dtype=torch.int64, device=dev)
+    val = torch.empty((Q, topk), dtype=torch.float32, device=dev)
+    E.eogp_score_topk(codes, scales, ks, Y[:16], topk, out_idx=idx[:16], out_score=val[:16], ws=ws)
+    torch.cuda.synchronize()
+    for c in range(len(E.KERNEL_CLASSES)):
+        E.eogp_timing_read(c)
+    E.eogp_timing_enable(True)
+    t0 = time.perf_counter()
+    E.eogp_score_topk(codes, scales, ks, Y, topk, out_idx=idx, out_score=val, ws=ws)
+    torch.cuda.synchronize()
+    total_s = time.perf_counter() - t0
+    pass_ms, passes = E.eogp_timing_read(E.KT_SCORE_PASS)
+    prep_ms, _ = E.eogp_timing_read(E.KT_SCORE_PREP)
+    merge_ms, _ = E.eogp_timing_read(E.KT_SCORE_MERGE)
+    E.eogp_timing_enable(False)
+    bytes_per_pass = N * U * (k // 8 + 2)
+    avg = pass_ms / max(1, passes)
+    gbs = bytes_per_pass / (avg * 1e-3) / 1e9
+    hbm_bound_ms = passes * bytes_per_pass / (HBM_PEAK_GBS * 1e9) * 1e3
+    mfma_bound_ms = 4.0 * Q * N * U * k / (INT8_PEAK_TOPS * 1e12) * 1e3
+    out = {"workload": w.name + " scoring", "codes": N, "modules": U, "bits_per_module": k,
+           "queries": Q, "topk": topk, "queries_per_pass": 16, "passes": passes,
+           "bytes_per_pass": bytes_per_pass, "ms_per_pass": avg, "hbm_GBps": gbs,
+           "peak_GBps": HBM_PEAK_GBS, "frac": gbs / HBM_PEAK_GBS,
+           "prep_ms": prep_ms, "merge_ms_total": merge_ms, "job_ms": 1000.0 * total_s,
+           "queries_per_s": Q / total_s,
+           "job_bound_ms": max(hbm_bound_ms, mfma_bound_ms),
+           "job_bound": {"hbm_ms": hbm_bound_ms, "int8_mfma_ms": mfma_bound_ms,
+                         "frac": max(hbm_bound_ms, mfma_bound_ms) / (1000.0 * total_s)}}
+    del codes, scales, Y, ws, idx, val
     torch.cuda.empty_cache()
     return out
 
@@ -541,8 +788,13 @@ def main(argv=None):
         elapsed = time.perf_counter() - t0
         kt = {name: E.eogp_timing_read(c) for name, c in E.KERNEL_CLASSES.items()}
         E.eogp_timing_enable(False)
-        ms_per_step = 1000.0 * elapsed / args.steps
-        value = st.B * args.steps / elapsed
+        ms_loop = 1000.0 * elapsed / args.steps
+        # the plan build (selection, weights, panel gathering: once per module
+        # per job of N_store examples) amortised over the job's steps
+        job_steps = st.N_store / st.B
+        plan_ms_step = st.plan_ms / job_steps
+        ms_per_step = ms_loop + plan_ms_step
+        value = st.B / (ms_per_step * 1e-3)
         rot_ms, rot_n = kt["rotation_gemm"]
         flops_launch = st.rotation_flops_per_step() * args.steps / max(1, rot_n)
         bytes_launch = st.rotation_bytes_per_step() * args.steps / max(1, rot_n)
@@ -593,7 +845,10 @@ def main(argv=None):
                 "launches": rot_n,
             },
             "kernel_ms_per_step": {name: ms / args.steps for name, (ms, n) in kt.items()},
+            "ms_per_step_loop": ms_loop,
             "plan_ms_total": st.plan_ms,
+            "plan_ms_amortised_per_step": plan_ms_step,
+            "score_pass_roofline": score_pass_roofline(st, kt["score_pass"]),
             "retained_axes_block0": {name: {"J": st.plans[u].n_rows, "K": st.plans[u].n_cols,
                                             "tiles": st.plans[u].n_tiles}
                                      for u, (name, _, _) in enumerate(st.shapes)},
@@ -661,19 +916,57 @@ def main(argv=None):
         del sq
         out["pca_fit"] = pca_fit_measurement(st, dev)
         log(f"pca fit: {out['pca_fit']['seconds']:.2f} s per module")
+        # the other reading of the code length (8,192 bits per example in total)
+        st.prepare_total_bits()
+        st.step_total_bits(0)
+        torch.cuda.synchronize()
+        for c in range(len(E.KERNEL_CLASSES)):
+            E.eogp_timing_read(c)
+        E.eogp_timing_enable(True)
+        ntb = max(1, args.steps // 4)
+        t0 = time.perf_counter()
+        for s_ in range(ntb):
+            st.step_total_bits(s_)
+        torch.cuda.synchronize()
+        el_tb = time.perf_counter() - t0
+        kt_tb = {name: E.eogp_timing_read(c) for name, c in E.KERNEL_CLASSES.items()}
+        E.eogp_timing_enable(False)
+        ms_tb = 1000.0 * el_tb / ntb + plan_ms_step
+        out["total_bits_reading"] = {
+            "metric": "train examples/s compressed to 1-bit codes, 8,192 code bits per example "
+                      "in total",
+            "k_per_module": st.k2, "bits_per_example": st.k2 * st.U,
+            "value": st.B / (ms_tb * 1e-3), "unit": "train examples/s", "steps": ntb,
+            "ms_per_step": ms_tb,
+            "kernel_ms_per_step": {name: ms / ntb for name, (ms, n) in kt_tb.items() if n},
+        }
+        log(f"total-bits reading: k_u={st.k2}, {ms_tb:.2f} ms/step")
+        del st.Pt2, st.X2, st.codes2, st.scales2, st.pca_ws2, st.score_ws2
         if not args.no_cpu_baseline:
+            # the EOGP-R leg wrote SRHT codes into the store: one PCA step
+            # (untimed) puts the bench's own codes back before they are checked
+            st.step(0)
+            torch.cuda.synchronize()
             t0 = time.time()
             out["cpu_baseline"] = cpu_baseline(st)
+            out["parity"] = st.parity
+            out["sign_mismatch_outside_band"] = st.parity["sign_mismatch_outside_band"]
             log(f"cpu baseline done ({time.time() - t0:.1f}s)")
         del st
         torch.cuda.empty_cache()
     if not args.no_olmo and not args.only_scoring:
         from paper_2609_37842_amd import synth as S
-        for key, w, B, nb in (("olmo2_1b", S.OLMO2_1B, 256, 16), ("olmo2_32b", S.OLMO2_32B, 64, 64)):
-            o = olmo_block(w, B, nb, dev)
+        for key, w, B, nb, res in (("olmo2_1b", S.OLMO2_1B, 256, 16, 1),
+                                   ("olmo2_32b", S.OLMO2_32B, 64, 64, 4)):
+            o = olmo_block(w, B, nb, dev, resident=res,
+                           cpu=(key == "olmo2_1b" and not args.no_cpu_baseline))
             log(f"{w.name}: {o['ms_per_block']:.1f} ms per block of {B}, "
                 f"{o['examples_per_s_full_model']:.2f} ex/s full model, rotation "
                 f"{o['rotation_roofline']['achieved']:.0f} TFLOP/s")
+            if key == "olmo2_1b" and not args.no_scoring:
+                o["scoring"] = olmo_scoring(w, dev)
+                log(f"{w.name} scoring: {o['scoring']['ms_per_pass']:.3f} ms/pass, "
+                    f"{o['scoring']['hbm_GBps']:.0f} GB/s, job {o['scoring']['job_ms']:.1f} ms")
             out[key] = o
     if not args.no_scoring and not args.only_olmo:
         sc = scoring_at_scale(args, dev)
