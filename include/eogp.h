@@ -258,6 +258,28 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride,
                             int64_t Q, int32_t topk, int64_t* out_idx, float* out_score,
                             float* full_scores, void* ws, size_t ws_bytes, void* stream);
 
+/* Scoring without a caller workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation): the same computation, arguments and results as
+ * eogp_score_topk, with the workspace taken from a 128 MiB array that the
+ * library holds in each GPU's memory until the process ends. The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine) and
+ * only enqueues work on `stream`. Limit: the call's workspace size, as
+ * eogp_score_topk_workspace_size reports it, must be at most 128 MiB
+ * (134217728 bytes), else EOGP_ERR_INVALID with nothing enqueued. One
+ * module of 16,384 bits fits any number of stored rows with up to 3,936
+ * queries per call; several modules need 64 bytes per stored row and
+ * module for each 16 queries (48 modules of 8,192 bits: about 38,000 rows for
+ * 16 queries). All calls on one GPU share that
+ * GPU's array: calls that overlap on one GPU (several streams or threads)
+ * race and must be serialised by the caller. Other errors as for
+ * eogp_score_topk. */
+eogp_status eogp_score_topk_noalloc(const uint8_t* codes, int64_t code_row_stride,
+                                    const uint16_t* scales, int64_t N, int32_t U,
+                                    const int64_t* k_per_module, const float* Y, int64_t ldy,
+                                    int64_t Q, int32_t topk, int64_t* out_idx, float* out_score,
+                                    float* full_scores, void* stream);
+
 /* ------------------------------------------------------------------------
  * EK-FAC corrected eigenvalues, the fitting pass that precedes selection
  * (Section 2.2, eq. ekfac_eigendecompose: Lambda[j, k] is the mean over

@@ -46,6 +46,8 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
                        int32_t U, const int64_t* kmod, const float* Y, int64_t ldy, int64_t Q,
                        int32_t topk, int64_t* out_idx, float* out_score, float* full, void* ws,
                        size_t ws_bytes, hipStream_t s);
+size_t score_scratch_bytes();
+eogp_status score_scratch(void** out);
 
 namespace {
 thread_local std::string g_last_error;
@@ -374,11 +376,11 @@ size_t eogp_score_topk_workspace_size(int64_t N, int64_t Q, int32_t U, const int
   return score_ws(N, Q, U, k_per_module, topk);
 }
 
-eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride, const uint16_t* scales,
-                            int64_t N, int32_t U, const int64_t* k_per_module, const float* Y,
-                            int64_t ldy, int64_t Q, int32_t topk, int64_t* out_idx,
-                            float* out_score, float* full_scores, void* ws, size_t ws_bytes,
-                            void* stream) {
+namespace {
+eogp_status check_score_args(const uint8_t* codes, int64_t code_row_stride,
+                             const uint16_t* scales, int64_t N, int32_t U,
+                             const int64_t* k_per_module, const float* Y, int64_t ldy, int64_t Q,
+                             int32_t topk, int64_t* out_idx, float* out_score) {
   if (N < 0 || Q < 0 || U < 1 || !k_per_module) return fail(EOGP_ERR_INVALID, "score_topk: bad sizes");
   if (topk < 1 || topk > score_max_topk()) return fail(EOGP_ERR_INVALID, "score_topk: topk out of range");
   if (N >= ((int64_t)1 << 32) - 1) return fail(EOGP_ERR_INVALID, "score_topk: N too large");
@@ -398,10 +400,44 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride, const
   if (Q > 0 && (!Y || !out_idx || !out_score)) return fail(EOGP_ERR_INVALID, "score_topk: NULL pointer");
   if (N > 0 && (!codes || !scales)) return fail(EOGP_ERR_INVALID, "score_topk: NULL pointer");
   if (Q > 65535) return fail(EOGP_ERR_INVALID, "score_topk: Q too large for one call");
+  return EOGP_OK;
+}
+}  // namespace
+
+eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride, const uint16_t* scales,
+                            int64_t N, int32_t U, const int64_t* k_per_module, const float* Y,
+                            int64_t ldy, int64_t Q, int32_t topk, int64_t* out_idx,
+                            float* out_score, float* full_scores, void* ws, size_t ws_bytes,
+                            void* stream) {
+  const eogp_status st = check_score_args(codes, code_row_stride, scales, N, U, k_per_module, Y,
+                                          ldy, Q, topk, out_idx, out_score);
+  if (st != EOGP_OK) return st;
   if (ws_bytes < score_ws(N, Q, U, k_per_module, topk) || !ws)
     return fail(EOGP_ERR_WORKSPACE, "score_topk: workspace too small");
   return score_topk(codes, code_row_stride, scales, N, U, k_per_module, Y, ldy, Q, topk, out_idx,
                     out_score, full_scores, ws, ws_bytes, S(stream));
+}
+
+eogp_status eogp_score_topk_noalloc(const uint8_t* codes, int64_t code_row_stride,
+                                    const uint16_t* scales, int64_t N, int32_t U,
+                                    const int64_t* k_per_module, const float* Y, int64_t ldy,
+                                    int64_t Q, int32_t topk, int64_t* out_idx, float* out_score,
+                                    float* full_scores, void* stream) {
+  eogp_status st = check_score_args(codes, code_row_stride, scales, N, U, k_per_module, Y, ldy, Q,
+                                    topk, out_idx, out_score);
+  if (st != EOGP_OK) return st;
+  const size_t need = score_ws(N, Q, U, k_per_module, topk);
+  if (need > score_scratch_bytes())
+    return fail(EOGP_ERR_INVALID, "score_topk_noalloc: this call needs " + std::to_string(need) +
+                                      " bytes of scratch, more than the " +
+                                      std::to_string(score_scratch_bytes()) +
+                                      " bytes the entry point holds per GPU (use eogp_score_topk "
+                                      "with a workspace, or fewer queries per call)");
+  void* scratch = nullptr;
+  st = score_scratch(&scratch);
+  if (st != EOGP_OK) return st;
+  return score_topk(codes, code_row_stride, scales, N, U, k_per_module, Y, ldy, Q, topk, out_idx,
+                    out_score, full_scores, scratch, score_scratch_bytes(), S(stream));
 }
 
 }  // extern "C"

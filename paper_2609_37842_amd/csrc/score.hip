@@ -37,9 +37,9 @@
 // that did not fit are inserted again, so no qualifying row is lost. Finally
 // each workgroup writes its top-k per query and a merge kernel reduces them.
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 #include <utility>
-#include <vector>
 
 #include "common.h"
 #include "timing.h"
@@ -825,15 +825,24 @@ Layout layout(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t topk
 }
 
 // Module ranges of the multi-module pass: n_rng consecutive ranges of
-// roughly equal step counts, each at least one module.
-void module_ranges(const std::vector<ModInfo>& hm, int64_t n_steps, int n_rng, int32_t* rng) {
-  const int U = (int)hm.size();
+// roughly equal step counts, each at least one module (one pass over the
+// module sizes, no host allocation).
+void module_ranges(const int64_t* kmod, int U, int sb, int64_t n_steps, int n_rng, int32_t* rng) {
+  auto steps = [&](int u) { return (kmod[u] + 8 * sb - 1) / (8 * sb); };
   rng[0] = 0;
+  int v = 1;                   // candidate start of the next range
+  int64_t base = steps(0);     // first step of module v
   for (int r = 1; r < n_rng; ++r) {
+    if (v <= rng[r - 1]) {     // range r - 1 keeps at least one module
+      base += steps(v);
+      ++v;
+    }
     const int64_t target = (n_steps * r + n_rng / 2) / n_rng;
     const int v_max = U - (n_rng - r);     // leaves a module for each later range
-    int v = rng[r - 1] + 1;                // at least one module in range r - 1
-    while (v < v_max && hm[v].sbase < target) ++v;
+    while (v < v_max && base < target) {
+      base += steps(v);
+      ++v;
+    }
     rng[r] = v;
   }
   rng[n_rng] = U;
@@ -887,22 +896,22 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     codes = pad;
   }
   const PassCfg cfg = pass_cfg(topk);
-  std::vector<ModInfo> hm(U);
+  // the module table, MOD_CHUNK entries per launch (kernel arguments)
   int64_t coff = 0, boff = 0, sbase = 0;
-  for (int u = 0; u < U; ++u) {
-    hm[u].k = (int32_t)kmod[u];
-    hm[u].coff = (int32_t)coff;
-    hm[u].boff = (int32_t)boff;
-    hm[u].sbase = (int32_t)sbase;
-    coff += kmod[u];
-    boff += kmod[u] / 8;
-    sbase += (kmod[u] + 8 * cfg.sb - 1) / (8 * cfg.sb);
-  }
   for (int u0 = 0; u0 < U; u0 += MOD_CHUNK) {
     ModChunk mc;
     mc.first = u0;
     mc.count = std::min(MOD_CHUNK, U - u0);
-    for (int i = 0; i < mc.count; ++i) mc.m[i] = hm[u0 + i];
+    for (int i = 0; i < mc.count; ++i) {
+      const int64_t k = kmod[u0 + i];
+      mc.m[i].k = (int32_t)k;
+      mc.m[i].coff = (int32_t)coff;
+      mc.m[i].boff = (int32_t)boff;
+      mc.m[i].sbase = (int32_t)sbase;
+      coff += k;
+      boff += k / 8;
+      sbase += (k + 8 * cfg.sb - 1) / (8 * cfg.sb);
+    }
     hipLaunchKernelGGL(k_mod_table, dim3(1), dim3(MOD_CHUNK), 0, s, mc, mods);
   }
   EOGP_LAUNCH_CHECK("module table");
@@ -933,7 +942,7 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
   a.cidx = ci;
   a.n_rng = L.n_rng;
   a.part = base + L.o_part;
-  if (U > 1) module_ranges(hm, L.n_steps, L.n_rng, a.rng);
+  if (U > 1) module_ranges(kmod, U, cfg.sb, L.n_steps, L.n_rng, a.rng);
   FoldArgs fa;
   fa.part = a.part;
   fa.scales = scales;
@@ -977,6 +986,41 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
                        out_idx, out_score);
     EOGP_LAUNCH_CHECK("score pass");
   }
+  return EOGP_OK;
+}
+
+// ---- scoring without a caller workspace ---------------------------------------
+// For callers that cannot allocate device memory (code under graph capture,
+// serving loops): the workspace of a scoring call lives in this file-scope
+// array, one copy per GPU, held until the process ends. Its device address is
+// looked up once per device, with that device current, and only that address
+// is handed to kernels. Every call on one GPU shares the array, so calls that
+// overlap on one GPU race; nothing in it has to start at zero (each call
+// writes every byte it reads).
+namespace {
+constexpr size_t kScratchBytes = size_t(128) << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+size_t score_scratch_bytes() { return kScratchBytes; }
+
+eogp_status score_scratch(void** out) {
+  int dev = 0;
+  EOGP_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(EOGP_ERR_UNSUPPORTED, "score_topk_noalloc: device index out of range");
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return check_hip(e, "score_topk_noalloc: scratch address");
+    if (!p) return fail(EOGP_ERR_DEVICE, "score_topk_noalloc: no scratch address");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return EOGP_OK;
 }
 

@@ -49,7 +49,7 @@ EXPORTED = (
     "eogp_sign_pack", "eogp_srht_project_workspace_size", "eogp_srht_project",
     "eogp_pca_fit_workspace_size", "eogp_pca_fit",
     "eogp_ekfac_workspace_size", "eogp_ekfac_eigenvalues",
-    "eogp_score_topk_workspace_size", "eogp_score_topk",
+    "eogp_score_topk_workspace_size", "eogp_score_topk", "eogp_score_topk_noalloc",
     "eogp_timing_enable", "eogp_timing_read",
     "eogp_status_string", "eogp_last_error", "eogp_version",
 )
@@ -97,6 +97,8 @@ def load(path: str | None = None):
                                                   c_i32]),
         "eogp_score_topk": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64), c_vp,
                                     c_i64, c_i64, c_i32, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
+        "eogp_score_topk_noalloc": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64),
+                                            c_vp, c_i64, c_i64, c_i32, c_vp, c_vp, c_vp, c_vp]),
         "eogp_timing_enable": (c_i32, [c_i32]),
         "eogp_timing_read": (c_i32, [c_i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(c_i64)]),
         "eogp_status_string": (ctypes.c_char_p, [c_i32]),
@@ -399,11 +401,7 @@ def eogp_score_topk_workspace_size(N, Q, k_per_module, topk) -> int:
     return int(load().eogp_score_topk_workspace_size(N, Q, len(k_per_module), ks, topk))
 
 
-def eogp_score_topk(codes, scales, k_per_module, Y, topk, full_scores=False, out_idx=None,
-                    out_score=None, ws=None, stream=None):
-    """Per-query top-k (index int64 [Q, topk], score float32 [Q, topk]) and
-    optionally every score (float32 [Q, N])."""
-    L = load()
+def _score_layout(codes, scales, k_per_module, Y):
     U = len(k_per_module)
     if codes.dtype != torch.uint8 or codes.dim() != 2 or (codes.shape[0] > 0 and codes.stride(1) != 1):
         raise ValueError("codes must be uint8 [N, row bytes] with unit column stride")
@@ -416,7 +414,43 @@ def eogp_score_topk(codes, scales, k_per_module, Y, topk, full_scores=False, out
     if Y.dtype != torch.float32 or Y.dim() != 2 or (Y.shape[0] > 0 and Y.stride(1) != 1):
         raise ValueError("Y must be float32 [Q, sum k_u] with unit column stride")
     _need_cuda(codes, scales, Y)
-    Q = Y.shape[0]
+    ksum = sum(int(k) for k in k_per_module)
+    # an empty tensor may report stride 0; with no rows any valid stride will do
+    cstride = codes.stride(0) if N > 0 else ksum // 8
+    ldy = Y.stride(0) if Y.shape[0] > 0 else ksum
+    return N, Y.shape[0], U, cstride, ldy
+
+
+def eogp_score_topk_noalloc(codes, scales, k_per_module, Y, topk, out_idx, out_score,
+                            full_scores=None, stream=None):
+    """eogp_score_topk without a workspace (see eogp_score_topk_noalloc in
+    eogp.h): the library's per-GPU scratch array serves as workspace, so the
+    call allocates nothing; outputs are the caller's (index int64 [Q, topk],
+    score float32 [Q, topk], optionally every score float32 [Q, N])."""
+    L = load()
+    N, Q, U, cstride, ldy = _score_layout(codes, scales, k_per_module, Y)
+    _need_cuda(out_idx, out_score, full_scores)
+    if (out_idx.dtype != torch.int64 or tuple(out_idx.shape) != (Q, topk) or not out_idx.is_contiguous()
+            or out_score.dtype != torch.float32 or tuple(out_score.shape) != (Q, topk)
+            or not out_score.is_contiguous()):
+        raise ValueError("out_idx / out_score must be contiguous int64 / float32 [Q, topk]")
+    if full_scores is not None and (full_scores.dtype != torch.float32 or
+                                    tuple(full_scores.shape) != (Q, N) or
+                                    not full_scores.is_contiguous()):
+        raise ValueError("full_scores must be contiguous float32 [Q, N]")
+    ks = (c_i64 * U)(*[int(k) for k in k_per_module])
+    _check(L.eogp_score_topk_noalloc(_ptr(codes), cstride, _ptr(scales), N, U, ks, _ptr(Y), ldy, Q,
+                                     topk, _ptr(out_idx), _ptr(out_score), _ptr(full_scores),
+                                     _stream(stream)))
+    return out_idx, out_score, full_scores
+
+
+def eogp_score_topk(codes, scales, k_per_module, Y, topk, full_scores=False, out_idx=None,
+                    out_score=None, ws=None, stream=None):
+    """Per-query top-k (index int64 [Q, topk], score float32 [Q, topk]) and
+    optionally every score (float32 [Q, N])."""
+    L = load()
+    N, Q, U, cstride, ldy = _score_layout(codes, scales, k_per_module, Y)
     ks = (c_i64 * U)(*[int(k) for k in k_per_module])
     if out_idx is None:
         out_idx = torch.empty((Q, topk), dtype=torch.int64, device=Y.device)
@@ -425,9 +459,6 @@ def eogp_score_topk(codes, scales, k_per_module, Y, topk, full_scores=False, out
     full = torch.empty((Q, N), dtype=torch.float32, device=Y.device) if full_scores else None
     need = int(L.eogp_score_topk_workspace_size(N, Q, U, ks, topk))
     ws, wsb = _workspace(need, Y.device, ws)
-    # an empty tensor may report stride 0; with no rows any valid stride will do
-    cstride = codes.stride(0) if N > 0 else sum(int(k) for k in k_per_module) // 8
-    ldy = Y.stride(0) if Q > 0 else sum(int(k) for k in k_per_module)
     _check(L.eogp_score_topk(_ptr(codes), cstride, _ptr(scales), N, U, ks, _ptr(Y), ldy, Q,
                              topk, _ptr(out_idx), _ptr(out_score), _ptr(full), _ptr(ws), wsb,
                              _stream(stream)))
