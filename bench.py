@@ -70,6 +70,9 @@ def parse(argv=None):
     ap.add_argument("--no-olmo", action="store_true",
                     help="skip the OLMo-2-1B and OLMo-2-32B per-block measurements")
     ap.add_argument("--only-olmo", action="store_true")
+    ap.add_argument("--olmo-prec", choices=["f16", "fast"], default="f16",
+                    help="OLMo-2 first stage: f16 = bf16 inputs taken exactly into fp16 products "
+                         "(bases and rotated tokens rounded to fp16), fast = bf16 products")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run a plain device copy of this many MiB 4 times (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters against known traffic)")
@@ -469,7 +472,10 @@ def cpu_baseline(st: Gpt2Step):
 # ---------------------------------------------------------------------------
 # Scoring at scale: 8M codes x 16384 bits, 512 queries, top-100
 # ---------------------------------------------------------------------------
-def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False):
+OLMO_GRAD_EXPONENT = 0    # OLMo-2-shaped output-gradients (std ~0.014) sit in fp16's normal range
+
+
+def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False, prec="f16"):
     """`resident` transformer blocks of an OLMo-2-shaped model (7 linears
     each, bf16 activations and output-gradients), each module with its own
     plan (gathered eigenvector panels) and its own fp16 P held in HBM at the
@@ -495,6 +501,8 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False):
             torch.cuda.synchronize()
             t1 = time.perf_counter()
             plan = E.eogp_plan_create(art["eigvals"], art["damping"], w.m, art["Q_A"], art["Q_S"])
+            if prec == "f16" and OLMO_GRAD_EXPONENT:
+                E.eogp_plan_set_input_exponents(plan, 0, OLMO_GRAD_EXPONENT)
             t_plan += time.perf_counter() - t1
             mods.append((f"{blk}.{name}", di, do, plan, art["Pt"]))
             del art
@@ -512,11 +520,12 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False):
     pws = torch.empty(E.eogp_pca_project_workspace_size(B, w.m, w.k, E.F16, E.PREC_FAST),
                       dtype=torch.uint8, device=dev)
     kb = w.k // 8
+    fs_prec = E.PREC_F16 if prec == "f16" else E.PREC_FAST
 
     def run():
         for u, (name, di, do, plan, Pt) in enumerate(mods):
             a, ds, mk = inputs[(di, do)]
-            E.eogp_rotate_retain_planned(plan, a, ds, mk, Z=Z, prec=E.PREC_FAST, ws=ws)
+            E.eogp_rotate_retain_planned(plan, a, ds, mk, Z=Z, prec=fs_prec, ws=ws)
             E.eogp_pca_project(Z, Pt, X=X, prec=E.PREC_FAST, ws=pws)
             E.eogp_sign_pack(X, codes[:, u * kb:(u + 1) * kb], scales[:, u:u + 1])
 
@@ -549,7 +558,10 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False):
         "blocks_resident": resident, "modules_resident": U,
         "hbm_resident_GiB": torch.cuda.memory_allocated() / 2**30,
         "valid_tokens_per_example": sum(v for v in valid.values()) / len(valid) / B,
-        "m": w.m, "k": w.k, "first_stage": "bf16 inputs, bf16 MFMA, fp32 accumulation",
+        "m": w.m, "k": w.k,
+        "first_stage": ("bf16 inputs taken exactly into fp16 MFMA (bases and rotated tokens "
+                        f"rounded to fp16, output-gradients times 2^{OLMO_GRAD_EXPONENT}), fp32 "
+                        "accumulation") if prec == "f16" else "bf16 inputs, bf16 MFMA, fp32 accumulation",
         "pca": "fp16 coordinates and P, fp32 accumulation",
         "ms_per_block": 1000.0 * el_job,
         "ms_per_block_loop": 1000.0 * el,
@@ -959,7 +971,7 @@ def main(argv=None):
         for key, w, B, nb, res in (("olmo2_1b", S.OLMO2_1B, 256, 16, 1),
                                    ("olmo2_32b", S.OLMO2_32B, 64, 64, 4)):
             o = olmo_block(w, B, nb, dev, resident=res,
-                           cpu=(key == "olmo2_1b" and not args.no_cpu_baseline))
+                           cpu=(key == "olmo2_1b" and not args.no_cpu_baseline), prec=args.olmo_prec)
             log(f"{w.name}: {o['ms_per_block']:.1f} ms per block of {B}, "
                 f"{o['examples_per_s_full_model']:.2f} ex/s full model, rotation "
                 f"{o['rotation_roofline']['achieved']:.0f} TFLOP/s")

@@ -53,12 +53,14 @@ typedef enum { EOGP_F32 = 0, EOGP_BF16 = 1, EOGP_F16 = 2 } eogp_dtype;
  * accumulation. ACCURATE: every fp32 operand is split into a high and a low
  * 16-bit part and the cross products are accumulated in fp32 (three MFMA
  * passes when both operands are fp32, two when one is already 16-bit), which
- * carries about 16 significant bits into each product. F16 (first stage
- * with fp32 inputs only): one MFMA pass on operands rounded once to fp16
- * (11 significant bits, 8 times finer than bf16), fp32 accumulation; inputs
- * are first multiplied by the plan's power-of-two exponents (see
+ * carries about 16 significant bits into each product. F16 (first stage and
+ * EK-FAC pass): one MFMA pass on operands rounded once to fp16 (11
+ * significant bits, 8 times finer than bf16), fp32 accumulation; inputs are
+ * first multiplied by the plan's power-of-two exponents (see
  * eogp_plan_set_input_exponents) so they sit inside fp16's normal range
- * (2^-14 <= |x| < 65504). */
+ * (2^-14 <= |x| < 65504). bf16 inputs enter this mode exactly inside that
+ * range (8 significant bits fit in fp16's 11); only the bases and the rotated
+ * tokens are rounded. */
 typedef enum { EOGP_PREC_FAST = 0, EOGP_PREC_ACCURATE = 1, EOGP_PREC_F16 = 2 } eogp_prec;
 
 /* ------------------------------------------------------------------------
@@ -139,12 +141,10 @@ eogp_status eogp_plan_set_input_exponents(eogp_plan* plan, int32_t e_acts, int32
  *              never read and may hold anything, NaN included.
  *   Z          [N, ldz] fp32, ldz >= m; columns m..ldz-1 are not written.
  *   prec       EOGP_PREC_ACCURATE keeps about 16 bits per product;
- *              EOGP_PREC_F16 (fp32 inputs only) rounds inputs and bases once to
- *              fp16 (relative error of a row of Z about 4e-4 for inputs inside
- *              fp16's normal range); EOGP_PREC_FAST rounds operands to bf16
- *              and keeps the rotated tokens in bf16 (about 3e-3 for fp32
- *              inputs; the natural mode for bf16 inputs).
- *              EOGP_ERR_UNSUPPORTED for EOGP_PREC_F16 with bf16 inputs.
+ *              EOGP_PREC_F16 rounds inputs and bases once to fp16 (relative
+ *              error of a row of Z about 5e-4 for inputs inside fp16's normal
+ *              range, fp32 or bf16); EOGP_PREC_FAST rounds operands to bf16
+ *              and keeps the rotated tokens in bf16 (about 3e-3).
  *   ws         workspace of at least eogp_rotate_retain_workspace_size bytes.
  * Sizes: N*T + 8N + 256 < 2^31 (the compacted token list is indexed in
  * 32 bits), else EOGP_ERR_INVALID.

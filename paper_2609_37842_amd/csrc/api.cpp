@@ -110,8 +110,6 @@ eogp_status check_first_stage(const eogp_plan* p, const void* acts, const void* 
   if (ldz < p->m) return fail(EOGP_ERR_INVALID, "rotate_retain: ldz < m");
   if (prec != EOGP_PREC_FAST && prec != EOGP_PREC_ACCURATE && prec != EOGP_PREC_F16)
     return fail(EOGP_ERR_INVALID, "rotate_retain: unknown precision mode");
-  if (prec == EOGP_PREC_F16 && dt != EOGP_F32)
-    return fail(EOGP_ERR_UNSUPPORTED, "rotate_retain: the fp16 mode takes fp32 inputs");
   if (N * T + 8 * N + 256 >= kMaxFlat)
     return fail(EOGP_ERR_INVALID, "rotate_retain: N*T + 8N + 256 must be < 2^31");
   return EOGP_OK;
@@ -314,8 +312,6 @@ eogp_status eogp_ekfac_eigenvalues(const void* acts, int64_t ld_acts, const void
     return fail(EOGP_ERR_UNSUPPORTED, "ekfac: inputs must be fp32 or bf16");
   if (prec != EOGP_PREC_FAST && prec != EOGP_PREC_ACCURATE && prec != EOGP_PREC_F16)
     return fail(EOGP_ERR_INVALID, "ekfac: unknown precision mode");
-  if (prec == EOGP_PREC_F16 && in_dtype != EOGP_F32)
-    return fail(EOGP_ERR_UNSUPPORTED, "ekfac: the fp16 mode takes fp32 inputs");
   if (ld_acts == 0) ld_acts = d_in;
   if (ld_grads == 0) ld_grads = d_out;
   if (ld_acts < d_in || ld_grads < d_out)

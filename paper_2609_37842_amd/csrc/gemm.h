@@ -8,7 +8,10 @@
 
 namespace eogp {
 
-enum class AType : int { F32 = 0, B16 = 1 };   // B16: bf16 or fp16 bit patterns
+// B16: bf16 or fp16 bit patterns used as the MFMA type; BF16_AS_F16: bf16 A
+// widened to fp32, scaled by a_scale and rounded to fp16 while it is staged
+// (fp16 MFMA; single-pass products on aligned rows only).
+enum class AType : int { F32 = 0, B16 = 1, BF16_AS_F16 = 2 };
 
 struct GemmArgs {
   // A: row r of the product reads row (a_rows ? a_rows[r] : r) of A.

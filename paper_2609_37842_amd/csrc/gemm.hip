@@ -555,8 +555,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
 
 constexpr int PT = 256;   // k_gemm_p: threads per workgroup
 
-// AT: 0 = fp32 A, 1 = 16-bit A (both with 16-byte aligned rows); B is a padded
-// panel; one part each; no split-K.
+// AT: 0 = fp32 A, 1 = 16-bit A used as it is, 2 = bf16 A widened, scaled
+// and rounded to fp16 while it is staged (all with 16-byte aligned rows); B is
+// a padded panel; one part each; no split-K.
 template <int AT, bool F16, bool SC>
 __global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_gemm_p(KParams kp) {
@@ -602,6 +603,7 @@ void k_gemm_p(KParams kp) {
   // 4 lanes per row (rows (tid >> 2) + 64 q, q < 4); B 4 lanes per row.
   constexpr int AQ = AT == 0 ? 8 : 4;
   constexpr int BQ = BNP / 64;
+  static_assert(AT != 2 || F16, "bf16 A is widened to fp16 for fp16 products only");
   const int a_r0 = AT == 0 ? (tid >> 3) : (tid >> 2);
   constexpr int a_rs = AT == 0 ? PT / 8 : PT / 4;
   const int a_pc = AT == 0 ? (tid & 7) : (tid & 3);
@@ -739,6 +741,23 @@ void k_gemm_p(KParams kp) {
           hv.x = cvt_pair<F16>(x.x, x.y);
           hv.y = cvt_pair<F16>(x.z, x.w);
           *reinterpret_cast<v2u*>(&sA[st][o]) = hv;
+        }
+      } else if constexpr (AT == 2) {
+        // bf16 pairs -> fp32 (exact) -> times 2^e (exact) -> fp16 pairs, nearest even
+#pragma unroll
+        for (int q = 0; q < AQ; ++q) {
+          const v4u w = RA.ra16[q];
+          uint32_t h[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float lo = __uint_as_float(w[e] << 16), hi = __uint_as_float(w[e] & 0xFFFF0000u);
+            if constexpr (SC) {
+              lo *= a_scale;
+              hi *= a_scale;
+            }
+            h[e] = cvt_pair<true>(lo, hi);
+          }
+          *reinterpret_cast<v4u*>(&sA[st][swz(a_r0 + a_rs * q, a_pc)]) = mk4(h[0], h[1], h[2], h[3]);
         }
       } else {
 #pragma unroll
@@ -977,6 +996,9 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
       return EOGP_OK;
     }
   }
+  if constexpr (AT == 2) {
+    return fail(EOGP_ERR_UNSUPPORTED, "gemm: bf16 A widened to fp16 needs aligned rows and a padded B panel");
+  } else {
   if (g.CT && kp.splits > 1) return fail(EOGP_ERR_UNSUPPORTED, "gemm: fp16 transposed output without split-K only");
   int64_t grid = std::min<int64_t>(tiles * kp.splits, kCus);
   if (grid >= kXcds) grid = grid / kXcds * kXcds;
@@ -989,6 +1011,7 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
     EOGP_LAUNCH_CHECK("gemm split sum");
   }
   return EOGP_OK;
+  }
 }
 
 }  // namespace
@@ -1036,6 +1059,9 @@ eogp_status gemm_nt2(const GemmArgs& g1, const GemmArgs& g2, AType a_type, int a
     if (f16 && sc) hipLaunchKernelGGL((k_gemm_p<0, true, true>), gd, bd, 0, s, kq);
     else if (f16) hipLaunchKernelGGL((k_gemm_p<0, true, false>), gd, bd, 0, s, kq);
     else hipLaunchKernelGGL((k_gemm_p<0, false, false>), gd, bd, 0, s, kq);
+  } else if (a_type == AType::BF16_AS_F16) {
+    if (sc) hipLaunchKernelGGL((k_gemm_p<2, true, true>), gd, bd, 0, s, kq);
+    else hipLaunchKernelGGL((k_gemm_p<2, true, false>), gd, bd, 0, s, kq);
   } else {
     if (f16) hipLaunchKernelGGL((k_gemm_p<1, true, false>), gd, bd, 0, s, kq);
     else hipLaunchKernelGGL((k_gemm_p<1, false, false>), gd, bd, 0, s, kq);
@@ -1054,6 +1080,11 @@ eogp_status gemm_nt(const GemmArgs& g, AType a_type, int a_parts, int b_parts, b
   const bool bc = !(g.b_padded && (g.ldb % 8 == 0) && ((uintptr_t)g.B_hi % 16 == 0) &&
                     (g.B_lo == nullptr || (uintptr_t)g.B_lo % 16 == 0));
   if (b_parts == 2 && g.B_lo == nullptr) return fail(EOGP_ERR_INVALID, "gemm: missing B low part");
+  if (a_type == AType::BF16_AS_F16) {
+    if (a_parts != 1 || b_parts != 1 || !f16)
+      return fail(EOGP_ERR_UNSUPPORTED, "gemm: bf16 A widened to fp16 is a single fp16 product");
+    return launch<2, 1, 1, true>(g, av, bc, s);
+  }
   if (!A32 && a_parts != 1) return fail(EOGP_ERR_INVALID, "gemm: 16-bit A cannot be split");
   if (A32 && a_parts == 1 && b_parts == 1 && !f16) return launch<0, 1, 1, false>(g, av, bc, s);
   if (A32 && a_parts == 2 && b_parts == 2 && !f16) return launch<0, 2, 2, false>(g, av, bc, s);

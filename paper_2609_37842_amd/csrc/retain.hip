@@ -344,10 +344,12 @@ eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
 
   // 2. rotations onto the used eigenvectors (rows = listed tokens; count on device)
   // FAST: bf16 operands; ACCURATE: bf16 high+low splits (three products);
-  // F16: fp32 inputs scaled by 2^e and rounded once to fp16, fp16 bases.
+  // F16: inputs scaled by 2^e and rounded once to fp16, fp16 bases.
   const bool accurate = prec == EOGP_PREC_ACCURATE;
   const bool f16 = prec == EOGP_PREC_F16;
-  const AType at = bf16_in ? AType::B16 : AType::F32;
+  // bf16 inputs in the F16 mode are widened, scaled and rounded to fp16 (exact
+  // inside fp16's normal range: bf16 carries 8 significant bits, fp16 11)
+  const AType at = bf16_in ? (f16 ? AType::BF16_AS_F16 : AType::B16) : AType::F32;
   const int a_parts = (accurate && !bf16_in) ? 2 : 1;
   const int b_parts = accurate ? 2 : 1;
   GemmArgs gs;

@@ -176,12 +176,15 @@ def test_gpt2_small_full_step_shape(si):
 @pytest.mark.parametrize("si", [4, 6])        # gate_proj 2048 -> 8192, down_proj 8192 -> 2048
 def test_olmo2_1b_bf16_modules(si):
     """OLMo-2-1B-shaped modules, bf16 inputs, T = 1024 with lengths
-    U{64..1024}, m = 32768: two sampled examples, all retained coordinates."""
+    U{64..1024}, m = 32768: two sampled examples, all retained coordinates,
+    in the bf16 mode, the accurate mode and the fp16 mode (bf16 inputs taken
+    exactly, bases and rotated tokens rounded to fp16)."""
     w = S.OLMO2_1B
     name, d_in, d_out = w.block[si]
     say(f"[full size] olmo2-1b {name}")
     first_stage_sampled(w, si, name, d_in, d_out, 12, w.T, torch.bfloat16,
-                        [(E.PREC_FAST, 2e-2), (E.PREC_ACCURATE, 2e-3)], [0, 11])
+                        [(E.PREC_FAST, 2e-2), (E.PREC_ACCURATE, 2e-3), (E.PREC_F16, 1e-3)],
+                        [0, 11])
 
 
 @pytest.mark.parametrize("si", [1, 5, 6])     # k_proj 5120 -> 1024, up 5120 -> 27648, down
@@ -195,7 +198,7 @@ def test_olmo2_32b_bf16_modules(si):
     g = np.random.default_rng(si)
     coords = np.sort(g.choice(w.m, 512, replace=False))
     first_stage_sampled(w, si, name, d_in, d_out, 3, w.T, torch.bfloat16,
-                        [(E.PREC_FAST, 2e-2)], [0, 2], coords=coords)
+                        [(E.PREC_FAST, 2e-2), (E.PREC_F16, 1e-3)], [0, 2], coords=coords)
 
 
 @pytest.mark.parametrize("wl", ["olmo2-1b", "olmo2-32b"])

@@ -258,11 +258,17 @@ def test_rotate_retain_bf16_inputs_fast_and_accurate():
     d_used = dt.float().cpu().numpy()
     plan = E.eogp_plan_create(d(lam), 1e-4, m, d(QA), d(QS))
     ref, _ = oracle_Z(a_used, d_used, mask, QA, QS, lam, 1e-4, m)
-    for prec, tol in ((E.PREC_FAST, 2e-2), (E.PREC_ACCURATE, 1e-3)):
+    # the fp16 mode takes bf16 inputs exactly (inside fp16's normal range) and
+    # rounds only the bases and the rotated tokens: the 1e-3 bound of fp32
+    # accumulation holds, with and without power-of-two input scaling
+    for prec, tol, ex in ((E.PREC_FAST, 2e-2, None), (E.PREC_ACCURATE, 1e-3, None),
+                          (E.PREC_F16, 1e-3, None), (E.PREC_F16, 1e-3, (-2, 9))):
+        if ex is not None:
+            E.eogp_plan_set_input_exponents(plan, *ex)
         Z = E.eogp_rotate_retain_planned(plan, at, dt, d(mask), prec=prec)
         torch.cuda.synchronize()
         err = rel_rows(Z.cpu().numpy(), ref)
-        say(f"   prec={prec} max rel {err.max():.2e}")
+        say(f"   prec={prec} exponents={ex} max rel {err.max():.2e}")
         assert err.max() <= tol
     plan.close()
 
@@ -384,9 +390,16 @@ def test_rotate_retain_fp16_mode_input_exponents():
     assert e0 > 3 * e1
     with pytest.raises(E.EogpError):
         E.eogp_plan_set_input_exponents(plan, 61, 0)
-    with pytest.raises(E.EogpError):
-        E.eogp_rotate_retain_planned(plan, d(a, torch.bfloat16), d(ds, torch.bfloat16), d(mask),
-                                     prec=E.PREC_F16)
+    # bf16 inputs of the same magnitudes: taken exactly into fp16 once the
+    # exponents bring them into range
+    ab, db = d(a, torch.bfloat16), d(ds, torch.bfloat16)
+    refb, _ = oracle_Z(ab.float().cpu().numpy(), db.float().cpu().numpy(), mask, QA, QS, lam,
+                       1e-14, m)
+    Zb = E.eogp_rotate_retain_planned(plan, ab, db, d(mask), prec=E.PREC_F16)
+    torch.cuda.synchronize()
+    eb = rel_rows(Zb.cpu().numpy(), refb).max()
+    say(f"   bf16 inputs with exponents {eb:.2e}")
+    assert eb <= 1e-3
     plan.close()
 
 
@@ -452,11 +465,12 @@ def test_ekfac_bf16_inputs():
     a, ds, mask, QA, QS, _ = random_problem(72, N, T, d_in, d_out, 10, lens_lo=8)
     at, dt = d(a, torch.bfloat16), d(ds, torch.bfloat16)
     ref = O.ekfac_eigenvalues(at.float().cpu().numpy(), dt.float().cpu().numpy(), mask, QA, QS) * N
-    for prec, tol in ((E.PREC_FAST, 2e-2), (E.PREC_ACCURATE, 1e-4)):
-        sq = E.eogp_ekfac_eigenvalues(at, dt, d(mask), d(QA), d(QS), prec=prec)
+    for prec, tol, ex in ((E.PREC_FAST, 2e-2, (0, 0)), (E.PREC_ACCURATE, 1e-4, (0, 0)),
+                          (E.PREC_F16, 3e-3, (0, 0)), (E.PREC_F16, 3e-3, (-1, 8))):
+        sq = E.eogp_ekfac_eigenvalues(at, dt, d(mask), d(QA), d(QS), prec=prec, exponents=ex)
         torch.cuda.synchronize()
         err = rel_fro(sq.cpu().numpy(), ref)
-        say(f"[ekfac] bf16 prec={prec}: fro {err:.2e}")
+        say(f"[ekfac] bf16 prec={prec} exponents={ex}: fro {err:.2e}")
         assert err <= tol
 
 
