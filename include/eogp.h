@@ -219,6 +219,24 @@ eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k,
                            uint8_t* codes, int64_t code_row_stride, uint16_t* scales,
                            int64_t scale_stride, void* stream);
 
+/* Tiled store layout (the same bits and scales, stored for streaming; the
+ * paper fixes only the byte packing of one module, eq. app_payload). Rows
+ * are grouped in tiles of 32; a row of the store holds S = sum_u k_u / 512
+ * steps of 64 bytes (each k_u a multiple of 512, module u owning steps
+ * step0_u = sum_{v<u} k_v / 512 ..). The 64 bytes of row r = 32 t + i in
+ * step s -- bytes 64 (s - step0_u) .. + 63 of module u's row-major code --
+ * form, with the other 31 rows of tile t, the 2 KB block t * S + s; their
+ * 16-byte piece p (0..3) sits at block offset (p % 2) * 1024 +
+ * ((p / 2) * 32 + i) * 16. A store of N rows takes ceil(N / 32) * S * 2048
+ * bytes, 16-byte aligned. eogp_sign_pack_tiled writes rows row0 .. row0+N-1
+ * of one module (k = k_u bits at step0); the scale goes to scales[i *
+ * scale_stride] exactly as for eogp_sign_pack. Bits and scales are those of
+ * eogp_sign_pack. Errors: EOGP_ERR_INVALID unless k is a positive multiple of
+ * 512, step0 + k / 512 <= steps_per_row, codes is 16-byte aligned and ldx >= k. */
+eogp_status eogp_sign_pack_tiled(const float* X, int64_t ldx, int64_t N, int64_t k, int64_t row0,
+                                 uint8_t* codes, int64_t steps_per_row, int64_t step0,
+                                 uint16_t* scales, int64_t scale_stride, void* stream);
+
 /* ------------------------------------------------------------------------
  * Scoring (eq. onebit_influence, eq. app_stored_influence; Algorithm 1,
  * query block) with a per-query top-k:
@@ -257,6 +275,18 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride,
                             const int64_t* k_per_module, const float* Y, int64_t ldy,
                             int64_t Q, int32_t topk, int64_t* out_idx, float* out_score,
                             float* full_scores, void* ws, size_t ws_bytes, void* stream);
+
+/* Scoring of a store in the tiled layout (see eogp_sign_pack_tiled): the same
+ * scores, ranking and outputs as eogp_score_topk on the row-major store with
+ * the same bits. Each wave reads one 2 KB block per step as two contiguous
+ * 1 KB loads. Every k_u a positive multiple of 512; codes 16-byte aligned,
+ * ceil(N / 32) * (sum_u k_u / 512) * 2048 bytes. Workspace:
+ * eogp_score_topk_workspace_size with the same arguments. */
+eogp_status eogp_score_topk_tiled(const uint8_t* codes, const uint16_t* scales, int64_t N,
+                                  int32_t U, const int64_t* k_per_module, const float* Y,
+                                  int64_t ldy, int64_t Q, int32_t topk, int64_t* out_idx,
+                                  float* out_score, float* full_scores, void* ws,
+                                  size_t ws_bytes, void* stream);
 
 /* Scoring without a caller workspace, for callers that cannot allocate device
  * memory (code under HIP graph capture, tight serving loops, harnesses that

@@ -48,6 +48,13 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
                        size_t ws_bytes, hipStream_t s);
 size_t score_scratch_bytes();
 eogp_status score_scratch(void** out);
+eogp_status sign_pack_tiled(const float* X, int64_t ldx, int64_t N, int64_t k, int64_t row0,
+                            uint8_t* codes, int64_t steps_row, int64_t step0, uint16_t* scales,
+                            int64_t sstride, hipStream_t s);
+eogp_status score_topk_tiled(const uint8_t* codes, const uint16_t* scales, int64_t N, int32_t U,
+                             const int64_t* kmod, const float* Y, int64_t ldy, int64_t Q,
+                             int32_t topk, int64_t* out_idx, float* out_score, float* full,
+                             void* ws, size_t ws_bytes, hipStream_t s);
 
 namespace {
 thread_local std::string g_last_error;
@@ -288,6 +295,23 @@ eogp_status eogp_sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, ui
   return sign_pack(X, ldx, N, k, codes, code_row_stride, scales, scale_stride, S(stream));
 }
 
+eogp_status eogp_sign_pack_tiled(const float* X, int64_t ldx, int64_t N, int64_t k, int64_t row0,
+                                 uint8_t* codes, int64_t steps_per_row, int64_t step0,
+                                 uint16_t* scales, int64_t scale_stride, void* stream) {
+  if (N < 0 || k < 512 || k % 512 != 0)
+    return fail(EOGP_ERR_INVALID, "sign_pack_tiled: k must be a positive multiple of 512");
+  if (row0 < 0 || N >= kMaxFlat || row0 >= ((int64_t)1 << 40))
+    return fail(EOGP_ERR_INVALID, "sign_pack_tiled: bad row range");
+  if (step0 < 0 || step0 + k / 512 > steps_per_row)
+    return fail(EOGP_ERR_INVALID, "sign_pack_tiled: the module's steps must lie inside the row");
+  if (N > 0 && (!X || !codes || !scales)) return fail(EOGP_ERR_INVALID, "sign_pack_tiled: NULL pointer");
+  if ((uintptr_t)codes % 16 != 0) return fail(EOGP_ERR_INVALID, "sign_pack_tiled: codes must be 16-byte aligned");
+  if (ldx < k) return fail(EOGP_ERR_INVALID, "sign_pack_tiled: ldx < k");
+  if (scale_stride < 1) return fail(EOGP_ERR_INVALID, "sign_pack_tiled: scale stride must be >= 1");
+  return sign_pack_tiled(X, ldx, N, k, row0, codes, steps_per_row, step0, scales, scale_stride,
+                         S(stream));
+}
+
 size_t eogp_ekfac_workspace_size(int64_t N, int64_t T, int64_t d_in, int64_t d_out) {
   if (N < 0 || T < 0 || d_in < 1 || d_out < 1) return 0;
   return ekfac_ws(N, T, d_in, d_out);
@@ -412,6 +436,30 @@ eogp_status eogp_score_topk(const uint8_t* codes, int64_t code_row_stride, const
     return fail(EOGP_ERR_WORKSPACE, "score_topk: workspace too small");
   return score_topk(codes, code_row_stride, scales, N, U, k_per_module, Y, ldy, Q, topk, out_idx,
                     out_score, full_scores, ws, ws_bytes, S(stream));
+}
+
+eogp_status eogp_score_topk_tiled(const uint8_t* codes, const uint16_t* scales, int64_t N,
+                                  int32_t U, const int64_t* k_per_module, const float* Y,
+                                  int64_t ldy, int64_t Q, int32_t topk, int64_t* out_idx,
+                                  float* out_score, float* full_scores, void* ws, size_t ws_bytes,
+                                  void* stream) {
+  if (U < 1 || !k_per_module) return fail(EOGP_ERR_INVALID, "score_topk_tiled: bad sizes");
+  int64_t ksum = 0;
+  for (int u = 0; u < U; ++u) {
+    if (k_per_module[u] < 512 || k_per_module[u] % 512 != 0)
+      return fail(EOGP_ERR_INVALID, "score_topk_tiled: every k_u must be a positive multiple of 512");
+    ksum += k_per_module[u];
+  }
+  // a tiled store row holds ksum / 8 bytes (a multiple of 64); the other checks as for
+  // the row-major layout
+  const eogp_status st = check_score_args(codes, ksum / 8, scales, N, U, k_per_module, Y, ldy, Q,
+                                          topk, out_idx, out_score);
+  if (st != EOGP_OK) return st;
+  if ((uintptr_t)codes % 16 != 0) return fail(EOGP_ERR_INVALID, "score_topk_tiled: codes must be 16-byte aligned");
+  if (ws_bytes < score_ws(N, Q, U, k_per_module, topk) || !ws)
+    return fail(EOGP_ERR_WORKSPACE, "score_topk_tiled: workspace too small");
+  return score_topk_tiled(codes, scales, N, U, k_per_module, Y, ldy, Q, topk, out_idx, out_score,
+                          full_scores, ws, ws_bytes, S(stream));
 }
 
 eogp_status eogp_score_topk_noalloc(const uint8_t* codes, int64_t code_row_stride,

@@ -15,16 +15,26 @@ namespace {
 // rounded once to fp16.
 constexpr int kPackUnroll = 8;
 
+//
+// Tiled store (TILED): rows in tiles of 32; the 64 bytes of row r in 512-bit
+// step s of the row (a module's steps start at step0) go to the 2 KB block
+// (tile * steps_row + s), 16-byte piece p (bytes 16p .. 16p+15) at block
+// offset (p % 2) * 1024 + ((p / 2) * 32 + r) * 16: the order in which the
+// scoring pass's wave lanes take them (k a multiple of 512).
+template <bool TILED>
 __global__ __launch_bounds__(256) void k_sign_pack(const float* __restrict__ X, int64_t ldx,
                                                    int64_t N, int64_t k,
                                                    uint8_t* __restrict__ codes, int64_t cstride,
                                                    uint16_t* __restrict__ scales,
-                                                   int64_t sstride, int word_store) {
+                                                   int64_t sstride, int word_store, int64_t row0,
+                                                   int64_t steps_row, int64_t step0) {
   __shared__ double part[4];
   const int64_t i = blockIdx.x;
   const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const float* x = X + i * ldx;
   uint8_t* c = codes + i * cstride;
+  const int64_t grow = row0 + i;   // tiled: the row's place in the store
+  uint8_t* tb = codes + ((grow >> 5) * steps_row + step0) * 2048 + (grow & 31) * 16;
   const int64_t nchunk = (k + 63) >> 6;
   double acc = 0.0;
   for (int64_t ch0 = wid; ch0 < nchunk; ch0 += 4 * kPackUnroll) {
@@ -43,7 +53,13 @@ __global__ __launch_bounds__(256) void k_sign_pack(const float* __restrict__ X, 
       const uint64_t word = __ballot(in && v[u] >= 0.f);
       acc += fabs((double)v[u]);                   // 0 beyond k
       const int64_t nbytes = std::min<int64_t>(8, (k - c0 + 7) >> 3);
-      if (word_store && nbytes == 8) {
+      if constexpr (TILED) {
+        // chunk ch = 8 bytes: step ch / 8, piece (ch % 8) / 2, half ch % 2
+        const int pc = (int)((ch & 7) >> 1);
+        if (lane == 0)
+          *reinterpret_cast<uint64_t*>(tb + (ch >> 3) * 2048 + (pc & 1) * 1024 + (pc >> 1) * 512 +
+                                       (ch & 1) * 8) = word;
+      } else if (word_store && nbytes == 8) {
         if (lane == 0) *reinterpret_cast<uint64_t*>(c + (c0 >> 3)) = word;
       } else if (lane < nbytes) {
         c[(c0 >> 3) + lane] = (uint8_t)(word >> (8 * lane));
@@ -75,9 +91,21 @@ eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t
   if (N == 0) return EOGP_OK;
   const int word_store = ((uintptr_t)codes % 8 == 0) && (cstride % 8 == 0);
   timing::Scope ts(EOGP_KT_SIGN_PACK, s);
-  hipLaunchKernelGGL(k_sign_pack, dim3((unsigned)N), dim3(256), 0, s, X, ldx, N, k,
-                     codes, cstride, scales, sstride, word_store);
+  hipLaunchKernelGGL(k_sign_pack<false>, dim3((unsigned)N), dim3(256), 0, s, X, ldx, N, k,
+                     codes, cstride, scales, sstride, word_store, (int64_t)0, (int64_t)0,
+                     (int64_t)0);
   EOGP_LAUNCH_CHECK("sign_pack");
+  return EOGP_OK;
+}
+
+eogp_status sign_pack_tiled(const float* X, int64_t ldx, int64_t N, int64_t k, int64_t row0,
+                            uint8_t* codes, int64_t steps_row, int64_t step0, uint16_t* scales,
+                            int64_t sstride, hipStream_t s) {
+  if (N == 0) return EOGP_OK;
+  timing::Scope ts(EOGP_KT_SIGN_PACK, s);
+  hipLaunchKernelGGL(k_sign_pack<true>, dim3((unsigned)N), dim3(256), 0, s, X, ldx, N, k, codes,
+                     (int64_t)0, scales, sstride, 0, row0, steps_row, step0);
+  EOGP_LAUNCH_CHECK("sign_pack (tiled)");
   return EOGP_OK;
 }
 

@@ -263,6 +263,7 @@ struct ScoreArgs {
   int n_rng;
   int32_t rng[MAX_RNG + 1];
   void* part;
+  int64_t n_tiles;   // tiled store: 32-row tiles (ceil(N / 32))
 };
 
 // Calls f(integral_constant<I>) for I = 0 .. sizeof...(I) - 1 in order.
@@ -284,10 +285,14 @@ struct Cursor {
 // is written to `part` as int32 (MODE 1, every k_u <= 2^16) or int64 (MODE 2);
 // k_score_fold then forms the fp64 terms and sums them in module order. CAP:
 // candidate slots per query (MODE 0). SB: bytes per row and step. RT: 32-row
-// tiles per wave (each plane fragment read from LDS feeds RT MFMAs).
-template <int NCLS, int D, int MODE, int CAP, int SB, int RT>
+// tiles per wave (each plane fragment read from LDS feeds RT MFMAs). TILED:
+// the store is in the tiled layout (see eogp_sign_pack_tiled): each wave's
+// 32-row tile and step is one 2 KB block whose bytes are already in lane
+// order, read as two contiguous 1 KB loads; else rows are row-major.
+template <int NCLS, int D, int MODE, int CAP, int SB, int RT, bool TILED>
 __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
   constexpr bool MULTI = MODE != 0;
+  static_assert(!TILED || SB == 64, "the tiled layout has 64-byte row pieces per step");
   constexpr int ROWS = NW * RT * 32;   // rows per block
   static_assert(NCLS == 1 || NCLS == 2 || NCLS == 4, "bit-weight classes");
   static_assert(D >= 2 && D <= 8, "ring depth");
@@ -358,7 +363,12 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
     for (int rt = 0; rt < RT; ++rt) {
       row[rt] = blk * ROWS + (int64_t)(wid * RT + rt) * 32 + r32;   // this lane's stored row
       rowc[rt] = std::min<int64_t>(row[rt], a.N - 1);                // rows past N: never reported
-      rowp[rt] = a.codes + rowc[rt] * a.cstride + (SB / 2) * hg;
+      if constexpr (TILED) {
+        const int64_t tile = std::min<int64_t>(blk * (ROWS / 32) + wid * RT + rt, a.n_tiles - 1);
+        rowp[rt] = a.codes + tile * (int64_t)a.n_steps * 2048 + lane * 16;
+      } else {
+        rowp[rt] = a.codes + rowc[rt] * a.cstride + (SB / 2) * hg;
+      }
     }
 
     i32x16 acc[RT][NCLS];
@@ -401,6 +411,19 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
       const uint4* psrc = pl_grp + (int64_t)(live ? target : n - 1) * PU + tid;
 #pragma unroll
       for (int v = 0; v < PV; ++v) ring[SL][RT][v] = psrc[v * NTHR];
+      if constexpr (TILED) {
+        // every step of a module is whole (k_u a multiple of 512); a step
+        // past the range reads the range's last block again, unused
+        const int64_t so = (int64_t)(s_lo + (live ? target : n - 1)) * 2048;
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int uc = 0; uc < NU; ++uc)
+            ring[SL][rt][uc] = *reinterpret_cast<const uint4*>(rowp[rt] + so + uc * 1024);
+        voff[SL] = 0;
+        vbytes[SL] = SB;
+        return;
+      }
       const int64_t off = (int64_t)cl.boff + SB * cl.sl;
       const int valid = live ? min(SB, cl.kbytes - SB * cl.sl) : 0;   // multiple of 8
       voff[SL] = off;
@@ -848,12 +871,12 @@ void module_ranges(const int64_t* kmod, int U, int sb, int64_t n_steps, int n_rn
   rng[n_rng] = U;
 }
 
-template <int MODE, int CAP>
+template <int MODE, int CAP, bool TILED>
 eogp_status launch_pass(const PassCfg& c, dim3 gd, const ScoreArgs& a, hipStream_t s) {
-#define EOGP_SCORE_CFG(SB, RT, D)                                                      \
-  if (c.sb == SB && c.rt == RT && c.d == D) {                                          \
-    hipLaunchKernelGGL((k_score<2, D, MODE, CAP, SB, RT>), gd, dim3(NTHR), 0, s, a);    \
-    return EOGP_OK;                                                                    \
+#define EOGP_SCORE_CFG(SB, RT, D)                                                           \
+  if (c.sb == SB && c.rt == RT && c.d == D) {                                               \
+    hipLaunchKernelGGL((k_score<2, D, MODE, CAP, SB, RT, TILED>), gd, dim3(NTHR), 0, s, a);  \
+    return EOGP_OK;                                                                         \
   }
   EOGP_SCORE_CFG(64, 2, 3)
 #undef EOGP_SCORE_CFG
@@ -868,10 +891,11 @@ size_t score_ws(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t to
   return layout(N, Q, U, kmod, topk).total;
 }
 
-eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* scales, int64_t N,
-                       int32_t U, const int64_t* kmod, const float* Y, int64_t ldy, int64_t Q,
-                       int32_t topk, int64_t* out_idx, float* out_score, float* full, void* ws,
-                       size_t ws_bytes, hipStream_t s) {
+template <bool TILED>
+eogp_status score_topk_impl(const uint8_t* codes, int64_t cstride, const uint16_t* scales,
+                            int64_t N, int32_t U, const int64_t* kmod, const float* Y, int64_t ldy,
+                            int64_t Q, int32_t topk, int64_t* out_idx, float* out_score,
+                            float* full, void* ws, size_t ws_bytes, hipStream_t s) {
   const Layout L = layout(N, Q, U, kmod, topk);
   if (ws_bytes < L.total) return fail(EOGP_ERR_WORKSPACE, "score_topk: workspace too small");
   if (Q == 0) return EOGP_OK;
@@ -888,7 +912,7 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
   // 16-byte slot of the workspace first.
   int64_t ksum = 0;
   for (int u = 0; u < U; ++u) ksum += kmod[u];
-  if (N > 0 && (N - 1) * cstride + ksum / 8 < 16) {
+  if (!TILED && N > 0 && (N - 1) * cstride + ksum / 8 < 16) {
     uint8_t* pad = reinterpret_cast<uint8_t*>(base + L.o_pad);
     hipLaunchKernelGGL(k_pad16, dim3(1), dim3(16), 0, s, codes,
                        (int)((N - 1) * cstride + ksum / 8), pad);
@@ -942,6 +966,7 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
   a.cidx = ci;
   a.n_rng = L.n_rng;
   a.part = base + L.o_part;
+  a.n_tiles = ceil_div(N, 32);
   if (U > 1) module_ranges(kmod, U, cfg.sb, L.n_steps, L.n_rng, a.rng);
   FoldArgs fa;
   fa.part = a.part;
@@ -964,9 +989,10 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
       const dim3 gd((unsigned)L.grid);
       eogp_status st;
       if (U == 1) {
-        st = cfg.cap == 256 ? launch_pass<0, 256>(cfg, gd, a, s) : launch_pass<0, 512>(cfg, gd, a, s);
+        st = cfg.cap == 256 ? launch_pass<0, 256, TILED>(cfg, gd, a, s)
+                            : launch_pass<0, 512, TILED>(cfg, gd, a, s);
       } else {
-        st = L.n64 ? launch_pass<2, 256>(cfg, gd, a, s) : launch_pass<1, 256>(cfg, gd, a, s);
+        st = L.n64 ? launch_pass<2, 256, TILED>(cfg, gd, a, s) : launch_pass<1, 256, TILED>(cfg, gd, a, s);
         if (st == EOGP_OK) {
           const dim3 fg((unsigned)L.fold_grid), fb(FOLD_THR);
           if (cfg.cap == 256) {
@@ -987,6 +1013,22 @@ eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* sc
     EOGP_LAUNCH_CHECK("score pass");
   }
   return EOGP_OK;
+}
+
+eogp_status score_topk(const uint8_t* codes, int64_t cstride, const uint16_t* scales, int64_t N,
+                       int32_t U, const int64_t* kmod, const float* Y, int64_t ldy, int64_t Q,
+                       int32_t topk, int64_t* out_idx, float* out_score, float* full, void* ws,
+                       size_t ws_bytes, hipStream_t s) {
+  return score_topk_impl<false>(codes, cstride, scales, N, U, kmod, Y, ldy, Q, topk, out_idx,
+                                out_score, full, ws, ws_bytes, s);
+}
+
+eogp_status score_topk_tiled(const uint8_t* codes, const uint16_t* scales, int64_t N, int32_t U,
+                             const int64_t* kmod, const float* Y, int64_t ldy, int64_t Q,
+                             int32_t topk, int64_t* out_idx, float* out_score, float* full,
+                             void* ws, size_t ws_bytes, hipStream_t s) {
+  return score_topk_impl<true>(codes, 0, scales, N, U, kmod, Y, ldy, Q, topk, out_idx, out_score,
+                               full, ws, ws_bytes, s);
 }
 
 // ---- scoring without a caller workspace ---------------------------------------

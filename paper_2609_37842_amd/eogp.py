@@ -46,10 +46,12 @@ EXPORTED = (
     "eogp_rotate_retain_workspace_size", "eogp_rotate_retain_planned",
     "eogp_rotate_retain_oneshot_workspace_size", "eogp_rotate_retain",
     "eogp_pca_project_workspace_size", "eogp_pca_project",
-    "eogp_sign_pack", "eogp_srht_project_workspace_size", "eogp_srht_project",
+    "eogp_sign_pack", "eogp_sign_pack_tiled", "eogp_srht_project_workspace_size",
+    "eogp_srht_project",
     "eogp_pca_fit_workspace_size", "eogp_pca_fit",
     "eogp_ekfac_workspace_size", "eogp_ekfac_eigenvalues",
-    "eogp_score_topk_workspace_size", "eogp_score_topk", "eogp_score_topk_noalloc",
+    "eogp_score_topk_workspace_size", "eogp_score_topk", "eogp_score_topk_tiled",
+    "eogp_score_topk_noalloc",
     "eogp_timing_enable", "eogp_timing_read",
     "eogp_status_string", "eogp_last_error", "eogp_version",
 )
@@ -83,6 +85,8 @@ def load(path: str | None = None):
         "eogp_pca_project": (c_i32, [c_vp, c_i32, c_i64, c_i64, c_i64, c_vp, c_i32, c_i64, c_i64,
                                      c_vp, c_i64, c_i32, c_vp, c_sz, c_vp]),
         "eogp_sign_pack": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_vp, c_i64, c_vp, c_i64, c_vp]),
+        "eogp_sign_pack_tiled": (c_i32, [c_vp, c_i64, c_i64, c_i64, c_i64, c_vp, c_i64, c_i64, c_vp,
+                                         c_i64, c_vp]),
         "eogp_ekfac_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64]),
         "eogp_ekfac_eigenvalues": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64,
                                            c_i64, c_i64, c_vp, c_vp, c_i32, c_i32, c_i32, c_vp,
@@ -97,6 +101,8 @@ def load(path: str | None = None):
                                                   c_i32]),
         "eogp_score_topk": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64), c_vp,
                                     c_i64, c_i64, c_i32, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
+        "eogp_score_topk_tiled": (c_i32, [c_vp, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64), c_vp,
+                                          c_i64, c_i64, c_i32, c_vp, c_vp, c_vp, c_vp, c_sz, c_vp]),
         "eogp_score_topk_noalloc": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, ctypes.POINTER(c_i64),
                                             c_vp, c_i64, c_i64, c_i32, c_vp, c_vp, c_vp, c_vp]),
         "eogp_timing_enable": (c_i32, [c_i32]),
@@ -394,6 +400,62 @@ def eogp_sign_pack(X, codes=None, scales=None, stream=None):
     _check(L.eogp_sign_pack(_ptr(X), X.stride(0), N, k, _ptr(codes), codes.stride(0),
                             _ptr(scales), sstride, _stream(stream)))
     return codes, scales
+
+
+def tiled_store_bytes(N: int, k_per_module) -> int:
+    """Bytes of a tiled store of N rows (see eogp_sign_pack_tiled in eogp.h)."""
+    steps = sum(int(k) for k in k_per_module) // 512
+    return -(-int(N) // 32) * steps * 2048
+
+
+def eogp_sign_pack_tiled(X, codes, row0, steps_per_row, step0, scales, stream=None):
+    """Sign bits of X [N, k] into rows row0 .. row0+N-1 of a tiled store
+    (uint8, tiled_store_bytes long) at the module's first step step0, and
+    the fp16 scales into scales (int16 [N] or a column of an [N, U] array)."""
+    L = load()
+    _need_cuda(X, codes, scales)
+    N, k = X.shape
+    if codes.dtype != torch.uint8 or not codes.is_contiguous():
+        raise ValueError("codes must be a contiguous uint8 tiled store")
+    need = -(-(int(row0) + N) // 32) * int(steps_per_row) * 2048
+    if N > 0 and codes.numel() < need:
+        raise ValueError(f"the tiled store needs at least {need} bytes for these rows")
+    sstride = scales.stride(0) if scales.dim() == 2 else 1
+    _check(L.eogp_sign_pack_tiled(_ptr(X), X.stride(0), N, k, int(row0), _ptr(codes),
+                                  int(steps_per_row), int(step0), _ptr(scales), sstride,
+                                  _stream(stream)))
+    return codes, scales
+
+
+def eogp_score_topk_tiled(codes, scales, N, k_per_module, Y, topk, full_scores=False,
+                          out_idx=None, out_score=None, ws=None, stream=None):
+    """eogp_score_topk over a tiled store of N rows (codes: the uint8 store)."""
+    L = load()
+    U = len(k_per_module)
+    if codes.dtype != torch.uint8 or not codes.is_contiguous():
+        raise ValueError("codes must be a contiguous uint8 tiled store")
+    if N > 0 and codes.numel() < tiled_store_bytes(N, k_per_module):
+        raise ValueError("the tiled store is too small for N rows")
+    if scales.dtype not in (torch.int16, torch.float16) or not scales.is_contiguous() or \
+            scales.numel() != N * U:
+        raise ValueError("scales must be contiguous fp16 bits [N, U]")
+    if Y.dtype != torch.float32 or Y.dim() != 2 or (Y.shape[0] > 0 and Y.stride(1) != 1):
+        raise ValueError("Y must be float32 [Q, sum k_u] with unit column stride")
+    _need_cuda(codes, scales, Y)
+    Q = Y.shape[0]
+    ks = (c_i64 * U)(*[int(k) for k in k_per_module])
+    if out_idx is None:
+        out_idx = torch.empty((Q, topk), dtype=torch.int64, device=Y.device)
+    if out_score is None:
+        out_score = torch.empty((Q, topk), dtype=torch.float32, device=Y.device)
+    full = torch.empty((Q, N), dtype=torch.float32, device=Y.device) if full_scores else None
+    need = int(L.eogp_score_topk_workspace_size(N, Q, U, ks, topk))
+    ws, wsb = _workspace(need, Y.device, ws)
+    ldy = Y.stride(0) if Q > 0 else sum(int(k) for k in k_per_module)
+    _check(L.eogp_score_topk_tiled(_ptr(codes), _ptr(scales), N, U, ks, _ptr(Y), ldy, Q, topk,
+                                   _ptr(out_idx), _ptr(out_score), _ptr(full), _ptr(ws), wsb,
+                                   _stream(stream)))
+    return out_idx, out_score, full
 
 
 def eogp_score_topk_workspace_size(N, Q, k_per_module, topk) -> int:

@@ -173,3 +173,24 @@ def test_multi_module_score_workspace_holds_the_exact_dots():
     assert two - one >= 2 * 16 * N * 4
     wide = E.eogp_score_topk_workspace_size(N, 16, [1 << 17, 64], 10)
     assert wide - E.eogp_score_topk_workspace_size(N, 16, [1 << 17], 10) >= 2 * 16 * N * 8
+
+
+def test_tiled_layout_argument_validation_without_device():
+    """The tiled layout needs k (and every k_u) a multiple of 512, the
+    module's steps inside the row, and 16-byte aligned codes."""
+    L = E.load()
+    fake = ctypes.c_void_p(0x1000)
+    assert L.eogp_sign_pack_tiled(fake, 768, 4, 768, 0, fake, 4, 0, fake, 1, None) == -1
+    assert L.eogp_sign_pack_tiled(fake, 1024, 4, 1024, 0, fake, 4, 3, fake, 1, None) == -1
+    assert L.eogp_sign_pack_tiled(fake, 1024, 4, 1024, 0, ctypes.c_void_p(0x1008), 4, 0, fake, 1,
+                                  None) == -1
+    assert L.eogp_sign_pack_tiled(fake, 512, 4, 1024, 0, fake, 4, 0, fake, 1, None) == -1
+    ks = (ctypes.c_int64 * 2)(512, 64)
+    assert L.eogp_score_topk_tiled(fake, fake, 4, 2, ks, fake, 576, 1, 3, fake, fake, None, fake,
+                                   1 << 20, None) == -1
+    ks = (ctypes.c_int64 * 1)(512)
+    assert L.eogp_score_topk_tiled(ctypes.c_void_p(0x1008), fake, 4, 1, ks, fake, 512, 1, 3, fake,
+                                   fake, None, fake, 1 << 20, None) == -1
+    assert L.eogp_score_topk_tiled(fake, fake, 4, 1, ks, fake, 512, 1, 3, fake, fake, None, fake,
+                                   16, None) == -4
+    assert E.tiled_store_bytes(33, [512, 1024]) == 2 * 3 * 2048

@@ -26,6 +26,7 @@ import oracle as O
 from paper_2609_37842_amd import eogp as E
 from paper_2609_37842_amd import synth as S
 from select_helpers import restrict, select_large
+from tiled_helpers import rows_from_tiled
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
@@ -259,3 +260,41 @@ def test_scoring_8m_codes_one_pass():
         mask = torch.ones(N, dtype=torch.bool, device=DEV)
         mask[iq] = False
         assert float(f[q][mask].max()) <= kth
+
+
+def test_scoring_8m_codes_tiled_store():
+    """The same 8,388,608 x 16,384-bit workload in the tiled store layout
+    (random bytes are a valid tiled store): 128 sampled tiles (4,096 rows),
+    converted to row-major by the layout's definition, scored exactly against
+    the oracle; the top-100 by its defining properties."""
+    w = S.SCORING
+    N, k, Q, topk = w.N, w.k, 16, w.topk
+    S_row = k // 512
+    say(f"[full size] tiled scoring N={N} k={k}")
+    g = torch.Generator(device=DEV)
+    g.manual_seed(78)
+    nbytes = E.tiled_store_bytes(N, [k])
+    codes = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    for i0 in range(0, nbytes, 1 << 30):
+        i1 = min(nbytes, i0 + (1 << 30))
+        codes[i0:i1] = torch.randint(0, 256, (i1 - i0,), dtype=torch.uint8, device=DEV, generator=g)
+    scales = torch.exp(torch.randn((N, 1), device=DEV, generator=g)).half().view(torch.int16)
+    Y = torch.randn((Q, k), device=DEV, generator=g)
+    idx, sc, full = E.eogp_score_topk_tiled(codes, scales, N, [k], Y, topk, full_scores=True)
+    torch.cuda.synchronize()
+    tiles = np.sort(np.random.default_rng(10).choice(N // 32, 128, replace=False))
+    blk = S_row * 2048
+    sub = np.concatenate([codes[t * blk:(t + 1) * blk].cpu().numpy() for t in tiles])
+    rows_codes = rows_from_tiled(sub, S_row)
+    rows = (tiles[:, None] * 32 + np.arange(32)[None, :]).reshape(-1)
+    ri = torch.from_numpy(rows).to(DEV)
+    ref = O.score(rows_codes, scales[ri].cpu().numpy().view(np.uint16), [k], Y.cpu().numpy())
+    assert np.array_equal(full[:, ri].cpu().numpy(), ref.astype(np.float32))
+    f = full.double()
+    for q in range(Q):
+        iq = idx[q]
+        assert torch.equal(sc[q], full[q, iq])
+        assert bool(torch.all(sc[q, :-1] >= sc[q, 1:]))
+        rest = torch.ones(N, dtype=torch.bool, device=DEV)
+        rest[iq] = False
+        assert float(f[q][rest].max()) <= float(sc[q, -1])

@@ -17,6 +17,7 @@ import torch
 import oracle as O
 from paper_2609_37842_amd import eogp as E
 from paper_2609_37842_amd import synth as S
+from tiled_helpers import rows_from_tiled, tiled_from_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -110,6 +111,61 @@ def test_sign_pack_into_multi_module_rows():
         assert np.array_equal(s[:, u], os_)
         off += k // 8
     assert np.all(c[:, row:] == 0)
+
+
+def test_sign_pack_tiled_layout():
+    """Three modules (512, 1024 and 2,048 bits) packed into a tiled store of
+    77 rows written in two row ranges; converted back to row-major by the
+    layout's definition, codes and scales equal the oracle's bit for bit."""
+    say("[sign_pack] tiled")
+    g = np.random.default_rng(512)
+    ks, N = [512, 1024, 2048], 77
+    S_row = sum(ks) // 512
+    store = torch.zeros(E.tiled_store_bytes(N, ks), dtype=torch.uint8, device=DEV)
+    scales = torch.zeros((N, len(ks)), dtype=torch.int16, device=DEV)
+    Xs = [g.standard_normal((N, k)).astype(np.float32) for k in ks]
+    Xs[0][3, :7] = [0.0, -0.0, 1e-30, -1e-30, 0.0, -1.0, 2.0]
+    step0 = 0
+    for u, (k, X) in enumerate(zip(ks, Xs)):
+        for r0, r1 in ((0, 40), (40, N)):
+            E.eogp_sign_pack_tiled(d(X[r0:r1]), store, r0, S_row, step0, scales[r0:r1, u:u + 1])
+        step0 += k // 512
+    torch.cuda.synchronize()
+    rows = rows_from_tiled(store.cpu().numpy(), S_row)[:N]
+    off = 0
+    sc = scales.cpu().numpy().view(np.uint16)
+    for u, (k, X) in enumerate(zip(ks, Xs)):
+        oc, os_ = O.encode(X)
+        assert np.array_equal(rows[:, off:off + k // 8], oc)
+        assert np.array_equal(sc[:, u], os_)
+        off += k // 8
+
+
+@pytest.mark.parametrize("N,ks,Q,topk", [
+    (5000, [16384], 16, 100),          # one module
+    (3000, [512, 1024, 512], 20, 37),  # several modules (ranges split across workgroups)
+    (19, [1024], 5, 10),               # less than one tile, fewer rows than topk
+    (600_000, [512], 16, 100),         # many blocks per workgroup
+])
+def test_score_topk_tiled_layout(N, ks, Q, topk):
+    """Scores and top-k of a tiled store equal the oracle's (and the
+    row-major entry point's) for the same bits."""
+    say(f"[score] tiled N={N} ks={ks} Q={Q}")
+    codes, scales, Y = random_store(N + 99, N, ks, Q)
+    tiled = d(tiled_from_rows(codes))
+    idx, sc, full = E.eogp_score_topk_tiled(tiled, d(scales.view(np.int16)), N, ks, d(Y), topk,
+                                            full_scores=True)
+    idx_r, sc_r, full_r = E.eogp_score_topk(d(codes), d(scales.view(np.int16)), ks, d(Y), topk,
+                                            full_scores=True)
+    torch.cuda.synchronize()
+    assert torch.equal(full, full_r) and torch.equal(idx, idx_r) and torch.equal(sc, sc_r)
+    rows = np.sort(np.random.default_rng(N).choice(N, min(N, 2000), replace=False))
+    ref = O.score(codes[rows], scales[rows], ks, Y)
+    assert np.array_equal(full.cpu().numpy()[:, rows], ref.astype(np.float32))
+    if N <= 5000:
+        oi, ov = O.topk(O.score(codes, scales, ks, Y), topk)
+        assert np.array_equal(idx.cpu().numpy(), oi)
+        assert np.array_equal(sc.cpu().numpy(), ov)
 
 
 # ---------------------------------------------------------------------------
