@@ -181,8 +181,10 @@ class Gpt2Step:
         self.Xall = torch.empty((Nt, U * self.k), dtype=f32, device=dev)
         self.Y = self.Xall[self.B:]
         g = S.torch_generator(w.config_id, 900001, dev)
-        self.codes = torch.randint(0, 256, (self.N_store, U * self.kb), dtype=torch.uint8,
-                                   device=dev, generator=g)
+        # the store in the tiled layout (32-row tiles, 2 KB per tile and 512-bit step)
+        self.steps_row = U * self.k // 512
+        self.codes = torch.randint(0, 256, (E.tiled_store_bytes(self.N_store, [self.k] * U),),
+                                   dtype=torch.uint8, device=dev, generator=g)
         self.scales = torch.exp(torch.randn((self.N_store, U), device=dev, generator=g)).half()
         self.scales = self.scales.view(torch.int16)
         ws = max(E.eogp_rotate_retain_workspace_size(p, Nt, self.T) for p in self.plans)
@@ -204,18 +206,19 @@ class Gpt2Step:
     def step(self, s):
         E = self.E
         slot = s % self.n_slots
-        codes = self.codes[slot * self.B:(slot + 1) * self.B]
-        scales = self.scales[slot * self.B:(slot + 1) * self.B]
+        row0 = slot * self.B
+        scales = self.scales[row0:row0 + self.B]
         k = self.k
         for u, (name, di, do) in enumerate(self.modules):
             E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
                                          Z=self.Z16, prec=self.prec, ws=self.ws)
             X = self.Xall[:, u * k:(u + 1) * k]
             E.eogp_pca_project(self.Z16, self.Pt[u], X=X, prec=self.pca_prec, ws=self.pca_ws)
-            E.eogp_sign_pack(X[:self.B], codes[:, u * self.kb:(u + 1) * self.kb],
-                             scales[:, u:u + 1])
-        E.eogp_score_topk(self.codes, self.scales, [k] * self.U, self.Y, self.topk,
-                          out_idx=self.out_idx, out_score=self.out_score, ws=self.score_ws)
+            E.eogp_sign_pack_tiled(X[:self.B], self.codes, row0, self.steps_row, u * (k // 512),
+                                   scales[:, u:u + 1])
+        E.eogp_score_topk_tiled(self.codes, self.scales, self.N_store, [k] * self.U, self.Y,
+                                self.topk, out_idx=self.out_idx, out_score=self.out_score,
+                                ws=self.score_ws)
 
     def prepare_srht(self):
         """Random draws of each module's SRHT (EOGP-R), resident on the device."""
@@ -231,18 +234,19 @@ class Gpt2Step:
         """One step of the EOGP-R variant: the SRHT replaces the PCA projection."""
         E = self.E
         slot = s % self.n_slots
-        codes = self.codes[slot * self.B:(slot + 1) * self.B]
-        scales = self.scales[slot * self.B:(slot + 1) * self.B]
+        row0 = slot * self.B
+        scales = self.scales[row0:row0 + self.B]
         k = self.k
         for u, (name, di, do) in enumerate(self.modules):
             E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
                                          Z=self.Z, prec=self.prec, ws=self.ws)
             X = self.Xall[:, u * k:(u + 1) * k]
             E.eogp_srht_project(self.Z, self.srht[u][0], self.srht[u][1], X=X)
-            E.eogp_sign_pack(X[:self.B], codes[:, u * self.kb:(u + 1) * self.kb],
-                             scales[:, u:u + 1])
-        E.eogp_score_topk(self.codes, self.scales, [k] * self.U, self.Y, self.topk,
-                          out_idx=self.out_idx, out_score=self.out_score, ws=self.score_ws)
+            E.eogp_sign_pack_tiled(X[:self.B], self.codes, row0, self.steps_row, u * (k // 512),
+                                   scales[:, u:u + 1])
+        E.eogp_score_topk_tiled(self.codes, self.scales, self.N_store, [k] * self.U, self.Y,
+                                self.topk, out_idx=self.out_idx, out_score=self.out_score,
+                                ws=self.score_ws)
 
     def prepare_total_bits(self):
         """The other reading of the workload's code length: 8,192 bits per
@@ -382,6 +386,17 @@ def sign_parity(bits_gpu, X_oracle):
             "mismatch_outside_band": int(outside.sum())}
 
 
+def store_rows(st, n_rows):
+    """Row-major codes [n_rows, U*k/8] of the first n_rows stored examples,
+    read out of the tiled store (row r = 32 t + i, step s, 16-byte piece p at
+    byte (t * S + s) * 2048 + (p % 2) * 1024 + ((p // 2) * 32 + i) * 16)."""
+    S_row = st.steps_row
+    tiles = -(-n_rows // 32)
+    t = st.codes[:tiles * S_row * 2048].cpu().numpy()
+    rows = t.reshape(tiles, S_row, 2, 2, 32, 16).transpose(0, 4, 1, 3, 2, 5)
+    return rows.reshape(tiles * 32, S_row * 64)[:n_rows]
+
+
 def cpu_baseline(st: Gpt2Step):
     import numpy as np
     import torch
@@ -408,7 +423,7 @@ def cpu_baseline(st: Gpt2Step):
         _, oscale = O.encode(X)
         per_shape[name] = (time.perf_counter() - t0) / n_ex
         # the bench's own codes of these examples (store rows 0.., module u)
-        cg = st.codes[:n_ex, u * st.kb:(u + 1) * st.kb].cpu().numpy()
+        cg = store_rows(st, n_ex)[:, u * st.kb:(u + 1) * st.kb]
         sg = st.scales[:n_ex, u].cpu().numpy().view(np.uint16).view(np.float16).astype(np.float64)
         so = oscale.view(np.float16).astype(np.float64)
         rec = sign_parity(O.unpack_bits(cg, st.k), X)
@@ -418,7 +433,7 @@ def cpu_baseline(st: Gpt2Step):
     per_example = len(st.modules) // len(st.shapes) * sum(per_shape.values())
     # queries of one step: same first stage + PCA, plus scoring against the store
     n_codes = 1000
-    codes = st.codes[:n_codes].cpu().numpy()
+    codes = store_rows(st, n_codes)
     scales = st.scales[:n_codes].cpu().numpy().view(np.uint16)
     Y = st.Y.cpu().numpy()
     t0 = time.perf_counter()
@@ -429,8 +444,8 @@ def cpu_baseline(st: Gpt2Step):
     # the GPU's scores of the same rows and queries (one extra call outside the
     # timed region, every score written)
     E = st.E
-    idx, val, full = E.eogp_score_topk(st.codes, st.scales, [st.k] * st.U, st.Y, st.topk,
-                                       full_scores=True, ws=None)
+    idx, val, full = E.eogp_score_topk_tiled(st.codes, st.scales, st.N_store, [st.k] * st.U, st.Y,
+                                             st.topk, full_scores=True)
     torch.cuda.synchronize()
     fg = full[:, :n_codes].cpu().numpy()
     exact = int(np.sum(fg == sc.astype(np.float32)))
@@ -655,26 +670,25 @@ def olmo_scoring(w, dev, n_queries=None):
     N, k, topk = w.N, w.k, w.topk
     Q = w.Q if n_queries is None else n_queries
     g = S.torch_generator(w.config_id, 910001, dev)
-    row = U * k // 8
-    codes = torch.empty((N, row), dtype=torch.uint8, device=dev)
-    step = max(1, (1 << 30) // row)
-    for i0 in range(0, N, step):
-        i1 = min(N, i0 + step)
-        codes[i0:i1] = torch.randint(0, 256, (i1 - i0, row), dtype=torch.uint8, device=dev,
-                                     generator=g)
+    ks = [k] * U
+    nbytes = E.tiled_store_bytes(N, ks)          # tiled layout (random bytes are a valid store)
+    codes = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    for i0 in range(0, nbytes, 1 << 30):
+        i1 = min(nbytes, i0 + (1 << 30))
+        codes[i0:i1] = torch.randint(0, 256, (i1 - i0,), dtype=torch.uint8, device=dev, generator=g)
     scales = torch.exp(torch.randn((N, U), device=dev, generator=g)).half().view(torch.int16)
     Y = torch.randn((Q, U * k), device=dev, generator=g)
-    ks = [k] * U
     ws = torch.empty(E.eogp_score_topk_workspace_size(N, Q, ks, topk), dtype=torch.uint8, device=dev)
     idx = torch.empty((Q, topk), dtype=torch.int64, device=dev)
     val = torch.empty((Q, topk), dtype=torch.float32, device=dev)
-    E.eogp_score_topk(codes, scales, ks, Y[:16], topk, out_idx=idx[:16], out_score=val[:16], ws=ws)
+    E.eogp_score_topk_tiled(codes, scales, N, ks, Y[:16], topk, out_idx=idx[:16],
+                            out_score=val[:16], ws=ws)
     torch.cuda.synchronize()
     for c in range(len(E.KERNEL_CLASSES)):
         E.eogp_timing_read(c)
     E.eogp_timing_enable(True)
     t0 = time.perf_counter()
-    E.eogp_score_topk(codes, scales, ks, Y, topk, out_idx=idx, out_score=val, ws=ws)
+    E.eogp_score_topk_tiled(codes, scales, N, ks, Y, topk, out_idx=idx, out_score=val, ws=ws)
     torch.cuda.synchronize()
     total_s = time.perf_counter() - t0
     pass_ms, passes = E.eogp_timing_read(E.KT_SCORE_PASS)
@@ -686,7 +700,8 @@ def olmo_scoring(w, dev, n_queries=None):
     gbs = bytes_per_pass / (avg * 1e-3) / 1e9
     hbm_bound_ms = passes * bytes_per_pass / (HBM_PEAK_GBS * 1e9) * 1e3
     mfma_bound_ms = 4.0 * Q * N * U * k / (INT8_PEAK_TOPS * 1e12) * 1e3
-    out = {"workload": w.name + " scoring", "codes": N, "modules": U, "bits_per_module": k,
+    out = {"workload": w.name + " scoring", "layout": "tiled", "codes": N, "modules": U,
+           "bits_per_module": k,
            "queries": Q, "topk": topk, "queries_per_pass": 16, "passes": passes,
            "bytes_per_pass": bytes_per_pass, "ms_per_pass": avg, "hbm_GBps": gbs,
            "peak_GBps": HBM_PEAK_GBS, "frac": gbs / HBM_PEAK_GBS,
@@ -707,26 +722,25 @@ def scoring_at_scale(args, dev):
     w = S.SCORING
     N, k, Q, topk = args.scoring_codes, w.k, args.scoring_queries, w.topk
     g = S.torch_generator(w.config_id, 1, dev)
-    codes = torch.empty((N, k // 8), dtype=torch.uint8, device=dev)
-    chunk = 1 << 20
-    for i0 in range(0, N, chunk):
-        i1 = min(N, i0 + chunk)
-        codes[i0:i1] = torch.randint(0, 256, (i1 - i0, k // 8), dtype=torch.uint8, device=dev,
-                                     generator=g)
+    nbytes = E.tiled_store_bytes(N, [k])       # tiled layout (random bytes are a valid store)
+    codes = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    for i0 in range(0, nbytes, 1 << 30):
+        i1 = min(nbytes, i0 + (1 << 30))
+        codes[i0:i1] = torch.randint(0, 256, (i1 - i0,), dtype=torch.uint8, device=dev, generator=g)
     scales = torch.exp(torch.randn((N, 1), device=dev, generator=g)).half().view(torch.int16)
     Y = torch.randn((Q, k), device=dev, generator=g)
     ws = torch.empty(E.eogp_score_topk_workspace_size(N, Q, [k], topk), dtype=torch.uint8,
                      device=dev)
     idx = torch.empty((Q, topk), dtype=torch.int64, device=dev)
     val = torch.empty((Q, topk), dtype=torch.float32, device=dev)
-    E.eogp_score_topk(codes, scales, [k], Y[:16], topk, out_idx=idx[:16], out_score=val[:16],
-                      ws=ws)                                   # warm-up
+    E.eogp_score_topk_tiled(codes, scales, N, [k], Y[:16], topk, out_idx=idx[:16],
+                            out_score=val[:16], ws=ws)         # warm-up
     torch.cuda.synchronize()
     for c in range(8):
         E.eogp_timing_read(c)
     E.eogp_timing_enable(True)
     t0 = time.perf_counter()
-    E.eogp_score_topk(codes, scales, [k], Y, topk, out_idx=idx, out_score=val, ws=ws)
+    E.eogp_score_topk_tiled(codes, scales, N, [k], Y, topk, out_idx=idx, out_score=val, ws=ws)
     torch.cuda.synchronize()
     total_s = time.perf_counter() - t0
     pass_ms, passes = E.eogp_timing_read(E.KT_SCORE_PASS)
@@ -741,7 +755,7 @@ def scoring_at_scale(args, dev):
     hbm_bound_ms = passes * bytes_per_pass / (HBM_PEAK_GBS * 1e9) * 1e3
     mfma_bound_ms = 4.0 * Q * N * k / (INT8_PEAK_TOPS * 1e12) * 1e3
     return {
-        "workload": w.name,
+        "workload": w.name, "layout": "tiled",
         "codes": N, "bits": k, "queries": Q, "topk": topk,
         "queries_per_pass": 16, "passes": passes,
         "bytes_per_pass": bytes_per_pass,

@@ -555,10 +555,18 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
 
 constexpr int PT = 256;   // k_gemm_p: threads per workgroup
 
+// The pipelined kernel reads B through a range-checked buffer descriptor when
+// the last column tile is padded and the rows fit a 31-bit byte range.
+inline bool use_buffer_b(const GemmArgs& g) {
+  return g.N % 256 != 0 && (double)g.N * (double)g.ldb * 2.0 < 2147483648.0;
+}
+
 // AT: 0 = fp32 A, 1 = 16-bit A used as it is, 2 = bf16 A widened, scaled
 // and rounded to fp16 while it is staged (all with 16-byte aligned rows); B is
 // a padded panel; one part each; no split-K.
-template <int AT, bool F16, bool SC>
+// BB: B through a range-checked buffer descriptor (padding rows skipped);
+// else plain loads with padding rows mapped to row 0.
+template <int AT, bool F16, bool SC, bool BB>
 __global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_gemm_p(KParams kp) {
   constexpr int BNP = 256;
@@ -660,11 +668,21 @@ void k_gemm_p(KParams kp) {
       if constexpr (AT == 0) pa32[q] = static_cast<const float*>(g.A) + a_off[q] + 4 * a_pc;
       else pa16[q] = static_cast<const uint16_t*>(g.A) + a_off[q] + 8 * a_pc;
     }
+    // BB: B through a buffer descriptor covering its first N rows: the rows of
+    // the last column tile at or beyond N (padding) read as zeros without a
+    // memory access, so the load path carries no padding (their products land
+    // in output columns that are never stored or never read). The host uses
+    // BB only when N * ldb * 2 < 2^31.
+    const uint32_t b_bytes = BB ? (uint32_t)(N * g.ldb * 2) : 0u;
+    const __amdgpu_buffer_rsrc_t b_rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)g.B_hi, (short)0, (int)b_bytes, 0x00020000);
+    uint32_t b_vo[BQ];   // byte offset of the lane's 16 bytes at k = 0
     int64_t b_off[BQ];
     const uint16_t* pb[BQ];
 #pragma unroll
     for (int q = 0; q < BQ; ++q) {
       const int64_t brow = n0 + b_r0 + 64 * q;
+      b_vo[q] = brow < N ? (uint32_t)(2 * (brow * g.ldb + 8 * b_pc)) : b_bytes;
       b_off[q] = (brow < N ? brow : 0) * g.ldb + 8 * b_pc;
       pb[q] = g.B_hi + b_off[q];
     }
@@ -696,8 +714,13 @@ void k_gemm_p(KParams kp) {
     };
     auto load_b = [&](int64_t k0, BRegs& R) {
 #pragma unroll
-      for (int q = 0; q < BQ; ++q)
-        R.rb[q] = *(const __attribute__((address_space(1))) v4u*)(pb[q] + k0);
+      for (int q = 0; q < BQ; ++q) {
+        if constexpr (BB)
+          R.rb[q] = __builtin_bit_cast(
+              v4u, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, b_vo[q] + (uint32_t)(2 * k0), 0, 0));
+        else
+          R.rb[q] = *(const __attribute__((address_space(1))) v4u*)(pb[q] + k0);
+      }
     };
     // The ragged slice: element-wise, bounds-checked (B is a padded panel, so
     // its columns up to round_up(K, 32) are readable and zero beyond K).
@@ -984,10 +1007,14 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
       if (grid >= kXcds) grid = grid / kXcds * kXcds;
       if (g.sched) hipLaunchKernelGGL(k_zero_sched, dim3(1), dim3(64), 0, s, g.sched);
       timing::Scope ts(g.timing_class, s);
-      if (F16 && g.a_scale != 1.f)
-        hipLaunchKernelGGL((k_gemm_p<AT, F16, true>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
-      else
-        hipLaunchKernelGGL((k_gemm_p<AT, F16, false>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
+      const bool bb = use_buffer_b(g);
+      if (F16 && g.a_scale != 1.f) {
+        if (bb) hipLaunchKernelGGL((k_gemm_p<AT, F16, true, true>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
+        else hipLaunchKernelGGL((k_gemm_p<AT, F16, true, false>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
+      } else {
+        if (bb) hipLaunchKernelGGL((k_gemm_p<AT, F16, false, true>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
+        else hipLaunchKernelGGL((k_gemm_p<AT, F16, false, false>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
+      }
       EOGP_LAUNCH_CHECK("gemm launch");
       if (kq.splits > 1) {
         split_sum(g, kq.splits, s);
@@ -1055,17 +1082,24 @@ eogp_status gemm_nt2(const GemmArgs& g1, const GemmArgs& g2, AType a_type, int a
   hipLaunchKernelGGL(k_zero_sched, dim3(1), dim3(64), 0, s, g1.sched);
   timing::Scope ts(g1.timing_class, s);
   const dim3 gd((unsigned)grid), bd(PT);
+  const bool bb = use_buffer_b(g1) && use_buffer_b(g2);
+#define EOGP_GEMM_P2(AT_, F16_, SC_)                                                   \
+  do {                                                                                 \
+    if (bb) hipLaunchKernelGGL((k_gemm_p<AT_, F16_, SC_, true>), gd, bd, 0, s, kq);    \
+    else hipLaunchKernelGGL((k_gemm_p<AT_, F16_, SC_, false>), gd, bd, 0, s, kq);      \
+  } while (0)
   if (a_type == AType::F32) {
-    if (f16 && sc) hipLaunchKernelGGL((k_gemm_p<0, true, true>), gd, bd, 0, s, kq);
-    else if (f16) hipLaunchKernelGGL((k_gemm_p<0, true, false>), gd, bd, 0, s, kq);
-    else hipLaunchKernelGGL((k_gemm_p<0, false, false>), gd, bd, 0, s, kq);
+    if (f16 && sc) EOGP_GEMM_P2(0, true, true);
+    else if (f16) EOGP_GEMM_P2(0, true, false);
+    else EOGP_GEMM_P2(0, false, false);
   } else if (a_type == AType::BF16_AS_F16) {
-    if (sc) hipLaunchKernelGGL((k_gemm_p<2, true, true>), gd, bd, 0, s, kq);
-    else hipLaunchKernelGGL((k_gemm_p<2, true, false>), gd, bd, 0, s, kq);
+    if (sc) EOGP_GEMM_P2(2, true, true);
+    else EOGP_GEMM_P2(2, true, false);
   } else {
-    if (f16) hipLaunchKernelGGL((k_gemm_p<1, true, false>), gd, bd, 0, s, kq);
-    else hipLaunchKernelGGL((k_gemm_p<1, false, false>), gd, bd, 0, s, kq);
+    if (f16) EOGP_GEMM_P2(1, true, false);
+    else EOGP_GEMM_P2(1, false, false);
   }
+#undef EOGP_GEMM_P2
   EOGP_LAUNCH_CHECK("gemm launch (two products)");
   return EOGP_OK;
 }

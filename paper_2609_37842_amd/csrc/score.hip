@@ -638,11 +638,11 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
   }
 }
 
-// Multi-module scores from the exact per-module dots: one thread per stored
-// row, the 16 queries of the group in registers; for u = 0 .. U-1 in order,
-// score += s_{i,u} * n * 2^-f (each term exact in fp64), then the rows are
-// offered to the per-query candidate lists as in k_score. Workgroups walk
-// blocks of 256 rows at a fixed stride.
+// Multi-module scores from the exact per-module dots: wave w of a workgroup
+// takes queries 4w .. 4w+3 of the group for 64 consecutive stored rows (one
+// per lane); for u = 0 .. U-1 in order, score += s_{i,u} * n * 2^-f (each
+// term exact in fp64), then the rows are offered to the per-query candidate
+// lists as in k_score. Workgroups walk blocks of 64 rows at a fixed stride.
 struct FoldArgs {
   const void* part;           // [U][QB][N] int32 or int64
   const uint16_t* scales;     // [N][U] fp16 bits
@@ -657,11 +657,14 @@ struct FoldArgs {
   uint32_t* cidx;
 };
 constexpr int FOLD_THR = 256;
+constexpr int FOLD_ROWS = 64;
+constexpr int FOLD_QW = QB / (FOLD_THR / 64);   // queries per wave
 
 template <int CAP, bool N64>
 __global__ __launch_bounds__(FOLD_THR) void k_score_fold(FoldArgs a) {
   __shared__ Cand<CAP> cd;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int q0 = __builtin_amdgcn_readfirstlane((tid >> 6) * FOLD_QW);   // wave-uniform
   const cptr<int32_t> cfq = (cptr<int32_t>)(a.fq);
   if (tid < QB) {
     cd.cnt[tid] = 0;
@@ -671,38 +674,41 @@ __global__ __launch_bounds__(FOLD_THR) void k_score_fold(FoldArgs a) {
   __syncthreads();
   const int32_t* p32 = static_cast<const int32_t*>(a.part);
   const int64_t* p64 = static_cast<const int64_t*>(a.part);
-  for (int64_t r0 = (int64_t)blockIdx.x * FOLD_THR; r0 < a.N; r0 += (int64_t)gridDim.x * FOLD_THR) {
-    const int64_t row = r0 + tid;
+  for (int64_t r0 = (int64_t)blockIdx.x * FOLD_ROWS; r0 < a.N;
+       r0 += (int64_t)gridDim.x * FOLD_ROWS) {
+    const int64_t row = r0 + lane;
     const bool ok = row < a.N;
     const int64_t rowc = ok ? row : a.N - 1;
-    double sc[QB];
+    double sc[FOLD_QW];
 #pragma unroll
-    for (int q = 0; q < QB; ++q) sc[q] = 0.0;
+    for (int j = 0; j < FOLD_QW; ++j) sc[j] = 0.0;
+#pragma unroll 4
     for (int u = 0; u < a.U; ++u) {
       const double sv = (double)f16_bits_to_f32(a.scales[rowc * a.U + u]);
-      const int64_t mo = (a.grp * a.U + u) * QB;
+      const int64_t mo = (a.grp * a.U + u) * QB + q0;
 #pragma unroll
-      for (int q = 0; q < QB; ++q) {
-        const int64_t o = ((int64_t)u * QB + q) * a.N + rowc;
+      for (int j = 0; j < FOLD_QW; ++j) {
+        const int64_t o = ((int64_t)u * QB + q0 + j) * a.N + rowc;
         const int64_t nn = N64 ? p64[o] : (int64_t)p32[o];
-        sc[q] += ldexp(sv * (double)nn, -cfq[mo + q]);
+        sc[j] += ldexp(sv * (double)nn, -cfq[mo + j]);
       }
     }
     uint32_t pend = 0;
 #pragma unroll
-    for (int q = 0; q < QB; ++q) {
-      const int64_t qg = a.grp * QB + q;
+    for (int j = 0; j < FOLD_QW; ++j) {
+      const int64_t qg = a.grp * QB + q0 + j;
       if (ok && qg < a.Q) {
-        if (a.full) a.full[qg * a.N + row] = (float)sc[q];
-        pend |= 1u << q;
+        if (a.full) a.full[qg * a.N + row] = (float)sc[j];
+        pend |= 1u << j;
       }
     }
     for (;;) {
 #pragma unroll
-      for (int q = 0; q < QB; ++q) {
-        const uint32_t bit = 1u << q;
+      for (int j = 0; j < FOLD_QW; ++j) {
+        const uint32_t bit = 1u << j;
+        const int q = q0 + j;
         if (pend & bit) {
-          const uint64_t key = order_key(sc[q]);
+          const uint64_t key = order_key(sc[j]);
           if (key < cd.thr[q]) {
             pend &= ~bit;
           } else {
@@ -829,7 +835,7 @@ Layout layout(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t topk
     const int64_t units = std::max<int64_t>(1, n_blocks * L.n_rng);
     L.grid = std::min<int64_t>(units, kCus);
     if (L.grid >= kXcds) L.grid = L.grid / kXcds * kXcds;
-    L.fold_grid = std::max<int64_t>(1, std::min<int64_t>(ceil_div(N, FOLD_THR), 2 * kCus));
+    L.fold_grid = std::max<int64_t>(1, std::min<int64_t>(ceil_div(N, FOLD_ROWS), 2 * kCus));
     lists = L.fold_grid;
     L.n64 = kmax > (1 << 16);   // |n| <= k 2^14 fits 32 bits up to k = 2^16
   }
