@@ -4,12 +4,22 @@
 // transform in Sylvester order (entry (r, i) = (-1)^popcount(r & i)),
 //   x_c = W(D J z)[rows[c]] / sqrt(k).
 //
-// p <= 32768: one workgroup per row. The row is read once (coalesced),
-// multiplied by the random signs and zero-padded into LDS; the butterfly
-// stages run in LDS two at a time (radix 4: each thread combines four elements
-// h apart), one radix-2 stage first when log2 p is odd; the kept rows are then
-// gathered and scaled. Cost: p log2 p additions per row, HBM traffic m + k
-// floats per row.
+// 1024 <= p <= 16384: one 256-thread workgroup per row, E = p / 256 values per
+// thread in registers. The transform is separable over the bits of the index,
+// and each bit's butterflies are applied once: (a) element t + 256 j of the
+// signed, zero-padded row is loaded into register j of thread t (coalesced) and
+// the bits 8 .. log2 p - 1 (those of j) are transformed in registers; (b) the
+// values go to LDS (one pad word per 64, so the next reads are free of bank
+// conflicts) and thread t takes elements E t .. E t + E - 1, transforms the low
+// log2 E bits in registers and the bits log2 E .. 7 (those of the lane index)
+// across lanes (DPP or shuffles); (c) the result goes to LDS once more and the
+// kept rows are gathered and scaled. LDS traffic: three row writes/reads and
+// the gather, against two per radix-4 stage before.
+//
+// Other p <= 32768: one workgroup per row, the butterfly stages in LDS two at a time
+// (radix 4: each thread combines four elements h apart), one radix-2 stage
+// first when log2 p is odd. Cost either way: p log2 p additions per row, HBM
+// traffic m + k floats per row.
 //
 // p > 32768 (up to 2^20): W_p = W_p1 (x) W_p2 in Sylvester order (index
 // i = i1 p2 + i2, p2 = 32768, p1 = p / p2 <= 32). One workgroup per (row,
@@ -19,6 +29,7 @@
 //   x_c = sum_j (-1)^popcount(r1 & j) S[j p2 + r2] / sqrt(k).
 // Extra HBM traffic: p floats written and k p1 read per row.
 #include <cmath>
+#include <type_traits>
 
 #include "common.h"
 #include "timing.h"
@@ -56,6 +67,98 @@ __device__ __forceinline__ void fwht_lds(float* L, int logp) {
       L[base + 3 * h] = b1 - b3;
     }
     __syncthreads();
+  }
+}
+
+// Unnormalised Walsh-Hadamard transform of E values in registers (index j).
+template <int E>
+__device__ __forceinline__ void fwht_regs(float (&v)[E]) {
+#pragma unroll
+  for (int h = 1; h < E; h <<= 1)
+#pragma unroll
+    for (int j = 0; j < E; ++j)
+      if ((j & h) == 0) {
+        const float a = v[j], b = v[j + h];
+        v[j] = a + b;
+        v[j + h] = a - b;
+      }
+}
+
+// The value of lane (lane ^ 2^b) (b < 6): DPP within quads for b < 2.
+template <int B>
+__device__ __forceinline__ float lane_xor(float x) {
+  if constexpr (B == 0)
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
+  else if constexpr (B == 1)
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));
+  else
+    return __shfl_xor(x, 1 << B);
+}
+
+__device__ __forceinline__ int srht_pad(int idx) { return idx + (idx >> 6); }
+
+template <int LOGP>
+__global__ __launch_bounds__(256) void k_srht_reg(const float* __restrict__ Z, int64_t ldz, int m,
+                                                  const int8_t* __restrict__ signs,
+                                                  const int32_t* __restrict__ rows, int k,
+                                                  float scale, float* __restrict__ X, int64_t ldx) {
+  constexpr int P = 1 << LOGP, E = P >> 8, LE = LOGP - 8;
+  static_assert(LOGP >= 10 && LOGP <= 14, "lane bits 0 .. 7 - log2 E must lie inside a wave");
+  extern __shared__ float L[];
+  const int t = threadIdx.x;
+  const int64_t i = blockIdx.x;
+  const float* z = Z + i * ldz;
+  float v[E];
+  // (a) element t + 256 j into register j: loads at clamped indices, selected
+  // afterwards (no branches, so all of them are in flight at once)
+  int8_t sg[E];
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    const int idx = min(t + 256 * j, m - 1);
+    v[j] = z[idx];
+    sg[j] = signs[idx];
+  }
+#pragma unroll
+  for (int j = 0; j < E; ++j) {
+    const bool in = t + 256 * j < m;
+    v[j] = in ? (sg[j] < 0 ? -v[j] : v[j]) : 0.f;
+  }
+  fwht_regs<E>(v);                                  //     bits 8 .. LOGP - 1
+#pragma unroll
+  for (int j = 0; j < E; ++j) L[srht_pad(t + 256 * j)] = v[j];
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < E; ++e) v[e] = L[srht_pad(E * t + e)];   // (b) bits 0 .. LE - 1
+  fwht_regs<E>(v);
+  auto cross = [&](auto b_c) __attribute__((always_inline)) {  //     bit LE + b, lane bit b
+    constexpr int B = decltype(b_c)::value;
+    const bool hi = (t >> B) & 1;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      const float o = lane_xor<B>(v[e]);
+      v[e] = hi ? o - v[e] : v[e] + o;
+    }
+  };
+  if constexpr (8 - LE > 0) cross(std::integral_constant<int, 0>{});
+  if constexpr (8 - LE > 1) cross(std::integral_constant<int, 1>{});
+  if constexpr (8 - LE > 2) cross(std::integral_constant<int, 2>{});
+  if constexpr (8 - LE > 3) cross(std::integral_constant<int, 3>{});
+  if constexpr (8 - LE > 4) cross(std::integral_constant<int, 4>{});
+  if constexpr (8 - LE > 5) cross(std::integral_constant<int, 5>{});
+  __syncthreads();                                  // every (b) read is done
+#pragma unroll
+  for (int e = 0; e < E; ++e) L[srht_pad(E * t + e)] = v[e];   // (c)
+  __syncthreads();
+  // gather of the kept rows (k <= p, so at most E per thread): every index
+  // requested before the first is used
+  float* x = X + i * ldx;
+  int r[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) r[e] = rows[min(t + 256 * e, k - 1)];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int c = t + 256 * e;
+    if (c < k) x[c] = (r[e] >= 0 && r[e] < P) ? L[srht_pad(r[e])] * scale : __builtin_nanf("");
   }
 }
 
@@ -156,6 +259,30 @@ eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, cons
     if (st != EOGP_OK) return st;
   }
   const float scale = (float)(1.0 / std::sqrt((double)k));
+  if (logp >= 10 && logp <= 14) {
+    const void* fns[5] = {(const void*)k_srht_reg<10>, (const void*)k_srht_reg<11>,
+                          (const void*)k_srht_reg<12>, (const void*)k_srht_reg<13>,
+                          (const void*)k_srht_reg<14>};
+    const int lds = (int)(sizeof(float) * (((size_t)1 << logp) + ((size_t)1 << logp) / 64));
+    const eogp_status st = ensure_dynamic_lds(fns[logp - 10], lds);
+    if (st != EOGP_OK) return st;
+    timing::Scope ts(EOGP_KT_SRHT, s);
+    for (int64_t r0 = 0; r0 < N; r0 += 0x7FFFFFFF) {
+      const int64_t nr = std::min<int64_t>(N - r0, 0x7FFFFFFF);
+      const dim3 g((unsigned)nr), b(256);
+      const float* z0 = Z + r0 * ldz;
+      float* x0 = X + r0 * ldx;
+      switch (logp) {
+        case 10: hipLaunchKernelGGL(k_srht_reg<10>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        case 11: hipLaunchKernelGGL(k_srht_reg<11>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        case 12: hipLaunchKernelGGL(k_srht_reg<12>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        case 13: hipLaunchKernelGGL(k_srht_reg<13>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        default: hipLaunchKernelGGL(k_srht_reg<14>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+      }
+    }
+    EOGP_LAUNCH_CHECK("srht_project");
+    return EOGP_OK;
+  }
   timing::Scope ts(EOGP_KT_SRHT, s);
   if (logp <= kSrhtMaxLog) {
     const int p = 1 << logp;

@@ -626,6 +626,8 @@ def test_ekfac_fp16_mode_input_exponents():
 @pytest.mark.parametrize("N,m,k", [
     (5, 1, 1), (7, 3, 4), (9, 512, 128), (4, 700, 300), (3, 16384, 8192), (2, 32768, 16384),
     (0, 64, 8),
+    # every width of the register form (p = 2^10 .. 2^15), k up to p
+    (4, 1500, 700), (3, 3000, 3000), (2, 5000, 8192), (3, 9000, 16384),
     # two-stage form (p > 32768): padded 40000 -> 65536, the OLMo-2-32B-shaped
     # module (m = 65,536, k = 32,768), the paper's timing configuration
     # (m = 262,144, k = 2,048), and the largest supported width
