@@ -63,6 +63,9 @@ def parse(argv=None):
     ap.add_argument("--pca-prec", choices=["accurate", "fast"], default="fast",
                     help="PCA projection with fp16 P (fast = fp16 coordinates, as the paper caches them)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--step-only", action="store_true",
+                    help="only the GPT-2-shaped steps (no EOGP-R, EK-FAC, PCA-fit or "
+                         "total-bits legs; for counter runs)")
     ap.add_argument("--no-scoring", action="store_true", help="skip the scoring-at-scale pass")
     ap.add_argument("--scoring-queries", type=int, default=512)
     ap.add_argument("--scoring-codes", type=int, default=8 * 1024 * 1024)
@@ -293,6 +296,23 @@ class Gpt2Step:
             p = self.plans[u]
             per_tok = 2 * (do * p.n_rows + di * p.n_cols)
             tot += per_tok * (self.valid_tokens + self.valid_q_tokens)
+        return tot
+
+    def rotation_executed_flops_per_step(self):
+        """MFMA flops the rotation launches execute: the compacted token rows
+        (each example's run padded to a multiple of 8 in the 16-bit modes)
+        rounded up to the 256-row tile, the used eigenvectors rounded up to the
+        256-column tile, the width rounded up to the 32-deep slice."""
+        import math
+        lens = self.mask.sum(dim=1).tolist()
+        rows = sum(-(-int(v) // 8) * 8 for v in lens) if self.prec != self.E.PREC_ACCURATE \
+            else sum(int(v) for v in lens)
+        rows = -(-rows // 256) * 256
+        up = lambda x, q: -(-x // q) * q
+        tot = 0
+        for u, (name, di, do) in enumerate(self.modules):
+            p = self.plans[u]
+            tot += 2 * rows * (up(do, 32) * up(p.n_rows, 256) + up(di, 32) * up(p.n_cols, 256))
         return tot
 
     def rotation_bytes_per_step(self):
@@ -826,6 +846,7 @@ def main(argv=None):
         bytes_launch = st.rotation_bytes_per_step() * args.steps / max(1, rot_n)
         avg_ms = rot_ms / max(1, rot_n)
         achieved = flops_launch / (avg_ms * 1e-3) / 1e12
+        exec_launch = st.rotation_executed_flops_per_step() * args.steps / max(1, rot_n)
         passes = 3 if st.prec == E.PREC_ACCURATE else 1
         trec = profiled_traffic() if st.prec == E.PREC_F16 else None
         traffic = trec["traffic_bytes_per_launch"] if trec else None
@@ -862,6 +883,11 @@ def main(argv=None):
                 "traffic": traffic,
                 "mfma_passes_per_flop": passes,
                 "executed_frac": passes * achieved / BF16_PEAK_TFLOPS,
+                "executed_flops_per_launch": exec_launch,
+                "executed_tflops": exec_launch * passes / (avg_ms * 1e-3) / 1e12,
+                "executed_frac_with_padding": exec_launch * passes / (avg_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                "limiter": ("vector-memory data path: TD busy 0.88, TA 0.53, MFMA busy 0.42 at "
+                            "1.80 GHz (profiles/rotation_gemm_counters.md)"),
                 "alg_flops_per_launch": flops_launch,
                 "alg_bytes_per_launch": bytes_launch,
                 "traffic_source": ("profiles/rotation_gemm_traffic.md (FETCH_SIZE x "
@@ -880,6 +906,9 @@ def main(argv=None):
                                      for u, (name, _, _) in enumerate(st.shapes)},
         })
         log(f"step {ms_per_step:.2f} ms, {value:.1f} ex/s, rotation {achieved:.1f} TFLOP/s alg")
+        if args.step_only:
+            print(json.dumps(out))
+            return 0
         # EOGP-R: the same step with the SRHT second stage (Appendix B.2)
         st.prepare_srht()
         nr = max(1, args.steps // 4)
