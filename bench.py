@@ -886,8 +886,9 @@ def main(argv=None):
                 "executed_flops_per_launch": exec_launch,
                 "executed_tflops": exec_launch * passes / (avg_ms * 1e-3) / 1e12,
                 "executed_frac_with_padding": exec_launch * passes / (avg_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
-                "limiter": ("vector-memory data path: TD busy 0.88, TA 0.53, MFMA busy 0.42 at "
-                            "1.80 GHz (profiles/rotation_gemm_counters.md)"),
+                "limiter": ("slice loop: L2 loads, LDS stores + fragment reads and MFMA each near a "
+                            "slice's MFMA time, one wave per SIMD; MFMA busy 0.42 at 1.80 GHz "
+                            "(profiles/rotation_gemm_counters.md)"),
                 "alg_flops_per_launch": flops_launch,
                 "alg_bytes_per_launch": bytes_launch,
                 "traffic_source": ("profiles/rotation_gemm_traffic.md (FETCH_SIZE x "
