@@ -12,6 +12,8 @@ struct eogp_plan {
   int64_t ld_out = 0;      // panel row length for Q_S columns (>= d_out, multiple of 32)
   int64_t ld_in = 0;       // panel row length for Q_A columns (>= d_in, multiple of 32)
   int64_t n_tiles = 0;     // active 32x32 (row, column) blocks
+  int64_t n_groups = 0;    // groups of active blocks sharing one operand block
+  bool group_rows = true;  // groups share a row block of S~ (else a column block of A~)
   int device = 0;
 
   // Device arrays, all owned by the plan (one allocation, `mem`).
@@ -19,6 +21,8 @@ struct eogp_plan {
   int32_t* ret_flat = nullptr;   // [m]   j*d_in + k, canonical order
   float* ret_w = nullptr;        // [m]   (Lambda_r + lambda)^-1/2
   int32_t* tiles = nullptr;      // [n_tiles][4] = {row block, col block, entry begin, entry end}
+  int32_t* groups = nullptr;     // [n_groups][4] = {first position in gtiles, count, shared block, 0}
+  int32_t* gtiles = nullptr;     // [n_tiles] tile indices, group by group
   int32_t* ent_r = nullptr;      // [m]   retained position of each entry, grouped by tile
   uint16_t* ent_loc = nullptr;   // [m]   (row in block) * 32 + (col in block)
   int32_t* ent_pos = nullptr;    // [m]   entry index of each retained position (inverse of ent_r)
@@ -37,6 +41,7 @@ struct eogp_plan {
 namespace eogp {
 constexpr int kPanelTile = 256;   // widest GEMM column tile; panels are padded to it
 constexpr int kBlk = 32;          // retained-product block edge
+constexpr int kRetGroup = 2;      // active blocks per group at most
 
 eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double damping,
                        int64_t m, const float* Q_A, const float* Q_S, hipStream_t s,

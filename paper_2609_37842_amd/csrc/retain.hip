@@ -130,67 +130,79 @@ __global__ __launch_bounds__(256) void k_retained(const float* __restrict__ St, 
   }
 }
 
-// 16-bit intermediates (fp16, or bf16 with BF): S~ and A~ in MFMA-fragment order (for every 32 rows j
-// and 16 tokens t one contiguous 1 KB block, j-major, 16 tokens per j; token
-// capacity ldt, at least 16 kRet16Unroll + 16 tokens past the last run);
-// example i's tokens are t = off[i] .. off[i] + len[i] - 1,
-// off[i] a multiple of 8. One wave per (active block, example) as above; each
-// v_mfma_f32_32x32x16_f16 takes 16 tokens: lane l feeds row l % 32 and tokens
-// 8 (l / 32) .. +7 of each operand with one 16-byte load (the wave reads one
-// whole 1 KB block, or two halves of neighbouring blocks when the run starts
-// at an odd multiple of 8). Tokens past the example's last one (padding, or
-// the next example) are zeroed in both operands before they reach the MFMA.
-constexpr int kRet16Unroll = 8;
+// 16-bit intermediates (fp16, or bf16 with BF): S~ and A~ in MFMA-fragment
+// order (for every 32 rows j and 16 tokens t one contiguous 1 KB block, j-major,
+// 16 tokens per j; token capacity ldt, at least 16 kRetGUnroll + 16 tokens past
+// the last run); example i's tokens are t = off[i] .. off[i] + len[i] - 1,
+// off[i] a multiple of 8. One wave per (group of up to kRetGroup active blocks
+// that share one operand block, example): SR, the group shares a row block of
+// S~ (else a column block of A~). Each v_mfma_f32_32x32x16_f16 takes 16
+// tokens: lane l feeds row l % 32 and tokens 8 (l / 32) .. +7 of each operand
+// with one 16-byte load (the wave reads one whole 1 KB block, or two halves of
+// neighbouring blocks when the run starts at an odd multiple of 8); a 16-token
+// step loads the shared block once and the other operand of every member, so
+// a group of L blocks loads 1 + L blocks per step instead of 2 L. Batches of
+// kRetGUnroll steps: all loads of a batch are issued first (a batch may read
+// up to 16 kRetGUnroll + 8 tokens past the run, inside the buffer's slack),
+// then the steps that hold tokens of the run are multiplied, the last one with
+// the tokens past the run (padding, or the next example) zeroed in both
+// operands.
+constexpr int kRetGUnroll = 4;
 
-template <bool BF>
-__global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__ St,
-                                                    const uint16_t* __restrict__ At, int64_t ldt,
-                                                    const int32_t* __restrict__ ex_off,
-                                                    const int32_t* __restrict__ ex_len,
-                                                    const int32_t* __restrict__ tiles, int n_tiles,
-                                                    const uint16_t* __restrict__ ent_loc,
-                                                    float out_scale, float* __restrict__ Zt,
-                                                    int64_t m, int64_t ex0, int64_t nex) {
+template <bool BF, bool SR>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4)))
+void k_retained16g(const uint16_t* __restrict__ St, const uint16_t* __restrict__ At, int64_t ldt,
+                   const int32_t* __restrict__ ex_off, const int32_t* __restrict__ ex_len,
+                   const int32_t* __restrict__ groups, int n_groups, const int32_t* __restrict__ gtiles,
+                   const int32_t* __restrict__ tiles, const uint16_t* __restrict__ ent_loc,
+                   float out_scale, float* __restrict__ Zt, int64_t m, int64_t ex0, int64_t nex) {
   typedef unsigned int v4u __attribute__((ext_vector_type(4)));
   __shared__ float blk[kRetWaves][32][33];
-  const int wid = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  // Workgroup b runs on XCD b % kXcds: the tile groups of one example all go
-  // to one XCD (examples dealt round-robin over the XCDs), so the example's S~
+  // wave index as a wave-uniform value, so that group data sit in scalar registers
+  const int wid = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)), lane = threadIdx.x & 63;
+  // Workgroup b runs on XCD b % kXcds: the groups of one example all go to
+  // one XCD (examples dealt round-robin over the XCDs), so the example's S~
   // and A~ blocks are fetched into one L2.
-  const int gx = (n_tiles + kRetWaves - 1) / kRetWaves;
+  const int gx = (n_groups + kRetWaves - 1) / kRetWaves;
   const int xb = blockIdx.x % kXcds, rb = blockIdx.x / kXcds;
   const int64_t ex_local = xb + (int64_t)kXcds * (rb / gx);
   if (ex_local >= nex) return;                 // whole workgroup leaves; no block barrier below
-  const int tile = (rb % gx) * kRetWaves + wid;
-  if (tile >= n_tiles) return;                 // whole wave leaves
+  const int grp = (rb % gx) * kRetWaves + wid;
+  if (grp >= n_groups) return;                 // whole wave leaves
   const int64_t i = ex0 + ex_local;
-  const int jb = tiles[4 * tile + 0], kb = tiles[4 * tile + 1];
-  const int e0 = tiles[4 * tile + 2], e1 = tiles[4 * tile + 3];
+  const int g0 = groups[4 * grp + 0], gc = groups[4 * grp + 1], shb = groups[4 * grp + 2];
   const int64_t t0 = ex_off[i] + 8 * (lane >> 5);   // this lane's first token
   const int n = ex_len[i];
   const int half = lane >> 5, col = lane & 31;
-  const int64_t groups = ldt / 16;
-  // element offset of (row block b, this lane's row, token t), t a multiple of 8
-  auto at_tok = [&](int64_t b, int64_t t) { return ((b * groups + (t >> 4)) * 32 + col) * 16 + (t & 15); };
-  const uint16_t* sp = St + at_tok(jb, t0);
-  const uint16_t* ap = At + at_tok(kb, t0);
-  // Advancing 16 tokens moves a lane one block (512 elements) on.
-  f32x16 acc;
+  const int64_t steps = ldt / 16;
+  // element offset of (block b, this lane's row, token t) is b * bstride + lane_off + 512 (t - t0) / 16
+  const int64_t bstride = steps * 512;
+  const int64_t lane_off = ((t0 >> 4) * 32 + col) * 16 + (t0 & 15);
+  const uint16_t* shp = (SR ? St : At) + shb * bstride + lane_off;
+  const uint16_t* vbase = (SR ? At : St) + lane_off;
+  int vb[kRetGroup];                           // the other operand's block of each member
 #pragma unroll
-  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-  // Batches of kRet16Unroll steps: all loads of a batch are issued first (a
-  // batch may read up to 16 kRet16Unroll tokens past the run, inside the
-  // buffer's slack), then the steps that hold tokens of the run are
-  // multiplied, the last one with the tokens past the run zeroed.
-  for (int t = 0; t < n; t += 16 * kRet16Unroll) {
-    v4u a[kRet16Unroll], b[kRet16Unroll];
+  for (int c = 0; c < kRetGroup; ++c) {
+    const int tile = gtiles[g0 + (c < gc ? c : gc - 1)];
+    vb[c] = SR ? tiles[4 * tile + 1] : tiles[4 * tile + 0];
+  }
+  f32x16 acc[kRetGroup];
 #pragma unroll
-    for (int u = 0; u < kRet16Unroll; ++u) {
-      a[u] = *reinterpret_cast<const v4u*>(sp + (int64_t)(t / 16 + u) * 512);
-      b[u] = *reinterpret_cast<const v4u*>(ap + (int64_t)(t / 16 + u) * 512);
-    }
+  for (int c = 0; c < kRetGroup; ++c)
 #pragma unroll
-    for (int u = 0; u < kRet16Unroll; ++u) {
+    for (int r = 0; r < 16; ++r) acc[c][r] = 0.f;
+  for (int t = 0; t < n; t += 16 * kRetGUnroll) {
+    v4u a[kRetGUnroll], b[kRetGroup][kRetGUnroll];
+#pragma unroll
+    for (int u = 0; u < kRetGUnroll; ++u) a[u] = *reinterpret_cast<const v4u*>(shp + (int64_t)(t / 16 + u) * 512);
+#pragma unroll
+    for (int c = 0; c < kRetGroup; ++c)
+      if (c < gc)
+#pragma unroll
+        for (int u = 0; u < kRetGUnroll; ++u)
+          b[c][u] = *reinterpret_cast<const v4u*>(vbase + vb[c] * bstride + (int64_t)(t / 16 + u) * 512);
+#pragma unroll
+    for (int u = 0; u < kRetGUnroll; ++u) {
       const int tu = t + 16 * u;
       if (tu >= n) break;
       const int rem = n - tu - 8 * half;       // valid tokens among this lane's eight
@@ -199,25 +211,42 @@ __global__ __launch_bounds__(256) void k_retained16(const uint16_t* __restrict__
         for (int d = 0; d < 4; ++d) {
           const uint32_t keep = (2 * d < rem ? 0x0000FFFFu : 0u) | (2 * d + 1 < rem ? 0xFFFF0000u : 0u);
           a[u][d] &= keep;
-          b[u][d] &= keep;
+#pragma unroll
+          for (int c = 0; c < kRetGroup; ++c)
+            if (c < gc) b[c][u][d] &= keep;
         }
       }
-      if constexpr (BF)
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a[u]),
-                                                      __builtin_bit_cast(bf16x8, b[u]), acc, 0, 0, 0);
-      else
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a[u]),
-                                                     __builtin_bit_cast(f16x8, b[u]), acc, 0, 0, 0);
+#pragma unroll
+      for (int c = 0; c < kRetGroup; ++c) {
+        if (c < gc) {
+          const v4u& x = SR ? a[u] : b[c][u];   // S~ operand (rows j)
+          const v4u& y = SR ? b[c][u] : a[u];   // A~ operand (columns k)
+          if constexpr (BF)
+            acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, x),
+                                                             __builtin_bit_cast(bf16x8, y), acc[c], 0, 0, 0);
+          else
+            acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, x),
+                                                            __builtin_bit_cast(f16x8, y), acc[c], 0, 0, 0);
+        }
+      }
     }
   }
-  // acc[r] holds C[8 (r / 4) + 4 half + r % 4][col]
+  // acc[c][r] holds block c's C[8 (r / 4) + 4 half + r % 4][col]
 #pragma unroll
-  for (int r = 0; r < 16; ++r) blk[wid][8 * (r >> 2) + 4 * half + (r & 3)][col] = acc[r];
-  __builtin_amdgcn_s_waitcnt(0);
-  __builtin_amdgcn_wave_barrier();
-  for (int e = e0 + lane; e < e1; e += 64) {
-    const int loc = ent_loc[e];
-    Zt[i * m + e] = out_scale * blk[wid][loc >> 5][loc & 31];
+  for (int c = 0; c < kRetGroup; ++c) {
+    if (c >= gc) break;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) blk[wid][8 * (r >> 2) + 4 * half + (r & 3)][col] = acc[c][r];
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+    const int tile = gtiles[g0 + c];
+    const int e0 = tiles[4 * tile + 2], e1 = tiles[4 * tile + 3];
+    for (int e = e0 + lane; e < e1; e += 64) {
+      const int loc = ent_loc[e];
+      Zt[i * m + e] = out_scale * blk[wid][loc >> 5][loc & 31];
+    }
+    __builtin_amdgcn_s_waitcnt(0);             // this block's reads of blk are done
+    __builtin_amdgcn_wave_barrier();
   }
 }
 
@@ -300,7 +329,7 @@ struct Work {
 };
 
 // Token capacity of the fp16 layout: runs padded to multiples of 8, the
-// 256-row output tiles of the rotation, and the up to 16 kRet16Unroll + 8
+// 256-row output tiles of the rotation, and the up to 16 kRetGUnroll + 8
 // tokens a batch of the retained products reads past the last run.
 int64_t f16_ldt(int64_t N, int64_t T) { return round_up(N * T + 8 * N + 256, 256); }
 
@@ -443,7 +472,8 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   }
   // examples per launch: the 2-D grid's y limit, and the 1-D grid of the fp16
   // kernel (kXcds x ceil(nex / kXcds) x tile groups) below 2^31
-  const int64_t gx64 = ceil_div(p->n_tiles, (int64_t)kRetWaves);
+  // the fp16 kernels take groups of blocks, the fp32 one single blocks
+  const int64_t gx64 = ceil_div(t16 ? p->n_groups : p->n_tiles, (int64_t)kRetWaves);
   const int64_t ex_chunk = std::max<int64_t>(
       kXcds, std::min<int64_t>(65535 / kXcds * kXcds,
                                (((int64_t)1 << 31) - 1) / (kXcds * std::max<int64_t>(1, gx64)) * kXcds));
@@ -453,14 +483,11 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
     const unsigned gx = (unsigned)gx64;
     if (t16) {
       const dim3 grid16((unsigned)(kXcds * ceil_div(nex, kXcds) * gx));
-      if (f16)
-        hipLaunchKernelGGL(k_retained16<false>, grid16, dim3(256), 0, s, w.St16, w.At16, w.ldt,
-                           w.cnt, w.len, p->tiles, (int)p->n_tiles, p->ent_loc, out_scale, w.Zt,
-                           p->m, ex0, nex);
-      else
-        hipLaunchKernelGGL(k_retained16<true>, grid16, dim3(256), 0, s, w.St16, w.At16, w.ldt,
-                           w.cnt, w.len, p->tiles, (int)p->n_tiles, p->ent_loc, out_scale, w.Zt,
-                           p->m, ex0, nex);
+      auto kfn = f16 ? (p->group_rows ? k_retained16g<false, true> : k_retained16g<false, false>)
+                     : (p->group_rows ? k_retained16g<true, true> : k_retained16g<true, false>);
+      hipLaunchKernelGGL(kfn, grid16, dim3(256), 0, s, w.St16, w.At16, w.ldt, w.cnt, w.len, p->groups,
+                         (int)p->n_groups, p->gtiles, p->tiles, p->ent_loc, out_scale, w.Zt, p->m,
+                         ex0, nex);
     } else {
       hipLaunchKernelGGL(k_retained, dim3(gx, (unsigned)nex), dim3(256), 0, s,
                          w.St, p->rows_pad, w.At, p->cols_pad, w.cnt, p->tiles, (int)p->n_tiles,

@@ -9,6 +9,8 @@
 // compaction keeps all larger keys and the first ties in index order, and a
 // rank count over the m survivors puts them in canonical order.
 #include <algorithm>
+#include <numeric>
+#include <vector>
 
 #include "plan.h"
 #include "scan.h"
@@ -435,6 +437,7 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   size_t pb = 0;
   auto padd = [&](size_t b) { size_t o = pb; pb = align256(pb + b); return o; };
   size_t q_ret = padd(m * 4), q_w = padd(m * 4), q_tiles = padd(std::max<int64_t>(n_active, 1) * 16);
+  size_t q_groups = padd(std::max<int64_t>(n_active, 1) * 16), q_gt = padd(std::max<int64_t>(n_active, 1) * 4);
   size_t q_er = padd(m * 4), q_el = padd(m * 2), q_ep = padd(m * 4);
   size_t q_sh = padd(p->rows_pad * p->ld_out * 2), q_sl = padd(p->rows_pad * p->ld_out * 2);
   size_t q_ah = padd(p->cols_pad * p->ld_in * 2), q_al = padd(p->cols_pad * p->ld_in * 2);
@@ -448,6 +451,8 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   p->ret_flat = (int32_t*)(base + q_ret);
   p->ret_w = (float*)(base + q_w);
   p->tiles = (int32_t*)(base + q_tiles);
+  p->groups = (int32_t*)(base + q_groups);
+  p->gtiles = (int32_t*)(base + q_gt);
   p->ent_r = (int32_t*)(base + q_er);
   p->ent_loc = (uint16_t*)(base + q_el);
   p->ent_pos = (int32_t*)(base + q_ep);
@@ -467,6 +472,52 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
                      kpos, rt, toff, cur, p->ent_r, p->ent_loc, p->ent_pos);
   hipLaunchKernelGGL(k_tile_desc, dim3(grid_for(nt, 256)), dim3(256), 0, s, tc, nt, n_kt, toff,
                      flag, p->tiles);
+  // Groups of active blocks that share one operand block, at most kRetGroup
+  // each: the retained products load a group's shared block once. Blocks are
+  // grouped by row block of S~ or by column block of A~, whichever loads fewer
+  // blocks in all (a run of L blocks sharing one loads ceil(L / kRetGroup) + L).
+  std::vector<int32_t> hgroups, hgt;
+  if (n_active > 0) {
+    std::vector<int32_t> ht((size_t)n_active * 4);
+    e = hipMemcpyAsync(ht.data(), p->tiles, ht.size() * 4, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+      free_plan(p);
+      return check_hip(e, "plan build: active blocks");
+    }
+    std::vector<int32_t> by_row((size_t)n_active), by_col((size_t)n_active);
+    std::iota(by_row.begin(), by_row.end(), 0);   // tiles are in (row, column) order
+    by_col = by_row;
+    std::stable_sort(by_col.begin(), by_col.end(),
+                     [&](int32_t a, int32_t b) { return ht[4 * a + 1] < ht[4 * b + 1]; });
+    auto loads = [&](const std::vector<int32_t>& ord, int axis) {
+      int64_t total = 0;
+      for (int64_t a = 0; a < n_active;) {
+        int64_t b = a;
+        while (b < n_active && ht[4 * ord[b] + axis] == ht[4 * ord[a] + axis]) ++b;
+        total += ceil_div(b - a, (int64_t)kRetGroup) + (b - a);
+        a = b;
+      }
+      return total;
+    };
+    p->group_rows = loads(by_row, 0) <= loads(by_col, 1);
+    const int axis = p->group_rows ? 0 : 1;
+    hgt = p->group_rows ? by_row : by_col;
+    for (int64_t a = 0; a < n_active;) {
+      int64_t b = a;
+      while (b < n_active && b - a < kRetGroup && ht[4 * hgt[b] + axis] == ht[4 * hgt[a] + axis]) ++b;
+      hgroups.insert(hgroups.end(), {(int32_t)a, (int32_t)(b - a), ht[4 * hgt[a] + axis], 0});
+      a = b;
+    }
+    p->n_groups = (int64_t)hgroups.size() / 4;
+    e = hipMemcpyAsync(p->groups, hgroups.data(), hgroups.size() * 4, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(p->gtiles, hgt.data(), hgt.size() * 4, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) {
+      free_plan(p);
+      return check_hip(e, "plan build: block groups");
+    }
+  }
   hipLaunchKernelGGL(k_gather_panel, dim3((unsigned)(p->rows_pad / 32), grid_for(p->ld_out, 32)),
                      dim3(256), 0, s, Q_S, d_out, jl, (int)p->n_rows, p->rows_pad, p->ld_out,
                      p->qs_hi, p->qs_lo, p->qs_f16);

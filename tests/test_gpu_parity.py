@@ -424,6 +424,31 @@ def test_rotate_retain_fp16_mode(shape):
     plan.close()
 
 
+@pytest.mark.parametrize("axis", ["rows", "cols"])
+def test_rotate_retain_block_groups(axis):
+    """Retained set inside one row block of S~ (or one column block of A~):
+    the retained products then load that block once for a group of active
+    blocks; both 16-bit modes match the oracle."""
+    N, T, d_in, d_out, m = 5, 120, 300, 260, 4000
+    say(f"[first stage] block groups sharing {axis}")
+    a, ds, mask, QA, QS, lam = random_problem(71 if axis == "rows" else 72, N, T, d_in, d_out, m,
+                                              lens_lo=3)
+    if axis == "rows":
+        lam[:32, :] += 100.0          # 32 x 300 > m entries: J = rows 0..31, one row block
+    else:
+        lam[:, :32] += 100.0          # K = columns 0..31, one column block
+    plan = E.eogp_plan_create(d(lam), 1e-4, m, d(QA), d(QS))
+    assert (plan.n_rows if axis == "rows" else plan.n_cols) == 32
+    ref, _ = oracle_Z(a, ds, mask, QA, QS, lam, 1e-4, m)
+    for prec, tol in ((E.PREC_F16, 1e-3), (E.PREC_FAST, 2e-2)):
+        Z = E.eogp_rotate_retain_planned(plan, d(a), d(ds), d(mask), prec=prec)
+        torch.cuda.synchronize()
+        err = rel_rows(Z.cpu().numpy(), ref)
+        say(f"   prec={prec} max rel {err.max():.2e}")
+        assert err.max() <= tol
+    plan.close()
+
+
 def test_rotate_retain_fp16_mode_input_exponents():
     """Gradients of order 1e-7 (below fp16's normal range) are brought into
     range by the plan's exponent; the result is then as accurate as for
