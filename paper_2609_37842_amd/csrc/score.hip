@@ -50,7 +50,9 @@ namespace {
 constexpr int QB = 16;                 // queries per pass
 constexpr int NW = 8;                  // waves per workgroup
 constexpr int NTHR = NW * 64;
-constexpr int MCAP = 512;              // candidate slots per query in the merge
+constexpr int MCAP = 1024;             // candidate slots of the merge's list
+constexpr int MRU = 2;                 // candidates per thread per merge round
+constexpr int MSPLIT = 16;             // first-level merge workgroups per query
 constexpr int MAX_TOPK = 256;
 
 // A step covers SB bytes (8 SB bits) of a module in every row: lane (row,
@@ -147,23 +149,27 @@ __global__ void k_mod_table(ModChunk c, ModInfo* __restrict__ mods) {
   if (i < c.count) mods[c.first + i] = c.m[i];
 }
 
-// One thread per plane byte, laid out [group][step][MFMA f][lane][j] with
-// f = 8 u + t: lane (M, g) = (lane % 32, lane / 32) is plane M / 16 (0: h,
-// 1: l) of query M % 16, byte j holds coordinate
-// 8 (sb s + sb / 2 g + 16 u + j) + t of the step's module (0 past the module),
-// sb = bytes per row and step.
-__global__ void k_query_planes(const float* __restrict__ Y, int64_t ldy, int64_t Q, int U,
-                               const ModInfo* __restrict__ mods, const int32_t* __restrict__ fq,
-                               int64_t n_steps, int64_t n_groups, int sb,
-                               int8_t* __restrict__ planes) {
+// Planes laid out [group][step][MFMA f][lane][j] with f = 8 u + t: lane
+// (M, g) = (lane % 32, lane / 32) is plane M / 16 (0: h, 1: l) of query M % 16,
+// byte j holds coordinate 8 (sb s + sb / 2 g + 16 u + j) + t of the step's
+// module (0 past the module), sb = bytes per row and step. One thread per
+// (group, step, u, g, query, t) forms the 16 bytes of both planes of its query:
+// eight neighbouring threads (t = 0..7) read eight neighbouring coordinates.
+__global__ __launch_bounds__(256) void k_query_planes(const float* __restrict__ Y, int64_t ldy,
+                                                      int64_t Q, int U,
+                                                      const ModInfo* __restrict__ mods,
+                                                      const int32_t* __restrict__ fq,
+                                                      int64_t n_steps, int64_t n_groups, int sb,
+                                                      int8_t* __restrict__ planes) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t step_bytes = (int64_t)sb * 256;          // sb / 4 KB
-  const int64_t total = n_groups * n_steps * step_bytes;
-  if (idx >= total) return;
-  const int j = (int)(idx & 15);
-  const int lane = (int)((idx >> 4) & 63);
-  const int fr = (int)((idx >> 10) % (sb / 4));
-  const int64_t gs = idx / step_bytes;
+  const int nu = sb / 32;                                 // 16-byte words per lane and step
+  const int64_t per_step = 256 * (int64_t)nu;             // threads per step
+  if (idx >= n_groups * n_steps * per_step) return;
+  const int t = (int)(idx & 7);
+  const int qn = (int)((idx >> 3) & 15);
+  const int g = (int)((idx >> 7) & 1);
+  const int uc = (int)((idx >> 8) % nu);
+  const int64_t gs = idx / per_step;
   const int64_t step = gs % n_steps;
   const int64_t grp = gs / n_steps;
   int lo = 0, hi = U - 1;                    // last module whose first step <= step
@@ -173,17 +179,26 @@ __global__ void k_query_planes(const float* __restrict__ Y, int64_t ldy, int64_t
   }
   const ModInfo md = mods[lo];
   const int64_t sl = step - md.sbase;
-  const int uc = fr >> 3, t = fr & 7;
-  const int M = lane & 31, g = lane >> 5;
-  const int qn = M & 15;
-  const int64_t c = 8 * (sb * sl + (sb / 2) * g + 16 * uc + j) + t;
   const int64_t q = grp * QB + qn;
-  int yi = 0;
-  if (q < Q && c < md.k)
-    yi = (int)rintf(ldexpf(Y[q * ldy + md.coff + c], fq[(grp * U + lo) * QB + qn]));
-  const int h = (yi + 128) >> 8;   // floor division (arithmetic shift)
-  const int l = yi - 256 * h;
-  planes[idx] = (int8_t)((M >> 4) ? l : h);
+  const int f = q < Q ? fq[(grp * U + lo) * QB + qn] : 0;
+  const int64_t c0 = 8 * (sb * sl + (sb / 2) * g + 16 * uc) + t;   // coordinate of byte 0
+  const float* y = Y + q * ldy + md.coff;
+  uint32_t hw[4] = {0u, 0u, 0u, 0u}, lw[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int jj = 0; jj < 16; ++jj) {
+    const int64_t c = c0 + 8 * jj;
+    int yi = 0;
+    if (q < Q && c < md.k) yi = (int)rintf(ldexpf(y[c], f));
+    const int h = (yi + 128) >> 8;   // floor division (arithmetic shift)
+    const int l = yi - 256 * h;
+    hw[jj >> 2] |= (uint32_t)(h & 0xFF) << (8 * (jj & 3));
+    lw[jj >> 2] |= (uint32_t)(l & 0xFF) << (8 * (jj & 3));
+  }
+  const int fr = 8 * uc + t;
+  int8_t* blk = planes + (gs * (sb / 4) + fr) * 1024;
+  const int lane = qn + 32 * g;   // plane h; plane l is lane + 16
+  *reinterpret_cast<uint4*>(blk + 16 * lane) = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+  *reinterpret_cast<uint4*>(blk + 16 * (lane + 16)) = make_uint4(lw[0], lw[1], lw[2], lw[3]);
 }
 
 // Copies a store of n < 16 bytes into a zero-padded 16-byte slot.
@@ -202,30 +217,34 @@ struct Cand {
   int overflow;
 };
 
-// Sort list n (all NTH threads), keep its first `topk`, update the threshold.
-// Entries past CAP (counted but not stored) are dropped here; their owners
-// insert them again.
+// Sort a list (all NTH threads of the block; the first power of two of slots
+// that holds its entries, padded with empty ones), keep its first `topk`,
+// update the threshold. Entries past CAP (counted but not stored) are dropped here;
+// their owners insert them again.
 template <int CAP, int NTH>
-__device__ void prune(Cand<CAP>& cd, int n, int topk) {
+__device__ __forceinline__ void prune_list(uint64_t* key, uint32_t* idx, int* cnt, uint64_t* thr,
+                                           int topk) {
   const int tid = threadIdx.x;
-  const int c = min(cd.cnt[n], CAP);
-  for (int i = c + tid; i < CAP; i += NTH) {
-    cd.key[n][i] = 0ull;
-    cd.idx[n][i] = 0xFFFFFFFFu;
+  const int c = min(*cnt, CAP);
+  int P = 2;                     // sorted length: the least power of two >= c (CAP at most)
+  while (P < c) P <<= 1;
+  for (int i = c + tid; i < P; i += NTH) {
+    key[i] = 0ull;
+    idx[i] = 0xFFFFFFFFu;
   }
   __syncthreads();
-  for (int k = 2; k <= CAP; k <<= 1) {
+  for (int k = 2; k <= P; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < CAP; i += NTH) {
+      for (int i = tid; i < P; i += NTH) {
         const int p = i ^ j;
         if (p > i) {
-          const uint64_t ka = cd.key[n][i], kb = cd.key[n][p];
-          const uint32_t ia = cd.idx[n][i], ib = cd.idx[n][p];
+          const uint64_t ka = key[i], kb = key[p];
+          const uint32_t ia = idx[i], ib = idx[p];
           const bool desc = (i & k) == 0;
           const bool ab = before(ka, ia, kb, ib);
           if (desc ? !ab : ab) {
-            cd.key[n][i] = kb; cd.key[n][p] = ka;
-            cd.idx[n][i] = ib; cd.idx[n][p] = ia;
+            key[i] = kb; key[p] = ka;
+            idx[i] = ib; idx[p] = ia;
           }
         }
       }
@@ -233,10 +252,14 @@ __device__ void prune(Cand<CAP>& cd, int n, int topk) {
     }
   }
   if (tid == 0) {
-    cd.thr[n] = (c >= topk) ? cd.key[n][topk - 1] : 0ull;
-    cd.cnt[n] = c < topk ? c : topk;
+    *thr = (c >= topk) ? key[topk - 1] : 0ull;
+    *cnt = c < topk ? c : topk;
   }
   __syncthreads();
+}
+template <int CAP, int NTH>
+__device__ __forceinline__ void prune(Cand<CAP>& cd, int n, int topk) {
+  prune_list<CAP, NTH>(cd.key[n], cd.idx[n], &cd.cnt[n], &cd.thr[n], topk);
 }
 
 constexpr int MAX_RNG = 64;   // module ranges of the multi-module pass
@@ -627,7 +650,10 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
     }
   }
   if constexpr (!MULTI) {
-    for (int qq = 0; qq < QB; ++qq) prune<CAP, NTHR>(cd, qq, a.topk);
+    // lists of at most topk entries are written as they are (the merge
+    // takes candidates in any order)
+    for (int qq = 0; qq < QB; ++qq)
+      if (cd.cnt[qq] > a.topk) prune<CAP, NTHR>(cd, qq, a.topk);
     for (int i = tid; i < QB * a.topk; i += NTHR) {
       const int qq = i / a.topk, e = i % a.topk;
       const int64_t o = ((int64_t)blockIdx.x * QB + qq) * a.topk + e;
@@ -733,7 +759,8 @@ __global__ __launch_bounds__(FOLD_THR) void k_score_fold(FoldArgs a) {
       __syncthreads();
     }
   }
-  for (int qq = 0; qq < QB; ++qq) prune<CAP, FOLD_THR>(cd, qq, a.topk);
+  for (int qq = 0; qq < QB; ++qq)
+    if (cd.cnt[qq] > a.topk) prune<CAP, FOLD_THR>(cd, qq, a.topk);
   for (int i = tid; i < QB * a.topk; i += FOLD_THR) {
     const int qq = i / a.topk, e = i % a.topk;
     const int64_t o = ((int64_t)blockIdx.x * QB + qq) * a.topk + e;
@@ -743,44 +770,77 @@ __global__ __launch_bounds__(FOLD_THR) void k_score_fold(FoldArgs a) {
   }
 }
 
-// One workgroup per query of the group: reduce the per-workgroup lists.
+// Reduction of the per-workgroup candidate lists ([G][QB][topk] keys and
+// indices, empty slots marked by index 0xFFFFFFFF) in two levels: workgroup
+// (n, sp) merges lists sp * per .. sp * per + per - 1 of query n of the group
+// into one list of the same form (!FINAL, list sp of the output), then one
+// workgroup per query merges those into the sorted top-k (FINAL). Each round
+// requests MRU candidates per thread before any is used; a list longer than
+// MCAP - 256 MRU is pruned before the next round, so a round always fits.
+struct MergeList {
+  uint64_t key[MCAP];
+  uint32_t idx[MCAP];
+  int cnt;
+  uint64_t thr;
+};
+template <bool FINAL>
 __global__ __launch_bounds__(256, 1) void k_merge(const uint64_t* __restrict__ ckey,
-                                                  const uint32_t* __restrict__ cidx, int G,
+                                                  const uint32_t* __restrict__ cidx, int G, int per,
                                                   int64_t grp, int64_t Q, int topk,
                                                   int64_t* __restrict__ out_idx,
-                                                  float* __restrict__ out_score) {
-  __shared__ Cand<MCAP> cd;   // only list 0 is used
-  const int n = blockIdx.x;
+                                                  float* __restrict__ out_score,
+                                                  uint64_t* __restrict__ okey,
+                                                  uint32_t* __restrict__ oidx) {
+  __shared__ MergeList ml;
+  const int n = blockIdx.x, sp = blockIdx.y;
   const int64_t q = grp * QB + n;
-  if (q >= Q) return;
+  if (q >= Q) return;                         // never read by the next level either
   const int tid = threadIdx.x;
   if (tid == 0) {
-    cd.cnt[0] = 0;
-    cd.thr[0] = 0ull;
+    ml.cnt = 0;
+    ml.thr = 0ull;
   }
   __syncthreads();
-  const int64_t total = (int64_t)G * topk;
-  for (int64_t base = 0; base < total; base += 256) {
-    const int64_t e = base + tid;
-    if (e < total) {
-      const int64_t wg = e / topk, j = e % topk;
-      const int64_t o = (wg * QB + n) * topk + j;
-      const uint64_t key = ckey[o];
-      const uint32_t id = cidx[o];
-      if (id != 0xFFFFFFFFu && key >= cd.thr[0]) {
-        const int pos = atomicAdd(&cd.cnt[0], 1);
-        cd.key[0][pos] = key;
-        cd.idx[0][pos] = id;
+  const int64_t l0 = (int64_t)sp * per;
+  const int64_t total = std::max<int64_t>(0, std::min<int64_t>(G - l0, per)) * topk;
+  for (int64_t base = 0; base < total; base += 256 * MRU) {
+    uint64_t key[MRU];
+    uint32_t id[MRU];
+#pragma unroll
+    for (int r = 0; r < MRU; ++r) {
+      const int64_t e = base + 256 * r + tid;
+      key[r] = 0ull;
+      id[r] = 0xFFFFFFFFu;
+      if (e < total) {
+        const int64_t wg = l0 + e / topk, j = e % topk;
+        const int64_t o = (wg * QB + n) * topk + j;
+        key[r] = ckey[o];
+        id[r] = cidx[o];
+      }
+    }
+    const uint64_t thr = ml.thr;
+#pragma unroll
+    for (int r = 0; r < MRU; ++r) {
+      if (id[r] != 0xFFFFFFFFu && key[r] >= thr) {
+        const int pos = atomicAdd(&ml.cnt, 1);
+        ml.key[pos] = key[r];
+        ml.idx[pos] = id[r];
       }
     }
     __syncthreads();
-    if (cd.cnt[0] > MCAP - 256) prune<MCAP, 256>(cd, 0, topk);
+    if (ml.cnt > MCAP - 256 * MRU) prune_list<MCAP, 256>(ml.key, ml.idx, &ml.cnt, &ml.thr, topk);
   }
-  prune<MCAP, 256>(cd, 0, topk);
+  if (FINAL || ml.cnt > topk) prune_list<MCAP, 256>(ml.key, ml.idx, &ml.cnt, &ml.thr, topk);
   for (int e = tid; e < topk; e += 256) {
-    const bool have = e < cd.cnt[0];
-    out_idx[q * topk + e] = have ? (int64_t)cd.idx[0][e] : -1;
-    out_score[q * topk + e] = have ? (float)key_value(cd.key[0][e]) : -__builtin_inff();
+    const bool have = e < ml.cnt;
+    if constexpr (FINAL) {
+      out_idx[q * topk + e] = have ? (int64_t)ml.idx[e] : -1;
+      out_score[q * topk + e] = have ? (float)key_value(ml.key[e]) : -__builtin_inff();
+    } else {
+      const int64_t o = ((int64_t)sp * QB + n) * topk + e;
+      okey[o] = have ? ml.key[e] : 0ull;
+      oidx[o] = have ? ml.idx[e] : 0xFFFFFFFFu;
+    }
   }
 }
 
@@ -808,7 +868,9 @@ struct Layout {
   int64_t step_bytes = 0;
   int n_rng = 1;         // module ranges of the multi-module pass
   bool n64 = false;      // multi-module dots stored in 64 bits
-  size_t o_mods = 0, o_fq = 0, o_ys = 0, o_pl = 0, o_ck = 0, o_ci = 0, o_part = 0, o_pad = 0,
+  int merge_split = 1;   // first-level merge workgroups per query
+  size_t o_mods = 0, o_fq = 0, o_ys = 0, o_pl = 0, o_ck = 0, o_ci = 0, o_ck2 = 0, o_ci2 = 0,
+         o_part = 0, o_pad = 0,
          total = 0;
 };
 
@@ -847,6 +909,9 @@ Layout layout(int64_t N, int64_t Q, int32_t U, const int64_t* kmod, int32_t topk
   L.o_pl = add((size_t)(L.n_groups * L.n_steps * L.step_bytes));
   L.o_ck = add((size_t)lists * QB * topk * 8);
   L.o_ci = add((size_t)lists * QB * topk * 4);
+  L.merge_split = (int)std::min<int64_t>(MSPLIT, std::max<int64_t>(1, lists / 8));
+  L.o_ck2 = add((size_t)L.merge_split * QB * topk * 8);
+  L.o_ci2 = add((size_t)L.merge_split * QB * topk * 4);
   L.o_part = add(U > 1 ? (size_t)U * QB * (size_t)N * (L.n64 ? 8 : 4) : 0);
   L.o_pad = add(16);   // a store of fewer than 16 bytes is copied here (see score_topk)
   L.total = b;
@@ -912,6 +977,8 @@ eogp_status score_topk_impl(const uint8_t* codes, int64_t cstride, const uint16_
   int8_t* planes = reinterpret_cast<int8_t*>(base + L.o_pl);
   uint64_t* ck = reinterpret_cast<uint64_t*>(base + L.o_ck);
   uint32_t* ci = reinterpret_cast<uint32_t*>(base + L.o_ci);
+  uint64_t* ck2 = reinterpret_cast<uint64_t*>(base + L.o_ck2);
+  uint32_t* ci2 = reinterpret_cast<uint32_t*>(base + L.o_ci2);
 
   // The pass reads 16 bytes at the store's start in place of bytes past a
   // module's end; a store with fewer readable bytes is copied into a zeroed
@@ -948,8 +1015,9 @@ eogp_status score_topk_impl(const uint8_t* codes, int64_t cstride, const uint16_
   timing::Scope tprep(EOGP_KT_SCORE_PREP, s);
   hipLaunchKernelGGL(k_query_stats, dim3((unsigned)(L.n_groups * QB), (unsigned)U), dim3(256), 0,
                      s, Y, ldy, Q, U, mods, fq, ys);
-  const int64_t pbytes = L.n_groups * L.n_steps * L.step_bytes;
-  hipLaunchKernelGGL(k_query_planes, dim3((unsigned)ceil_div(pbytes, 256)), dim3(256), 0, s, Y,
+  // one thread per 16 bytes of each of the two planes
+  const int64_t pthreads = L.n_groups * L.n_steps * L.step_bytes / 32;
+  hipLaunchKernelGGL(k_query_planes, dim3((unsigned)ceil_div(pthreads, 256)), dim3(256), 0, s, Y,
                      ldy, Q, U, mods, fq, L.n_steps, L.n_groups, cfg.sb, planes);
   EOGP_LAUNCH_CHECK("query preparation");
   timing::end(tprep.slot, s);
@@ -1014,8 +1082,16 @@ eogp_status score_topk_impl(const uint8_t* codes, int64_t cstride, const uint16_
     }
     timing::Scope tm(EOGP_KT_SCORE_MERGE, s);
     const int lists = (int)(U == 1 ? L.grid : L.fold_grid);
-    hipLaunchKernelGGL(k_merge, dim3(QB), dim3(256), 0, s, ck, ci, lists, grp, Q, topk,
-                       out_idx, out_score);
+    const int sp = L.merge_split, per = (int)ceil_div(lists, sp);
+    if (sp > 1) {
+      hipLaunchKernelGGL(k_merge<false>, dim3(QB, sp), dim3(256), 0, s, ck, ci, lists, per, grp, Q,
+                         topk, nullptr, nullptr, ck2, ci2);
+      hipLaunchKernelGGL(k_merge<true>, dim3(QB), dim3(256), 0, s, ck2, ci2, sp, sp, grp, Q, topk,
+                         out_idx, out_score, nullptr, nullptr);
+    } else {
+      hipLaunchKernelGGL(k_merge<true>, dim3(QB), dim3(256), 0, s, ck, ci, lists, lists, grp, Q,
+                         topk, out_idx, out_score, nullptr, nullptr);
+    }
     EOGP_LAUNCH_CHECK("score pass");
   }
   return EOGP_OK;
