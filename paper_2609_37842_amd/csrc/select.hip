@@ -173,25 +173,30 @@ __global__ void k_make_keys(const float* __restrict__ lam, const int32_t* sel, i
   }
 }
 
-// rank(x) = #{y : key[y] > key[x]} (keys are distinct); ret[rank] = sel[x].
+// rank(x) = #{y : key[y] > key[x]} (keys are distinct), counted in chunks of
+// kRankChunk keys: workgroup (bx, by) adds the count over chunks by,
+// by + gridDim.y, ... to rank[x] for its 256 keys x (rank zeroed beforehand).
+constexpr int kRankChunk = 512;
 __global__ __launch_bounds__(256) void k_rank(const uint64_t* __restrict__ keys, int64_t m,
-                                              const int32_t* __restrict__ sel,
-                                              int32_t* __restrict__ ret) {
-  __shared__ uint64_t sk[2048];
-  int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  uint64_t K = (x < m) ? keys[x] : ~0ull;
-  int64_t rank = 0;
-  for (int64_t base = 0; base < m; base += 2048) {
-    for (int j = threadIdx.x; j < 2048; j += 256)
-      sk[j] = (base + j < m) ? keys[base + j] : 0ull;
+                                              int* __restrict__ rank) {
+  __shared__ uint64_t sk[kRankChunk];
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const uint64_t K = (x < m) ? keys[x] : ~0ull;
+  int c = 0;
+  for (int64_t base = (int64_t)blockIdx.y * kRankChunk; base < m; base += (int64_t)gridDim.y * kRankChunk) {
+    __syncthreads();   // the previous chunk's readers are done
+    for (int j = threadIdx.x; j < kRankChunk; j += 256) sk[j] = (base + j < m) ? keys[base + j] : 0ull;
     __syncthreads();
-    int cnt = (int)((m - base) < 2048 ? (m - base) : 2048);
-    int c = 0;
+    const int cnt = (int)std::min<int64_t>(m - base, kRankChunk);
     for (int j = 0; j < cnt; ++j) c += (sk[j] > K);
-    rank += c;
-    __syncthreads();
   }
-  if (x < m) ret[rank] = sel[x];
+  if (x < m && c) atomicAdd(&rank[x], c);
+}
+// ret[rank(x)] = sel[x]
+__global__ void k_rank_place(const int* __restrict__ rank, const int32_t* __restrict__ sel,
+                             int64_t m, int32_t* __restrict__ ret) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x < m) ret[rank[x]] = sel[x];
 }
 
 __global__ void k_finalize(const float* __restrict__ lam, const int32_t* __restrict__ ret,
@@ -212,33 +217,37 @@ __global__ void k_finalize(const float* __restrict__ lam, const int32_t* __restr
 
 // Order the used rows (or columns) by (retained count desc, index asc): rows
 // holding many retained axes come first, which packs the retained set into
-// few 32 x 32 blocks (a staircase when Lambda is close to a product).
+// few 32 x 32 blocks (a staircase when Lambda is close to a product). Ranks
+// are counted in chunks as in k_rank (rank zeroed beforehand), then placed.
 __global__ __launch_bounds__(256) void k_rank_lines(const int* __restrict__ cnt, int64_t d,
-                                                    int* __restrict__ pos,
-                                                    int* __restrict__ list, int* n_used) {
-  __shared__ int sc[2048];
-  int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  int c = (x < d) ? cnt[x] : 0;
-  int rank = 0;
-  for (int64_t base = 0; base < d; base += 2048) {
-    for (int j = threadIdx.x; j < 2048; j += 256) sc[j] = (base + j < d) ? cnt[base + j] : 0;
+                                                    int* __restrict__ rank) {
+  __shared__ int sc[kRankChunk];
+  const int64_t x = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int c = (x < d) ? cnt[x] : 0;
+  int r = 0;
+  for (int64_t base = (int64_t)blockIdx.y * kRankChunk; base < d; base += (int64_t)gridDim.y * kRankChunk) {
+    __syncthreads();   // the previous chunk's readers are done
+    for (int j = threadIdx.x; j < kRankChunk; j += 256) sc[j] = (base + j < d) ? cnt[base + j] : 0;
     __syncthreads();
-    int lim = (int)((d - base) < 2048 ? (d - base) : 2048);
+    const int lim = (int)std::min<int64_t>(d - base, kRankChunk);
     for (int j = 0; j < lim; ++j) {
-      int cj = sc[j];
-      int64_t xj = base + j;
-      rank += (cj > 0) && (cj > c || (cj == c && xj < x));
+      const int cj = sc[j];
+      const int64_t xj = base + j;
+      r += (cj > 0) && (cj > c || (cj == c && xj < x));
     }
-    __syncthreads();
   }
-  if (x < d) {
-    if (c > 0) {
-      pos[x] = rank;
-      list[rank] = (int)x;
-      atomicAdd(n_used, 1);
-    } else {
-      pos[x] = -1;
-    }
+  if (x < d && c > 0 && r) atomicAdd(&rank[x], r);
+}
+__global__ void k_place_lines(const int* __restrict__ cnt, const int* __restrict__ rank, int64_t d,
+                              int* __restrict__ pos, int* __restrict__ list, int* n_used) {
+  const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= d) return;
+  if (cnt[x] > 0) {
+    pos[x] = rank[x];
+    list[rank[x]] = (int)x;
+    atomicAdd(n_used, 1);
+  } else {
+    pos[x] = -1;
   }
 }
 
@@ -363,6 +372,7 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   size_t o_jpos = add(d_out * 4), o_kpos = add(d_in * 4);
   size_t o_jl = add(d_out * 4), o_kl = add(d_in * 4);
   size_t o_tc = add(nt * 4), o_rt = add(m * 4);
+  size_t o_rk = add(m * 4), o_rj = add(d_out * 4), o_rkk = add(d_in * 4);   // rank counters
   size_t o_toff = add((nt + 1) * 8), o_flag = add((nt + 1) * 8), o_cur = add(nt * 4);
   size_t o_ret = add(m * 4), o_w = add(m * 4);
   char* tmp = nullptr;
@@ -377,6 +387,7 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   int *jpos = (int*)(tmp + o_jpos), *kpos = (int*)(tmp + o_kpos);
   int *jl = (int*)(tmp + o_jl), *kl = (int*)(tmp + o_kl);
   int *tc = (int*)(tmp + o_tc), *rt = (int*)(tmp + o_rt), *cur = (int*)(tmp + o_cur);
+  int *rk = (int*)(tmp + o_rk), *rj = (int*)(tmp + o_rj), *rkk = (int*)(tmp + o_rkk);
   long long *toff = (long long*)(tmp + o_toff), *flag = (long long*)(tmp + o_flag);
   int32_t* ret = (int32_t*)(tmp + o_ret);
   float* w = (float*)(tmp + o_w);
@@ -396,13 +407,19 @@ eogp_status build_plan(const float* eigvals, int64_t d_out, int64_t d_in, double
   hipLaunchKernelGGL(k_sel_write, dim3((unsigned)nb), dim3(256), 0, s, eigvals, n, st, cgt, ceq,
                      (long long)m, sel);
   hipLaunchKernelGGL(k_make_keys, dim3(grid_for(m, 256)), dim3(256), 0, s, eigvals, sel, m, keys);
-  hipLaunchKernelGGL(k_rank, dim3(grid_for(m, 256)), dim3(256), 0, s, keys, m, sel, ret);
+  hipLaunchKernelGGL(k_rank, dim3(grid_for(m, 256), std::min(grid_for(m, kRankChunk), 65535u)), dim3(256), 0, s, keys,
+                     m, rk);
+  hipLaunchKernelGGL(k_rank_place, dim3(grid_for(m, 256)), dim3(256), 0, s, rk, sel, m, ret);
   hipLaunchKernelGGL(k_finalize, dim3(grid_for(m, 256)), dim3(256), 0, s, eigvals, ret, m, d_in,
                      damping, w, cj, ck, st);
-  hipLaunchKernelGGL(k_rank_lines, dim3(grid_for(d_out, 256)), dim3(256), 0, s, cj, d_out, jpos,
+  hipLaunchKernelGGL(k_rank_lines, dim3(grid_for(d_out, 256), std::min(grid_for(d_out, kRankChunk), 65535u)), dim3(256),
+                     0, s, cj, d_out, rj);
+  hipLaunchKernelGGL(k_rank_lines, dim3(grid_for(d_in, 256), std::min(grid_for(d_in, kRankChunk), 65535u)), dim3(256),
+                     0, s, ck, d_in, rkk);
+  hipLaunchKernelGGL(k_place_lines, dim3(grid_for(d_out, 256)), dim3(256), 0, s, cj, rj, d_out, jpos,
                      jl, &st->n_rows);
-  hipLaunchKernelGGL(k_rank_lines, dim3(grid_for(d_in, 256)), dim3(256), 0, s, ck, d_in, kpos, kl,
-                     &st->n_cols);
+  hipLaunchKernelGGL(k_place_lines, dim3(grid_for(d_in, 256)), dim3(256), 0, s, ck, rkk, d_in, kpos,
+                     kl, &st->n_cols);
   hipLaunchKernelGGL(k_tile_count, dim3(grid_for(m, 256)), dim3(256), 0, s, ret, m, d_in, jpos,
                      kpos, n_kt, tc, rt);
   hipLaunchKernelGGL(k_tile_prep, dim3(grid_for(nt, 256)), dim3(256), 0, s, tc, nt, toff, flag);
