@@ -553,7 +553,9 @@ __global__ __launch_bounds__(NTHR, 1) void k_gemm(KParams kp) {
   }
 }
 
-constexpr int PT = 256;   // k_gemm_p: threads per workgroup
+// k_gemm_p: waves per workgroup (4: one per SIMD, 128 x 128 each; 8: two per
+// SIMD, 128 x 64 each), chosen for every pipelined launch.
+constexpr int kPipeWaves = 8;
 
 // The pipelined kernel reads B through a range-checked buffer descriptor when
 // the last column tile is padded and the rows fit a 31-bit byte range.
@@ -566,11 +568,14 @@ inline bool use_buffer_b(const GemmArgs& g) {
 // a padded panel; one part each; no split-K.
 // BB: B through a range-checked buffer descriptor (padding rows skipped);
 // else plain loads with padding rows mapped to row 0.
-template <int AT, bool F16, bool SC, bool BB>
-__global__ __launch_bounds__(PT) __attribute__((amdgpu_waves_per_eu(1, 1)))
+// NWV: waves per workgroup (4 or 8), NWV / 4 per SIMD.
+template <int AT, bool F16, bool SC, bool BB, int NWV>
+__global__ __launch_bounds__(NWV * 64) __attribute__((amdgpu_waves_per_eu(NWV / 4, NWV / 4)))
 void k_gemm_p(KParams kp) {
+  static_assert(NWV == 4 || NWV == 8, "4 or 8 waves");
+  constexpr int PT = NWV * 64;
   constexpr int BNP = 256;
-  constexpr int WI = 4, WJ = 4;          // 128 x 128 per wave
+  constexpr int WI = 4, WJ = NWV == 4 ? 4 : 2;   // 128 x 128 or 128 x 64 per wave
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * BK];
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][BNP * BK];
   __shared__ int64_t sOff[BM];
@@ -606,11 +611,14 @@ void k_gemm_p(KParams kp) {
     pos = sPos;
   }
 
-  const int wm = (wid >> 1) * 128, wn = (wid & 1) * 128;
-  // Staging: fp32 A 8 lanes per row (rows (tid >> 3) + 32 q, q < 8); 16-bit A
-  // 4 lanes per row (rows (tid >> 2) + 64 q, q < 4); B 4 lanes per row.
-  constexpr int AQ = AT == 0 ? 8 : 4;
-  constexpr int BQ = BNP / 64;
+  const int wm = NWV == 4 ? (wid >> 1) * 128 : (wid >> 2) * 128;
+  const int wn = NWV == 4 ? (wid & 1) * 128 : (wid & 3) * 64;
+  // Staging: fp32 A 8 lanes per row (rows (tid >> 3) + PT / 8 q); 16-bit A
+  // 4 lanes per row (rows (tid >> 2) + PT / 4 q); B 4 lanes per row (rows
+  // (tid >> 2) + PT / 4 q).
+  constexpr int AQ = AT == 0 ? BM / (PT / 8) : BM / (PT / 4);
+  constexpr int B_RS = PT / 4;
+  constexpr int BQ = BNP / B_RS;
   static_assert(AT != 2 || F16, "bf16 A is widened to fp16 for fp16 products only");
   const int a_r0 = AT == 0 ? (tid >> 3) : (tid >> 2);
   constexpr int a_rs = AT == 0 ? PT / 8 : PT / 4;
@@ -650,7 +658,7 @@ void k_gemm_p(KParams kp) {
     const bool ragged = ((kend - kbeg) % BK) != 0;
 
     __syncthreads();                     // previous unit's readers of sOff / stages are done
-    {
+    if (tid < BM) {
       const int64_t row = m0 + tid;
       const bool ok = row < M;
       const int64_t src = g.a_rows ? (int64_t)g.a_rows[ok ? row : m0] : (ok ? row : m0);
@@ -681,7 +689,7 @@ void k_gemm_p(KParams kp) {
     const uint16_t* pb[BQ];
 #pragma unroll
     for (int q = 0; q < BQ; ++q) {
-      const int64_t brow = n0 + b_r0 + 64 * q;
+      const int64_t brow = n0 + b_r0 + B_RS * q;
       b_vo[q] = brow < N ? (uint32_t)(2 * (brow * g.ldb + 8 * b_pc)) : b_bytes;
       b_off[q] = (brow < N ? brow : 0) * g.ldb + 8 * b_pc;
       pb[q] = g.B_hi + b_off[q];
@@ -791,7 +799,7 @@ void k_gemm_p(KParams kp) {
     auto stage_b = [&](int st, const BRegs& R) {
 #pragma unroll
       for (int q = 0; q < BQ; ++q)
-        *reinterpret_cast<v4u*>(&sB[st][swz(b_r0 + 64 * q, b_pc)]) = R.rb[q];
+        *reinterpret_cast<v4u*>(&sB[st][swz(b_r0 + B_RS * q, b_pc)]) = R.rb[q];
     };
     auto read_frag = [&](int st, int ks, Frag& F) {
       const int ch = 2 * ks + (lane >> 5);
@@ -1008,12 +1016,13 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
       if (g.sched) hipLaunchKernelGGL(k_zero_sched, dim3(1), dim3(64), 0, s, g.sched);
       timing::Scope ts(g.timing_class, s);
       const bool bb = use_buffer_b(g);
+      const dim3 gd((unsigned)grid), bd(kPipeWaves * 64);
       if (F16 && g.a_scale != 1.f) {
-        if (bb) hipLaunchKernelGGL((k_gemm_p<AT, F16, true, true>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
-        else hipLaunchKernelGGL((k_gemm_p<AT, F16, true, false>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
+        if (bb) hipLaunchKernelGGL((k_gemm_p<AT, F16, true, true, kPipeWaves>), gd, bd, 0, s, kq);
+        else hipLaunchKernelGGL((k_gemm_p<AT, F16, true, false, kPipeWaves>), gd, bd, 0, s, kq);
       } else {
-        if (bb) hipLaunchKernelGGL((k_gemm_p<AT, F16, false, true>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
-        else hipLaunchKernelGGL((k_gemm_p<AT, F16, false, false>), dim3((unsigned)grid), dim3(PT), 0, s, kq);
+        if (bb) hipLaunchKernelGGL((k_gemm_p<AT, F16, false, true, kPipeWaves>), gd, bd, 0, s, kq);
+        else hipLaunchKernelGGL((k_gemm_p<AT, F16, false, false, kPipeWaves>), gd, bd, 0, s, kq);
       }
       EOGP_LAUNCH_CHECK("gemm launch");
       if (kq.splits > 1) {
@@ -1081,12 +1090,12 @@ eogp_status gemm_nt2(const GemmArgs& g1, const GemmArgs& g2, AType a_type, int a
   const bool sc = f16 && (g1.a_scale != 1.f || g2.a_scale != 1.f);
   hipLaunchKernelGGL(k_zero_sched, dim3(1), dim3(64), 0, s, g1.sched);
   timing::Scope ts(g1.timing_class, s);
-  const dim3 gd((unsigned)grid), bd(PT);
+  const dim3 gd((unsigned)grid), bd(kPipeWaves * 64);
   const bool bb = use_buffer_b(g1) && use_buffer_b(g2);
-#define EOGP_GEMM_P2(AT_, F16_, SC_)                                                   \
-  do {                                                                                 \
-    if (bb) hipLaunchKernelGGL((k_gemm_p<AT_, F16_, SC_, true>), gd, bd, 0, s, kq);    \
-    else hipLaunchKernelGGL((k_gemm_p<AT_, F16_, SC_, false>), gd, bd, 0, s, kq);      \
+#define EOGP_GEMM_P2(AT_, F16_, SC_)                                                               \
+  do {                                                                                             \
+    if (bb) hipLaunchKernelGGL((k_gemm_p<AT_, F16_, SC_, true, kPipeWaves>), gd, bd, 0, s, kq);    \
+    else hipLaunchKernelGGL((k_gemm_p<AT_, F16_, SC_, false, kPipeWaves>), gd, bd, 0, s, kq);      \
   } while (0)
   if (a_type == AType::F32) {
     if (f16 && sc) EOGP_GEMM_P2(0, true, true);
