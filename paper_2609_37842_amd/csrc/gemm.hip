@@ -47,6 +47,7 @@
 // Small-M problems split K; each split writes its own fp32 partial tile and a
 // second kernel adds the partials in split order (deterministic).
 #include <algorithm>
+#include <type_traits>
 
 #include "gemm.h"
 #include "timing.h"
@@ -849,22 +850,24 @@ void k_gemm_p(KParams kp) {
       load_a(clamp(2), A0);
     }
     __syncthreads();
-    read_frag(0, 0, F0);
 
     // One slice i in stage st (F0 holds its first half; the registers hold
     // slices i+1 and i+2 of A and B; RB is the B buffer holding slice i+1).
     // Scheduling hints keep the three regions apart and spread each region's
-    // MFMAs over its other work.
-    auto iter = [&](int st, int64_t i, ARegs& Anext, BRegs& RB) {
+    // MFMAs over its other work. ACT: the wave has columns below N; a wave
+    // whose columns all lie in the padding of the last column tile only
+    // stages its share of the operands (its accumulators stay zero).
+    auto iter = [&](auto act_c, int st, int64_t i, ARegs& Anext, BRegs& RB) {
+      constexpr bool ACT = decltype(act_c)::value;
       const int64_t k3 = clamp(i + 3);
       // region 1a: second-half fragment reads; B of slice i+1 to LDS; B of
       // slice i+3 requested before A of slice i+3, so that a wait for B never
       // waits for the A request behind it
       __builtin_amdgcn_sched_barrier(0);
-      read_frag(st, 1, F1);
+      if constexpr (ACT) read_frag(st, 1, F1);
       stage_b(st ^ 1, RB);
       load_b(k3, RB);
-      mma_part(F0, 0, NMB);
+      if constexpr (ACT) mma_part(F0, 0, NMB);
 #pragma unroll
       for (int m = 0; m < NMB; ++m) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                     // MFMA
@@ -876,7 +879,7 @@ void k_gemm_p(KParams kp) {
       __builtin_amdgcn_sched_barrier(0);
       // region 1b: the rest of the first half beside A of slice i+1 (convert,
       // LDS) and the request of A of slice i+3
-      mma_part(F0, 1, NMB);
+      if constexpr (ACT) mma_part(F0, 1, NMB);
       stage_a(st ^ 1, Anext);
       load_a(k3, Anext);
 #pragma unroll
@@ -891,22 +894,30 @@ void k_gemm_p(KParams kp) {
       __builtin_amdgcn_sched_barrier(0);
       // region 2: next slice's first-half fragments in flight under this
       // slice's second-half MFMAs
-      read_frag(st ^ 1, 0, F0);
-      mma(F1);
+      if constexpr (ACT) {
+        read_frag(st ^ 1, 0, F0);
+        mma(F1);
+      }
       __builtin_amdgcn_sched_group_barrier(0x100, WI + WJ, 2);
       __builtin_amdgcn_sched_group_barrier(0x008, WI * WJ, 2);
       __builtin_amdgcn_sched_barrier(0);
     };
-    int64_t p = 0;
-    for (; p + 2 <= nk; p += 2) {
-      iter(0, p, A1, RB);
-      iter(1, p + 1, A0, RB2);
-    }
-    if (p < nk) {                            // odd count: the last slice is in stage 0
-      read_frag(0, 1, F1);
-      mma(F0);
-      mma(F1);
-    }
+    auto slices = [&](auto act_c) {
+      constexpr bool ACT = decltype(act_c)::value;
+      if constexpr (ACT) read_frag(0, 0, F0);
+      int64_t p = 0;
+      for (; p + 2 <= nk; p += 2) {
+        iter(act_c, 0, p, A1, RB);
+        iter(act_c, 1, p + 1, A0, RB2);
+      }
+      if (ACT && p < nk) {                   // odd count: the last slice is in stage 0
+        read_frag(0, 1, F1);
+        mma(F0);
+        mma(F1);
+      }
+    };
+    if (n0 + wn < N) slices(std::true_type{});
+    else slices(std::false_type{});
     float* C = g.C;
     int64_t ldc = g.ldc;
     if (splits > 1) {
