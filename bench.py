@@ -302,7 +302,8 @@ class Gpt2Step:
         """MFMA flops the rotation launches execute: the compacted token rows
         (each example's run padded to a multiple of 8 in the 16-bit modes)
         rounded up to the 256-row tile, the used eigenvectors rounded up to the
-        256-column tile, the width rounded up to the 32-deep slice."""
+        64 columns of a wave (a wave wholly in the last column tile's padding
+        skips its MFMAs), the width rounded up to the 32-deep slice."""
         import math
         lens = self.mask.sum(dim=1).tolist()
         rows = sum(-(-int(v) // 8) * 8 for v in lens) if self.prec != self.E.PREC_ACCURATE \
@@ -312,7 +313,7 @@ class Gpt2Step:
         tot = 0
         for u, (name, di, do) in enumerate(self.modules):
             p = self.plans[u]
-            tot += 2 * rows * (up(do, 32) * up(p.n_rows, 256) + up(di, 32) * up(p.n_cols, 256))
+            tot += 2 * rows * (up(do, 32) * up(p.n_rows, 64) + up(di, 32) * up(p.n_cols, 64))
         return tot
 
     def rotation_bytes_per_step(self):

@@ -95,40 +95,45 @@ __device__ __forceinline__ float lane_xor(float x) {
     return __shfl_xor(x, 1 << B);
 }
 
-__device__ __forceinline__ int srht_pad(int idx) { return idx + (idx >> 6); }
+// LDS slot of element idx: one pad word per 2^SH elements, so the stride-2^SH
+// reads of the transposed pass fall into distinct banks.
+template <int SH>
+__device__ __forceinline__ int srht_pad(int idx) { return idx + (idx >> SH); }
 
-template <int LOGP>
-__global__ __launch_bounds__(256) void k_srht_reg(const float* __restrict__ Z, int64_t ldz, int m,
+// LT: log2 of the threads per row (8 or 9).
+template <int LOGP, int LT>
+__global__ __launch_bounds__(1 << LT) void k_srht_reg(const float* __restrict__ Z, int64_t ldz, int m,
                                                   const int8_t* __restrict__ signs,
                                                   const int32_t* __restrict__ rows, int k,
                                                   float scale, float* __restrict__ X, int64_t ldx) {
-  constexpr int P = 1 << LOGP, E = P >> 8, LE = LOGP - 8;
-  static_assert(LOGP >= 10 && LOGP <= 14, "lane bits 0 .. 7 - log2 E must lie inside a wave");
+  constexpr int NT = 1 << LT, P = 1 << LOGP, E = P >> LT, LE = LOGP - LT;
+  static_assert(LT == 8 || LT == 9, "256 or 512 threads per row");
+  static_assert(LE >= 1 && LT - LE <= 6, "the cross-lane bits (thread bits 0 .. LT - LE - 1) lie inside a wave");
   extern __shared__ float L[];
   const int t = threadIdx.x;
   const int64_t i = blockIdx.x;
   const float* z = Z + i * ldz;
   float v[E];
-  // (a) element t + 256 j into register j: loads at clamped indices, selected
+  // (a) element t + NT j into register j: loads at clamped indices, selected
   // afterwards (no branches, so all of them are in flight at once)
   int8_t sg[E];
 #pragma unroll
   for (int j = 0; j < E; ++j) {
-    const int idx = min(t + 256 * j, m - 1);
+    const int idx = min(t + NT * j, m - 1);
     v[j] = z[idx];
     sg[j] = signs[idx];
   }
 #pragma unroll
   for (int j = 0; j < E; ++j) {
-    const bool in = t + 256 * j < m;
+    const bool in = t + NT * j < m;
     v[j] = in ? (sg[j] < 0 ? -v[j] : v[j]) : 0.f;
   }
-  fwht_regs<E>(v);                                  //     bits 8 .. LOGP - 1
+  fwht_regs<E>(v);                                  //     bits LT .. LOGP - 1
 #pragma unroll
-  for (int j = 0; j < E; ++j) L[srht_pad(t + 256 * j)] = v[j];
+  for (int j = 0; j < E; ++j) L[srht_pad<LE>(t + NT * j)] = v[j];
   __syncthreads();
 #pragma unroll
-  for (int e = 0; e < E; ++e) v[e] = L[srht_pad(E * t + e)];   // (b) bits 0 .. LE - 1
+  for (int e = 0; e < E; ++e) v[e] = L[srht_pad<LE>(E * t + e)];   // (b) bits 0 .. LE - 1
   fwht_regs<E>(v);
   auto cross = [&](auto b_c) __attribute__((always_inline)) {  //     bit LE + b, lane bit b
     constexpr int B = decltype(b_c)::value;
@@ -139,26 +144,26 @@ __global__ __launch_bounds__(256) void k_srht_reg(const float* __restrict__ Z, i
       v[e] = hi ? o - v[e] : v[e] + o;
     }
   };
-  if constexpr (8 - LE > 0) cross(std::integral_constant<int, 0>{});
-  if constexpr (8 - LE > 1) cross(std::integral_constant<int, 1>{});
-  if constexpr (8 - LE > 2) cross(std::integral_constant<int, 2>{});
-  if constexpr (8 - LE > 3) cross(std::integral_constant<int, 3>{});
-  if constexpr (8 - LE > 4) cross(std::integral_constant<int, 4>{});
-  if constexpr (8 - LE > 5) cross(std::integral_constant<int, 5>{});
+  if constexpr (LT - LE > 0) cross(std::integral_constant<int, 0>{});
+  if constexpr (LT - LE > 1) cross(std::integral_constant<int, 1>{});
+  if constexpr (LT - LE > 2) cross(std::integral_constant<int, 2>{});
+  if constexpr (LT - LE > 3) cross(std::integral_constant<int, 3>{});
+  if constexpr (LT - LE > 4) cross(std::integral_constant<int, 4>{});
+  if constexpr (LT - LE > 5) cross(std::integral_constant<int, 5>{});
   __syncthreads();                                  // every (b) read is done
 #pragma unroll
-  for (int e = 0; e < E; ++e) L[srht_pad(E * t + e)] = v[e];   // (c)
+  for (int e = 0; e < E; ++e) L[srht_pad<LE>(E * t + e)] = v[e];   // (c)
   __syncthreads();
   // gather of the kept rows (k <= p, so at most E per thread): every index
   // requested before the first is used
   float* x = X + i * ldx;
   int r[E];
 #pragma unroll
-  for (int e = 0; e < E; ++e) r[e] = rows[min(t + 256 * e, k - 1)];
+  for (int e = 0; e < E; ++e) r[e] = rows[min(t + NT * e, k - 1)];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const int c = t + 256 * e;
-    if (c < k) x[c] = (r[e] >= 0 && r[e] < P) ? L[srht_pad(r[e])] * scale : __builtin_nanf("");
+    const int c = t + NT * e;
+    if (c < k) x[c] = (r[e] >= 0 && r[e] < P) ? L[srht_pad<LE>(r[e])] * scale : __builtin_nanf("");
   }
 }
 
@@ -260,24 +265,27 @@ eogp_status srht_project(const float* Z, int64_t ldz, int64_t N, int64_t m, cons
   }
   const float scale = (float)(1.0 / std::sqrt((double)k));
   if (logp >= 10 && logp <= 14) {
-    const void* fns[5] = {(const void*)k_srht_reg<10>, (const void*)k_srht_reg<11>,
-                          (const void*)k_srht_reg<12>, (const void*)k_srht_reg<13>,
-                          (const void*)k_srht_reg<14>};
-    const int lds = (int)(sizeof(float) * (((size_t)1 << logp) + ((size_t)1 << logp) / 64));
+    // 2^10 <= p <= 2^14: one row per workgroup, p / NT values per thread in
+    // registers; 512 threads from p = 2^12 (more waves per CU for the same LDS)
+    const int lt = logp >= 12 ? 9 : 8;
+    const void* fns[5] = {(const void*)k_srht_reg<10, 8>, (const void*)k_srht_reg<11, 8>,
+                          (const void*)k_srht_reg<12, 9>, (const void*)k_srht_reg<13, 9>,
+                          (const void*)k_srht_reg<14, 9>};
+    const int lds = (int)(sizeof(float) * (((size_t)1 << logp) + ((size_t)1 << lt)));   // p + NT slots
     const eogp_status st = ensure_dynamic_lds(fns[logp - 10], lds);
     if (st != EOGP_OK) return st;
     timing::Scope ts(EOGP_KT_SRHT, s);
     for (int64_t r0 = 0; r0 < N; r0 += 0x7FFFFFFF) {
       const int64_t nr = std::min<int64_t>(N - r0, 0x7FFFFFFF);
-      const dim3 g((unsigned)nr), b(256);
+      const dim3 g((unsigned)nr), b(1u << lt);
       const float* z0 = Z + r0 * ldz;
       float* x0 = X + r0 * ldx;
       switch (logp) {
-        case 10: hipLaunchKernelGGL(k_srht_reg<10>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
-        case 11: hipLaunchKernelGGL(k_srht_reg<11>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
-        case 12: hipLaunchKernelGGL(k_srht_reg<12>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
-        case 13: hipLaunchKernelGGL(k_srht_reg<13>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
-        default: hipLaunchKernelGGL(k_srht_reg<14>, g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        case 10: hipLaunchKernelGGL((k_srht_reg<10, 8>), g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        case 11: hipLaunchKernelGGL((k_srht_reg<11, 8>), g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        case 12: hipLaunchKernelGGL((k_srht_reg<12, 9>), g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        case 13: hipLaunchKernelGGL((k_srht_reg<13, 9>), g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
+        default: hipLaunchKernelGGL((k_srht_reg<14, 9>), g, b, lds, s, z0, ldz, (int)m, signs, rows, (int)k, scale, x0, ldx); break;
       }
     }
     EOGP_LAUNCH_CHECK("srht_project");
