@@ -212,9 +212,11 @@ class Gpt2Step:
         row0 = slot * self.B
         scales = self.scales[row0:row0 + self.B]
         k = self.k
+        # one valid-token list for the batch, shared by all modules
+        E.eogp_compact_tokens(self.mask, self.mask.shape[0], self.T, self.prec, self.ws)
         for u, (name, di, do) in enumerate(self.modules):
-            E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
-                                         Z=self.Z16, prec=self.prec, ws=self.ws)
+            E.eogp_rotate_retain_compacted(self.plans[u], self.A[name], self.D[name], self.ws,
+                                           Z=self.Z16, prec=self.prec)
             X = self.Xall[:, u * k:(u + 1) * k]
             E.eogp_pca_project(self.Z16, self.Pt[u], X=X, prec=self.pca_prec, ws=self.pca_ws)
             E.eogp_sign_pack_tiled(X[:self.B], self.codes, row0, self.steps_row, u * (k // 512),
@@ -240,9 +242,10 @@ class Gpt2Step:
         row0 = slot * self.B
         scales = self.scales[row0:row0 + self.B]
         k = self.k
+        E.eogp_compact_tokens(self.mask, self.mask.shape[0], self.T, self.prec, self.ws)
         for u, (name, di, do) in enumerate(self.modules):
-            E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
-                                         Z=self.Z, prec=self.prec, ws=self.ws)
+            E.eogp_rotate_retain_compacted(self.plans[u], self.A[name], self.D[name], self.ws,
+                                           Z=self.Z, prec=self.prec)
             X = self.Xall[:, u * k:(u + 1) * k]
             E.eogp_srht_project(self.Z, self.srht[u][0], self.srht[u][1], X=X)
             E.eogp_sign_pack_tiled(X[:self.B], self.codes, row0, self.steps_row, u * (k // 512),
@@ -279,9 +282,10 @@ class Gpt2Step:
         k2, kb2 = self.k2, self.k2 // 8
         codes = self.codes2[slot * self.B:(slot + 1) * self.B]
         scales = self.scales2[slot * self.B:(slot + 1) * self.B]
+        E.eogp_compact_tokens(self.mask, self.mask.shape[0], self.T, self.prec, self.ws)
         for u, (name, di, do) in enumerate(self.modules):
-            E.eogp_rotate_retain_planned(self.plans[u], self.A[name], self.D[name], self.mask,
-                                         Z=self.Z16, prec=self.prec, ws=self.ws)
+            E.eogp_rotate_retain_compacted(self.plans[u], self.A[name], self.D[name], self.ws,
+                                           Z=self.Z16, prec=self.prec)
             X = self.X2[:, u * k2:(u + 1) * k2]
             E.eogp_pca_project(self.Z16, self.Pt2[u], X=X, prec=self.pca_prec, ws=self.pca_ws2)
             E.eogp_sign_pack(X[:self.B], codes[:, u * kb2:(u + 1) * kb2], scales[:, u:u + 1])

@@ -163,6 +163,30 @@ eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
                                        eogp_prec prec, void* ws, size_t ws_bytes,
                                        void* stream);
 
+/* The valid-token list shared by every module of a batch (Algorithm 1 runs
+ * per example; all linear modules of an example see the same token mask).
+ * eogp_compact_tokens writes the list for (token_mask, N, T) into the head of
+ * a first-stage workspace: eogp_compact_tokens_workspace_size(N, T) bytes
+ * (0 for invalid sizes), which every eogp_rotate_retain_workspace_size for
+ * the same N and T includes. `prec` selects the list's layout: runs of each
+ * example padded to 8 tokens for EOGP_PREC_F16 and EOGP_PREC_FAST, packed for
+ * EOGP_PREC_ACCURATE. eogp_rotate_retain_compacted then runs the planned first
+ * stage of one module without compacting again; its arguments are those of
+ * eogp_rotate_retain_planned without the mask, and ws must hold the list
+ * written for the same N, T and a `prec` of the same layout (the list is not
+ * checked: another list gives wrong coordinates, with every access inside
+ * the workspace and the token rows). Sizes and errors as for the planned
+ * call; both calls only enqueue work. */
+size_t eogp_compact_tokens_workspace_size(int64_t N, int64_t T);
+eogp_status eogp_compact_tokens(const uint8_t* token_mask, int64_t N, int64_t T, eogp_prec prec,
+                                void* ws, size_t ws_bytes, void* stream);
+eogp_status eogp_rotate_retain_compacted(const eogp_plan* plan, const void* acts,
+                                         int64_t ld_acts, const void* out_grads,
+                                         int64_t ld_grads, eogp_dtype in_dtype, int64_t N,
+                                         int64_t T, void* Z, eogp_dtype z_dtype, int64_t ldz,
+                                         eogp_prec prec, void* ws, size_t ws_bytes,
+                                         void* stream);
+
 /* One-shot form with the paper's arguments: builds a plan from
  * (eigvals, damping, m, Q_A, Q_S), runs the first stage, releases the plan.
  * Synchronises `stream`. Workspace: eogp_rotate_retain_oneshot_workspace_size

@@ -17,7 +17,10 @@ size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T);
 eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
                           int64_t ld_grads, bool bf16_in,
                           const uint8_t* mask, int64_t N, int64_t T, void* Z, bool z16, int64_t ldz,
-                          int prec, void* ws, size_t ws_bytes, hipStream_t s);
+                          int prec, bool compacted, void* ws, size_t ws_bytes, hipStream_t s);
+size_t compact_ws(int64_t N, int64_t T);
+eogp_status compact_tokens(const uint8_t* mask, int64_t N, int64_t T, int prec, void* ws,
+                           size_t ws_bytes, hipStream_t s);
 eogp_status sign_pack(const float* X, int64_t ldx, int64_t N, int64_t k, uint8_t* codes,
                       int64_t cstride, uint16_t* scales, int64_t sstride, hipStream_t s);
 size_t pca_ws(int64_t N, int64_t m, int64_t k, eogp_dtype p_dtype);
@@ -121,6 +124,35 @@ eogp_status check_first_stage(const eogp_plan* p, const void* acts, const void* 
     return fail(EOGP_ERR_INVALID, "rotate_retain: N*T + 8N + 256 must be < 2^31");
   return EOGP_OK;
 }
+eogp_status planned_first_stage(const eogp_plan* plan, const void* acts, int64_t ld_acts,
+                                const void* out_grads, int64_t ld_grads, eogp_dtype in_dtype,
+                                const uint8_t* token_mask, bool compacted, int64_t N, int64_t T,
+                                void* Z, eogp_dtype z_dtype, int64_t ldz, eogp_prec prec, void* ws,
+                                size_t ws_bytes, void* stream) {
+  eogp_status st = check_first_stage(plan, acts, out_grads, in_dtype, N, T, Z, ldz, prec);
+  if (st != EOGP_OK) return st;
+  if (z_dtype != EOGP_F32 && z_dtype != EOGP_F16)
+    return fail(EOGP_ERR_INVALID, "rotate_retain: Z must be fp32 or fp16");
+  if (ld_acts == 0) ld_acts = plan->d_in;
+  if (ld_grads == 0) ld_grads = plan->d_out;
+  if (ld_acts < plan->d_in || ld_grads < plan->d_out)
+    return fail(EOGP_ERR_INVALID, "rotate_retain: token stride smaller than the width");
+  if (in_dtype == EOGP_BF16 &&
+      (ld_acts % 8 || ld_grads % 8 || (uintptr_t)acts % 16 || (uintptr_t)out_grads % 16))
+    return fail(EOGP_ERR_UNSUPPORTED,
+                "rotate_retain: bf16 token rows must start on 16-byte boundaries");
+  if (N * T * std::max(ld_acts, ld_grads) >= ((int64_t)1 << 62))
+    return fail(EOGP_ERR_INVALID, "rotate_retain: inputs too large");
+  if (N == 0) return EOGP_OK;
+  if (ws_bytes < rotate_retain_ws(plan, N, T) || !ws)
+    return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
+  int dev = -1;
+  if (hipGetDevice(&dev) == hipSuccess && dev != plan->device)
+    return fail(EOGP_ERR_INVALID, "rotate_retain: plan belongs to another device");
+  return rotate_retain(plan, acts, ld_acts, out_grads, ld_grads, in_dtype == EOGP_BF16,
+                       token_mask, N, T, Z, z_dtype == EOGP_F16, ldz, (int)prec, compacted, ws,
+                       ws_bytes, S(stream));
+}
 }  // namespace
 
 extern "C" {
@@ -190,34 +222,41 @@ size_t eogp_rotate_retain_workspace_size(const eogp_plan* plan, int64_t N, int64
   return rotate_retain_ws(plan, N, T);
 }
 
+
 eogp_status eogp_rotate_retain_planned(const eogp_plan* plan, const void* acts,
                                        int64_t ld_acts, const void* out_grads, int64_t ld_grads,
                                        eogp_dtype in_dtype, const uint8_t* token_mask, int64_t N,
                                        int64_t T, void* Z, eogp_dtype z_dtype, int64_t ldz,
                                        eogp_prec prec, void* ws, size_t ws_bytes, void* stream) {
-  eogp_status st = check_first_stage(plan, acts, out_grads, in_dtype, N, T, Z, ldz, prec);
-  if (st != EOGP_OK) return st;
-  if (z_dtype != EOGP_F32 && z_dtype != EOGP_F16)
-    return fail(EOGP_ERR_INVALID, "rotate_retain: Z must be fp32 or fp16");
-  if (ld_acts == 0) ld_acts = plan->d_in;
-  if (ld_grads == 0) ld_grads = plan->d_out;
-  if (ld_acts < plan->d_in || ld_grads < plan->d_out)
-    return fail(EOGP_ERR_INVALID, "rotate_retain: token stride smaller than the width");
-  if (in_dtype == EOGP_BF16 &&
-      (ld_acts % 8 || ld_grads % 8 || (uintptr_t)acts % 16 || (uintptr_t)out_grads % 16))
-    return fail(EOGP_ERR_UNSUPPORTED,
-                "rotate_retain: bf16 token rows must start on 16-byte boundaries");
-  if (N * T * std::max(ld_acts, ld_grads) >= ((int64_t)1 << 62))
-    return fail(EOGP_ERR_INVALID, "rotate_retain: inputs too large");
+  return planned_first_stage(plan, acts, ld_acts, out_grads, ld_grads, in_dtype, token_mask, false,
+                             N, T, Z, z_dtype, ldz, prec, ws, ws_bytes, stream);
+}
+
+size_t eogp_compact_tokens_workspace_size(int64_t N, int64_t T) {
+  if (N < 0 || T < 0 || N * T + 8 * N + 256 >= kMaxFlat) return 0;
+  return compact_ws(N, T);
+}
+
+eogp_status eogp_compact_tokens(const uint8_t* token_mask, int64_t N, int64_t T, eogp_prec prec,
+                                void* ws, size_t ws_bytes, void* stream) {
+  if (N < 0 || T < 0) return fail(EOGP_ERR_INVALID, "compact_tokens: negative size");
+  if (N * T + 8 * N + 256 >= kMaxFlat)
+    return fail(EOGP_ERR_INVALID, "compact_tokens: N*T + 8N + 256 must be < 2^31");
+  if (prec != EOGP_PREC_ACCURATE && prec != EOGP_PREC_FAST && prec != EOGP_PREC_F16)
+    return fail(EOGP_ERR_INVALID, "compact_tokens: unknown precision");
   if (N == 0) return EOGP_OK;
-  if (ws_bytes < rotate_retain_ws(plan, N, T) || !ws)
-    return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
-  int dev = -1;
-  if (hipGetDevice(&dev) == hipSuccess && dev != plan->device)
-    return fail(EOGP_ERR_INVALID, "rotate_retain: plan belongs to another device");
-  return rotate_retain(plan, acts, ld_acts, out_grads, ld_grads, in_dtype == EOGP_BF16,
-                       token_mask, N, T, Z, z_dtype == EOGP_F16, ldz, (int)prec, ws, ws_bytes,
-                       S(stream));
+  if (!ws || ws_bytes < compact_ws(N, T))
+    return fail(EOGP_ERR_WORKSPACE, "compact_tokens: workspace too small");
+  return compact_tokens(token_mask, N, T, (int)prec, ws, ws_bytes, S(stream));
+}
+
+eogp_status eogp_rotate_retain_compacted(const eogp_plan* plan, const void* acts, int64_t ld_acts,
+                                         const void* out_grads, int64_t ld_grads,
+                                         eogp_dtype in_dtype, int64_t N, int64_t T, void* Z,
+                                         eogp_dtype z_dtype, int64_t ldz, eogp_prec prec,
+                                         void* ws, size_t ws_bytes, void* stream) {
+  return planned_first_stage(plan, acts, ld_acts, out_grads, ld_grads, in_dtype, nullptr, true, N,
+                             T, Z, z_dtype, ldz, prec, ws, ws_bytes, stream);
 }
 
 size_t eogp_rotate_retain_oneshot_workspace_size(int64_t N, int64_t T, int64_t d_in,

@@ -333,11 +333,12 @@ struct Work {
 // tokens a batch of the retained products reads past the last run.
 int64_t f16_ldt(int64_t N, int64_t T) { return round_up(N * T + 8 * N + 256, 256); }
 
+size_t token_bytes(int64_t N, int64_t T) {
+  return align256((N + 1) * 4) + align256((size_t)N * 4) + align256((size_t)(N * T + 8 * N) * 4);
+}
+
 size_t work_bytes(const eogp_plan* p, int64_t N, int64_t T) {
-  size_t b = 0;
-  b += align256((N + 1) * 4);
-  b += align256((size_t)N * 4);
-  b += align256((size_t)(N * T + 8 * N) * 4);
+  size_t b = token_bytes(N, T);
   const size_t f32b = align256((size_t)N * T * p->rows_pad * 4) + align256((size_t)N * T * p->cols_pad * 4);
   const int64_t ldt = f16_ldt(N, T);
   const size_t f16b = align256((size_t)ldt * p->rows_pad * 2) + align256((size_t)ldt * p->cols_pad * 2);
@@ -353,23 +354,34 @@ size_t rotate_retain_ws(const eogp_plan* p, int64_t N, int64_t T) { return work_
 
 namespace {
 
-// Steps 1 and 2: compaction of the valid tokens and the two rotations onto
-// the plan's eigenvector panels; fills w (carved from ws). t16: fp16
-// transposed intermediates with runs aligned to 8 tokens (else fp32,
-// token-major, runs packed).
+// Step 1: the valid-token list (counts, per-example lengths, token indices)
+// at the head of the workspace. t16: runs aligned to 8 tokens (the 16-bit
+// fragment-order intermediates), else packed.
+eogp_status compact_into(const uint8_t* mask, int64_t N, int64_t T, bool t16, int32_t* cnt,
+                         int32_t* len, int32_t* tok, hipStream_t s) {
+  const unsigned g4 = (unsigned)ceil_div(N, 4);
+  timing::Scope ts(EOGP_KT_COMPACTION, s);
+  hipLaunchKernelGGL(k_count_valid, dim3(g4), dim3(256), 0, s, mask, N, T, t16 ? 8 : 1, cnt, len);
+  EOGP_HIP(scan_exclusive(cnt, N, s));
+  hipLaunchKernelGGL(k_write_tokens, dim3(g4), dim3(256), 0, s, mask, N, T, cnt, tok);
+  EOGP_LAUNCH_CHECK("token compaction");
+  return EOGP_OK;
+}
+
+// Steps 1 and 2: compaction of the valid tokens (unless `compact` is false:
+// the list is then already in w) and the two rotations onto the plan's
+// eigenvector panels; fills w (carved from ws). t16: fp16 transposed
+// intermediates with runs aligned to 8 tokens (else fp32, token-major, runs
+// packed).
 eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
                           const void* grads, int64_t ld_grads, bool bf16_in, const uint8_t* mask,
-                          int64_t N, int64_t T, int prec, bool t16, Work& w, hipStream_t s) {
+                          int64_t N, int64_t T, int prec, bool t16, bool compact, Work& w,
+                          hipStream_t s) {
   // 1. compaction
-  const unsigned g4 = (unsigned)ceil_div(N, 4);
-  {
-    timing::Scope ts(EOGP_KT_COMPACTION, s);
-    hipLaunchKernelGGL(k_count_valid, dim3(g4), dim3(256), 0, s, mask, N, T, t16 ? 8 : 1, w.cnt,
-                       t16 ? w.len : nullptr);
-    EOGP_HIP(scan_exclusive(w.cnt, N, s));
-    hipLaunchKernelGGL(k_write_tokens, dim3(g4), dim3(256), 0, s, mask, N, T, w.cnt, w.tok);
+  if (compact) {
+    const eogp_status st = compact_into(mask, N, T, t16, w.cnt, w.len, w.tok, s);
+    if (st != EOGP_OK) return st;
   }
-  EOGP_LAUNCH_CHECK("token compaction");
 
   // 2. rotations onto the used eigenvectors (rows = listed tokens; count on device)
   // FAST: bf16 operands; ACCURATE: bf16 high+low splits (three products);
@@ -427,11 +439,17 @@ eogp_status rotate_tokens(const eogp_plan* p, const void* acts, int64_t ld_acts,
   return gemm_nt2(first, second, at, a_parts, b_parts, f16, s);
 }
 
-Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
-  Work w;
+// The token list heads every first-stage workspace (eogp_compact_tokens
+// fills it alone): counts [N + 1], lengths [N], token indices [N T + 8 N].
+void carve_tokens(int64_t N, int64_t T, Carve& cv, Work& w) {
   w.cnt = cv.take<int32_t>(N + 1);
   w.len = cv.take<int32_t>(N);
   w.tok = cv.take<int32_t>((size_t)(N * T + 8 * N));
+}
+
+Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
+  Work w;
+  carve_tokens(N, T, cv, w);
   // the fp32 and fp16 layouts share one region
   const size_t f32b = align256((size_t)N * T * p->rows_pad * 4) + align256((size_t)N * T * p->cols_pad * 4);
   w.ldt = f16_ldt(N, T);
@@ -448,10 +466,24 @@ Work carve_work(const eogp_plan* p, int64_t N, int64_t T, Carve& cv) {
 
 }  // namespace
 
+size_t compact_ws(int64_t N, int64_t T) { return token_bytes(N, T); }
+
+eogp_status compact_tokens(const uint8_t* mask, int64_t N, int64_t T, int prec, void* ws,
+                           size_t ws_bytes, hipStream_t s) {
+  if (ws_bytes < token_bytes(N, T)) return fail(EOGP_ERR_WORKSPACE, "compact_tokens: workspace too small");
+  Carve cv(ws, ws_bytes);
+  Work w;
+  carve_tokens(N, T, cv, w);
+  return compact_into(mask, N, T, prec != EOGP_PREC_ACCURATE, w.cnt, w.len, w.tok, s);
+}
+
+// compacted: the token list is already at the head of ws (compact_tokens or
+// an earlier call with the same mask, sizes and precision class).
 eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts, const void* grads,
                           int64_t ld_grads, bool bf16_in,
                           const uint8_t* mask, int64_t N, int64_t T, void* Z, bool z16,
-                          int64_t ldz, int prec, void* ws, size_t ws_bytes, hipStream_t s) {
+                          int64_t ldz, int prec, bool compacted, void* ws, size_t ws_bytes,
+                          hipStream_t s) {
   if (ws_bytes < work_bytes(p, N, T)) return fail(EOGP_ERR_WORKSPACE, "rotate_retain: workspace too small");
   Carve cv(ws, ws_bytes);
   Work w = carve_work(p, N, T, cv);
@@ -460,7 +492,7 @@ eogp_status rotate_retain(const eogp_plan* p, const void* acts, int64_t ld_acts,
   // modes; fp32 token-major ones in the ACCURATE mode
   const bool t16 = prec != EOGP_PREC_ACCURATE;
   eogp_status st = rotate_tokens(p, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, t16,
-                                 w, s);
+                                 !compacted, w, s);
   if (st != EOGP_OK) return st;
 
   // 3. retained products, half-whitened, in canonical order
@@ -752,7 +784,7 @@ eogp_status ekfac_pass(const void* acts, int64_t ld_acts, const void* grads, int
   float* part = cv.take<float>((size_t)sq16_splits(N, d_in, d_out) * d_out * d_in);
   const bool f16 = prec == EOGP_PREC_F16;
   eogp_status st = rotate_tokens(&q, acts, ld_acts, grads, ld_grads, bf16_in, mask, N, T, prec, f16,
-                                 w, s);
+                                 true, w, s);
   if (st != EOGP_OK) return st;
   timing::Scope ts(EOGP_KT_EKFAC, s);
   if (f16) {

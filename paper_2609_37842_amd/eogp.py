@@ -44,6 +44,7 @@ EXPORTED = (
     "eogp_plan_create", "eogp_plan_destroy", "eogp_plan_get_info", "eogp_plan_copy_retained",
     "eogp_plan_set_input_exponents",
     "eogp_rotate_retain_workspace_size", "eogp_rotate_retain_planned",
+    "eogp_compact_tokens_workspace_size", "eogp_compact_tokens", "eogp_rotate_retain_compacted",
     "eogp_rotate_retain_oneshot_workspace_size", "eogp_rotate_retain",
     "eogp_pca_project_workspace_size", "eogp_pca_project",
     "eogp_sign_pack", "eogp_sign_pack_tiled", "eogp_srht_project_workspace_size",
@@ -77,6 +78,10 @@ def load(path: str | None = None):
         "eogp_rotate_retain_workspace_size": (c_sz, [c_vp, c_i64, c_i64]),
         "eogp_rotate_retain_planned": (c_i32, [c_vp, c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64,
                                                c_i64, c_vp, c_i32, c_i64, c_i32, c_vp, c_sz, c_vp]),
+        "eogp_compact_tokens_workspace_size": (c_sz, [c_i64, c_i64]),
+        "eogp_compact_tokens": (c_i32, [c_vp, c_i64, c_i64, c_i32, c_vp, c_sz, c_vp]),
+        "eogp_rotate_retain_compacted": (c_i32, [c_vp, c_vp, c_i64, c_vp, c_i64, c_i32, c_i64, c_i64,
+                                                 c_vp, c_i32, c_i64, c_i32, c_vp, c_sz, c_vp]),
         "eogp_rotate_retain_oneshot_workspace_size": (c_sz, [c_i64, c_i64, c_i64, c_i64, c_i64]),
         "eogp_rotate_retain": (c_i32, [c_vp, c_i64, c_vp, c_i64, c_i32, c_vp, c_i64, c_i64, c_i64,
                                        c_i64, c_vp, c_vp, c_vp, ctypes.c_double, c_i64, c_vp, c_i64,
@@ -228,29 +233,71 @@ def eogp_rotate_retain_workspace_size(plan: eogp_plan, N: int, T: int) -> int:
     return int(load().eogp_rotate_retain_workspace_size(plan._h, N, T))
 
 
-def eogp_rotate_retain_planned(plan: eogp_plan, acts, out_grads, token_mask=None, Z=None,
-                               prec=PREC_ACCURATE, ws=None, stream=None):
-    """Z [N, m] (float32) of the batch; see eogp_rotate_retain_planned in eogp.h."""
-    L = load()
-    _need_cuda(acts, out_grads, token_mask, Z)
+def _first_stage_args(plan, acts, out_grads, Z):
+    """Checks shared by the planned first-stage calls; returns (N, T, ld_a, ld_g, Z)."""
+    _need_cuda(acts, out_grads, Z)
     N, T, d_in = acts.shape
     if tuple(out_grads.shape) != (N, T, plan.d_out) or d_in != plan.d_in:
         raise ValueError("acts [N,T,d_in] / out_grads [N,T,d_out] do not match the plan")
     ld_a, ld_g = _token_stride(acts, "acts"), _token_stride(out_grads, "out_grads")
-    if token_mask is not None and (token_mask.dtype != torch.uint8 or tuple(token_mask.shape) != (N, T)
-                                   or not token_mask.is_contiguous()):
-        raise ValueError("token_mask must be contiguous uint8 [N, T]")
     if Z is None:
         Z = torch.empty((N, plan.m), dtype=torch.float32, device=acts.device)
     if (Z.dtype not in (torch.float32, torch.float16) or Z.dim() != 2 or Z.stride(1) != 1
             or Z.shape[0] != N):
         raise ValueError("Z must be float32 or float16 [N, >= m] with unit column stride")
+    return N, T, ld_a, ld_g, Z
+
+
+def eogp_rotate_retain_planned(plan: eogp_plan, acts, out_grads, token_mask=None, Z=None,
+                               prec=PREC_ACCURATE, ws=None, stream=None):
+    """Z [N, m] (float32) of the batch; see eogp_rotate_retain_planned in eogp.h."""
+    L = load()
+    _need_cuda(token_mask)
+    N, T, ld_a, ld_g, Z = _first_stage_args(plan, acts, out_grads, Z)
+    if token_mask is not None and (token_mask.dtype != torch.uint8 or tuple(token_mask.shape) != (N, T)
+                                   or not token_mask.is_contiguous()):
+        raise ValueError("token_mask must be contiguous uint8 [N, T]")
     need = eogp_rotate_retain_workspace_size(plan, N, T)
     ws, wsb = _workspace(need, acts.device, ws)
     _check(L.eogp_rotate_retain_planned(plan._h, _ptr(acts), ld_a, _ptr(out_grads), ld_g,
                                         _acts_dtype(acts, out_grads), _ptr(token_mask), N, T,
                                         _ptr(Z), _DTYPE_CODE[Z.dtype], Z.stride(0), prec, _ptr(ws),
                                         wsb, _stream(stream)))
+    return Z
+
+
+def eogp_compact_tokens_workspace_size(N: int, T: int) -> int:
+    return int(load().eogp_compact_tokens_workspace_size(N, T))
+
+
+def eogp_compact_tokens(token_mask, N: int, T: int, prec, ws, stream=None):
+    """Valid-token list of (token_mask, N, T) into the head of the first-stage
+    workspace `ws` (a uint8 device tensor); see eogp_compact_tokens in eogp.h."""
+    L = load()
+    if ws is None:
+        raise ValueError("eogp_compact_tokens writes into a caller's first-stage workspace")
+    _need_cuda(token_mask, ws)
+    if token_mask is not None and (token_mask.dtype != torch.uint8 or tuple(token_mask.shape) != (N, T)
+                                   or not token_mask.is_contiguous()):
+        raise ValueError("token_mask must be contiguous uint8 [N, T]")
+    ws, wsb = _workspace(eogp_compact_tokens_workspace_size(N, T), ws.device, ws)
+    _check(L.eogp_compact_tokens(_ptr(token_mask), N, T, prec, _ptr(ws), wsb, _stream(stream)))
+
+
+def eogp_rotate_retain_compacted(plan: eogp_plan, acts, out_grads, ws, Z=None, prec=PREC_ACCURATE,
+                                 stream=None):
+    """The planned first stage with the token list already in `ws` (written by
+    eogp_compact_tokens for the same N, T and precision layout)."""
+    L = load()
+    if ws is None:
+        raise ValueError("the compacted first stage reads the token list from ws")
+    _need_cuda(ws)
+    N, T, ld_a, ld_g, Z = _first_stage_args(plan, acts, out_grads, Z)
+    ws, wsb = _workspace(eogp_rotate_retain_workspace_size(plan, N, T), acts.device, ws)
+    _check(L.eogp_rotate_retain_compacted(plan._h, _ptr(acts), ld_a, _ptr(out_grads), ld_g,
+                                          _acts_dtype(acts, out_grads), N, T, _ptr(Z),
+                                          _DTYPE_CODE[Z.dtype], Z.stride(0), prec, _ptr(ws), wsb,
+                                          _stream(stream)))
     return Z
 
 

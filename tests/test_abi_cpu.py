@@ -52,6 +52,30 @@ def test_plan_argument_validation_without_device():
     assert L.eogp_plan_set_input_exponents(None, 0, 0) == -1
 
 
+def test_token_compaction_argument_validation_without_device():
+    """eogp_compact_tokens / eogp_rotate_retain_compacted reject bad arguments
+    before touching the device; the list's size query matches the head of
+    every first-stage workspace."""
+    L = E.load()
+    fake = ctypes.c_void_p(0x1000)
+    align = lambda b: -(-b // 256) * 256
+    N, T = 5, 7
+    assert L.eogp_compact_tokens_workspace_size(N, T) == align(4 * (N + 1)) + align(4 * N) + align(4 * (N * T + 8 * N))
+    assert L.eogp_compact_tokens_workspace_size(-1, T) == 0
+    assert L.eogp_compact_tokens_workspace_size(1 << 20, 1 << 12) == 0     # N*T + 8N + 256 >= 2^31
+    assert L.eogp_compact_tokens(fake, -1, T, E.PREC_F16, fake, 1 << 20, None) == -1
+    assert L.eogp_compact_tokens(fake, 1 << 20, 1 << 12, E.PREC_F16, fake, 1 << 40, None) == -1
+    assert L.eogp_compact_tokens(fake, N, T, 9, fake, 1 << 20, None) == -1            # precision
+    assert L.eogp_compact_tokens(fake, N, T, E.PREC_F16, fake, 16, None) == -4        # workspace
+    assert L.eogp_compact_tokens(fake, N, T, E.PREC_F16, None, 1 << 20, None) == -4
+    assert L.eogp_compact_tokens(fake, 0, T, E.PREC_F16, None, 0, None) == 0          # nothing to do
+    # the compacted first stage: NULL plan, Z dtype
+    assert L.eogp_rotate_retain_compacted(None, fake, 0, fake, 0, 0, N, T, fake, 0, 8, 1, fake,
+                                          1 << 20, None) == -1
+    with pytest.raises(ValueError):
+        E.eogp_rotate_retain_compacted(None, None, None, None)
+
+
 def test_encode_and_score_argument_validation_without_device():
     L = E.load()
     fake = ctypes.c_void_p(0x1000)

@@ -449,6 +449,37 @@ def test_rotate_retain_block_groups(axis):
     plan.close()
 
 
+def test_rotate_retain_compacted_matches_planned():
+    """One token list (eogp_compact_tokens) serves several modules of a batch:
+    eogp_rotate_retain_compacted gives the planned call's Z bit for bit, in
+    every precision, for two plans of different widths, with empty and
+    ragged examples."""
+    say("[first stage] shared token list")
+    N, T = 6, 90
+    probs = []
+    for seed, (d_in, d_out, m) in ((81, (97, 130, 900)), (82, (64, 257, 1200))):
+        a, ds, _, QA, QS, lam = random_problem(seed, N, T, d_in, d_out, m, nan_masked=False)
+        probs.append((a, ds, QA, QS, lam, m))
+    g = np.random.default_rng(83)
+    lens = g.integers(0, T + 1, size=N)
+    lens[1] = 0                                          # an example with no valid token
+    mask = S.prefix_mask(lens, T)
+    plans = [E.eogp_plan_create(d(lam), 1e-4, m, d(QA), d(QS)) for (_, _, QA, QS, lam, m) in probs]
+    need = max(E.eogp_rotate_retain_workspace_size(p, N, T) for p in plans)
+    ws = torch.empty(need, dtype=torch.uint8, device=DEV)
+    for prec in (E.PREC_F16, E.PREC_FAST, E.PREC_ACCURATE):
+        E.eogp_compact_tokens(d(mask), N, T, prec, ws)
+        for p, (a, ds, QA, QS, lam, m) in zip(plans, probs):
+            af, df = d(S.fill_masked(a, mask)), d(S.fill_masked(ds, mask))
+            Zc = E.eogp_rotate_retain_compacted(p, af, df, ws, prec=prec)
+            Zp = E.eogp_rotate_retain_planned(p, af, df, d(mask), prec=prec)
+            torch.cuda.synchronize()
+            assert torch.equal(Zc, Zp), f"prec {prec}"
+            assert torch.all(Zc[1] == 0)
+    for p in plans:
+        p.close()
+
+
 def test_rotate_retain_fp16_mode_input_exponents():
     """Gradients of order 1e-7 (below fp16's normal range) are brought into
     range by the plan's exponent; the result is then as accurate as for
