@@ -3,16 +3,17 @@
 // Two kernels share the staging conventions below.
 //
 // k_gemm_p (single-pass products on aligned operands: the rotations, and the
-// PCA projection with split-K). A 256-thread
-// workgroup (4 wave64s, one per SIMD) owns a 256 x 256 output tile; each wave
-// computes 128 x 128 with v_mfma_f32_32x32x16 blocks accumulating in the
-// accumulation registers. K advances 32 at a time through two LDS stages. One
-// iteration per slice, one block barrier: the second half-slice's fragments
-// are read and the first half's 16 MFMAs issue beside the staging of the next
-// slice (B, then A converted while it is written) and the global requests for
-// later slices; after the barrier the next slice's first-half fragments are
-// read while the second half's MFMAs issue. A and B are requested two slices
-// before they are staged (two register buffers each).
+// PCA projection with split-K). A workgroup owns a 256 x 256 output tile with
+// 8 wave64s (two per SIMD, 128 x 64 each; the kernel also builds with 4 waves
+// of 128 x 128) computing with v_mfma_f32_32x32x16 blocks. K advances 32 at a
+// time through two LDS stages. One iteration per slice, one block barrier:
+// the second half-slice's fragments are read and the first half's MFMAs issue
+// beside the staging of the next slice (B, then A converted while it is
+// written) and the global requests for later slices; after the barrier the
+// next slice's first-half fragments are read while the second half's MFMAs
+// issue. A and B are requested two slices before they are staged (two
+// register buffers each). A wave whose columns all lie in the padding of the
+// last column tile stages its share and skips its fragment reads and MFMAs.
 //
 // k_gemm (everything else: bf16x3 products, unaligned or bounds-checked
 // operands). A 512-thread workgroup (8 waves, two per SIMD)
