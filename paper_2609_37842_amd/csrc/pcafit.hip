@@ -25,6 +25,7 @@
 #include <mutex>
 
 #include "common.h"
+#include "pcafit_layout.h"
 #include "timing.h"
 
 namespace eogp {
@@ -202,28 +203,6 @@ rocblas_handle solver_handle(eogp_status* st) {
   }
   handles[dev] = h;
   return h;
-}
-
-struct FitLayout {
-  size_t g, w, v, vs, ints, solver, total;
-};
-
-// The eigenvector array handed to dsyevdx gets all n columns: rocSOLVER
-// documents that the columns of its eigenvector output may serve as internal
-// workspace, so an array sized for the k requested vectors could be written
-// past its end (here: over V_s, the status words and the solver workspace).
-FitLayout fit_layout(int64_t n, int64_t k, size_t solver_bytes) {
-  FitLayout L;
-  size_t o = 0;
-  auto take = [&](size_t b) { size_t r = o; o = align256(o + b); return r; };
-  L.ints = take(4 * sizeof(int));
-  L.solver = take(solver_bytes);
-  L.g = take((size_t)n * n * 8);
-  L.w = take((size_t)n * 8);
-  L.v = take((size_t)n * n * 8);
-  L.vs = take((size_t)n * k * 8);
-  L.total = o;
-  return L;
 }
 
 // The full divide-and-conquer solver (dsyevd) when many vectors are asked
