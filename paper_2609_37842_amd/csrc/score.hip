@@ -26,10 +26,11 @@
 // w) with t = s + w, w = t mod NCLS: its bytes are 0 or 2^w, so the MFMA adds
 // 2^w times the wanted sum into accumulator class w, and n1 = sum_w acc_w /
 // 2^w (exact shifts: every term of acc_w is a multiple of 2^w). One shift
-// serves NCLS masks, so the expansion costs (1 + NCLS) / NCLS ... 1 VALU op
-// per 4 bits instead of 2. The query planes are prepared in exactly that
-// order: byte j of lane (M, g) of MFMA (u, t) in step s of a module holds
-// coordinate 8 (64 s + 32 g + 16 u + j) + t.
+// serves NCLS masks, and one 64-bit shift serves two words, so with NCLS = 2
+// expanding 16 bytes for their 8 MFMAs takes 32 ANDs and 6 shifts (a shift
+// and an AND per word and MFMA would take 64). The query planes are prepared
+// in exactly that order: byte j of lane (M, g) of MFMA (u, t) in step s of a
+// module holds coordinate 8 (64 s + 32 g + 16 u + j) + t.
 //
 // After the last module the workgroup's scores are filtered against a
 // per-query threshold into an LDS candidate list (score desc, index asc). A
@@ -76,6 +77,16 @@ struct ModInfo {
   int32_t boff;    // first byte of the module in a code row
   int32_t sbase;   // first step of the module
 };
+
+// Logical right shift of a register pair by s in one VALU instruction. The
+// compiler turns a 64-bit shift whose result is masked to bits that never
+// cross the halves back into two 32-bit shifts; here the bits that do cross
+// are masked away by the caller, so one instruction serves two words.
+__device__ __forceinline__ uint64_t shr_pair(uint64_t x, int s) {
+  uint64_t r;
+  asm("v_lshrrev_b64 %0, %1, %2" : "=v"(r) : "s"(s), "v"(x));
+  return r;
+}
 
 __device__ __forceinline__ uint64_t order_key(double x) {
   uint64_t u = (uint64_t)__double_as_longlong(x);
@@ -548,11 +559,18 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
 #pragma unroll
         for (int rt = 0; rt < RT; ++rt) {
           const uint4 c = ring[SL][rt][uc];
+          // bits shifted across the halves land at 32 - sh and above, never
+          // under the mask (its highest bit is 24 + w, and sh + w <= 7)
+          uint64_t p0 = ((uint64_t)c.y << 32) | c.x, p1 = ((uint64_t)c.w << 32) | c.z;
+          if (sh) {
+            p0 = shr_pair(p0, sh);
+            p1 = shr_pair(p1, sh);
+          }
           i32x4 av;
-          av[0] = (int)((c.x >> sh) & mk);
-          av[1] = (int)((c.y >> sh) & mk);
-          av[2] = (int)((c.z >> sh) & mk);
-          av[3] = (int)((c.w >> sh) & mk);
+          av[0] = (int)((uint32_t)p0 & mk);
+          av[1] = (int)((uint32_t)(p0 >> 32) & mk);
+          av[2] = (int)((uint32_t)p1 & mk);
+          av[3] = (int)((uint32_t)(p1 >> 32) & mk);
           acc[rt][w] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fr[f % 3], av, acc[rt][w], 0, 0, 0);
         }
         // per round: the read two rounds ahead, then each tile's expansion and MFMA
