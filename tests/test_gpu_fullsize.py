@@ -174,10 +174,11 @@ def test_gpt2_small_full_step_shape(si):
                       <= 2 * np.spacing(so).astype(np.float64))
 
 
-@pytest.mark.parametrize("si", [4, 6])        # gate_proj 2048 -> 8192, down_proj 8192 -> 2048
-def test_olmo2_1b_bf16_modules(si):
-    """OLMo-2-1B-shaped modules, bf16 inputs, T = 1024 with lengths
-    U{64..1024}, m = 32768: two sampled examples, all retained coordinates,
+@pytest.mark.parametrize("si", [0, 4, 6])     # q_proj 2048 -> 2048 (the shape of k, v, o too),
+def test_olmo2_1b_bf16_modules(si):            # gate_proj 2048 -> 8192, down_proj 8192 -> 2048
+    """OLMo-2-1B-shaped modules (every distinct shape of the block), bf16
+    inputs, T = 1024 with lengths U{64..1024}, m = 32768: two sampled
+    examples, all retained coordinates,
     in the bf16 mode, the accurate mode and the fp16 mode (bf16 inputs taken
     exactly, bases and rotated tokens rounded to fp16)."""
     w = S.OLMO2_1B
@@ -188,9 +189,10 @@ def test_olmo2_1b_bf16_modules(si):
                         [0, 11])
 
 
-@pytest.mark.parametrize("si", [1, 5, 6])     # k_proj 5120 -> 1024, up 5120 -> 27648, down
-def test_olmo2_32b_bf16_modules(si):
-    """OLMo-2-32B-shaped modules (grouped-query k_proj, MLP up and down), bf16
+@pytest.mark.parametrize("si", [0, 1, 5, 6])  # q_proj 5120 -> 5120, k_proj 5120 -> 1024, up
+def test_olmo2_32b_bf16_modules(si):            # 5120 -> 27648, down 27648 -> 5120
+    """OLMo-2-32B-shaped modules (every distinct shape of the block: q_proj
+    as o_proj, grouped-query k_proj as v_proj, MLP up as gate, down), bf16
     inputs, T = 2048, m = 65536: 512 sampled retained coordinates of two
     examples; the whole retained set is checked bit-exactly."""
     w = S.OLMO2_32B
