@@ -300,3 +300,52 @@ def test_scoring_8m_codes_tiled_store():
         rest = torch.ones(N, dtype=torch.bool, device=DEV)
         rest[iq] = False
         assert float(f[q][rest].max()) <= float(sc[q, -1])
+
+
+def test_scoring_olmo2_1b_store_tiled():
+    """The OLMo-2-1B-shaped store the bench scores: 100,000 rows x 112 modules
+    x 16,384 bits in the tiled layout (23 GB; random bytes are a valid tiled
+    store), per-module fp16 scales, 16 queries, top-100 (the several-module
+    pass: module ranges split across workgroups, exact per-module dots summed
+    in module order). 8 sampled tiles (256 rows), converted to row-major by
+    the layout's definition, are scored exactly against the oracle; the
+    top-100 is checked by the properties that define it."""
+    w = S.OLMO2_1B
+    U = len(w.modules)
+    N, k, Q, topk = w.N, w.k, 16, w.topk
+    ks = [k] * U
+    S_row = U * k // 512
+    say(f"[full size] olmo2-1b store N={N} U={U} k={k}")
+    g = torch.Generator(device=DEV)
+    g.manual_seed(112)
+    nbytes = E.tiled_store_bytes(N, ks)
+    codes = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    for i0 in range(0, nbytes, 1 << 30):
+        i1 = min(nbytes, i0 + (1 << 30))
+        codes[i0:i1] = torch.randint(0, 256, (i1 - i0,), dtype=torch.uint8, device=DEV, generator=g)
+    scales = torch.exp(torch.randn((N, U), device=DEV, generator=g)).half().view(torch.int16)
+    Y = torch.randn((Q, U * k), device=DEV, generator=g)
+    idx, sc, full = E.eogp_score_topk_tiled(codes, scales, N, ks, Y, topk, full_scores=True)
+    torch.cuda.synchronize()
+    n_tiles = -(-N // 32)
+    tiles = np.sort(np.random.default_rng(11).choice(n_tiles - 1, 7, replace=False))
+    tiles = np.append(tiles, n_tiles - 1)            # the last tile (rows past N unused)
+    blk = S_row * 2048
+    sub = np.concatenate([codes[t * blk:(t + 1) * blk].cpu().numpy() for t in tiles])
+    rows_codes = rows_from_tiled(sub, S_row)
+    rows = (tiles[:, None] * 32 + np.arange(32)[None, :]).reshape(-1)
+    keep = rows < N
+    rows, rows_codes = rows[keep], rows_codes[keep]
+    ri = torch.from_numpy(rows).to(DEV)
+    ref = O.score(rows_codes, scales[ri].cpu().numpy().view(np.uint16), ks, Y.cpu().numpy())
+    assert np.array_equal(full[:, ri].cpu().numpy(), ref.astype(np.float32))
+    f = full.double()
+    for q in range(Q):
+        iq = idx[q]
+        assert torch.equal(sc[q], full[q, iq])
+        assert bool(torch.all(sc[q, :-1] >= sc[q, 1:]))
+        rest = torch.ones(N, dtype=torch.bool, device=DEV)
+        rest[iq] = False
+        assert float(f[q][rest].max()) <= float(sc[q, -1])
+    del codes
+    torch.cuda.empty_cache()
