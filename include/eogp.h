@@ -22,7 +22,10 @@
  *     only enqueue work on it and return, except eogp_plan_create, the
  *     one-shot eogp_rotate_retain and eogp_pca_fit, which synchronise `stream`
  *     once. Host arrays passed to an enqueuing call (such as k_per_module)
- *     are read before the call returns and may be released at once.
+ *     are read before the call returns and may be released at once. The
+ *     enqueuing calls launch kernels only (eogp_plan_copy_retained a
+ *     device-to-device copy): no allocation, memset or host wait, so a
+ *     sequence of them can be captured in a HIP graph and replayed.
  *   - Argument errors return EOGP_ERR_INVALID before anything is enqueued;
  *     EOGP_ERR_UNSUPPORTED marks a valid but unimplemented dtype/shape mix;
  *     EOGP_ERR_DEVICE a HIP launch or runtime error; EOGP_ERR_WORKSPACE a
