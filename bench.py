@@ -515,7 +515,7 @@ def cpu_baseline(st: Gpt2Step):
 OLMO_GRAD_EXPONENT = 0    # OLMo-2-shaped output-gradients (std ~0.014) sit in fp16's normal range
 
 
-def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False, prec="f16"):
+def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False, prec="f16", cpu_ex=4):
     """`resident` transformer blocks of an OLMo-2-shaped model (7 linears
     each, bf16 activations and output-gradients), each module with its own
     plan (gathered eigenvector panels) and its own fp16 P held in HBM at the
@@ -619,7 +619,7 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False, prec="f
     }
     if cpu:
         out["cpu_baseline"], out["parity"] = olmo_cpu_baseline(w, mods, inputs, codes, scales, B,
-                                                               n_model_blocks, out)
+                                                               n_model_blocks, out, n_ex=cpu_ex)
     for (_, _, _, plan, _) in mods:
         plan.close()
     del mods, inputs, Z, X, codes, scales, ws, pws
@@ -627,11 +627,14 @@ def olmo_block(w, B, n_model_blocks, dev, reps=3, resident=1, cpu=False, prec="f
     return out
 
 
-def olmo_cpu_baseline(w, mods, inputs, codes, scales, B, n_model_blocks, meas, n_ex=4):
+def olmo_cpu_baseline(w, mods, inputs, codes, scales, B, n_model_blocks, meas, n_ex=4,
+                      pca_chunk=4096):
     """The oracle on a bounded sample of the OLMo-2 block: n_ex examples
     through the first block's module of each distinct shape (first stage, PCA,
     encoding), extrapolated to the whole model; and the sign bits of this
-    run's codes for those examples against the oracle's."""
+    run's codes for those examples against the oracle's. P comes to the host
+    pca_chunk directions at a time (each output coordinate depends on its own
+    direction only); only the oracle's calls are timed."""
     import numpy as np
 
     import oracle as O
@@ -648,8 +651,7 @@ def olmo_cpu_baseline(w, mods, inputs, codes, scales, B, n_model_blocks, meas, n
         QA = art["Q_A"].double().cpu().numpy()
         QS = art["Q_S"].double().cpu().numpy()
         lam = art["eigvals"].cpu().numpy()
-        P = art["Pt"].cpu().numpy().astype(np.float64).T
-        del art
+        Pt = art["Pt"]
         a, ds, mk = inputs[(di, do)]
         a = a[:n_ex].float().double().cpu().numpy()
         ds = ds[:n_ex].float().double().cpu().numpy()
@@ -657,12 +659,22 @@ def olmo_cpu_baseline(w, mods, inputs, codes, scales, B, n_model_blocks, meas, n
         ret = O.select_retained(lam, float(S.recipe_damping(w)), w.m)
         t0 = time.perf_counter()
         Zo = np.stack([O.first_stage_tokens(a[i], ds[i], mk[i], QA, QS, ret) for i in range(n_ex)])
-        Xo = O.pca_project(Zo, P)
+        t_oracle = time.perf_counter() - t0
+        del QA, QS
+        Xo = np.empty((n_ex, w.k))
+        for c0 in range(0, w.k, pca_chunk):
+            Pc = Pt[c0:c0 + pca_chunk].cpu().numpy().astype(np.float64).T   # [m, chunk]
+            t0 = time.perf_counter()
+            Xo[:, c0:c0 + Pc.shape[1]] = O.pca_project(Zo, Pc)
+            t_oracle += time.perf_counter() - t0
+            del Pc
+        t0 = time.perf_counter()
         O.encode(Xo)
-        per_shape[name] = (time.perf_counter() - t0) / n_ex
+        t_oracle += time.perf_counter() - t0
+        per_shape[name] = t_oracle / n_ex
         cg = codes[:n_ex, si * kb:(si + 1) * kb].cpu().numpy()
         parity[name] = sign_parity(O.unpack_bits(cg, w.k), Xo)
-        del P, QA, QS
+        del art, Pt
     shape_of = {}
     for (name, di, do) in w.block:
         shape_of[name] = seen[(di, do)]
@@ -1017,10 +1029,12 @@ def main(argv=None):
         torch.cuda.empty_cache()
     if not args.no_olmo and not args.only_scoring:
         from paper_2609_37842_amd import synth as S
-        for key, w, B, nb, res in (("olmo2_1b", S.OLMO2_1B, 256, 16, 1),
-                                   ("olmo2_32b", S.OLMO2_32B, 64, 64, 4)):
-            o = olmo_block(w, B, nb, dev, resident=res,
-                           cpu=(key == "olmo2_1b" and not args.no_cpu_baseline), prec=args.olmo_prec)
+        # (the oracle's sample: 4 examples per shape of the 1B block, one 2,048-token
+        # example per shape of the 32B block)
+        for key, w, B, nb, res, cpu_ex in (("olmo2_1b", S.OLMO2_1B, 256, 16, 1, 4),
+                                           ("olmo2_32b", S.OLMO2_32B, 64, 64, 4, 1)):
+            o = olmo_block(w, B, nb, dev, resident=res, cpu=not args.no_cpu_baseline,
+                           prec=args.olmo_prec, cpu_ex=cpu_ex)
             log(f"{w.name}: {o['ms_per_block']:.1f} ms per block of {B}, "
                 f"{o['examples_per_s_full_model']:.2f} ex/s full model, rotation "
                 f"{o['rotation_roofline']['achieved']:.0f} TFLOP/s")
