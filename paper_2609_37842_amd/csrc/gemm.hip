@@ -1001,7 +1001,7 @@ eogp_status launch(const GemmArgs& g, bool av, bool bc, hipStream_t s) {
   }
   if constexpr (AP == 1 && BP == 1) {
     if (av && !bc) {
-      // single-pass product: the pipelined 4-wave kernel, 256 x 256 tiles.
+      // single-pass product: the pipelined kernel (kPipeWaves waves), 256 x 256 tiles.
       // Split K (host-known M, scratch given) when that shortens the
       // estimated time: rounds of units x slices per unit, plus the partial
       // sums (one slice of a 256 x 256 tile ~ 1.4 us; partials at ~5 TB/s).
