@@ -7,13 +7,15 @@
 // 8 wave64s (two per SIMD, 128 x 64 each; the kernel also builds with 4 waves
 // of 128 x 128) computing with v_mfma_f32_32x32x16 blocks. K advances 32 at a
 // time through two LDS stages. One iteration per slice, one block barrier:
-// the second half-slice's fragments are read and the first half's MFMAs issue
-// beside the staging of the next slice (B, then A converted while it is
-// written) and the global requests for later slices; after the barrier the
-// next slice's first-half fragments are read while the second half's MFMAs
-// issue. A and B are requested two slices before they are staged (two
-// register buffers each). A wave whose columns all lie in the padding of the
-// last column tile stages its share and skips its fragment reads and MFMAs.
+// the first half's MFMAs issue, A fragment by A fragment, beside the staging
+// of the next slice (B, then A converted while it is written) and the global
+// requests for later slices, and each A fragment's register is refilled with
+// the second half's fragment as soon as its MFMAs have issued; after the
+// barrier the second half's MFMAs issue the same way while the next slice's
+// first-half fragments are read. A and B are requested two slices before they
+// are staged (two register buffers each). A wave whose columns all lie in the
+// padding of the last column tile stages its share and skips its fragment
+// reads and MFMAs.
 //
 // k_gemm (everything else: bf16x3 products, unaligned or bounds-checked
 // operands). A 512-thread workgroup (8 waves, two per SIMD)
@@ -583,7 +585,10 @@ void k_gemm_p(KParams kp) {
   __shared__ int64_t sOff[BM];
   __shared__ int sPos;
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index through readfirstlane: the compiler then treats the per-wave
+  // branch below as uniform (two separate loops, not one masked after the other)
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   // Units of each product: tiles x splits (M from the device count when given).
   auto units_of = [&](int pi) -> int64_t {
     const GemmArgs& q = pi ? kp.g2 : kp.g;
@@ -708,10 +713,10 @@ void k_gemm_p(KParams kp) {
       v4u ra16[AT == 0 ? 1 : AQ];
     };
     struct BRegs { v4u rb[BQ]; };
-    struct Frag { v4u a[WI]; v4u b[WJ]; };
     ARegs A0, A1;
     BRegs RB, RB2;
-    Frag F0, F1;
+    v4u fa[WI];                 // A fragments of the half slice being multiplied
+    v4u fb0[WJ], fb1[WJ];       // B fragments of the first and second half
 
     auto load_a = [&](int64_t k0, ARegs& R) {
       if constexpr (AT == 0) {
@@ -762,10 +767,11 @@ void k_gemm_p(KParams kp) {
       }
       load_b(k0, R);
     };
-    auto stage_a = [&](int st, const ARegs& RA) {
+    auto stage_a = [&](int st, const ARegs& RA, int q0, int q1) {
       if constexpr (AT == 0) {
 #pragma unroll
         for (int q = 0; q < AQ; ++q) {
+          if (q < q0 || q >= q1) continue;
           const int r = a_r0 + a_rs * q;
           const int o = swz(r, a_pc >> 1) + 4 * (a_pc & 1);
           v4f x = RA.ra[q];
@@ -779,6 +785,7 @@ void k_gemm_p(KParams kp) {
         // bf16 pairs -> fp32 (exact) -> times 2^e (exact) -> fp16 pairs, nearest even
 #pragma unroll
         for (int q = 0; q < AQ; ++q) {
+          if (q < q0 || q >= q1) continue;
           const v4u w = RA.ra16[q];
           uint32_t h[4];
 #pragma unroll
@@ -795,7 +802,8 @@ void k_gemm_p(KParams kp) {
       } else {
 #pragma unroll
         for (int q = 0; q < AQ; ++q)
-          *reinterpret_cast<v4u*>(&sA[st][swz(a_r0 + a_rs * q, a_pc)]) = RA.ra16[q];
+          if (q >= q0 && q < q1)
+            *reinterpret_cast<v4u*>(&sA[st][swz(a_r0 + a_rs * q, a_pc)]) = RA.ra16[q];
       }
     };
     auto stage_b = [&](int st, const BRegs& R) {
@@ -803,14 +811,15 @@ void k_gemm_p(KParams kp) {
       for (int q = 0; q < BQ; ++q)
         *reinterpret_cast<v4u*>(&sB[st][swz(b_r0 + B_RS * q, b_pc)]) = R.rb[q];
     };
-    auto read_frag = [&](int st, int ks, Frag& F) {
+    auto read_a = [&](int st, int ks, int i) -> v4u {
+      const int ch = 2 * ks + (lane >> 5);
+      return *reinterpret_cast<const v4u*>(&sA[st][swz(wm + 32 * i + (lane & 31), ch)]);
+    };
+    auto read_b = [&](int st, int ks, v4u (&fb)[WJ]) {
       const int ch = 2 * ks + (lane >> 5);
 #pragma unroll
-      for (int i = 0; i < WI; ++i)
-        F.a[i] = *reinterpret_cast<const v4u*>(&sA[st][swz(wm + 32 * i + (lane & 31), ch)]);
-#pragma unroll
       for (int j = 0; j < WJ; ++j)
-        F.b[j] = *reinterpret_cast<const v4u*>(&sB[st][swz(wn + 32 * j + (lane & 31), ch)]);
+        fb[j] = *reinterpret_cast<const v4u*>(&sB[st][swz(wn + 32 * j + (lane & 31), ch)]);
     };
 
     f32x16 acc[WI][WJ];
@@ -820,102 +829,146 @@ void k_gemm_p(KParams kp) {
       for (int j = 0; j < WJ; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    constexpr int NM = WI * WJ;               // MFMAs per half slice
-    constexpr int NMB = NM / 4;               // of those, issued beside the B work
-    // MFMAs with index < lim (from = 0) or >= lim (from = 1) of a half slice.
-    auto mma_part = [&](const Frag& F, int from, int lim) {
+    // Fragments: fa holds the A fragments of the half slice being multiplied,
+    // fb0 and fb1 the B fragments of a slice's first and second half. The
+    // MFMAs of a half are issued A fragment by A fragment, so fragment i of
+    // the next half is read into fa[i] as soon as its own MFMAs have issued
+    // (32 fragment registers instead of two full sets of 48).
+    static_assert(WI == 4, "the first half's four segments take one A fragment each");
+    auto pair = [&](int i, const v4u (&fb)[WJ]) {
 #pragma unroll
-      for (int j = 0; j < WJ; ++j)
-#pragma unroll
-        for (int i = 0; i < WI; ++i) {
-          const int m = j * WI + i;
-          if ((from == 0 && m < lim) || (from == 1 && m >= lim))
-            acc[i][j] = mfma32<F16>(F.a[i], F.b[j], acc[i][j]);
-        }
+      for (int j = 0; j < WJ; ++j) acc[i][j] = mfma32<F16>(fa[i], fb[j], acc[i][j]);
     };
-    auto mma = [&](const Frag& F) { mma_part(F, 1, 0); };
+    // Scheduling-group masks: MFMA 0x008, VALU 0x002, global load 0x020,
+    // LDS read 0x100, LDS write 0x200.
 
-    // prologue: slice 0 staged; slices 1 and 2 requested (A into A1 and A0,
-    // B into RB and RB2)
+    // prologue: slice 0 staged; slices 1 and 2 requested in the order the
+    // loop issues them (B then A of each slice), so that the load counter
+    // holds the same sequence on entry as after every iteration
     if (ragged) load_tail(slice_k0(0), A0, RB);
     else {
       load_a(slice_k0(0), A0);
       load_b(slice_k0(0), RB);
     }
-    stage_a(0, A0);
+    stage_a(0, A0, 0, AQ);
     stage_b(0, RB);
     if (nk > 1) {
       load_b(clamp(1), RB);
-      load_b(clamp(2), RB2);
       load_a(clamp(1), A1);
+      load_b(clamp(2), RB2);
       load_a(clamp(2), A0);
     }
     __syncthreads();
 
-    // One slice i in stage st (F0 holds its first half; the registers hold
-    // slices i+1 and i+2 of A and B; RB is the B buffer holding slice i+1).
-    // Scheduling hints keep the three regions apart and spread each region's
-    // MFMAs over its other work. ACT: the wave has columns below N; a wave
-    // whose columns all lie in the padding of the last column tile only
-    // stages its share of the operands (its accumulators stay zero).
+    // One slice i in stage st (fa and fb0 hold its first half; the registers
+    // hold slices i+1 and i+2 of A and B; RB is the B buffer holding slice
+    // i+1, Anext the A buffer). ACT: the wave has columns below N; a wave whose
+    // columns all lie in the padding of the last column tile only stages its
+    // share of the operands (its accumulators stay zero).
     auto iter = [&](auto act_c, int st, int64_t i, ARegs& Anext, BRegs& RB) {
       constexpr bool ACT = decltype(act_c)::value;
       const int64_t k3 = clamp(i + 3);
-      // region 1a: second-half fragment reads; B of slice i+1 to LDS; B of
-      // slice i+3 requested before A of slice i+3, so that a wait for B never
-      // waits for the A request behind it
+      // First half, in four segments of one A fragment each: its MFMAs, then
+      // its second-half fragment read into fa[i]; beside them B of slice i+1
+      // to LDS and B of slice i+3 requested (segment 0), A of slice i+1
+      // converted and written to LDS (segments 1 and 2), A of slice i+3
+      // requested (segment 3). B is requested before A, so that a wait for B
+      // never waits for the A request behind it.
       __builtin_amdgcn_sched_barrier(0);
-      if constexpr (ACT) read_frag(st, 1, F1);
+      if constexpr (ACT) {
+        read_b(st, 1, fb1);
+        pair(0, fb0);
+        fa[0] = read_a(st, 1, 0);
+      }
       stage_b(st ^ 1, RB);
       load_b(k3, RB);
-      if constexpr (ACT) mma_part(F0, 0, NMB);
-#pragma unroll
-      for (int m = 0; m < NMB; ++m) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                     // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, (WI + WJ + NMB - 1) / NMB, 0);   // LDS read
-        __builtin_amdgcn_sched_group_barrier(0x200, (BQ + NMB - 1) / NMB, 0);   // LDS write
-        __builtin_amdgcn_sched_group_barrier(0x020, (BQ + NMB - 1) / NMB, 0);   // global load
-        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);                     // VALU
+      if constexpr (ACT) {
+        __builtin_amdgcn_sched_group_barrier(0x100, WJ, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
-      // region 1b: the rest of the first half beside A of slice i+1 (convert,
-      // LDS) and the request of A of slice i+3
-      if constexpr (ACT) mma_part(F0, 1, NMB);
-      stage_a(st ^ 1, Anext);
-      load_a(k3, Anext);
-#pragma unroll
-      for (int m = 0; m < NM - NMB; ++m) {
+      if constexpr (ACT) {
+        pair(1, fb0);
+        fa[1] = read_a(st, 1, 1);
+      }
+      stage_a(st ^ 1, Anext, 0, (AQ + 1) / 2);
+      if constexpr (ACT) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
-        __builtin_amdgcn_sched_group_barrier(0x002, 5, 1);
-        if (m < AQ) __builtin_amdgcn_sched_group_barrier(0x200, 1, 1);
-        if (m >= NM - NMB - AQ) __builtin_amdgcn_sched_group_barrier(0x020, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 1);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 1);
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 1);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (ACT) {
+        pair(2, fb0);
+        fa[2] = read_a(st, 1, 2);
+      }
+      stage_a(st ^ 1, Anext, (AQ + 1) / 2, AQ);
+      if constexpr (ACT) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 2);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 2);
+        __builtin_amdgcn_sched_group_barrier(0x002, 3, 2);
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 2);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 2);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (ACT) {
+        pair(3, fb0);
+        fa[3] = read_a(st, 1, 3);
+      }
+      load_a(k3, Anext);
+      if constexpr (ACT) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 3);
+        __builtin_amdgcn_sched_group_barrier(0x020, 2, 3);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 3);
+        __builtin_amdgcn_sched_group_barrier(0x020, 2, 3);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 3);
       }
       __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
       __builtin_amdgcn_sched_barrier(0);
-      // region 2: next slice's first-half fragments in flight under this
-      // slice's second-half MFMAs
+      // Second half (fa, fb1): the next slice's first-half fragments are read
+      // from the other stage, fb0 first, then fa[i] behind fragment i's MFMAs.
       if constexpr (ACT) {
-        read_frag(st ^ 1, 0, F0);
-        mma(F1);
+        read_b(st ^ 1, 0, fb0);
+#pragma unroll
+        for (int i2 = 0; i2 < WI; ++i2) {
+          pair(i2, fb1);
+          fa[i2] = read_a(st ^ 1, 0, i2);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x100, WJ, 4);
+#pragma unroll
+        for (int i2 = 0; i2 < WI; ++i2) {
+          __builtin_amdgcn_sched_group_barrier(0x008, WJ, 4);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 4);
+        }
       }
-      __builtin_amdgcn_sched_group_barrier(0x100, WI + WJ, 2);
-      __builtin_amdgcn_sched_group_barrier(0x008, WI * WJ, 2);
       __builtin_amdgcn_sched_barrier(0);
     };
     auto slices = [&](auto act_c) {
       constexpr bool ACT = decltype(act_c)::value;
-      if constexpr (ACT) read_frag(0, 0, F0);
+      if constexpr (ACT) {
+        read_b(0, 0, fb0);
+#pragma unroll
+        for (int i2 = 0; i2 < WI; ++i2) fa[i2] = read_a(0, 0, i2);
+      }
       int64_t p = 0;
       for (; p + 2 <= nk; p += 2) {
         iter(act_c, 0, p, A1, RB);
         iter(act_c, 1, p + 1, A0, RB2);
       }
-      if (ACT && p < nk) {                   // odd count: the last slice is in stage 0
-        read_frag(0, 1, F1);
-        mma(F0);
-        mma(F1);
-      }
+      // odd count: the last slice is in stage 0 (its iteration also restages
+      // that slice and reads fragments of it that are never multiplied)
+      if (p < nk) iter(act_c, 0, p, A1, RB);
     };
     if (n0 + wn < N) slices(std::true_type{});
     else slices(std::false_type{});
