@@ -334,7 +334,9 @@ __global__ __launch_bounds__(NTHR) void k_score(ScoreArgs a) {
   constexpr int NU = SS::NU, FR = SS::FR, PU = SS::PU, PV = SS::PV;
   __shared__ __attribute__((aligned(16))) uint4 sP[2][PU];
   __shared__ Cand<MULTI ? 1 : CAP> cd;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  // the wave index through readfirstlane: wave-uniform for the compiler, so the
+  // row and tile arithmetic that depends on it stays scalar
+  const int tid = threadIdx.x, lane = tid & 63, wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r32 = lane & 31, hg = lane >> 5;
   const cptr<int32_t> cmods = (cptr<int32_t>)(a.mods);   // ModInfo fields, 4 per module
   const cptr<int32_t> cfq = (cptr<int32_t>)(a.fq);
