@@ -842,9 +842,9 @@ void k_gemm_p(KParams kp) {
     // Scheduling-group masks: MFMA 0x008, VALU 0x002, global load 0x020,
     // LDS read 0x100, LDS write 0x200.
 
-    // prologue: slice 0 staged; slices 1 and 2 requested in the order the
-    // loop issues them (B then A of each slice), so that the load counter
-    // holds the same sequence on entry as after every iteration
+    // prologue: slice 0 staged; slices 1 and 2 (those that exist) requested in
+    // the order the loop issues them (B then A of each slice), so that the
+    // load counter holds the same sequence on entry as after every iteration
     if (ragged) load_tail(slice_k0(0), A0, RB);
     else {
       load_a(slice_k0(0), A0);
@@ -855,6 +855,8 @@ void k_gemm_p(KParams kp) {
     if (nk > 1) {
       load_b(clamp(1), RB);
       load_a(clamp(1), A1);
+    }
+    if (nk > 2) {
       load_b(clamp(2), RB2);
       load_a(clamp(2), A0);
     }
@@ -865,8 +867,9 @@ void k_gemm_p(KParams kp) {
     // i+1, Anext the A buffer). ACT: the wave has columns below N; a wave whose
     // columns all lie in the padding of the last column tile only stages its
     // share of the operands (its accumulators stay zero).
-    auto iter = [&](auto act_c, int st, int64_t i, ARegs& Anext, BRegs& RB) {
+    auto iter = [&](auto act_c, auto ld_c, int st, int64_t i, ARegs& Anext, BRegs& RB) {
       constexpr bool ACT = decltype(act_c)::value;
+      constexpr bool LD = decltype(ld_c)::value;   // slice i+3 exists and is requested
       const int64_t k3 = clamp(i + 3);
       // First half, in four segments of one A fragment each: its MFMAs, then
       // its second-half fragment read into fa[i]; beside them B of slice i+1
@@ -881,7 +884,7 @@ void k_gemm_p(KParams kp) {
         fa[0] = read_a(st, 1, 0);
       }
       stage_b(st ^ 1, RB);
-      load_b(k3, RB);
+      if constexpr (LD) load_b(k3, RB);
       if constexpr (ACT) {
         __builtin_amdgcn_sched_group_barrier(0x100, WJ, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
@@ -925,7 +928,7 @@ void k_gemm_p(KParams kp) {
         pair(3, fb0);
         fa[3] = read_a(st, 1, 3);
       }
-      load_a(k3, Anext);
+      if constexpr (LD) load_a(k3, Anext);
       if constexpr (ACT) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 3);
         __builtin_amdgcn_sched_group_barrier(0x020, 2, 3);
@@ -961,14 +964,25 @@ void k_gemm_p(KParams kp) {
 #pragma unroll
         for (int i2 = 0; i2 < WI; ++i2) fa[i2] = read_a(0, 0, i2);
       }
+      constexpr std::true_type LD;
+      constexpr std::false_type NOLD;
       int64_t p = 0;
-      for (; p + 2 <= nk; p += 2) {
-        iter(act_c, 0, p, A1, RB);
-        iter(act_c, 1, p + 1, A0, RB2);
+      for (; p + 5 <= nk; p += 2) {          // slices p + 3 and p + 4 exist
+        iter(act_c, LD, 0, p, A1, RB);
+        iter(act_c, LD, 1, p + 1, A0, RB2);
       }
-      // odd count: the last slice is in stage 0 (its iteration also restages
-      // that slice and reads fragments of it that are never multiplied)
-      if (p < nk) iter(act_c, 0, p, A1, RB);
+      if (p + 4 == nk) {                     // slice p + 3 is the last to request
+        iter(act_c, LD, 0, p, A1, RB);
+        iter(act_c, NOLD, 1, p + 1, A0, RB2);
+        p += 2;
+      }
+      // the last one to three slices: everything they stage is requested, so
+      // no request runs past the unit's last slice (an odd count ends in
+      // stage 0 with one iteration)
+      for (; p < nk; p += 2) {
+        iter(act_c, NOLD, 0, p, A1, RB);
+        if (p + 1 < nk) iter(act_c, NOLD, 1, p + 1, A0, RB2);
+      }
     };
     if (n0 + wn < N) slices(std::true_type{});
     else slices(std::false_type{});
