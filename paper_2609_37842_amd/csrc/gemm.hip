@@ -149,40 +149,48 @@ typedef unsigned int v2u __attribute__((ext_vector_type(2)));
 // 8 (r / 4) + 4 (l / 32) + r % 4 of each block. fp32 C: bounds-checked stores.
 // 16-bit CT (fragment order, see GemmArgs; fp16 or bf16): four consecutive
 // rows of one column are 8 contiguous bytes; no checks.
+//
+// The 16-bit fragment-order part (F16OUT: fp16 entries, else bf16).
+// Rows 16p .. 16p+15 of a block are one 16-token group: lanes l < 32 hold
+// rows +0..3 (q = 2p) and +8..11 (q = 2p+1), lanes l >= 32 rows +4..7 and
+// +12..15. One swap between lane l and lane l + 32 gives lane l tokens 0..7
+// and lane l + 32 tokens 8..15 of column l % 32, so each wave store writes
+// one whole 1 KB block.
+template <int WI, int WJ, bool F16OUT>
+__device__ __forceinline__ void store_ct(const GemmArgs& g, int64_t r0, int64_t c0, int lane,
+                                         const f32x16 (&acc)[WI][WJ]) {
+  const int64_t groups = g.ldct / 16;
+  const int half = lane >> 5;
+#pragma unroll
+  for (int i = 0; i < WI; ++i)
+#pragma unroll
+    for (int j = 0; j < WJ; ++j) {
+      const int64_t cb = (c0 + 32 * j) / 32;
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const f32x16& a = acc[i][j];
+        const uint32_t x0 = cvt_pair<F16OUT>(a[8 * p + 0], a[8 * p + 1]);
+        const uint32_t x1 = cvt_pair<F16OUT>(a[8 * p + 2], a[8 * p + 3]);
+        const uint32_t y0 = cvt_pair<F16OUT>(a[8 * p + 4], a[8 * p + 5]);
+        const uint32_t y1 = cvt_pair<F16OUT>(a[8 * p + 6], a[8 * p + 7]);
+        const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
+        const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
+        const int64_t grp = (r0 + 32 * i + 16 * p) / 16;
+        uint16_t* dst = g.CT + ((cb * groups + grp) * 32 + (lane & 31)) * 16 + 8 * half;
+        *reinterpret_cast<v4u*>(dst) = mk4(s0[0], s1[0], s0[1], s1[1]);
+      }
+    }
+}
+
 template <int WI, int WJ>
 __device__ __forceinline__ void store_tile(const GemmArgs& g, float* C, int64_t ldc, int64_t M,
                                            int64_t N, int64_t r0, int64_t c0, int lane,
                                            const f32x16 (&acc)[WI][WJ]) {
   if (g.CT) {
-    // Rows 16p .. 16p+15 of a block are one 16-token group: lanes l < 32 hold
-    // rows +0..3 (q = 2p) and +8..11 (q = 2p+1), lanes l >= 32 rows +4..7 and
-    // +12..15. One swap between lane l and lane l + 32 gives lane l tokens
-    // 0..7 and lane l + 32 tokens 8..15 of column l % 32, so each wave store
-    // writes one whole 1 KB block.
-    const int64_t groups = g.ldct / 16;
-    const int half = lane >> 5;
-#pragma unroll
-    for (int i = 0; i < WI; ++i)
-#pragma unroll
-      for (int j = 0; j < WJ; ++j) {
-        const int64_t cb = (c0 + 32 * j) / 32;
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          const f32x16& a = acc[i][j];
-          auto cvt = [&](float u, float v) {
-            return g.ct_bf16 ? cvt_pair<false>(u, v) : cvt_pair<true>(u, v);
-          };
-          const uint32_t x0 = cvt(a[8 * p + 0], a[8 * p + 1]);
-          const uint32_t x1 = cvt(a[8 * p + 2], a[8 * p + 3]);
-          const uint32_t y0 = cvt(a[8 * p + 4], a[8 * p + 5]);
-          const uint32_t y1 = cvt(a[8 * p + 6], a[8 * p + 7]);
-          const auto s0 = __builtin_amdgcn_permlane32_swap(x0, y0, false, false);
-          const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
-          const int64_t grp = (r0 + 32 * i + 16 * p) / 16;
-          uint16_t* dst = g.CT + ((cb * groups + grp) * 32 + (lane & 31)) * 16 + 8 * half;
-          *reinterpret_cast<v4u*>(dst) = mk4(s0[0], s1[0], s0[1], s1[1]);
-        }
-      }
+    // the entry type is chosen once per tile (chosen per value pair, it
+    // compiled to a branch around every conversion)
+    if (g.ct_bf16) store_ct<WI, WJ, false>(g, r0, c0, lane, acc);
+    else store_ct<WI, WJ, true>(g, r0, c0, lane, acc);
     return;
   }
 #pragma unroll
