@@ -904,7 +904,7 @@ def main(argv=None):
                 "executed_tflops": exec_launch * passes / (avg_ms * 1e-3) / 1e12,
                 "executed_frac_with_padding": exec_launch * passes / (avg_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
                 "limiter": ("slice loop: L2 loads, LDS stores + fragment reads and MFMA each near a "
-                            "slice's MFMA time, two waves per SIMD; MFMA busy 0.44 at 1.77 GHz "
+                            "slice's MFMA time, two waves per SIMD; MFMA busy 0.46 at 1.77 GHz "
                             "(profiles/rotation_gemm_counters.md)"),
                 "alg_flops_per_launch": flops_launch,
                 "alg_bytes_per_launch": bytes_launch,
