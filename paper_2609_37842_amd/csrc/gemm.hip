@@ -177,7 +177,10 @@ __device__ __forceinline__ void store_ct(const GemmArgs& g, int64_t r0, int64_t 
         const auto s1 = __builtin_amdgcn_permlane32_swap(x1, y1, false, false);
         const int64_t grp = (r0 + 32 * i + 16 * p) / 16;
         uint16_t* dst = g.CT + ((cb * groups + grp) * 32 + (lane & 31)) * 16 + 8 * half;
-        *reinterpret_cast<v4u*>(dst) = mk4(s0[0], s1[0], s0[1], s1[1]);
+        // streaming store: the rotated tokens are read once, by a later
+        // kernel, so their lines need not stay in L2 beside the token rows
+        // that the unit's neighbours re-read
+        __builtin_nontemporal_store(mk4(s0[0], s1[0], s0[1], s1[1]), reinterpret_cast<v4u*>(dst));
       }
     }
 }
